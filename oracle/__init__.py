@@ -1,0 +1,151 @@
+"""CPU oracle for YOSO attention (fp64, plain loops in C).
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the CPU-baseline leg of
+the bench are the only users.  The product path (the HIP library and its Python
+binding) never imports this package, and this package imports nothing from it.
+
+Each wrapper converts its inputs to contiguous fp64 / uint16 arrays and calls the
+matching routine in ``yoso_oracle.c``; see that file for the paper passages the
+routines follow.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "yoso_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (no fast-math: fp64 operations stay as written)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-std=c99", "-D_DEFAULT_SOURCE", "-fPIC", "-shared",
+                               "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+            build()
+        lib = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        I64, I32 = ctypes.c_int64, ctypes.c_int
+        lib.oracle_hash.argtypes = [P, I64, I64, I32, P, I32, I32, P, P]
+        lib.oracle_forward.argtypes = [P, P, P, I64, I64, I64, I32, I32, I32, P]
+        lib.oracle_backward.argtypes = [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, P, P, P]
+        lib.oracle_backward_d2.argtypes = [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, P, P]
+        lib.oracle_expectation.argtypes = [P, P, P, P, I64, I64, I64, I32, I32, P, P, P, P, P]
+        lib.oracle_collision_prob.argtypes = [ctypes.c_double, I32]
+        lib.oracle_collision_prob.restype = ctypes.c_double
+        for fn in ("oracle_hash", "oracle_forward", "oracle_backward", "oracle_backward_d2",
+                   "oracle_expectation"):
+            getattr(lib, fn).restype = None
+        _lib = lib
+    return _lib
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _u16(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.uint16)
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def hash_codes(x, R, m: int, tau: int, with_margin: bool = False):
+    """codes[bh, m, n] (uint16) of rows x[bh, n, d] under hyperplanes R[d, m*tau].
+
+    With ``with_margin`` also returns min_b |projection| per (bh, h, i)."""
+    x = _f64(x)
+    R = _f64(R)
+    bh, n, d = x.shape
+    assert R.shape == (d, m * tau)
+    codes = np.zeros((bh, m, n), np.uint16)
+    margin = np.zeros((bh, m, n), np.float64) if with_margin else None
+    _load().oracle_hash(_ptr(x), bh, n, d, _ptr(R), m, tau, _ptr(codes),
+                        _ptr(margin) if with_margin else None)
+    return (codes, margin) if with_margin else codes
+
+
+def forward(qc, kc, v, m: int, tau: int) -> np.ndarray:
+    qc, kc, v = _u16(qc), _u16(kc), _f64(v)
+    bh, nk, d = v.shape
+    nq = qc.shape[2]
+    assert qc.shape == (bh, m, nq) and kc.shape == (bh, m, nk)
+    y = np.zeros((bh, nq, d), np.float64)
+    _load().oracle_forward(_ptr(qc), _ptr(kc), _ptr(v), bh, nq, nk, d, m, tau, _ptr(y))
+    return y
+
+
+def backward(qc, kc, q, k, v, dy, m: int, tau: int):
+    """(dq, dk, dv) of the sampled surrogate backward, pairwise bucket form."""
+    qc, kc = _u16(qc), _u16(kc)
+    q, k, v, dy = _f64(q), _f64(k), _f64(v), _f64(dy)
+    bh, nq, d = q.shape
+    nk = k.shape[1]
+    dq = np.zeros((bh, nq, d))
+    dk = np.zeros((bh, nk, d))
+    dv = np.zeros((bh, nk, d))
+    _load().oracle_backward(_ptr(qc), _ptr(kc), _ptr(q), _ptr(k), _ptr(v), _ptr(dy),
+                            bh, nq, nk, d, m, tau, _ptr(dq), _ptr(dk), _ptr(dv))
+    return dq, dk, dv
+
+
+def backward_d2(qc, kc, q, k, v, dy, m: int, tau: int):
+    """(dq, dk) of the same surrogate via d runs of the bucket-table subroutine."""
+    qc, kc = _u16(qc), _u16(kc)
+    q, k, v, dy = _f64(q), _f64(k), _f64(v), _f64(dy)
+    bh, nq, d = q.shape
+    nk = k.shape[1]
+    dq = np.zeros((bh, nq, d))
+    dk = np.zeros((bh, nk, d))
+    _load().oracle_backward_d2(_ptr(qc), _ptr(kc), _ptr(q), _ptr(k), _ptr(v), _ptr(dy),
+                               bh, nq, nk, d, m, tau, _ptr(dq), _ptr(dk))
+    return dq, dk
+
+
+def expectation(q, k, v, dy, tau: int, true_grad: bool = False):
+    """E[Y], E[dV], E[dQ], E[dK] over hash functions (and the true dQ if asked)."""
+    q, k, v, dy = _f64(q), _f64(k), _f64(v), _f64(dy)
+    bh, nq, d = q.shape
+    nk = k.shape[1]
+    ey = np.zeros((bh, nq, d))
+    edv = np.zeros((bh, nk, d))
+    edq = np.zeros((bh, nq, d))
+    edk = np.zeros((bh, nk, d))
+    tdq = np.zeros((bh, nq, d)) if true_grad else None
+    _load().oracle_expectation(_ptr(q), _ptr(k), _ptr(v), _ptr(dy), bh, nq, nk, d, tau,
+                               _ptr(ey), _ptr(edv), _ptr(edq), _ptr(edk),
+                               _ptr(tdq) if true_grad else None)
+    out = (ey, edv, edq, edk)
+    return out + (tdq,) if true_grad else out
+
+
+def collision_prob(x: float, tau: int) -> float:
+    return _load().oracle_collision_prob(float(x), int(tau))
+
+
+def run_all(inp: dict, m: int, tau: int, heads: Optional[slice] = None):
+    """Hash + forward + backward for a batch of heads; returns a dict of fp64 arrays."""
+    sl = heads if heads is not None else slice(None)
+    q, k, v, dy = inp["q"][sl], inp["k"][sl], inp["v"][sl], inp["dy"][sl]
+    qc = hash_codes(q, inp["R"], m, tau)
+    kc = hash_codes(k, inp["R"], m, tau)
+    y = forward(qc, kc, v, m, tau)
+    dq, dk, dv = backward(qc, kc, q, k, v, dy, m, tau)
+    return dict(qc=qc, kc=kc, y=y, dq=dq, dk=dk, dv=dv)

@@ -1,0 +1,281 @@
+/*
+ * YOSO attention: plain, slow CPU oracle in fp64.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may include, link or
+ * call this file; only the tests, the smoke check and the CPU baseline of the
+ * bench use it.  It shares no code with the HIP path.
+ *
+ * Every routine follows the paper's text (You Only Sample (Almost) Once,
+ * arXiv 2111.09714) step by step, with the obvious loops and no blocking:
+ *
+ *   hash        Sec. 3.2 overview + Fig. 2 caption: a code is tau concatenated
+ *               random-hyperplane (sign) hashes; m independent hashes.
+ *   forward     Sec. 3.2 overview: per hash, a table of 2^tau d-vectors holds the
+ *               sum of the values whose key falls in each bucket; a query reads
+ *               the bucket of its own code.  Sec. 3.1: the output is the average
+ *               over the m hashes.
+ *   backward    Sec. 3.3: eq. (gradient-v) for dV (the table machinery with the
+ *               roles of queries and keys swapped); eq. (pseudo-gradient-q) for the
+ *               lower-bound surrogate dQ evaluated on the sampled B, and the
+ *               symmetric expression for dK; all averaged over the m hashes.
+ *   backward_d2 the same surrogate written as eq. (backward-d2): d runs of the
+ *               bucket-table subroutine, used to cross-check the pairwise form.
+ *   expectation eq. (yoso-expectation): E[B_ij] = (1 - arccos(q_i.k_j)/pi)^tau,
+ *               giving E[Y], E[dV], E[dQ], E[dK], and the true dQ of
+ *               eq. (gradient-q) for reference.
+ *
+ * Conventions (readings of points the paper leaves open):
+ *   - bit b of hash h is [ sum_l x_l R[l][h*tau+b] > 0 ] (strict), code = sum_b bit_b 2^b;
+ *   - the same hyperplanes hash queries and keys; the backward reuses the
+ *     forward's codes;
+ *   - m-hash averaging is the arithmetic mean, applied to Y, dV, dQ, dK;
+ *   - empty buckets contribute 0 (no renormalisation);
+ *   - tensors are row-major: x[bh][i][l], codes[bh][h][i].
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define CODE(codes, b, h, i, m, n) ((codes)[(((int64_t)(b) * (m) + (h)) * (n)) + (i)])
+
+/* Sign-random-projection hash.  x: [bh][n][d], R: [d][m*tau].
+ * codes: [bh][m][n]; minabs (optional): [bh][m][n], the smallest |projection|
+ * over the tau hyperplanes of each (row, hash), used to tell which bits sit so
+ * close to a hyperplane that rounding may flip them. */
+void oracle_hash(const double *x, int64_t bh, int64_t n, int d,
+                 const double *R, int m, int tau,
+                 uint16_t *codes, double *minabs)
+{
+    const int ncol = m * tau;
+    for (int64_t b = 0; b < bh; b++) {
+        for (int64_t i = 0; i < n; i++) {
+            const double *row = x + (b * n + i) * d;
+            for (int h = 0; h < m; h++) {
+                unsigned code = 0;
+                double closest = INFINITY;
+                for (int bit = 0; bit < tau; bit++) {
+                    const int col = h * tau + bit;
+                    double s = 0.0;
+                    for (int l = 0; l < d; l++)
+                        s += row[l] * R[(int64_t)l * ncol + col];
+                    if (s > 0.0)
+                        code |= 1u << bit;
+                    if (fabs(s) < closest)
+                        closest = fabs(s);
+                }
+                CODE(codes, b, h, i, m, n) = (uint16_t)code;
+                if (minabs)
+                    CODE(minabs, b, h, i, m, n) = closest;
+            }
+        }
+    }
+}
+
+/* One run of the bucket-table subroutine for a single (head, hash):
+ * table[c] = sum over sources s with src_code[s] == c of val[s]   (width w)
+ * out[t]  += weight * table[dst_code[t]]                          for every target t
+ * This is the scatter/gather of the Sec. 3.2 overview. */
+static void table_pass(const uint16_t *src_code, const double *val, int64_t n_src,
+                       const uint16_t *dst_code, int64_t n_dst, int w, int tau,
+                       double weight, double *out, double *table)
+{
+    const int64_t buckets = (int64_t)1 << tau;
+    memset(table, 0, sizeof(double) * buckets * w);
+    for (int64_t s = 0; s < n_src; s++)
+        for (int l = 0; l < w; l++)
+            table[(int64_t)src_code[s] * w + l] += val[s * w + l];
+    for (int64_t t = 0; t < n_dst; t++)
+        for (int l = 0; l < w; l++)
+            out[t * w + l] += weight * table[(int64_t)dst_code[t] * w + l];
+}
+
+/* Forward: y[bh][i] = (1/m) sum_h sum_{j : kc_h(j) == qc_h(i)} v[bh][j]. */
+void oracle_forward(const uint16_t *qc, const uint16_t *kc, const double *v,
+                    int64_t bh, int64_t nq, int64_t nk, int d, int m, int tau,
+                    double *y)
+{
+    double *table = malloc(sizeof(double) * ((size_t)1 << tau) * d);
+    memset(y, 0, sizeof(double) * bh * nq * d);
+    for (int64_t b = 0; b < bh; b++)
+        for (int h = 0; h < m; h++)
+            table_pass(&CODE(kc, b, h, 0, m, nk), v + b * nk * d, nk,
+                       &CODE(qc, b, h, 0, m, nq), nq, d, tau, 1.0 / m,
+                       y + b * nq * d, table);
+    free(table);
+}
+
+/* Backward.
+ * dv = (1/m) sum_h B_h^T dy                        (eq. gradient-v, sampled form)
+ * dq = tau/(2m) sum_h [(dy v^T) .* B_h] k          (eq. pseudo-gradient-q, sampled)
+ * dk = tau/(2m) sum_h [(dy v^T) .* B_h]^T q        (the symmetric expression)
+ * dQ/dK are evaluated bucket by bucket over colliding pairs. */
+void oracle_backward(const uint16_t *qc, const uint16_t *kc,
+                     const double *q, const double *k, const double *v, const double *dy,
+                     int64_t bh, int64_t nq, int64_t nk, int d, int m, int tau,
+                     double *dq, double *dk, double *dv)
+{
+    const int64_t buckets = (int64_t)1 << tau;
+    double *table = malloc(sizeof(double) * buckets * d);
+    /* bucket membership lists: start[c] .. start[c+1] index into members */
+    int64_t *qstart = malloc(sizeof(int64_t) * (buckets + 1));
+    int64_t *kstart = malloc(sizeof(int64_t) * (buckets + 1));
+    int64_t *qmem = malloc(sizeof(int64_t) * (nq > 0 ? nq : 1));
+    int64_t *kmem = malloc(sizeof(int64_t) * (nk > 0 ? nk : 1));
+    int64_t *fill = malloc(sizeof(int64_t) * buckets);
+    const double scale = (double)tau / (2.0 * m);
+
+    memset(dq, 0, sizeof(double) * bh * nq * d);
+    memset(dk, 0, sizeof(double) * bh * nk * d);
+    memset(dv, 0, sizeof(double) * bh * nk * d);
+
+    for (int64_t b = 0; b < bh; b++) {
+        const double *qb = q + b * nq * d, *kb = k + b * nk * d;
+        const double *vb = v + b * nk * d, *dyb = dy + b * nq * d;
+        double *dqb = dq + b * nq * d, *dkb = dk + b * nk * d;
+        for (int h = 0; h < m; h++) {
+            const uint16_t *qch = &CODE(qc, b, h, 0, m, nq);
+            const uint16_t *kch = &CODE(kc, b, h, 0, m, nk);
+
+            /* dV: table of dy keyed by query codes, read at key codes. */
+            table_pass(qch, dyb, nq, kch, nk, d, tau, 1.0 / m, dv + b * nk * d, table);
+
+            /* Group rows by bucket (a plain counting sort). */
+            for (int64_t c = 0; c <= buckets; c++) qstart[c] = kstart[c] = 0;
+            for (int64_t i = 0; i < nq; i++) qstart[qch[i] + 1]++;
+            for (int64_t j = 0; j < nk; j++) kstart[kch[j] + 1]++;
+            for (int64_t c = 0; c < buckets; c++) {
+                qstart[c + 1] += qstart[c];
+                kstart[c + 1] += kstart[c];
+            }
+            for (int64_t c = 0; c < buckets; c++) fill[c] = qstart[c];
+            for (int64_t i = 0; i < nq; i++) qmem[fill[qch[i]]++] = i;
+            for (int64_t c = 0; c < buckets; c++) fill[c] = kstart[c];
+            for (int64_t j = 0; j < nk; j++) kmem[fill[kch[j]]++] = j;
+
+            /* Every colliding pair (i, j): s = dy_i . v_j,
+             * dq_i += scale * s * k_j,  dk_j += scale * s * q_i. */
+            for (int64_t c = 0; c < buckets; c++) {
+                for (int64_t a = qstart[c]; a < qstart[c + 1]; a++) {
+                    const int64_t i = qmem[a];
+                    for (int64_t e = kstart[c]; e < kstart[c + 1]; e++) {
+                        const int64_t j = kmem[e];
+                        double s = 0.0;
+                        for (int l = 0; l < d; l++)
+                            s += dyb[i * d + l] * vb[j * d + l];
+                        for (int l = 0; l < d; l++) {
+                            dqb[i * d + l] += scale * s * kb[j * d + l];
+                            dkb[j * d + l] += scale * s * qb[i * d + l];
+                        }
+                    }
+                }
+            }
+        }
+    }
+    free(table); free(qstart); free(kstart); free(qmem); free(kmem); free(fill);
+}
+
+/* The same dQ, dK surrogate in the form of eq. (backward-d2):
+ *   dq_i = (1/m) sum_h sum_l dy_{i,l} sum_j B_h(i,j) (v_{j,l} (tau/2) k_j)
+ * i.e. for every value dimension l one bucket-table run whose table rows are
+ * the d-vectors v_{j,l} (tau/2) k_j, read at the query codes and weighted by
+ * dy_{i,l}.  dk is the mirror image: tables of dy_{i,l} (tau/2) q_i keyed by the
+ * query codes, read at the key codes and weighted by v_{j,l}. */
+void oracle_backward_d2(const uint16_t *qc, const uint16_t *kc,
+                        const double *q, const double *k, const double *v, const double *dy,
+                        int64_t bh, int64_t nq, int64_t nk, int d, int m, int tau,
+                        double *dq, double *dk)
+{
+    const int64_t buckets = (int64_t)1 << tau;
+    double *table = malloc(sizeof(double) * buckets * d);
+    double *rows = malloc(sizeof(double) * (nq > nk ? nq : nk) * d + 1);
+    double *part = malloc(sizeof(double) * (nq > nk ? nq : nk) * d + 1);
+    memset(dq, 0, sizeof(double) * bh * nq * d);
+    memset(dk, 0, sizeof(double) * bh * nk * d);
+    for (int64_t b = 0; b < bh; b++) {
+        const double *qb = q + b * nq * d, *kb = k + b * nk * d;
+        const double *vb = v + b * nk * d, *dyb = dy + b * nq * d;
+        for (int h = 0; h < m; h++) {
+            const uint16_t *qch = &CODE(qc, b, h, 0, m, nq);
+            const uint16_t *kch = &CODE(kc, b, h, 0, m, nk);
+            for (int l = 0; l < d; l++) {
+                /* dQ: table rows v_{j,l} (tau/2) k_j keyed by key codes. */
+                for (int64_t j = 0; j < nk; j++)
+                    for (int e = 0; e < d; e++)
+                        rows[j * d + e] = vb[j * d + l] * (tau / 2.0) * kb[j * d + e];
+                memset(part, 0, sizeof(double) * nq * d);
+                table_pass(kch, rows, nk, qch, nq, d, tau, 1.0, part, table);
+                for (int64_t i = 0; i < nq; i++)
+                    for (int e = 0; e < d; e++)
+                        dq[(b * nq + i) * d + e] += dyb[i * d + l] * part[i * d + e] / m;
+                /* dK: table rows dy_{i,l} (tau/2) q_i keyed by query codes. */
+                for (int64_t i = 0; i < nq; i++)
+                    for (int e = 0; e < d; e++)
+                        rows[i * d + e] = dyb[i * d + l] * (tau / 2.0) * qb[i * d + e];
+                memset(part, 0, sizeof(double) * nk * d);
+                table_pass(qch, rows, nq, kch, nk, d, tau, 1.0, part, table);
+                for (int64_t j = 0; j < nk; j++)
+                    for (int e = 0; e < d; e++)
+                        dk[(b * nk + j) * d + e] += vb[j * d + l] * part[j * d + e] / m;
+            }
+        }
+    }
+    free(table); free(rows); free(part);
+}
+
+/* Collision probability of eq. (yoso-expectation) for a cosine similarity x. */
+double oracle_collision_prob(double x, int tau)
+{
+    if (x > 1.0) x = 1.0;
+    if (x < -1.0) x = -1.0;
+    return pow(1.0 - acos(x) / M_PI, tau);
+}
+
+/* Exact expectation over hash functions (YOSO-E), O(n^2 d):
+ *   P_ij = (1 - arccos(cos(q_i, k_j))/pi)^tau
+ *   ey  = P v,  edv = P^T dy,
+ *   edq = (tau/2) [(dy v^T) .* P] k,  edk = (tau/2) [(dy v^T) .* P]^T q,
+ *   tdq (optional) = [(dy v^T) .* tau P^{(tau-1)/tau} ./ (pi sqrt(1 - cos^2))] k,
+ *   the true gradient of eq. (gradient-q) for unit rows (diverges as cos -> 1).
+ * The cosine is taken of the rows as given, normalised by their norms. */
+void oracle_expectation(const double *q, const double *k, const double *v, const double *dy,
+                        int64_t bh, int64_t nq, int64_t nk, int d, int tau,
+                        double *ey, double *edv, double *edq, double *edk, double *tdq)
+{
+    memset(ey, 0, sizeof(double) * bh * nq * d);
+    memset(edv, 0, sizeof(double) * bh * nk * d);
+    memset(edq, 0, sizeof(double) * bh * nq * d);
+    memset(edk, 0, sizeof(double) * bh * nk * d);
+    if (tdq) memset(tdq, 0, sizeof(double) * bh * nq * d);
+    for (int64_t b = 0; b < bh; b++) {
+        const double *qb = q + b * nq * d, *kb = k + b * nk * d;
+        const double *vb = v + b * nk * d, *dyb = dy + b * nq * d;
+        for (int64_t i = 0; i < nq; i++) {
+            for (int64_t j = 0; j < nk; j++) {
+                double dot = 0.0, nqi = 0.0, nkj = 0.0, g = 0.0;
+                for (int l = 0; l < d; l++) {
+                    dot += qb[i * d + l] * kb[j * d + l];
+                    nqi += qb[i * d + l] * qb[i * d + l];
+                    nkj += kb[j * d + l] * kb[j * d + l];
+                    g += dyb[i * d + l] * vb[j * d + l];
+                }
+                double cosv = dot / sqrt(nqi * nkj);
+                if (cosv > 1.0) cosv = 1.0;
+                if (cosv < -1.0) cosv = -1.0;
+                const double p = pow(1.0 - acos(cosv) / M_PI, tau);
+                for (int l = 0; l < d; l++) {
+                    ey[(b * nq + i) * d + l] += p * vb[j * d + l];
+                    edv[(b * nk + j) * d + l] += p * dyb[i * d + l];
+                    edq[(b * nq + i) * d + l] += (tau / 2.0) * g * p * kb[j * d + l];
+                    edk[(b * nk + j) * d + l] += (tau / 2.0) * g * p * qb[i * d + l];
+                }
+                if (tdq) {
+                    const double w = tau * pow(1.0 - acos(cosv) / M_PI, tau - 1)
+                                     / (M_PI * sqrt(1.0 - cosv * cosv));
+                    for (int l = 0; l < d; l++)
+                        tdq[(b * nq + i) * d + l] += g * w * kb[j * d + l];
+                }
+            }
+        }
+    }
+}

@@ -1,0 +1,293 @@
+"""Pins of the CPU oracle against facts the paper and the mathematics fix.
+
+None of these re-types the oracle's own formula: each check is a hand-worked
+example, a closed form, a special case, an invariant, a brute-force count on tiny
+inputs, or a Monte-Carlo law of the hash family.  Together they are chosen so
+that a dropped term, a wrong sign, a swapped index or a transposed operand in
+any oracle routine fails at least one of them.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+def _unit(a):
+    return a / np.linalg.norm(a, axis=-1, keepdims=True)
+
+
+def _rand_problem(seed, bh=2, nq=23, nk=19, d=5, m=3, tau=3):
+    g = _rng(seed)
+    q = _unit(g.standard_normal((bh, nq, d)))
+    k = _unit(g.standard_normal((bh, nk, d)))
+    v = g.standard_normal((bh, nk, d))
+    dy = g.standard_normal((bh, nq, d))
+    R = g.standard_normal((d, m * tau))
+    return q, k, v, dy, R
+
+
+def _brute_collisions(qc, kc):
+    """B[bh, h, i, j] = [qc_h(i) == kc_h(j)] by direct comparison of every pair."""
+    return (qc[:, :, :, None] == kc[:, :, None, :]).astype(np.float64)
+
+
+# ---------------------------------------------------------------- worked examples
+
+def test_hash_worked_example(golden):
+    g = golden["hash"]
+    x = np.array(g["x"])[None]
+    codes = oracle.hash_codes(x, np.array(g["R"]), g["m"], g["tau"])
+    np.testing.assert_array_equal(codes[0], np.array(g["codes"]))
+
+
+def test_forward_backward_worked_example(golden):
+    g = golden["forward_backward"]
+    m, tau = g["m"], g["tau"]
+    qc = np.array(g["qc"], np.uint16)[None]
+    kc = np.array(g["kc"], np.uint16)[None]
+    q, k, v, dy = (np.array(g[s])[None] for s in ("q", "k", "v", "dy"))
+    np.testing.assert_allclose(oracle.forward(qc, kc, v, m, tau)[0], g["y"], rtol=0, atol=1e-12)
+    dq, dk, dv = oracle.backward(qc, kc, q, k, v, dy, m, tau)
+    np.testing.assert_allclose(dv[0], g["dv"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dq[0], g["dq"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dk[0], g["dk"], rtol=0, atol=1e-12)
+    dq2, dk2 = oracle.backward_d2(qc, kc, q, k, v, dy, m, tau)
+    np.testing.assert_allclose(dq2[0], g["dq"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dk2[0], g["dk"], rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------- hash special cases
+
+def test_hash_basis_vectors_read_signs_of_R():
+    """For x = e_l the projection on column c is R[l, c] itself, so bit b of hash h
+    must be [R[l, h*tau+b] > 0] and -e_l must give the complement."""
+    d, m, tau = 8, 4, 5
+    R = _rng(1).standard_normal((d, m * tau))
+    x = np.eye(d)[None]
+    codes = oracle.hash_codes(x, R, m, tau)
+    neg = oracle.hash_codes(-x, R, m, tau)
+    for l in range(d):
+        for h in range(m):
+            want = sum(1 << b for b in range(tau) if R[l, h * tau + b] > 0)
+            assert codes[0, h, l] == want
+            assert neg[0, h, l] == (~want) & ((1 << tau) - 1)
+
+
+def test_hash_scale_invariance_and_margin():
+    q, _, _, _, R = _rand_problem(2, bh=1, nq=50, d=16, m=6, tau=7)
+    c1, margin = oracle.hash_codes(q, R, 6, 7, with_margin=True)
+    c2 = oracle.hash_codes(q * 3.75, R, 6, 7)
+    np.testing.assert_array_equal(c1, c2)
+    # the margin is the smallest |projection| over the tau hyperplanes of a hash
+    proj = q[0] @ R
+    want = np.abs(proj).reshape(50, 6, 7).min(axis=2).T
+    np.testing.assert_allclose(margin[0], want, rtol=1e-12)
+
+
+# ---------------------------------------------------------------- hash law
+
+def _angle_pair(theta, d, seed):
+    g = _rng(seed)
+    a = _unit(g.standard_normal(d))
+    b = g.standard_normal(d)
+    b = _unit(b - (b @ a) * a)
+    return np.stack([a, math.cos(theta) * a + math.sin(theta) * b])
+
+
+@pytest.mark.parametrize("d", [3, 64])
+@pytest.mark.parametrize("tau", [1, 8])
+@pytest.mark.parametrize("theta", [0.05, math.pi / 4, math.pi / 2, 2 * math.pi / 3, math.pi - 0.05])
+def test_collision_frequency_matches_closed_form(d, tau, theta):
+    """Per-code collision probability of tau concatenated hyperplane hashes is
+    (1 - theta/pi)^tau (eq. yoso-expectation; tau = 1 is Charikar's 1 - theta/pi)."""
+    S = 100_000 if tau == 8 else 20_000
+    x = _angle_pair(theta, d, seed=int(theta * 1000) + d + tau)
+    R = _rng(10 + d + tau).standard_normal((d, S * tau))
+    codes = oracle.hash_codes(x[None], R, S, tau)[0]
+    hits = codes[:, 0] == codes[:, 1]
+    p = (1 - theta / math.pi) ** tau
+    assert abs(hits.mean() - p) <= 5 * math.sqrt(p * (1 - p) / S) + 1e-12
+    # hashes use disjoint columns, so collisions of consecutive hashes are independent
+    joint = (hits[0::2] & hits[1::2]).mean()
+    half = S // 2
+    assert abs(joint - p * p) <= 5 * math.sqrt(p * p * (1 - p * p) / half) + 1e-12
+
+
+def test_collision_prob_closed_form_points():
+    """Fig. 2: p(1) = 1, p(0) = 2^-tau, p(-1) = 0, and p is increasing."""
+    for tau in (1, 2, 8, 9):
+        assert oracle.collision_prob(1.0, tau) == 1.0
+        assert abs(oracle.collision_prob(0.0, tau) - 2.0 ** -tau) < 1e-15
+        assert oracle.collision_prob(-1.0, tau) == 0.0
+        xs = np.linspace(-1, 1, 101)
+        ps = [oracle.collision_prob(x, tau) for x in xs]
+        assert all(b >= a for a, b in zip(ps, ps[1:]))
+
+
+def test_surrogate_is_lower_bound_of_true_derivative():
+    """Sec. 3.3 / Fig. 2: (tau/2) p(x) <= p'(x) on (-1, 1), p'(x) = tau (1-acos(x)/pi)^(tau-1) / (pi sqrt(1-x^2))."""
+    for tau in (1, 2, 4, 8, 9, 16):
+        xs = np.linspace(-0.999999, 0.999999, 20001)
+        p1 = 1 - np.arccos(xs) / math.pi
+        dp = tau * p1 ** (tau - 1) / (math.pi * np.sqrt(1 - xs ** 2))
+        assert np.all(tau / 2 * p1 ** tau <= dp * (1 + 1e-12))
+
+
+# ---------------------------------------------------------------- forward
+
+def test_forward_matches_brute_force_pairs():
+    q, k, v, dy, R = _rand_problem(3)
+    m, tau = 3, 3
+    qc, kc = oracle.hash_codes(q, R, m, tau), oracle.hash_codes(k, R, m, tau)
+    B = _brute_collisions(qc, kc)
+    want = np.einsum("bhij,bjd->bid", B, v) / m
+    np.testing.assert_allclose(oracle.forward(qc, kc, v, m, tau), want, rtol=0, atol=1e-12)
+
+
+def test_forward_ones_counts_collisions():
+    """Plugging V = 1 gives B 1 (Sec. 3.1, normalising attention): integer counts / m."""
+    q, k, _, _, R = _rand_problem(4, nq=40, nk=31, d=6, m=5, tau=2)
+    m, tau = 5, 2
+    qc, kc = oracle.hash_codes(q, R, m, tau), oracle.hash_codes(k, R, m, tau)
+    y = oracle.forward(qc, kc, np.ones(k.shape), m, tau) * m
+    np.testing.assert_allclose(y, np.round(y), rtol=0, atol=1e-12)
+    y = np.round(y)
+    counts = sum((qc[:, h, :, None] == kc[:, h, None, :]).sum(-1) for h in range(m))
+    np.testing.assert_array_equal(y[..., 0], counts)
+
+
+def test_forward_keys_equal_queries_collide_with_themselves():
+    q, _, _, _, R = _rand_problem(5, nq=17, d=4, m=7, tau=4)
+    m, tau = 7, 4
+    c = oracle.hash_codes(q, R, m, tau)
+    e = np.zeros((q.shape[0], 17, 17))
+    e[:, np.arange(17), np.arange(17)] = 1.0   # v_j = e_j reads column j of C
+    y = oracle.forward(c, c, e, m, tau) * m
+    np.testing.assert_allclose(np.diagonal(y, axis1=1, axis2=2), m, rtol=0, atol=1e-12)
+
+
+def test_forward_empty_keys_give_zero():
+    qc = np.zeros((1, 2, 5), np.uint16)
+    kc = np.zeros((1, 2, 0), np.uint16)
+    y = oracle.forward(qc, kc, np.zeros((1, 0, 3)), 2, 4)
+    assert y.shape == (1, 5, 3) and not y.any()
+
+
+# ---------------------------------------------------------------- backward
+
+def test_dv_is_adjoint_of_forward():
+    """Y is linear in V, so <dY, Y> = <dV, V> exactly (eq. gradient-v, sampled)."""
+    q, k, v, dy, R = _rand_problem(6)
+    m, tau = 3, 3
+    qc, kc = oracle.hash_codes(q, R, m, tau), oracle.hash_codes(k, R, m, tau)
+    y = oracle.forward(qc, kc, v, m, tau)
+    _, _, dv = oracle.backward(qc, kc, q, k, v, dy, m, tau)
+    assert abs(np.sum(dy * y) - np.sum(dv * v)) < 1e-10
+    # finite difference of the sampled forward in V along a random direction
+    e = _rng(7).standard_normal(v.shape)
+    fd = np.sum(dy * (oracle.forward(qc, kc, v + 0.5 * e, m, tau) - y)) / 0.5
+    assert abs(fd - np.sum(dv * e)) < 1e-9
+
+
+def test_dqdk_pairwise_equals_backward_d2():
+    """eq. (pseudo-gradient-q) evaluated pair by pair equals eq. (backward-d2)."""
+    q, k, v, dy, R = _rand_problem(8, nq=29, nk=33, d=6, m=4, tau=2)
+    m, tau = 4, 2
+    qc, kc = oracle.hash_codes(q, R, m, tau), oracle.hash_codes(k, R, m, tau)
+    dq, dk, _ = oracle.backward(qc, kc, q, k, v, dy, m, tau)
+    dq2, dk2 = oracle.backward_d2(qc, kc, q, k, v, dy, m, tau)
+    np.testing.assert_allclose(dq, dq2, rtol=0, atol=1e-11)
+    np.testing.assert_allclose(dk, dk2, rtol=0, atol=1e-11)
+
+
+def test_backward_matches_dense_masked_brute_force():
+    q, k, v, dy, R = _rand_problem(9)
+    m, tau = 3, 3
+    qc, kc = oracle.hash_codes(q, R, m, tau), oracle.hash_codes(k, R, m, tau)
+    C = _brute_collisions(qc, kc).sum(axis=1)            # [bh, nq, nk]
+    S = np.einsum("bid,bjd->bij", dy, v)                  # dY V^T
+    W = tau / (2 * m) * S * C
+    dq, dk, dv = oracle.backward(qc, kc, q, k, v, dy, m, tau)
+    np.testing.assert_allclose(dq, np.einsum("bij,bjd->bid", W, k), rtol=0, atol=1e-11)
+    np.testing.assert_allclose(dk, np.einsum("bij,bid->bjd", W, q), rtol=0, atol=1e-11)
+    np.testing.assert_allclose(dv, np.einsum("bij,bid->bjd", C / m, dy), rtol=0, atol=1e-11)
+
+
+def test_dq_dk_inner_products_agree():
+    """<dQ, Q> = <dK, K> = tau/(2m) sum_ij C_ij (dY_i.V_j)(Q_i.K_j) for the surrogate."""
+    q, k, v, dy, R = _rand_problem(10, nq=31, nk=27, d=7, m=5, tau=2)
+    m, tau = 5, 2
+    qc, kc = oracle.hash_codes(q, R, m, tau), oracle.hash_codes(k, R, m, tau)
+    dq, dk, _ = oracle.backward(qc, kc, q, k, v, dy, m, tau)
+    a, b = np.sum(dq * q), np.sum(dk * k)
+    assert abs(a - b) < 1e-10 * max(1.0, abs(a))
+
+
+# ---------------------------------------------------------------- Monte-Carlo laws
+
+def _mc_batches(q, k, v, dy, tau, hashes, batches, seed):
+    """Average of the sampled forward/backward over `hashes` fresh hash functions,
+    repeated for `batches` independent batches."""
+    d = q.shape[-1]
+    outs = []
+    g = _rng(seed)
+    for _ in range(batches):
+        R = g.standard_normal((d, hashes * tau))
+        qc, kc = oracle.hash_codes(q, R, hashes, tau), oracle.hash_codes(k, R, hashes, tau)
+        y = oracle.forward(qc, kc, v, hashes, tau)
+        dq, dk, dv = oracle.backward(qc, kc, q, k, v, dy, hashes, tau)
+        outs.append(np.stack([y, dq, dk, dv]))
+    return np.stack(outs)  # [batches, 4, bh, n, d]
+
+
+def test_monte_carlo_mean_converges_to_expectation():
+    """YOSO-m -> YOSO-E (Sec. 3.1): the average over many hashes tends to P V, and the
+    backward average to P^T dY and (tau/2)[(dY V^T) .* P] K (eqs. gradient-v,
+    pseudo-gradient-q).  Fig. 1 setting: n = 32 keys in 3 dimensions."""
+    g = _rng(11)
+    tau = 4
+    q = _unit(g.standard_normal((1, 32, 3)))
+    k = _unit(g.standard_normal((1, 32, 3)))
+    v = g.standard_normal((1, 32, 3))
+    dy = g.standard_normal((1, 32, 3))
+    ey, edv, edq, edk = oracle.expectation(q, k, v, dy, tau)
+    want = np.stack([ey, edq, edk, edv])
+    samples = _mc_batches(q, k, v, dy, tau, hashes=256, batches=40, seed=12)
+    mean = samples.mean(0)
+    se = samples.std(0, ddof=1) / math.sqrt(samples.shape[0])
+    z = np.abs(mean - want) / np.maximum(se, 1e-12)
+    assert np.all(z < 6.0), z.max()
+    # error falls roughly like 1/sqrt(number of hashes)
+    small = _mc_batches(q, k, v, dy, tau, hashes=64, batches=1, seed=13)[0]
+    large = _mc_batches(q, k, v, dy, tau, hashes=4096, batches=1, seed=14)[0]
+    e_small = np.linalg.norm(small - want)
+    e_large = np.linalg.norm(large - want)
+    assert e_large < e_small / 3.0  # sqrt(64) = 8 in expectation
+
+
+def test_true_gradient_matches_finite_difference_of_expectation():
+    """eq. (gradient-q): the derivative of <dY, P V> in q_i along a tangent direction."""
+    g = _rng(15)
+    tau, d = 3, 5
+    q = _unit(g.standard_normal((1, 4, d)))
+    k = _unit(g.standard_normal((1, 6, d)))
+    v = g.standard_normal((1, 6, d))
+    dy = g.standard_normal((1, 4, d))
+    _, _, _, _, tdq = oracle.expectation(q, k, v, dy, tau, true_grad=True)
+    i = 2
+    t = g.standard_normal(d)
+    t -= (t @ q[0, i]) * q[0, i]
+    t /= np.linalg.norm(t)
+    def loss(eps):
+        qq = q.copy()
+        qq[0, i] = _unit(q[0, i] + eps * t)
+        return np.sum(dy * oracle.expectation(qq, k, v, dy, tau)[0])
+    h = 1e-5
+    fd = (loss(h) - loss(-h)) / (2 * h)
+    assert abs(fd - tdq[0, i] @ t) < 1e-6 * max(1.0, abs(fd))
