@@ -1,0 +1,130 @@
+/*
+ * yoso.h -- C ABI of the MI355X (gfx950) YOSO-attention library (libyoso.so).
+ *
+ * YOSO attention (You Only Sample (Almost) Once, arXiv 2111.09714) replaces the
+ * softmax matrix by Bernoulli variables B_ij = [f(q_i) == f(k_j)] realised by
+ * one locality-sensitive hash f per sample (Sec. 3.1, eq. yoso-formulation),
+ * and averages m such samples.  With unit-length rows Q, K (Remark 1; the
+ * experiments l2-normalise them, Sec. 4) and values V:
+ *
+ *   Y  = (1/m) sum_h B_h(Q,K) V                                   (Sec. 3.1-3.2)
+ *   dV = (1/m) sum_h B_h^T dY                                     (eq. gradient-v)
+ *   dQ = tau/(2m) sum_h [(dY V^T) .* B_h] K                      (eq. pseudo-gradient-q)
+ *   dK = tau/(2m) sum_h [(dY V^T) .* B_h]^T Q                    (the symmetric form)
+ *
+ * Conventions shared by every call:
+ *   - Every tensor pointer is a DEVICE pointer owned by the caller; the library
+ *     allocates nothing and keeps no state between calls.
+ *   - Tensors are dense row-major: x[bh][i][l] with bh = batch*heads flattened,
+ *     i the row (token) and l < d the feature; codes[bh][h][i].
+ *   - All device pointers must be 16-byte aligned.
+ *   - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
+ *     default stream).  Outputs are overwritten, never accumulated into.
+ *   - Every argument check happens on the host before any HIP call, so a bad
+ *     call returns an error without touching the device.  A HIP launch error is
+ *     returned as YOSO_ERR_DEVICE; yoso_last_error() then holds its text.
+ *   - Limits: d == 64; 1 <= tau <= 12; 1 <= m <= 64; m*tau <= 512;
+ *     0 <= n <= 65536 per tensor; bh >= 0.  Zero-sized tensors are valid.
+ *   - Inputs must be finite.  The hash stages rows through fp16 pairs after a
+ *     2^8 scaling, so |x| must stay below 255 (unit rows always do) and |R| below
+ *     65504; V and dY must stay below 32768 in magnitude.
+ */
+#ifndef YOSO_H
+#define YOSO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    YOSO_OK = 0,
+    YOSO_ERR_NULL = 1,      /* a required pointer is NULL (and its tensor is not empty) */
+    YOSO_ERR_SHAPE = 2,     /* bh < 0, n out of [0, 65536], or d != 64 */
+    YOSO_ERR_HASH = 3,      /* tau, m or m*tau out of range */
+    YOSO_ERR_DTYPE = 4,     /* unknown yoso_dtype */
+    YOSO_ERR_ALIGN = 5,     /* a device pointer is not 16-byte aligned */
+    YOSO_ERR_WORKSPACE = 6, /* workspace NULL or smaller than yoso_workspace_size() */
+    YOSO_ERR_DEVICE = 7,    /* a HIP call failed; see yoso_last_error() */
+    YOSO_ERR_OP = 8         /* unknown yoso_op */
+} yoso_status;
+
+/* Storage type of Q, K, V, dY and of the outputs Y, dQ, dK, dV.  Arithmetic is
+ * fp32 either way (fp32 tables and accumulators); bf16 outputs are rounded to
+ * nearest even once at the end. */
+typedef enum { YOSO_F32 = 0, YOSO_BF16 = 1 } yoso_dtype;
+
+typedef enum { YOSO_OP_HASH = 0, YOSO_OP_FORWARD = 1, YOSO_OP_BACKWARD = 2 } yoso_op;
+
+/*
+ * Sign-random-projection hash (Sec. 3.2 overview; Fig. 2 caption: tau
+ * concatenated hyperplane hashes, collision probability (1 - theta/pi)^tau).
+ *
+ *   codes[b][h][i] = sum_{t<tau} [ x[b][i] . R[:, h*tau + t] > 0 ] << t
+ *
+ * x      [bh][n][d]  rows to hash (fp32 or bf16 per dtype); Q and K are hashed
+ *                    with the same R so that B_ij = [codes_q == codes_k].
+ * R      [d][m*tau]  fp32 hyperplanes, column h*tau+t = hyperplane t of hash h.
+ * codes  [bh][m][n]  uint16 output, low tau bits used (consumers read only the
+ *                    low tau bits of the codes they are given).
+ * The sign test is strict (a zero projection gives bit 0).  Bits whose
+ * projection lies within about 1e-6 of zero may differ from an exact-arithmetic
+ * evaluation; everywhere else the code is exact.
+ */
+yoso_status yoso_hash(const void *x, yoso_dtype dtype, int64_t bh, int64_t n, int32_t d,
+                      const float *R, int32_t m, int32_t tau, uint16_t *codes, void *stream);
+
+/*
+ * Forward (Sec. 3.2 overview: per hash, a table of 2^tau buckets holding the sum
+ * of V over the keys hashed to each bucket; each query reads the bucket of its
+ * own code; Sec. 3.1: the m samples are averaged).
+ *
+ *   y[b][i] = (1/m) sum_h sum_{j : kcodes[b][h][j] == qcodes[b][h][i]} v[b][j]
+ *
+ * qcodes [bh][m][n_q], kcodes [bh][m][n_k]  from yoso_hash with the same R.
+ * v      [bh][n_k][d],  y [bh][n_q][d]  (dtype).  Queries whose buckets are empty
+ * get 0 (no renormalisation).
+ * workspace: yoso_workspace_size(YOSO_OP_FORWARD, ...) bytes (may be 0, then
+ * workspace may be NULL).
+ */
+yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const void *v,
+                         yoso_dtype dtype, int64_t bh, int64_t n_q, int64_t n_k, int32_t d,
+                         int32_t m, int32_t tau, void *y, void *workspace, size_t workspace_bytes,
+                         void *stream);
+
+/*
+ * Backward of the forward above, reusing its codes (Sec. 3.3):
+ *   dv = (1/m) sum_h B_h^T dy                          eq. (gradient-v), sampled form
+ *   dq = tau/(2m) sum_h [(dy v^T) .* B_h] k           eq. (pseudo-gradient-q), sampled
+ *   dk = tau/(2m) sum_h [(dy v^T) .* B_h]^T q         symmetric counterpart for K
+ * with B_h(i,j) = [qcodes[b][h][i] == kcodes[b][h][j]].  dq, dk use the paper's
+ * lower-bound surrogate (tau/2) p of the collision-probability derivative.
+ *
+ * q, dy, dq [bh][n_q][d];  k, v, dk, dv [bh][n_k][d]  (dtype).
+ * workspace: yoso_workspace_size(YOSO_OP_BACKWARD, ...) bytes; the call uses
+ * it as scratch (bucket offsets, row permutations, fp32 accumulators).
+ */
+yoso_status yoso_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q,
+                          const void *k, const void *v, const void *dy, yoso_dtype dtype,
+                          int64_t bh, int64_t n_q, int64_t n_k, int32_t d, int32_t m, int32_t tau,
+                          void *dq, void *dk, void *dv, void *workspace, size_t workspace_bytes,
+                          void *stream);
+
+/* Bytes of device workspace that `op` needs for these arguments (written to
+ * *bytes).  Validates the arguments exactly as the call itself does. */
+yoso_status yoso_workspace_size(yoso_op op, yoso_dtype dtype, int64_t bh, int64_t n_q,
+                                int64_t n_k, int32_t d, int32_t m, int32_t tau, size_t *bytes);
+
+/* Static description of a status code. */
+const char *yoso_status_string(yoso_status status);
+
+/* Detail of the last failing call on this thread ("" if none). */
+const char *yoso_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* YOSO_H */

@@ -1,0 +1,179 @@
+"""MI355X (gfx950) YOSO attention: Python binding of libyoso.so.
+
+The binding only marshals arguments: every step of the computation runs in the
+HIP kernels behind the C ABI declared in include/yoso.h.  There is no fallback:
+if the library is missing or a call fails, an exception is raised.
+
+Function names follow the C ABI:
+    yoso_hash(x, R, m, tau, codes)                     codes[bh, m, n] (int16/uint16 storage)
+    yoso_forward(qcodes, kcodes, v, m, tau, y, ws)     y = (1/m) sum_h B_h v
+    yoso_backward(qcodes, kcodes, q, k, v, dy, m, tau, dq, dk, dv, ws)
+    yoso_workspace_size(op, dtype, bh, n_q, n_k, d, m, tau) -> bytes
+Tensors are torch tensors on the GPU, contiguous, [bh, n, 64], float32 or
+bfloat16.  Work is enqueued on the current torch stream unless `stream` is given.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+__all__ = [
+    "YosoError", "F32", "BF16", "OP_HASH", "OP_FORWARD", "OP_BACKWARD",
+    "lib", "lib_path", "yoso_workspace_size", "yoso_hash", "yoso_forward", "yoso_backward",
+    "workspace", "hash_qk", "forward", "backward",
+]
+
+F32, BF16 = 0, 1
+OP_HASH, OP_FORWARD, OP_BACKWARD = 0, 1, 2
+STATUS = {0: "YOSO_OK", 1: "YOSO_ERR_NULL", 2: "YOSO_ERR_SHAPE", 3: "YOSO_ERR_HASH", 4: "YOSO_ERR_DTYPE",
+          5: "YOSO_ERR_ALIGN", 6: "YOSO_ERR_WORKSPACE", 7: "YOSO_ERR_DEVICE", 8: "YOSO_ERR_OP"}
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_PKG, "libyoso.so")
+_lib = None
+
+
+class YosoError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        super().__init__(f"{STATUS.get(status, status)}: {detail}")
+
+
+def lib_path() -> str:
+    return _LIB_PATH
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libyoso.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise ImportError(f"{_LIB_PATH} is missing: build it with `python -m paper_2111_09714_amd.build`")
+        L = ctypes.CDLL(_LIB_PATH)
+        P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+        L.yoso_hash.argtypes = [P, I32, I64, I64, I32, P, I32, I32, P, P]
+        L.yoso_forward.argtypes = [P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, SZ, P]
+        L.yoso_backward.argtypes = [P, P, P, P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, P, P, SZ, P]
+        L.yoso_workspace_size.argtypes = [I32, I32, I64, I64, I64, I32, I32, I32, ctypes.POINTER(SZ)]
+        for fn in ("yoso_hash", "yoso_forward", "yoso_backward", "yoso_workspace_size"):
+            getattr(L, fn).restype = ctypes.c_int
+        L.yoso_status_string.argtypes = [ctypes.c_int]
+        L.yoso_status_string.restype = ctypes.c_char_p
+        L.yoso_last_error.argtypes = []
+        L.yoso_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        raise YosoError(status, lib().yoso_last_error().decode())
+
+
+# ------------------------------------------------------------------ tensor marshalling
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype} (float32 or bfloat16)")
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensor must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t.data_ptr() if t.numel() > 0 else None
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _codes_ok(c) -> None:
+    import torch
+    if c.dtype not in (torch.int16, torch.uint16):
+        raise TypeError("codes must be int16 or uint16 tensors (16-bit storage)")
+
+
+def yoso_workspace_size(op: int, dtype: int, bh: int, n_q: int, n_k: int, d: int, m: int, tau: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(lib().yoso_workspace_size(op, dtype, bh, n_q, n_k, d, m, tau, ctypes.byref(out)))
+    return out.value
+
+
+def yoso_hash(x, R, m: int, tau: int, codes, stream=None) -> None:
+    """codes[b, h, i] = sum_t [x[b, i] . R[:, h*tau + t] > 0] << t."""
+    _codes_ok(codes)
+    bh, n, d = x.shape
+    _check(lib().yoso_hash(_ptr(x), _dtype_code(x), bh, n, d, _ptr(R), m, tau, _ptr(codes), _stream(stream)))
+
+
+def yoso_forward(qcodes, kcodes, v, m: int, tau: int, y, ws=None, stream=None) -> None:
+    """y = (1/m) sum_h B_h v with B_h(i, j) = [qcodes[:, h, i] == kcodes[:, h, j]]."""
+    _codes_ok(qcodes)
+    _codes_ok(kcodes)
+    bh, n_k, d = v.shape
+    n_q = y.shape[1]
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().yoso_forward(_ptr(qcodes), _ptr(kcodes), _ptr(v), _dtype_code(v), bh, n_q, n_k, d, m, tau,
+                              _ptr(y), _ptr(ws), nbytes, _stream(stream)))
+
+
+def yoso_backward(qcodes, kcodes, q, k, v, dy, m: int, tau: int, dq, dk, dv, ws, stream=None) -> None:
+    """dv = (1/m) sum_h B_h^T dy;  dq, dk = tau/(2m) sum_h [(dy v^T) .* B_h] k, ...^T q."""
+    _codes_ok(qcodes)
+    _codes_ok(kcodes)
+    bh, n_q, d = q.shape
+    n_k = k.shape[1]
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().yoso_backward(_ptr(qcodes), _ptr(kcodes), _ptr(q), _ptr(k), _ptr(v), _ptr(dy), _dtype_code(q),
+                               bh, n_q, n_k, d, m, tau, _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws), nbytes,
+                               _stream(stream)))
+
+
+# ------------------------------------------------------------------ allocating conveniences
+
+def workspace(op: int, x, m: int, tau: int, n_k: Optional[int] = None):
+    """A uint8 device tensor large enough for `op` on tensors shaped like x ([bh, n_q, 64])."""
+    import torch
+    bh, n_q, d = x.shape
+    n_k = n_q if n_k is None else n_k
+    nbytes = yoso_workspace_size(op, _dtype_code(x), bh, n_q, n_k, d, m, tau)
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=x.device)
+
+
+def hash_qk(q, k, R, m: int, tau: int):
+    """Codes of Q and K under the same hyperplanes (fresh int16 tensors)."""
+    import torch
+    qc = torch.empty((q.shape[0], m, q.shape[1]), dtype=torch.int16, device=q.device)
+    kc = torch.empty((k.shape[0], m, k.shape[1]), dtype=torch.int16, device=k.device)
+    yoso_hash(q, R, m, tau, qc)
+    yoso_hash(k, R, m, tau, kc)
+    return qc, kc
+
+
+def forward(qcodes, kcodes, v, m: int, tau: int, n_q: Optional[int] = None):
+    import torch
+    n_q = qcodes.shape[2] if n_q is None else n_q
+    y = torch.empty((v.shape[0], n_q, v.shape[2]), dtype=v.dtype, device=v.device)
+    ws = workspace(OP_FORWARD, y, m, tau, n_k=v.shape[1])
+    yoso_forward(qcodes, kcodes, v, m, tau, y, ws)
+    return y
+
+
+def backward(qcodes, kcodes, q, k, v, dy, m: int, tau: int):
+    import torch
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = workspace(OP_BACKWARD, q, m, tau, n_k=k.shape[1])
+    yoso_backward(qcodes, kcodes, q, k, v, dy, m, tau, dq, dk, dv, ws)
+    return dq, dk, dv

@@ -1,0 +1,107 @@
+// Shared device helpers of the gfx950 YOSO kernels (internal header).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace yoso {
+
+constexpr int D = 64;  // head dimension supported by the kernels
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+// Exact widening of bf16 bit patterns.
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+    return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// fp32 -> bf16, round to nearest even (inputs are finite).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return static_cast<uint16_t>(u >> 16);
+}
+
+// Load 8 consecutive elements of a row (fp32 or bf16 storage) as fp32.
+// `p` must be 16-byte aligned for fp32 and 16-byte aligned for bf16.
+template <bool BF16>
+__device__ __forceinline__ void load8(const void *base, int64_t elem_off, float out[8]) {
+    if constexpr (BF16) {
+        const uint4 w = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(base) + elem_off);
+        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            out[2 * i] = __uint_as_float(ws[i] << 16);
+            out[2 * i + 1] = __uint_as_float(ws[i] & 0xFFFF0000u);
+        }
+    } else {
+        const float4 *p = reinterpret_cast<const float4 *>(static_cast<const float *>(base) + elem_off);
+        const float4 a = p[0], b = p[1];
+        out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
+        out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
+    }
+}
+
+// Load one element (fp32 or bf16 storage) as fp32.
+template <bool BF16>
+__device__ __forceinline__ float load1(const void *base, int64_t elem_off) {
+    if constexpr (BF16)
+        return bf16_to_f32(static_cast<const uint16_t *>(base)[elem_off]);
+    else
+        return static_cast<const float *>(base)[elem_off];
+}
+
+// Split fp32 values into an fp16 pair (hi + lo) after multiplying by `scale`
+// (a power of two, so the scaling is exact).  hi + lo carries about 22
+// significant bits: enough that the three MFMA products hi*hi, hi*lo, lo*hi
+// reproduce an fp32 dot product to ~1e-6 relative.
+__device__ __forceinline__ void split8(const float v[8], float scale, half8 &hi, half8 &lo) {
+#pragma unroll
+    for (int i = 0; i < 8; i++) {
+        const float s = v[i] * scale;
+        const _Float16 h = static_cast<_Float16>(s);
+        hi[i] = h;
+        lo[i] = static_cast<_Float16>(s - static_cast<float>(h));
+    }
+}
+
+__device__ __forceinline__ void split4(const float v[4], float scale, half4 &hi, half4 &lo) {
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        const float s = v[i] * scale;
+        const _Float16 h = static_cast<_Float16>(s);
+        hi[i] = h;
+        lo[i] = static_cast<_Float16>(s - static_cast<float>(h));
+    }
+}
+
+// Three-product fp16 emulation of an fp32 MFMA step: acc += a*b.
+__device__ __forceinline__ floatx4 mfma3_16x16x32(const half8 &ah, const half8 &al, const half8 &bh,
+                                                  const half8 &bl, floatx4 acc) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bh, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bh, acc, 0, 0, 0);
+    return acc;
+}
+
+__device__ __forceinline__ floatx4 mfma3_16x16x16(const half4 &ah, const half4 &al, const half4 &bh,
+                                                  const half4 &bl, floatx4 acc) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x16f16(ah, bh, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x16f16(ah, bl, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x16f16(al, bh, acc, 0, 0, 0);
+    return acc;
+}
+
+// Workgroups are dispatched to the 8 XCDs round-robin (id % 8).  Remap so that
+// consecutive logical ids land on the same XCD and share its L2; the mapping is
+// a bijection on [0, n) for any n.
+__device__ __forceinline__ int64_t xcd_remap(int64_t id, int64_t n) {
+    constexpr int64_t X = 8;
+    const int64_t q = n / X, r = n % X;
+    const int64_t x = id % X, i = id / X;
+    return x * q + (x < r ? x : r) + i;
+}
+
+}  // namespace yoso

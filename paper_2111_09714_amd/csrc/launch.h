@@ -1,0 +1,43 @@
+// Host-side launchers of the YOSO kernels (internal to libyoso).
+// Arguments are assumed valid: the C ABI layer checks them first.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace yoso {
+
+// LDS bytes that one table workgroup may use for bucket tables.
+constexpr size_t kTableLdsBudget = 128 * 1024;
+// Widest feature slice per table workgroup (wider slices run out of registers).
+constexpr int kTableMaxDS = 16;
+
+struct TablePlan {
+    int G;        // hashes whose tables share LDS at once
+    int DS;       // feature dims per workgroup
+    int groups;   // ceil(m / G)
+    size_t lds;   // table bytes = 2^tau * G * DS * 4
+};
+
+TablePlan plan_table(int m, int tau);
+size_t table_workspace_bytes(bool bf16, int64_t bh, int64_t n_dst, int m, int tau);
+size_t hash_lds_bytes(int m, int tau);
+
+struct BackwardLayout {
+    size_t qoff, koff, qperm, kperm, qsorted, ksorted, dq_acc, dk_acc, table, total;
+};
+BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m, int tau);
+
+hipError_t launch_hash(const void *x, bool bf16, int64_t bh, int64_t n, const float *R, int m, int tau,
+                       uint16_t *codes, hipStream_t stream);
+
+hipError_t launch_table(const uint16_t *src_codes, const void *values, const uint16_t *dst_codes, void *out,
+                        bool bf16, int64_t bh, int64_t n_src, int64_t n_dst, int m, int tau, void *workspace,
+                        hipStream_t stream);
+
+hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
+                           const void *v, const void *dy, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m,
+                           int tau, void *dq, void *dk, void *dv, void *workspace, hipStream_t stream);
+
+}  // namespace yoso

@@ -1,0 +1,173 @@
+// C ABI of libyoso: argument validation, workspace sizing and dispatch.
+// Every check runs on the host before the first HIP call.
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "../../include/yoso.h"
+#include "launch.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+yoso_status fail(yoso_status s, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+yoso_status device_status(hipError_t e, const char *what) {
+    if (e == hipSuccess) return YOSO_OK;
+    return fail(YOSO_ERR_DEVICE, "%s: %s (%s)", what, hipGetErrorName(e), hipGetErrorString(e));
+}
+
+constexpr int64_t kMaxN = 65536;
+constexpr int64_t kMaxGrid = 0x7fffffff;
+
+yoso_status check_dtype(yoso_dtype dt) {
+    if (dt != YOSO_F32 && dt != YOSO_BF16) return fail(YOSO_ERR_DTYPE, "unknown dtype %d", (int)dt);
+    return YOSO_OK;
+}
+
+yoso_status check_shape(int64_t bh, int64_t n_q, int64_t n_k, int32_t d, int32_t m) {
+    if (d != 64) return fail(YOSO_ERR_SHAPE, "d = %d; only d = 64 is supported", d);
+    if (bh < 0) return fail(YOSO_ERR_SHAPE, "bh = %lld < 0", (long long)bh);
+    if (n_q < 0 || n_q > kMaxN) return fail(YOSO_ERR_SHAPE, "n_q = %lld outside [0, 65536]", (long long)n_q);
+    if (n_k < 0 || n_k > kMaxN) return fail(YOSO_ERR_SHAPE, "n_k = %lld outside [0, 65536]", (long long)n_k);
+    // grid limits: 2*bh*m sort blocks, bh*64 table blocks, 64-row hash tiles
+    if (m > 0 && bh > kMaxGrid / (2 * (int64_t)m))
+        return fail(YOSO_ERR_SHAPE, "bh = %lld too large for m = %d", (long long)bh, m);
+    if (bh > kMaxGrid / 64) return fail(YOSO_ERR_SHAPE, "bh = %lld too large", (long long)bh);
+    return YOSO_OK;
+}
+
+yoso_status check_hash(int32_t m, int32_t tau) {
+    if (tau < 1 || tau > 12) return fail(YOSO_ERR_HASH, "tau = %d outside [1, 12]", tau);
+    if (m < 1 || m > 64) return fail(YOSO_ERR_HASH, "m = %d outside [1, 64]", m);
+    if (m * tau > 512) return fail(YOSO_ERR_HASH, "m*tau = %d > 512", m * tau);
+    return YOSO_OK;
+}
+
+yoso_status check_ptr(const void *p, int64_t elems, const char *name) {
+    if (elems == 0) return YOSO_OK;
+    if (p == nullptr) return fail(YOSO_ERR_NULL, "%s is NULL", name);
+    if (reinterpret_cast<uintptr_t>(p) & 15u) return fail(YOSO_ERR_ALIGN, "%s is not 16-byte aligned", name);
+    return YOSO_OK;
+}
+
+size_t required_workspace(yoso_op op, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int32_t m, int32_t tau) {
+    switch (op) {
+        case YOSO_OP_HASH: return 0;
+        case YOSO_OP_FORWARD: return yoso::table_workspace_bytes(bf16, bh, n_q, m, tau);
+        case YOSO_OP_BACKWARD: return yoso::backward_layout(bf16, bh, n_q, n_k, m, tau).total;
+    }
+    return 0;
+}
+
+yoso_status check_workspace(const void *ws, size_t have, size_t need) {
+    if (need == 0) return YOSO_OK;
+    if (ws == nullptr) return fail(YOSO_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", need);
+    if (have < need) return fail(YOSO_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
+    if (reinterpret_cast<uintptr_t>(ws) & 15u) return fail(YOSO_ERR_ALIGN, "workspace is not 16-byte aligned");
+    return YOSO_OK;
+}
+
+#define YOSO_TRY(expr)                         \
+    do {                                       \
+        const yoso_status _s = (expr);         \
+        if (_s != YOSO_OK) return _s;          \
+    } while (0)
+
+}  // namespace
+
+extern "C" {
+
+const char *yoso_status_string(yoso_status status) {
+    switch (status) {
+        case YOSO_OK: return "ok";
+        case YOSO_ERR_NULL: return "null pointer";
+        case YOSO_ERR_SHAPE: return "unsupported shape";
+        case YOSO_ERR_HASH: return "tau or m out of range";
+        case YOSO_ERR_DTYPE: return "unknown dtype";
+        case YOSO_ERR_ALIGN: return "misaligned pointer";
+        case YOSO_ERR_WORKSPACE: return "workspace missing or too small";
+        case YOSO_ERR_DEVICE: return "HIP error";
+        case YOSO_ERR_OP: return "unknown op";
+    }
+    return "unknown status";
+}
+
+const char *yoso_last_error(void) { return g_last_error; }
+
+yoso_status yoso_workspace_size(yoso_op op, yoso_dtype dtype, int64_t bh, int64_t n_q, int64_t n_k, int32_t d,
+                                int32_t m, int32_t tau, size_t *bytes) {
+    g_last_error[0] = '\0';
+    if (op != YOSO_OP_HASH && op != YOSO_OP_FORWARD && op != YOSO_OP_BACKWARD)
+        return fail(YOSO_ERR_OP, "unknown op %d", (int)op);
+    YOSO_TRY(check_dtype(dtype));
+    YOSO_TRY(check_shape(bh, n_q, n_k, d, m));
+    YOSO_TRY(check_hash(m, tau));
+    if (bytes == nullptr) return fail(YOSO_ERR_NULL, "bytes is NULL");
+    *bytes = required_workspace(op, dtype == YOSO_BF16, bh, n_q, n_k, m, tau);
+    return YOSO_OK;
+}
+
+yoso_status yoso_hash(const void *x, yoso_dtype dtype, int64_t bh, int64_t n, int32_t d, const float *R,
+                      int32_t m, int32_t tau, uint16_t *codes, void *stream) {
+    g_last_error[0] = '\0';
+    YOSO_TRY(check_dtype(dtype));
+    YOSO_TRY(check_shape(bh, n, 0, d, m));
+    YOSO_TRY(check_hash(m, tau));
+    YOSO_TRY(check_ptr(x, bh * n * d, "x"));
+    YOSO_TRY(check_ptr(R, (int64_t)d * m * tau, "R"));
+    YOSO_TRY(check_ptr(codes, bh * n * m, "codes"));
+    return device_status(yoso::launch_hash(x, dtype == YOSO_BF16, bh, n, R, m, tau, codes,
+                                           static_cast<hipStream_t>(stream)),
+                         "yoso_hash");
+}
+
+yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const void *v, yoso_dtype dtype,
+                         int64_t bh, int64_t n_q, int64_t n_k, int32_t d, int32_t m, int32_t tau, void *y,
+                         void *workspace, size_t workspace_bytes, void *stream) {
+    g_last_error[0] = '\0';
+    YOSO_TRY(check_dtype(dtype));
+    YOSO_TRY(check_shape(bh, n_q, n_k, d, m));
+    YOSO_TRY(check_hash(m, tau));
+    YOSO_TRY(check_ptr(qcodes, bh * m * n_q, "qcodes"));
+    YOSO_TRY(check_ptr(kcodes, bh * m * n_k, "kcodes"));
+    YOSO_TRY(check_ptr(v, bh * n_k * d, "v"));
+    YOSO_TRY(check_ptr(y, bh * n_q * d, "y"));
+    const bool bf16 = dtype == YOSO_BF16;
+    YOSO_TRY(check_workspace(workspace, workspace_bytes, required_workspace(YOSO_OP_FORWARD, bf16, bh, n_q, n_k, m, tau)));
+    return device_status(yoso::launch_table(kcodes, v, qcodes, y, bf16, bh, n_k, n_q, m, tau, workspace,
+                                            static_cast<hipStream_t>(stream)),
+                         "yoso_forward");
+}
+
+yoso_status yoso_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
+                          const void *v, const void *dy, yoso_dtype dtype, int64_t bh, int64_t n_q, int64_t n_k,
+                          int32_t d, int32_t m, int32_t tau, void *dq, void *dk, void *dv, void *workspace,
+                          size_t workspace_bytes, void *stream) {
+    g_last_error[0] = '\0';
+    YOSO_TRY(check_dtype(dtype));
+    YOSO_TRY(check_shape(bh, n_q, n_k, d, m));
+    YOSO_TRY(check_hash(m, tau));
+    YOSO_TRY(check_ptr(qcodes, bh * m * n_q, "qcodes"));
+    YOSO_TRY(check_ptr(kcodes, bh * m * n_k, "kcodes"));
+    YOSO_TRY(check_ptr(q, bh * n_q * d, "q"));
+    YOSO_TRY(check_ptr(k, bh * n_k * d, "k"));
+    YOSO_TRY(check_ptr(v, bh * n_k * d, "v"));
+    YOSO_TRY(check_ptr(dy, bh * n_q * d, "dy"));
+    YOSO_TRY(check_ptr(dq, bh * n_q * d, "dq"));
+    YOSO_TRY(check_ptr(dk, bh * n_k * d, "dk"));
+    YOSO_TRY(check_ptr(dv, bh * n_k * d, "dv"));
+    const bool bf16 = dtype == YOSO_BF16;
+    YOSO_TRY(check_workspace(workspace, workspace_bytes, required_workspace(YOSO_OP_BACKWARD, bf16, bh, n_q, n_k, m, tau)));
+    return device_status(yoso::launch_backward(qcodes, kcodes, q, k, v, dy, bf16, bh, n_q, n_k, m, tau, dq, dk, dv,
+                                               workspace, static_cast<hipStream_t>(stream)),
+                         "yoso_backward");
+}
+
+}  // extern "C"

@@ -1,0 +1,149 @@
+"""Host-side checks of the C ABI: the library loads, exports what include/yoso.h
+declares, and rejects every bad argument before touching the device.
+
+No call here reaches a kernel: each one carries at least one invalid argument, and
+the library validates everything on the host before its first HIP call.  The
+device pointers are fake (never dereferenced)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2111_09714_amd as Y
+from paper_2111_09714_amd import build as ybuild
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x10000  # 16-byte aligned, never dereferenced
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(Y.lib_path()):
+        ybuild.build()
+    return Y.lib()
+
+
+def _declared_symbols():
+    text = open(os.path.join(ROOT, "include", "yoso.h")).read()
+    return sorted(set(re.findall(r"\b(yoso_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = _declared_symbols()
+    assert {"yoso_hash", "yoso_forward", "yoso_backward", "yoso_workspace_size",
+            "yoso_status_string", "yoso_last_error"} <= set(names)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_status_strings(L):
+    for s in range(9):
+        assert L.yoso_status_string(s)
+    assert L.yoso_status_string(0) == b"ok"
+
+
+def _hash(L, x=FAKE, dtype=0, bh=2, n=128, d=64, R=FAKE, m=32, tau=8, codes=FAKE):
+    return L.yoso_hash(x, dtype, bh, n, d, R, m, tau, codes, None)
+
+
+def _fwd(L, qc=FAKE, kc=FAKE, v=FAKE, dtype=0, bh=2, nq=128, nk=128, d=64, m=32, tau=8, y=FAKE,
+         ws=FAKE, wsb=1 << 30):
+    return L.yoso_forward(qc, kc, v, dtype, bh, nq, nk, d, m, tau, y, ws, wsb, None)
+
+
+def _bwd(L, dtype=0, bh=2, nq=128, nk=128, d=64, m=32, tau=8, ws=FAKE, wsb=1 << 30, **ptrs):
+    p = dict(qc=FAKE, kc=FAKE, q=FAKE, k=FAKE, v=FAKE, dy=FAKE, dq=FAKE, dk=FAKE, dv=FAKE)
+    p.update(ptrs)
+    return L.yoso_backward(p["qc"], p["kc"], p["q"], p["k"], p["v"], p["dy"], dtype, bh, nq, nk, d, m, tau,
+                           p["dq"], p["dk"], p["dv"], ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=7), 4),
+    (dict(d=32), 2),
+    (dict(bh=-1), 2),
+    (dict(n=65537), 2),
+    (dict(n=-3), 2),
+    (dict(tau=0), 3),
+    (dict(tau=13), 3),
+    (dict(m=0), 3),
+    (dict(m=65), 3),
+    (dict(m=64, tau=9), 3),   # m*tau = 576 > 512
+    (dict(x=None), 1),
+    (dict(R=None), 1),
+    (dict(codes=None), 1),
+    (dict(x=FAKE + 4), 5),
+    (dict(codes=FAKE + 2), 5),
+])
+def test_hash_rejects(L, kw, status):
+    assert _hash(L, **kw) == status
+    assert L.yoso_last_error()
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=2), 4),
+    (dict(d=128), 2),
+    (dict(nq=70000), 2),
+    (dict(nk=-1), 2),
+    (dict(tau=20), 3),
+    (dict(qc=None), 1),
+    (dict(kc=None), 1),
+    (dict(v=None), 1),
+    (dict(y=None), 1),
+    (dict(v=FAKE + 8), 5),
+])
+def test_forward_rejects(L, kw, status):
+    assert _fwd(L, **kw) == status
+
+
+def test_forward_workspace_checks(L):
+    # tau = 12, m = 64 needs several hash groups, and bf16 output needs an fp32 accumulator
+    need = Y.yoso_workspace_size(Y.OP_FORWARD, Y.BF16, 2, 128, 128, 64, 32, 12)
+    assert need > 0
+    assert _fwd(L, dtype=1, tau=12, ws=None, wsb=0) == 6
+    assert _fwd(L, dtype=1, tau=12, ws=FAKE, wsb=need - 1) == 6
+    assert _fwd(L, dtype=1, tau=12, ws=FAKE + 4, wsb=need) == 5
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=-1), 4),
+    (dict(d=0), 2),
+    (dict(m=100), 3),
+    (dict(q=None), 1),
+    (dict(dy=None), 1),
+    (dict(dk=None), 1),
+    (dict(dv=FAKE + 1), 5),
+    (dict(ws=None), 6),
+    (dict(wsb=16), 6),
+])
+def test_backward_rejects(L, kw, status):
+    assert _bwd(L, **kw) == status
+
+
+def test_empty_tensors_need_no_pointers(L):
+    # zero-sized tensors are valid and their pointers may be NULL; with every size 0
+    # nothing is launched, so these calls return OK even without a GPU.
+    assert _hash(L, bh=0, x=None, codes=None) == 0
+    assert _hash(L, n=0, x=None, codes=None) == 0
+    assert _fwd(L, bh=0, qc=None, kc=None, v=None, y=None, ws=None, wsb=0) == 0
+
+
+def test_workspace_sizes():
+    # backward workspace: bucket offsets + permutations + sorted codes (+ fp32 accumulators for bf16)
+    f32 = Y.yoso_workspace_size(Y.OP_BACKWARD, Y.F32, 32, 4096, 4096, 64, 32, 8)
+    bf = Y.yoso_workspace_size(Y.OP_BACKWARD, Y.BF16, 32, 4096, 4096, 64, 32, 8)
+    units = 32 * 32
+    assert f32 >= units * (2 * 257 * 4 + 4 * 4096 * 2)
+    assert bf >= f32 + 2 * 32 * 4096 * 64 * 4
+    assert Y.yoso_workspace_size(Y.OP_HASH, Y.F32, 32, 4096, 4096, 64, 32, 8) == 0
+    assert Y.yoso_workspace_size(Y.OP_FORWARD, Y.F32, 32, 4096, 4096, 64, 32, 8) == 0
+    with pytest.raises(Y.YosoError):
+        Y.yoso_workspace_size(9, Y.F32, 1, 1, 1, 64, 1, 1)
+
+
+def test_binding_refuses_host_tensors():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros(1, 16, 64)
+    with pytest.raises(ValueError):
+        Y.yoso_hash(x, torch.zeros(64, 16), 2, 8, torch.zeros(1, 2, 16, dtype=torch.int16))
