@@ -1,0 +1,188 @@
+#!/usr/bin/env python3
+"""YOSO attention forward + backward throughput on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+    codes_q = hash(Q), codes_k = hash(K)       (yoso_hash, twice)
+    Y = forward(codes, V)                      (yoso_forward)
+    dQ, dK, dV = backward(codes, Q, K, V, dY)  (yoso_backward)
+for every (batch, head) of the workload (default: 16 x 2 heads, n = 4096, d = 64,
+m = 32 hashes of tau = 8 bits, fp32).  Inputs are resident in HBM before the
+timed region; W warm-up steps are followed by K timed steps bracketed by device
+synchronisation.  One JSON line is printed on stdout.
+
+Per-kernel durations come from HIP events that the library records around each
+of its launches on the launch stream (yoso_timing_enable); the roofline object
+describes the kernel with the largest total time.  The CPU baseline is the fp64
+oracle, timed on this machine's host cores on a stated sample of heads.
+"""
+from __future__ import annotations
+
+import argparse
+import concurrent.futures
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "YOSO attention fwd+bwd tokens/sec at n=4096,d=64,m=32,tau=8; % HBM roofline"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+FP16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense fp16/bf16 matrix peak
+
+
+def kernel_algorithmic(w, kernel: str, launches_per_step: int):
+    """Algorithmic bytes (and flops, if any) one launch of `kernel` must move,
+    as shares of the 11*n*d*e bytes per head of the whole path:
+      hash_kernel   reads one of Q, K                         n*d*e per head
+      table_kernel  forward: reads V, writes Y; dV: reads dY, writes dV   2*n*d*e
+      pairs_kernel  reads Q, K, V, dY, writes dQ, dK          6*n*d*e
+    Per launch = per head x heads (each launch covers every head)."""
+    nde = w.n * w.d * w.elem_bytes
+    per_head = {"hash_kernel": nde, "table_kernel": 2 * nde, "pairs_kernel": 6 * nde}.get(kernel)
+    if per_head is None:
+        return None
+    return per_head * w.bh
+
+
+def cpu_baseline(w, inp, heads):
+    """Time the oracle (hash + forward + backward) on `heads`, one head per thread."""
+    import oracle
+    oracle._load()
+    threads = min(len(os.sched_getaffinity(0)), len(heads))
+
+    def one(h):
+        oracle.run_all(inp, w.m, w.tau, heads=slice(h, h + 1))
+
+    t0 = time.perf_counter()
+    with concurrent.futures.ThreadPoolExecutor(max_workers=threads) as ex:
+        list(ex.map(one, heads))
+    wall = time.perf_counter() - t0
+    step_equiv = wall * w.bh / len(heads)
+    return {
+        "value": w.tokens / step_equiv,
+        "unit": "tokens/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"{len(heads)} of {w.bh} heads of the same workload (hash+forward+backward, fp64 C oracle, "
+                  f"one head per thread); {wall:.2f} s wall, scaled by {w.bh}/{len(heads)}",
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="lra_n4096")
+    ap.add_argument("--cpu-heads", type=int, default=-1, help="heads in the oracle sample (-1: all)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): "
+              "the (batch, head) units of YOSO attention are independent, so N GPUs would each run "
+              "this same kernel sequence on BH/N heads with no communication.", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2111_09714_amd as Y
+    from workloads import WORKLOADS, make_inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    w = WORKLOADS[args.workload]
+    inp = make_inputs(w)
+    tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+    dev = torch.device("cuda:0")
+    q, k, v, dy = (torch.from_numpy(inp[s]).to(dev).to(tdt).contiguous() for s in ("q", "k", "v", "dy"))
+    R = torch.from_numpy(inp["R"]).to(dev)
+    qc = torch.empty((w.bh, w.m, w.n), dtype=torch.int16, device=dev)
+    kc = torch.empty_like(qc)
+    y = torch.empty_like(q)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws_f = Y.workspace(Y.OP_FORWARD, q, w.m, w.tau)
+    ws_b = Y.workspace(Y.OP_BACKWARD, q, w.m, w.tau)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        Y.yoso_hash(q, R, w.m, w.tau, qc, stream)
+        Y.yoso_hash(k, R, w.m, w.tau, kc, stream)
+        Y.yoso_forward(qc, kc, v, w.m, w.tau, y, ws_f, stream)
+        Y.yoso_backward(qc, kc, q, k, v, dy, w.m, w.tau, dq, dk, dv, ws_b, stream)
+
+    Y.yoso_timing_enable(4 * (args.steps + args.warmup) + 8)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    Y.yoso_timing_reset()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        step()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    ms_per_step = ms_total / args.steps
+
+    kernels = {}
+    for name in ("hash_kernel", "table_kernel", "sort_kernel", "pairs_kernel", "zero_kernel",
+                 "to_bf16_kernel", "f32_to_bf16_kernel"):
+        tot, n = Y.yoso_timing_query(name)
+        if n:
+            kernels[name] = {"launches_per_step": n / args.steps, "avg_us": 1000.0 * tot / n,
+                             "share_of_step": tot / ms_total}
+    Y.yoso_timing_enable(0)
+    dominant = max(kernels, key=lambda kname: kernels[kname]["avg_us"] * kernels[kname]["launches_per_step"])
+    alg = kernel_algorithmic(w, dominant, kernels[dominant]["launches_per_step"])
+    avg_s = kernels[dominant]["avg_us"] * 1e-6
+    roofline = None
+    if alg is not None:
+        achieved = alg / avg_s / 1e9
+        roofline = {"kernel": dominant, "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                    "algorithmic_bytes_per_launch": alg, "avg_launch_us": round(kernels[dominant]["avg_us"], 2)}
+
+    tokens_per_s = w.tokens / (ms_per_step * 1e-3)
+    alg_step_bytes = 11 * w.n * w.d * w.elem_bytes * w.bh
+    hbm_frac = alg_step_bytes / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        nh = w.bh if args.cpu_heads < 0 else min(args.cpu_heads, w.bh)
+        cpu = cpu_baseline(w, inp, list(range(nh)))
+
+    out = {
+        "metric": METRIC,
+        "value": round(tokens_per_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if w.dtype == "f32" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "heads": w.heads, "seq_len": w.n, "head_dim": w.d,
+                   "tau": w.tau, "hashes": w.m, "inputs": w.dist},
+        "hbm_roofline_frac": round(hbm_frac, 4),
+        "algorithmic_bytes_per_step": alg_step_bytes,
+        "roofline": roofline,
+        "kernels": {kn: {kk: round(vv, 3) for kk, vv in kv.items()} for kn, kv in kernels.items()},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -123,6 +123,23 @@ const char *yoso_status_string(yoso_status status);
 /* Detail of the last failing call on this thread ("" if none). */
 const char *yoso_last_error(void);
 
+/*
+ * Kernel timing (a benchmarking aid, off by default).
+ * yoso_timing_enable(capacity > 0) makes every later kernel launch of the
+ * library record a pair of HIP events around itself on its launch stream, for
+ * up to `capacity` launches per kernel name (events are created on a kernel's
+ * first launch and live until the next yoso_timing_enable call; 0 disables and
+ * frees them).  yoso_timing_reset() forgets the launches recorded so far.
+ * yoso_timing_query() waits for the recorded events of `kernel` ("hash_kernel",
+ * "table_kernel", "sort_kernel", "pairs_kernel", "zero_kernel", "to_bf16_kernel",
+ * "f32_to_bf16_kernel") and returns the summed duration and the launch count.
+ * Not thread-safe with respect to concurrent launches on other threads' streams
+ * beyond the pool bookkeeping, which is locked.
+ */
+yoso_status yoso_timing_enable(int32_t capacity);
+yoso_status yoso_timing_reset(void);
+yoso_status yoso_timing_query(const char *kernel, double *total_ms, int64_t *launches);
+
 #ifdef __cplusplus
 }
 #endif

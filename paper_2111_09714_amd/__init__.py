@@ -21,6 +21,7 @@ from typing import Optional
 __all__ = [
     "YosoError", "F32", "BF16", "OP_HASH", "OP_FORWARD", "OP_BACKWARD",
     "lib", "lib_path", "yoso_workspace_size", "yoso_hash", "yoso_forward", "yoso_backward",
+    "yoso_timing_enable", "yoso_timing_reset", "yoso_timing_query",
     "workspace", "hash_qk", "forward", "backward",
 ]
 
@@ -62,6 +63,11 @@ def lib() -> ctypes.CDLL:
         L.yoso_status_string.restype = ctypes.c_char_p
         L.yoso_last_error.argtypes = []
         L.yoso_last_error.restype = ctypes.c_char_p
+        L.yoso_timing_enable.argtypes = [I32]
+        L.yoso_timing_reset.argtypes = []
+        L.yoso_timing_query.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(I64)]
+        for fn in ("yoso_timing_enable", "yoso_timing_reset", "yoso_timing_query"):
+            getattr(L, fn).restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -139,6 +145,21 @@ def yoso_backward(qcodes, kcodes, q, k, v, dy, m: int, tau: int, dq, dk, dv, ws,
     _check(lib().yoso_backward(_ptr(qcodes), _ptr(kcodes), _ptr(q), _ptr(k), _ptr(v), _ptr(dy), _dtype_code(q),
                                bh, n_q, n_k, d, m, tau, _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws), nbytes,
                                _stream(stream)))
+
+
+def yoso_timing_enable(capacity: int) -> None:
+    _check(lib().yoso_timing_enable(capacity))
+
+
+def yoso_timing_reset() -> None:
+    _check(lib().yoso_timing_reset())
+
+
+def yoso_timing_query(kernel: str):
+    """(total_ms, launches) recorded for `kernel` since the last reset (synchronises)."""
+    ms, n = ctypes.c_double(0.0), ctypes.c_int64(0)
+    _check(lib().yoso_timing_query(kernel.encode(), ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
 
 
 # ------------------------------------------------------------------ allocating conveniences

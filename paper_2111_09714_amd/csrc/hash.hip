@@ -20,6 +20,7 @@
 // of one hash, i.e. 128 contiguous bytes).
 #include "common.h"
 #include "launch.h"
+#include "timing.h"
 
 namespace yoso {
 
@@ -150,6 +151,7 @@ hipError_t launch_hash(const void *x, bool bf16, int64_t bh, int64_t n, const fl
     const int64_t tiles = (rows + kHashRowsPerTile - 1) / kHashRowsPerTile;
     const int64_t grid = tiles < 1024 ? tiles : 1024;
     const size_t lds = hash_lds_bytes(m, tau);
+    KernelTimer timer("hash_kernel", stream);
     if (bf16) {
         hipLaunchKernelGGL(hash_kernel<true>, dim3((unsigned)grid), dim3(256), lds, stream, x, rows, n, R, m,
                            tau, codes, tiles);

@@ -28,6 +28,7 @@
 // scaled by 2^8 before splitting (undone on the way out).
 #include "common.h"
 #include "launch.h"
+#include "timing.h"
 
 namespace yoso {
 
@@ -306,18 +307,24 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
     float *dq32 = bf16 ? reinterpret_cast<float *>(ws + L.dq_acc) : static_cast<float *>(dq);
     float *dk32 = bf16 ? reinterpret_cast<float *>(ws + L.dk_acc) : static_cast<float *>(dk);
     const int64_t nq_el = bh * n_q * D, nk_el = bh * n_k * D;
-    if (nq_el) hipLaunchKernelGGL(zero_kernel, dim3(elementwise_grid(nq_el)), dim3(256), 0, stream, dq32, nq_el);
-    if (nk_el) hipLaunchKernelGGL(zero_kernel, dim3(elementwise_grid(nk_el)), dim3(256), 0, stream, dk32, nk_el);
+    {
+        KernelTimer timer("zero_kernel", stream);
+        if (nq_el) hipLaunchKernelGGL(zero_kernel, dim3(elementwise_grid(nq_el)), dim3(256), 0, stream, dq32, nq_el);
+        if (nk_el) hipLaunchKernelGGL(zero_kernel, dim3(elementwise_grid(nk_el)), dim3(256), 0, stream, dk32, nk_el);
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     const int64_t units = bh * m;
     if (units > 0 && n_q > 0 && n_k > 0) {
         const size_t sort_lds = ((size_t)(1 << tau) + kSortThreads) * 4;
+        {
+        KernelTimer timer("sort_kernel", stream);
         hipLaunchKernelGGL(sort_kernel, dim3((unsigned)(2 * units)), dim3(kSortThreads), sort_lds, stream, qcodes,
                            kcodes, units, n_q, n_k, tau, reinterpret_cast<int32_t *>(ws + L.qoff),
                            reinterpret_cast<int32_t *>(ws + L.koff), reinterpret_cast<uint16_t *>(ws + L.qperm),
                            reinterpret_cast<uint16_t *>(ws + L.kperm), reinterpret_cast<uint16_t *>(ws + L.qsorted),
                            reinterpret_cast<uint16_t *>(ws + L.ksorted));
+        }
         if ((e = hipGetLastError()) != hipSuccess) return e;
 
         PairArgs a;
@@ -331,6 +338,7 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
         a.dq = dq32; a.dk = dk32;
         a.bh = bh; a.n_q = n_q; a.n_k = n_k; a.m = m; a.tau = tau;
         a.scale = (float)tau / (2.0f * (float)m);
+        KernelTimer timer("pairs_kernel", stream);
         if (bf16)
             hipLaunchKernelGGL(pairs_kernel<true>, dim3((unsigned)units), dim3(kPairThreads), 0, stream, a);
         else
@@ -338,6 +346,7 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (bf16) {
+        KernelTimer timer("to_bf16_kernel", stream);
         if (nq_el)
             hipLaunchKernelGGL(to_bf16_kernel, dim3(elementwise_grid(nq_el)), dim3(256), 0, stream, dq32,
                                static_cast<uint16_t *>(dq), nq_el);

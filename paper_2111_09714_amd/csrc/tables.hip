@@ -26,6 +26,7 @@
 // same value rows meet in one L2.
 #include "common.h"
 #include "launch.h"
+#include "timing.h"
 
 namespace yoso {
 
@@ -214,6 +215,7 @@ template <bool BF16>
 hipError_t launch_table_ds(int ds, const TableArgs &a, size_t lds, hipStream_t stream) {
     const int64_t blocks = a.bh * (D / ds);
     const dim3 grid((unsigned)blocks), block(kTableThreads);
+    KernelTimer timer("table_kernel", stream);
     switch (ds) {
 #define YOSO_CASE(X)                                                                      \
     case X:                                                                               \
@@ -275,6 +277,7 @@ hipError_t launch_table(const uint16_t *src_codes, const void *values, const uin
     if (p.groups > 1 && bf16) {
         const int64_t count = bh * n_dst * D;
         const int64_t blocks = (count + 255) / 256 < 4096 ? (count + 255) / 256 : 4096;
+        KernelTimer timer("f32_to_bf16_kernel", stream);
         hipLaunchKernelGGL(f32_to_bf16_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, a.acc,
                            static_cast<uint16_t *>(out), count);
         e = hipGetLastError();
