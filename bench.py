@@ -33,15 +33,17 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense fp16/bf16 matrix peak
 
 
-def kernel_algorithmic(w, kernel: str, launches_per_step: int):
-    """Algorithmic bytes (and flops, if any) one launch of `kernel` must move,
-    as shares of the 11*n*d*e bytes per head of the whole path:
-      hash_kernel   reads one of Q, K                         n*d*e per head
-      table_kernel  forward: reads V, writes Y; dV: reads dY, writes dV   2*n*d*e
-      pairs_kernel  reads Q, K, V, dY, writes dQ, dK          6*n*d*e
-    Per launch = per head x heads (each launch covers every head)."""
+def kernel_algorithmic(w, kernel: str):
+    """Algorithmic bytes one launch of `kernel` must move (each launch covers every head):
+      hash_kernel    reads one of Q, K                                  n*d*e per head
+      table_kernel   forward: reads V, writes Y; dV: reads dY, writes dV  2*n*d*e
+      pass_kernel    reads Q, K, V, dY (both the dQ and the dK pass)      4*n*d*e
+      reduce_kernel  writes one of dQ, dK                               n*d*e
+    Everything else these kernels move (codes, per-hash partial rows, re-reads of
+    rows for every hash) is implementation traffic and is not credited."""
     nde = w.n * w.d * w.elem_bytes
-    per_head = {"hash_kernel": nde, "table_kernel": 2 * nde, "pairs_kernel": 6 * nde}.get(kernel)
+    per_head = {"hash_kernel": nde, "table_kernel": 2 * nde, "pass_kernel": 4 * nde,
+                "reduce_kernel": nde}.get(kernel)
     if per_head is None:
         return None
     return per_head * w.bh
@@ -103,7 +105,7 @@ def main() -> int:
     dev = torch.device("cuda:0")
     q, k, v, dy = (torch.from_numpy(inp[s]).to(dev).to(tdt).contiguous() for s in ("q", "k", "v", "dy"))
     R = torch.from_numpy(inp["R"]).to(dev)
-    qc = torch.empty((w.bh, w.m, w.n), dtype=torch.int16, device=dev)
+    qc = torch.empty((w.bh, w.n, w.m), dtype=torch.int16, device=dev)
     kc = torch.empty_like(qc)
     y = torch.empty_like(q)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
@@ -133,15 +135,14 @@ def main() -> int:
     ms_per_step = ms_total / args.steps
 
     kernels = {}
-    for name in ("hash_kernel", "table_kernel", "sort_kernel", "pairs_kernel", "zero_kernel",
-                 "to_bf16_kernel", "f32_to_bf16_kernel"):
+    for name in ("hash_kernel", "table_kernel", "sort_kernel", "pass_kernel", "reduce_kernel", "zero_kernel"):
         tot, n = Y.yoso_timing_query(name)
         if n:
             kernels[name] = {"launches_per_step": n / args.steps, "avg_us": 1000.0 * tot / n,
                              "share_of_step": tot / ms_total}
     Y.yoso_timing_enable(0)
     dominant = max(kernels, key=lambda kname: kernels[kname]["avg_us"] * kernels[kname]["launches_per_step"])
-    alg = kernel_algorithmic(w, dominant, kernels[dominant]["launches_per_step"])
+    alg = kernel_algorithmic(w, dominant)
     avg_s = kernels[dominant]["avg_us"] * 1e-6
     roofline = None
     if alg is not None:

@@ -14,9 +14,11 @@
  *
  * Conventions shared by every call:
  *   - Every tensor pointer is a DEVICE pointer owned by the caller; the library
- *     allocates nothing and keeps no state between calls.
+ *     allocates nothing and keeps no state between calls (beyond the opt-in
+ *     timing pool below).
  *   - Tensors are dense row-major: x[bh][i][l] with bh = batch*heads flattened,
- *     i the row (token) and l < d the feature; codes[bh][h][i].
+ *     i the row (token) and l < d the feature.  Hash codes are codes[bh][i][h]:
+ *     the m codes of a row are contiguous.
  *   - All device pointers must be 16-byte aligned.
  *   - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
  *     default stream).  Outputs are overwritten, never accumulated into.
@@ -27,7 +29,15 @@
  *     0 <= n <= 65536 per tensor; bh >= 0.  Zero-sized tensors are valid.
  *   - Inputs must be finite.  The hash stages rows through fp16 pairs after a
  *     2^8 scaling, so |x| must stay below 255 (unit rows always do) and |R| below
- *     65504; V and dY must stay below 32768 in magnitude.
+ *     65504; V and dY entries and their dot products times tau/(2m) must stay
+ *     below 65504 in magnitude.
+ *   - Precision.  Y and dV are accumulated as exact fixed-point integers: each
+ *     value of a 2-16 wide feature slice is rounded to a multiple of 2^-k, where
+ *     2^k is the largest power of two keeping n_src * max|slice value| * 2^k
+ *     below 2^30; everything after that rounding is exact, so Y and dV are
+ *     bitwise reproducible.  dQ and dK use fp32 accumulation of products formed
+ *     from fp16 (hi, lo) pairs (about 22 significant bits) and are reproducible
+ *     too: every partial is written once and summed in hash order.
  */
 #ifndef YOSO_H
 #define YOSO_H
@@ -42,7 +52,7 @@ extern "C" {
 typedef enum {
     YOSO_OK = 0,
     YOSO_ERR_NULL = 1,      /* a required pointer is NULL (and its tensor is not empty) */
-    YOSO_ERR_SHAPE = 2,     /* bh < 0, n out of [0, 65536], or d != 64 */
+    YOSO_ERR_SHAPE = 2,     /* bh < 0, n out of [0, 65536], d != 64, or bh*n too large */
     YOSO_ERR_HASH = 3,      /* tau, m or m*tau out of range */
     YOSO_ERR_DTYPE = 4,     /* unknown yoso_dtype */
     YOSO_ERR_ALIGN = 5,     /* a device pointer is not 16-byte aligned */
@@ -52,8 +62,8 @@ typedef enum {
 } yoso_status;
 
 /* Storage type of Q, K, V, dY and of the outputs Y, dQ, dK, dV.  Arithmetic is
- * fp32 either way (fp32 tables and accumulators); bf16 outputs are rounded to
- * nearest even once at the end. */
+ * fp32 (or exact integer) either way; bf16 outputs are rounded to nearest even
+ * once at the end. */
 typedef enum { YOSO_F32 = 0, YOSO_BF16 = 1 } yoso_dtype;
 
 typedef enum { YOSO_OP_HASH = 0, YOSO_OP_FORWARD = 1, YOSO_OP_BACKWARD = 2 } yoso_op;
@@ -62,12 +72,12 @@ typedef enum { YOSO_OP_HASH = 0, YOSO_OP_FORWARD = 1, YOSO_OP_BACKWARD = 2 } yos
  * Sign-random-projection hash (Sec. 3.2 overview; Fig. 2 caption: tau
  * concatenated hyperplane hashes, collision probability (1 - theta/pi)^tau).
  *
- *   codes[b][h][i] = sum_{t<tau} [ x[b][i] . R[:, h*tau + t] > 0 ] << t
+ *   codes[b][i][h] = sum_{t<tau} [ x[b][i] . R[:, h*tau + t] > 0 ] << t
  *
  * x      [bh][n][d]  rows to hash (fp32 or bf16 per dtype); Q and K are hashed
  *                    with the same R so that B_ij = [codes_q == codes_k].
  * R      [d][m*tau]  fp32 hyperplanes, column h*tau+t = hyperplane t of hash h.
- * codes  [bh][m][n]  uint16 output, low tau bits used (consumers read only the
+ * codes  [bh][n][m]  uint16 output, low tau bits used (consumers read only the
  *                    low tau bits of the codes they are given).
  * The sign test is strict (a zero projection gives bit 0).  Bits whose
  * projection lies within about 1e-6 of zero may differ from an exact-arithmetic
@@ -81,13 +91,13 @@ yoso_status yoso_hash(const void *x, yoso_dtype dtype, int64_t bh, int64_t n, in
  * of V over the keys hashed to each bucket; each query reads the bucket of its
  * own code; Sec. 3.1: the m samples are averaged).
  *
- *   y[b][i] = (1/m) sum_h sum_{j : kcodes[b][h][j] == qcodes[b][h][i]} v[b][j]
+ *   y[b][i] = (1/m) sum_h sum_{j : kcodes[b][j][h] == qcodes[b][i][h]} v[b][j]
  *
- * qcodes [bh][m][n_q], kcodes [bh][m][n_k]  from yoso_hash with the same R.
+ * qcodes [bh][n_q][m], kcodes [bh][n_k][m]  from yoso_hash with the same R.
  * v      [bh][n_k][d],  y [bh][n_q][d]  (dtype).  Queries whose buckets are empty
  * get 0 (no renormalisation).
- * workspace: yoso_workspace_size(YOSO_OP_FORWARD, ...) bytes (may be 0, then
- * workspace may be NULL).
+ * workspace: yoso_workspace_size(YOSO_OP_FORWARD, ...) bytes (0 for every shape
+ * whose tables fit in one LDS pass; then workspace may be NULL).
  */
 yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const void *v,
                          yoso_dtype dtype, int64_t bh, int64_t n_q, int64_t n_k, int32_t d,
@@ -99,12 +109,13 @@ yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const v
  *   dv = (1/m) sum_h B_h^T dy                          eq. (gradient-v), sampled form
  *   dq = tau/(2m) sum_h [(dy v^T) .* B_h] k           eq. (pseudo-gradient-q), sampled
  *   dk = tau/(2m) sum_h [(dy v^T) .* B_h]^T q         symmetric counterpart for K
- * with B_h(i,j) = [qcodes[b][h][i] == kcodes[b][h][j]].  dq, dk use the paper's
+ * with B_h(i,j) = [qcodes[b][i][h] == kcodes[b][j][h]].  dq, dk use the paper's
  * lower-bound surrogate (tau/2) p of the collision-probability derivative.
  *
  * q, dy, dq [bh][n_q][d];  k, v, dk, dv [bh][n_k][d]  (dtype).
- * workspace: yoso_workspace_size(YOSO_OP_BACKWARD, ...) bytes; the call uses
- * it as scratch (bucket offsets, row permutations, fp32 accumulators).
+ * workspace: yoso_workspace_size(YOSO_OP_BACKWARD, ...) bytes of scratch: the
+ * per-hash bucket orders and one fp32 partial row per (row, hash) for dq and dk,
+ * about 4*m*d*(n_q + n_k)*bh bytes.
  */
 yoso_status yoso_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q,
                           const void *k, const void *v, const void *dy, yoso_dtype dtype,
@@ -131,8 +142,8 @@ const char *yoso_last_error(void);
  * first launch and live until the next yoso_timing_enable call; 0 disables and
  * frees them).  yoso_timing_reset() forgets the launches recorded so far.
  * yoso_timing_query() waits for the recorded events of `kernel` ("hash_kernel",
- * "table_kernel", "sort_kernel", "pairs_kernel", "zero_kernel", "to_bf16_kernel",
- * "f32_to_bf16_kernel") and returns the summed duration and the launch count.
+ * "table_kernel", "sort_kernel", "pass_kernel", "reduce_kernel", "zero_kernel")
+ * and returns the summed duration and the launch count.
  * Not thread-safe with respect to concurrent launches on other threads' streams
  * beyond the pool bookkeeping, which is locked.
  */

@@ -5,7 +5,7 @@ HIP kernels behind the C ABI declared in include/yoso.h.  There is no fallback:
 if the library is missing or a call fails, an exception is raised.
 
 Function names follow the C ABI:
-    yoso_hash(x, R, m, tau, codes)                     codes[bh, m, n] (int16/uint16 storage)
+    yoso_hash(x, R, m, tau, codes)                     codes[bh, n, m] (int16/uint16 storage)
     yoso_forward(qcodes, kcodes, v, m, tau, y, ws)     y = (1/m) sum_h B_h v
     yoso_backward(qcodes, kcodes, q, k, v, dy, m, tau, dq, dk, dv, ws)
     yoso_workspace_size(op, dtype, bh, n_q, n_k, d, m, tau) -> bytes
@@ -111,6 +111,12 @@ def _codes_ok(c) -> None:
         raise TypeError("codes must be int16 or uint16 tensors (16-bit storage)")
 
 
+def _expect(t, shape, name: str) -> None:
+    """The C ABI cannot see buffer sizes, so shapes are checked here before any launch."""
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
 def yoso_workspace_size(op: int, dtype: int, bh: int, n_q: int, n_k: int, d: int, m: int, tau: int) -> int:
     out = ctypes.c_size_t(0)
     _check(lib().yoso_workspace_size(op, dtype, bh, n_q, n_k, d, m, tau, ctypes.byref(out)))
@@ -118,18 +124,23 @@ def yoso_workspace_size(op: int, dtype: int, bh: int, n_q: int, n_k: int, d: int
 
 
 def yoso_hash(x, R, m: int, tau: int, codes, stream=None) -> None:
-    """codes[b, h, i] = sum_t [x[b, i] . R[:, h*tau + t] > 0] << t."""
+    """codes[b, i, h] = sum_t [x[b, i] . R[:, h*tau + t] > 0] << t."""
     _codes_ok(codes)
     bh, n, d = x.shape
+    _expect(R, (d, m * tau), "R")
+    _expect(codes, (bh, n, m), "codes")
     _check(lib().yoso_hash(_ptr(x), _dtype_code(x), bh, n, d, _ptr(R), m, tau, _ptr(codes), _stream(stream)))
 
 
 def yoso_forward(qcodes, kcodes, v, m: int, tau: int, y, ws=None, stream=None) -> None:
-    """y = (1/m) sum_h B_h v with B_h(i, j) = [qcodes[:, h, i] == kcodes[:, h, j]]."""
+    """y = (1/m) sum_h B_h v with B_h(i, j) = [qcodes[:, i, h] == kcodes[:, j, h]]."""
     _codes_ok(qcodes)
     _codes_ok(kcodes)
     bh, n_k, d = v.shape
     n_q = y.shape[1]
+    _expect(y, (bh, n_q, d), "y")
+    _expect(qcodes, (bh, n_q, m), "qcodes")
+    _expect(kcodes, (bh, n_k, m), "kcodes")
     nbytes = ws.numel() * ws.element_size() if ws is not None else 0
     _check(lib().yoso_forward(_ptr(qcodes), _ptr(kcodes), _ptr(v), _dtype_code(v), bh, n_q, n_k, d, m, tau,
                               _ptr(y), _ptr(ws), nbytes, _stream(stream)))
@@ -141,6 +152,10 @@ def yoso_backward(qcodes, kcodes, q, k, v, dy, m: int, tau: int, dq, dk, dv, ws,
     _codes_ok(kcodes)
     bh, n_q, d = q.shape
     n_k = k.shape[1]
+    for t, shape, name in ((k, (bh, n_k, d), "k"), (v, (bh, n_k, d), "v"), (dy, (bh, n_q, d), "dy"),
+                           (dq, (bh, n_q, d), "dq"), (dk, (bh, n_k, d), "dk"), (dv, (bh, n_k, d), "dv"),
+                           (qcodes, (bh, n_q, m), "qcodes"), (kcodes, (bh, n_k, m), "kcodes")):
+        _expect(t, shape, name)
     nbytes = ws.numel() * ws.element_size() if ws is not None else 0
     _check(lib().yoso_backward(_ptr(qcodes), _ptr(kcodes), _ptr(q), _ptr(k), _ptr(v), _ptr(dy), _dtype_code(q),
                                bh, n_q, n_k, d, m, tau, _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws), nbytes,
@@ -176,8 +191,8 @@ def workspace(op: int, x, m: int, tau: int, n_k: Optional[int] = None):
 def hash_qk(q, k, R, m: int, tau: int):
     """Codes of Q and K under the same hyperplanes (fresh int16 tensors)."""
     import torch
-    qc = torch.empty((q.shape[0], m, q.shape[1]), dtype=torch.int16, device=q.device)
-    kc = torch.empty((k.shape[0], m, k.shape[1]), dtype=torch.int16, device=k.device)
+    qc = torch.empty((q.shape[0], q.shape[1], m), dtype=torch.int16, device=q.device)
+    kc = torch.empty((k.shape[0], k.shape[1], m), dtype=torch.int16, device=k.device)
     yoso_hash(q, R, m, tau, qc)
     yoso_hash(k, R, m, tau, kc)
     return qc, kc
@@ -185,7 +200,7 @@ def hash_qk(q, k, R, m: int, tau: int):
 
 def forward(qcodes, kcodes, v, m: int, tau: int, n_q: Optional[int] = None):
     import torch
-    n_q = qcodes.shape[2] if n_q is None else n_q
+    n_q = qcodes.shape[1] if n_q is None else n_q
     y = torch.empty((v.shape[0], n_q, v.shape[2]), dtype=v.dtype, device=v.device)
     ws = workspace(OP_FORWARD, y, m, tau, n_k=v.shape[1])
     yoso_forward(qcodes, kcodes, v, m, tau, y, ws)

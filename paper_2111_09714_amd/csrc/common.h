@@ -94,6 +94,50 @@ __device__ __forceinline__ floatx4 mfma3_16x16x16(const half4 &ah, const half4 &
     return acc;
 }
 
+// ---- cross-lane sums without LDS traffic (DPP and the gfx950 permlane swaps)
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Butterfly sum over aligned groups of W lanes (W a power of two, 1 <= W <= 64):
+// every lane of a group ends with the group's total.  Must run with all lanes
+// of each group active.  Steps: xor 1 and xor 2 (quad_perm), the other quad of
+// a half-row (row_half_mirror), the other half-row (row_mirror), the other row
+// of a row pair (permlane16_swap), the other half of the wave (permlane32_swap).
+__device__ __forceinline__ float group_sum(float x, int W) {
+    if (W >= 2) x += dpp_mov<0xB1>(x);   // quad_perm [1,0,3,2]
+    if (W >= 4) x += dpp_mov<0x4E>(x);   // quad_perm [2,3,0,1]
+    if (W >= 8) x += dpp_mov<0x141>(x);  // row_half_mirror
+    if (W >= 16) x += dpp_mov<0x140>(x); // row_mirror
+    if (W >= 32) {
+        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    }
+    if (W >= 64) {
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+    }
+    return x;
+}
+
+// Maximum over the whole wave (every lane gets it).
+__device__ __forceinline__ float wave_max(float x) {
+    x = fmaxf(x, dpp_mov<0xB1>(x));
+    x = fmaxf(x, dpp_mov<0x4E>(x));
+    x = fmaxf(x, dpp_mov<0x141>(x));
+    x = fmaxf(x, dpp_mov<0x140>(x));
+    {
+        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    }
+    {
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+        x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    }
+    return x;
+}
+
 // Workgroups are dispatched to the 8 XCDs round-robin (id % 8).  Remap so that
 // consecutive logical ids land on the same XCD and share its L2; the mapping is
 // a bijection on [0, n) for any n.

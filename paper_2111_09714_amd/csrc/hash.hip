@@ -16,8 +16,8 @@
 // and all ceil(m*tau/16) column tiles.  R is converted once per workgroup into
 // fp16 MFMA B-fragments in LDS.  Signs are gathered with wave ballots into a
 // per-row bit vector in LDS, from which each hash's tau-bit field is cut and
-// stored as uint16 in the [bh][m][n] layout (a wave stores 64 consecutive rows
-// of one hash, i.e. 128 contiguous bytes).
+// stored as uint16 in the [bh][n][m] layout (the m codes of a row are
+// contiguous).
 #include "common.h"
 #include "launch.h"
 #include "timing.h"
@@ -30,7 +30,7 @@ constexpr int kHashRowsPerTile = 64;
 constexpr int kHashGroup = 8;  // column tiles accumulated at once (8 x floatx4)
 
 template <bool BF16>
-__global__ __launch_bounds__(256) void hash_kernel(const void *__restrict__ x, int64_t rows, int64_t n,
+__global__ __launch_bounds__(256) void hash_kernel(const void *__restrict__ x, int64_t rows,
                                                    const float *__restrict__ R, int m, int tau,
                                                    uint16_t *__restrict__ codes, int64_t num_tiles) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -118,17 +118,17 @@ __global__ __launch_bounds__(256) void hash_kernel(const void *__restrict__ x, i
         }
         __syncthreads();
 
-        // Cut the tau-bit field of every (row, hash) out of the row's bit vector.
+        // Cut the tau-bit field of every (row, hash) out of the row's bit vector;
+        // consecutive threads write consecutive hashes of a row.
         const uint32_t mask = (1u << tau) - 1u;
         for (int p = tid; p < kHashRowsPerTile * m; p += 256) {
-            const int r = p & 63, h = p >> 6;
+            const int r = p / m, h = p - r * m;
             const int64_t grow = tile * kHashRowsPerTile + r;
             if (grow < rows) {
                 const int o = h * tau, w = o >> 5, s = o & 31;
                 uint32_t v = bits[r * NWP + w] >> s;
                 if (s + tau > 32) v |= bits[r * NWP + w + 1] << (32 - s);
-                const int64_t b = grow / n, i = grow - b * n;
-                codes[(b * m + h) * n + i] = static_cast<uint16_t>(v & mask);
+                codes[grow * m + h] = static_cast<uint16_t>(v & mask);
             }
         }
         __syncthreads();
@@ -153,11 +153,11 @@ hipError_t launch_hash(const void *x, bool bf16, int64_t bh, int64_t n, const fl
     const size_t lds = hash_lds_bytes(m, tau);
     KernelTimer timer("hash_kernel", stream);
     if (bf16) {
-        hipLaunchKernelGGL(hash_kernel<true>, dim3((unsigned)grid), dim3(256), lds, stream, x, rows, n, R, m,
-                           tau, codes, tiles);
+        hipLaunchKernelGGL(hash_kernel<true>, dim3((unsigned)grid), dim3(256), lds, stream, x, rows, R, m, tau,
+                           codes, tiles);
     } else {
-        hipLaunchKernelGGL(hash_kernel<false>, dim3((unsigned)grid), dim3(256), lds, stream, x, rows, n, R, m,
-                           tau, codes, tiles);
+        hipLaunchKernelGGL(hash_kernel<false>, dim3((unsigned)grid), dim3(256), lds, stream, x, rows, R, m, tau,
+                           codes, tiles);
     }
     return hipGetLastError();
 }

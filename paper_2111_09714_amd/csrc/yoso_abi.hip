@@ -36,10 +36,13 @@ yoso_status check_shape(int64_t bh, int64_t n_q, int64_t n_k, int32_t d, int32_t
     if (bh < 0) return fail(YOSO_ERR_SHAPE, "bh = %lld < 0", (long long)bh);
     if (n_q < 0 || n_q > kMaxN) return fail(YOSO_ERR_SHAPE, "n_q = %lld outside [0, 65536]", (long long)n_q);
     if (n_k < 0 || n_k > kMaxN) return fail(YOSO_ERR_SHAPE, "n_k = %lld outside [0, 65536]", (long long)n_k);
-    // grid limits: 2*bh*m sort blocks, bh*64 table blocks, 64-row hash tiles
+    // grid limits: 2*bh*m sort and pair blocks, bh*32 table blocks, bh*n/16 reduce blocks
     if (m > 0 && bh > kMaxGrid / (2 * (int64_t)m))
         return fail(YOSO_ERR_SHAPE, "bh = %lld too large for m = %d", (long long)bh, m);
     if (bh > kMaxGrid / 64) return fail(YOSO_ERR_SHAPE, "bh = %lld too large", (long long)bh);
+    const int64_t nmax = n_q > n_k ? n_q : n_k;
+    if (nmax > 0 && bh > kMaxGrid * 16 / nmax)
+        return fail(YOSO_ERR_SHAPE, "bh*n = %lld*%lld too large", (long long)bh, (long long)nmax);
     return YOSO_OK;
 }
 

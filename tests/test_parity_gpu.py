@@ -43,7 +43,8 @@ def to_dev(a, dtype):
 
 
 def codes_np(t):
-    return t.cpu().numpy().view(np.uint16)
+    """GPU codes [bh, n, m] as the oracle's [bh, m, n] layout."""
+    return np.ascontiguousarray(t.cpu().numpy().view(np.uint16).transpose(0, 2, 1))
 
 
 def rel_err(gpu, ref):
@@ -154,8 +155,8 @@ def test_golden_worked_example(golden):
     m, tau = g["m"], g["tau"]
     pad = lambda a: np.pad(np.array(a, np.float32), ((0, 0), (0, 62)))[None]
     q, k, v, dy = (to_dev(pad(g[s]), "f32") for s in ("q", "k", "v", "dy"))
-    qc = torch.from_numpy(np.array(g["qc"], np.int16)[None]).cuda()
-    kc = torch.from_numpy(np.array(g["kc"], np.int16)[None]).cuda()
+    qc = torch.from_numpy(np.ascontiguousarray(np.array(g["qc"], np.int16).T)[None]).cuda()
+    kc = torch.from_numpy(np.ascontiguousarray(np.array(g["kc"], np.int16).T)[None]).cuda()
     y = Y.forward(qc, kc, v, m, tau, n_q=2)
     dq, dk, dv = Y.backward(qc, kc, q, k, v, dy, m, tau)
     torch.cuda.synchronize()
@@ -170,7 +171,7 @@ def test_golden_hash_example(golden):
     m, tau = g["m"], g["tau"]
     x = np.pad(np.array(g["x"], np.float32), ((0, 0), (0, 61)))[None]
     R = np.pad(np.array(g["R"], np.float32), ((0, 61), (0, 0)))
-    codes = torch.empty((1, m, x.shape[1]), dtype=torch.int16, device="cuda")
+    codes = torch.empty((1, x.shape[1], m), dtype=torch.int16, device="cuda")
     Y.yoso_hash(to_dev(x, "f32"), torch.from_numpy(R).cuda(), m, tau, codes)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(codes_np(codes)[0], np.array(g["codes"]))
