@@ -12,20 +12,23 @@
 //   dQ_i = s sum_h sum_{j in bucket_h(i)} (dy_i . v_j) k_j
 //   dK_j = s sum_h sum_{i in bucket_h(j)} (v_j . dy_i) q_i        (s = tau/(2m))
 // so one "pass" routine serves both: rows x with row vectors a_x, partners y in
-// the same bucket with vectors a'_y and b_y, out_x = s sum (a_x . a'_y) b_y.
+// the same bucket with vectors a'_y and b_y, out_x = s sum_y (a_x . a'_y) b_y.
 //
 // Kernels:
 //   sort_kernel    one workgroup per (head, hash, side): histogram of the codes,
-//                  exclusive scan -> bucket offsets, then row ids and codes in
-//                  bucket order (a counting sort in LDS).
+//                  exclusive scan -> bucket offsets, then the rows in bucket order
+//                  as packed entries (code << 16 | row) (a counting sort in LDS).
 //   pass_kernel    one workgroup per (head, hash, side).  Each wave walks 16-row
 //                  tiles of sorted rows; the partners that can collide with a tile
 //                  form one contiguous range of sorted partners, visited 16 at a
 //                  time:  S^T = A'_y A_x^T (16x16x32 MFMA), masked by code equality,
-//                  out^T += B_y^T S^T (16x16x16 MFMA).  The finished tile is the
-//                  hash's share of out for those rows; it is stored, not added,
-//                  into a partial buffer [bh][n][m][64] (each row of each hash is
-//                  written exactly once, so no atomics are needed).
+//                  out^T += B_y^T S^T (16x16x16 MFMA).  The partner rows of the next
+//                  sub-tile are fetched while the current one computes; B_y is
+//                  transposed through a per-wave LDS tile.  The finished tile is the
+//                  hash's share of out for those rows; it is stored, not added, into a
+//                  partial buffer [bh][n][m][64] (each row of each hash is written
+//                  exactly once, so no atomics are needed).  Partials are fp32, or
+//                  bf16 when the outputs are bf16.
 //   reduce_kernel  out[b][x] = sum over the m hashes of the partial rows, in hash
 //                  order (deterministic), written as fp32 or bf16.
 // gfx950's global fp32 atomics sustain roughly 1.3 TB/s of payload, so a plain
@@ -42,7 +45,10 @@ namespace {
 
 constexpr int kSortThreads = 256;
 constexpr int kPassThreads = 256;
+constexpr int kPassWaves = kPassThreads / 64;
 constexpr int kReduceThreads = 256;
+constexpr int kTileStride = 68;        // floats per row of the per-wave transpose tile (bank-conflict padding)
+constexpr size_t kPassStageBudget = 24 * 1024;  // LDS bytes for staged partner entries + offsets
 
 // ---------------------------------------------------------------- counting sort
 // codes are [bh][n][m]; unit = b*m + h reads column h with stride m.
@@ -50,10 +56,8 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
                                                             const uint16_t *__restrict__ kcodes, int m,
                                                             int64_t n_q, int64_t n_k, int tau,
                                                             int32_t *__restrict__ qoff, int32_t *__restrict__ koff,
-                                                            uint16_t *__restrict__ qperm,
-                                                            uint16_t *__restrict__ kperm,
-                                                            uint16_t *__restrict__ qsorted,
-                                                            uint16_t *__restrict__ ksorted) {
+                                                            uint32_t *__restrict__ qent,
+                                                            uint32_t *__restrict__ kent) {
     extern __shared__ int32_t cnt[];  // [buckets] counts, then cursors; + [kSortThreads] scan scratch
     int32_t *scan = cnt + (1 << tau);
     const int64_t unit = blockIdx.x >> 1;
@@ -63,8 +67,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
     const int64_t n = kside ? n_k : n_q;
     const uint16_t *codes = (kside ? kcodes : qcodes) + b * n * m + h;
     int32_t *off = (kside ? koff : qoff) + unit * ((1 << tau) + 1);
-    uint16_t *perm = (kside ? kperm : qperm) + unit * n;
-    uint16_t *sorted = (kside ? ksorted : qsorted) + unit * n;
+    uint32_t *ent = (kside ? kent : qent) + unit * n;
     const int B = 1 << tau;
     const int tid = threadIdx.x;
 
@@ -97,188 +100,271 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
     __syncthreads();
 
     for (int64_t i = tid; i < n; i += kSortThreads) {
-        const int c = codes[i * m] & (B - 1);
+        const uint32_t c = codes[i * m] & (B - 1);
         const int32_t pos = atomicAdd(&cnt[c], 1);
-        perm[pos] = static_cast<uint16_t>(i);
-        sorted[pos] = static_cast<uint16_t>(c);
+        ent[pos] = (c << 16) | static_cast<uint32_t>(i);
     }
 }
 
 // ---------------------------------------------------------------- pair passes
 struct Side {
-    const uint16_t *perm, *sorted;  // [units][n] rows in bucket order and their codes
-    const int32_t *off;             // [units][2^tau + 1] bucket offsets
+    const uint32_t *ent;  // [units][n] (code << 16 | row) in bucket order
+    const int32_t *off;   // [units][2^tau + 1] bucket offsets
     int64_t n;
 };
 
 struct PassArgs {
     Side q, k;
     const void *qv, *kv, *vv, *dyv;  // Q, K, V, dY [bh][n][64]
-    float *pq, *pk;                  // partials [bh][n][m][64]
+    void *pq, *pk;                   // partials [bh][n][m][64] (fp32, or bf16 for bf16 storage)
     int64_t bh;
     int m, tau;
     float scale;                     // tau / (2m)
 };
 
-// out_x (for the 16 sorted rows of a tile) = scale * sum_{y in bucket(x)} (a_x . a'_y) b_y,
-// stored at part[(row0 + x) * m + h][0:64].
+// 8 consecutive values of a row (fp32 or bf16 storage) as two float4.
 template <bool BF16>
-__device__ __forceinline__ void pass_run(const Side &rows, const Side &par, const void *a_row, const void *a_par,
-                                         const void *b_par, float *part, int64_t unit, int64_t b, int h, int m,
-                                         int tau, float scale) {
-    const int nbk = (1 << tau) + 1;
-    const uint16_t *rperm = rows.perm + unit * rows.n;
-    const uint16_t *rsorted = rows.sorted + unit * rows.n;
-    const int32_t *poff = par.off + unit * nbk;
-    const uint16_t *pperm = par.perm + unit * par.n;
-    const uint16_t *psorted = par.sorted + unit * par.n;
-    const int64_t rrow0 = b * rows.n, prow0 = b * par.n;
-
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int g = lane >> 4, c = lane & 15;
-    const int64_t tiles = (rows.n + 15) >> 4;
-
-    for (int64_t rt = wave; rt < tiles; rt += kPassThreads / 64) {
-        const int64_t p0 = rt * 16;
-        const int64_t plast = (p0 + 15 < rows.n) ? p0 + 15 : rows.n - 1;
-        const int cfirst = rsorted[p0], clast = rsorted[plast];
-        const int64_t pbeg = poff[cfirst], pend = poff[clast + 1];
-
-        // row-side operand: a_x as the B operand of S^T (lane (g, c): row c, dims kb*32 + g*8 + [0,8))
-        const bool rv_c = p0 + c < rows.n;
-        const int64_t rrow_c = rv_c ? rrow0 + rperm[p0 + c] : 0;
-        const int rcode_c = rv_c ? rsorted[p0 + c] : -2;
-        floatx4 outT[4];
-#pragma unroll
-        for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-        if (pbeg < pend) {
-            half8 ah[2], al[2];
-#pragma unroll
-            for (int kb = 0; kb < 2; kb++) {
-                float t[8];
-                if (rv_c) {
-                    load8<BF16>(a_row, rrow_c * D + kb * 32 + g * 8, t);
-                } else {
-#pragma unroll
-                    for (int i = 0; i < 8; i++) t[i] = 0.f;
-                }
-                split8(t, 1.0f, ah[kb], al[kb]);
-            }
-            for (int64_t y0 = pbeg; y0 < pend; y0 += 16) {
-                // partner a'_y as the A operand of S^T (lane (g, c): partner c)
-                const bool pv_c = y0 + c < pend;
-                const int64_t prow_c = pv_c ? prow0 + pperm[y0 + c] : 0;
-                half8 ph[2], pl[2];
-#pragma unroll
-                for (int kb = 0; kb < 2; kb++) {
-                    float t[8];
-                    if (pv_c) {
-                        load8<BF16>(a_par, prow_c * D + kb * 32 + g * 8, t);
-                    } else {
-#pragma unroll
-                        for (int i = 0; i < 8; i++) t[i] = 0.f;
-                    }
-                    split8(t, 1.0f, ph[kb], pl[kb]);
-                }
-                // partner b_y^T as A fragments of the output product:
-                // lane (g, c) holds dims 16dt + c of partners y0 + 4g + [0,4)
-                int pcode_r[4];
-                int64_t prow_r[4];
-                bool pv_r[4];
-#pragma unroll
-                for (int i = 0; i < 4; i++) {
-                    const int64_t p = y0 + 4 * g + i;
-                    pv_r[i] = p < pend;
-                    prow_r[i] = pv_r[i] ? prow0 + pperm[p] : 0;
-                    pcode_r[i] = pv_r[i] ? psorted[p] : -3;
-                }
-                half4 bh[4], bl[4];
-#pragma unroll
-                for (int dt = 0; dt < 4; dt++) {
-                    float t[4];
-#pragma unroll
-                    for (int i = 0; i < 4; i++)
-                        t[i] = pv_r[i] ? load1<BF16>(b_par, prow_r[i] * D + dt * 16 + c) : 0.f;
-                    split4(t, 256.0f, bh[dt], bl[dt]);
-                }
-                // S^T[partner 4g+i][row c]
-                floatx4 st = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int kb = 0; kb < 2; kb++) st = mfma3_16x16x32(ph[kb], pl[kb], ah[kb], al[kb], st);
-                float sv[4];
-#pragma unroll
-                for (int i = 0; i < 4; i++) sv[i] = (pcode_r[i] == rcode_c) ? st[i] * scale : 0.f;
-                half4 sh, sl;
-                split4(sv, 1.0f, sh, sl);
-                // out^T[dim 16dt + 4g + i][row c] += sum_y b^T[dim][y] S^T[y][row]
-#pragma unroll
-                for (int dt = 0; dt < 4; dt++) outT[dt] = mfma3_16x16x16(bh[dt], bl[dt], sh, sl, outT[dt]);
-            }
-        }
-        // lane (g, c) holds out[row c][dims 16dt + 4g + (0..3)]
-        if (rv_c) {
-            float *dst = part + ((rrow_c * m) + h) * D + 4 * g;
-#pragma unroll
-            for (int dt = 0; dt < 4; dt++) {
-                const float4 o = make_float4(outT[dt][0] * (1.0f / 256.0f), outT[dt][1] * (1.0f / 256.0f),
-                                             outT[dt][2] * (1.0f / 256.0f), outT[dt][3] * (1.0f / 256.0f));
-                *reinterpret_cast<float4 *>(dst + dt * 16) = o;
-            }
-        }
+__device__ __forceinline__ void load8v(const void *base, int64_t off, float4 &lo, float4 &hi) {
+    if constexpr (BF16) {
+        const uint4 w = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(base) + off);
+        lo = make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xFFFF0000u), __uint_as_float(w.y << 16),
+                         __uint_as_float(w.y & 0xFFFF0000u));
+        hi = make_float4(__uint_as_float(w.z << 16), __uint_as_float(w.z & 0xFFFF0000u), __uint_as_float(w.w << 16),
+                         __uint_as_float(w.w & 0xFFFF0000u));
+    } else {
+        const float4 *p = reinterpret_cast<const float4 *>(static_cast<const float *>(base) + off);
+        lo = p[0];
+        hi = p[1];
     }
 }
 
+__device__ __forceinline__ float4 zero_if(bool keep, float4 v) {
+    return keep ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+// Operands of one 16-partner sub-tile, as loaded (fp32).
+struct PartnerRegs {
+    float4 a[4];      // a'_y of partner c: dims kb*32 + g*8 + [0,8) as a[2kb], a[2kb+1]
+    float4 bv[4];     // b_y of partner c, same dims (transposed through LDS before use)
+    int code_r[4];    // codes of partners 4g + i (negative past the range)
+};
+
+// Loads are unconditional (a row of this head is always valid memory) and the
+// values past the range are zeroed afterwards, so no branch sits between the
+// issue of the loads and their use.
 template <bool BF16>
+__device__ __forceinline__ void load_partners(PartnerRegs &r, const uint32_t *pent, int64_t y0, int64_t pend,
+                                              int64_t prow0, const void *a_par, const void *b_par, int g, int c) {
+    const bool ok = y0 + c < pend;
+    const uint32_t e = pent[ok ? y0 + c : y0];
+    const int64_t row = prow0 + (e & 0xFFFFu);
+#pragma unroll
+    for (int kb = 0; kb < 2; kb++) {
+        load8v<BF16>(a_par, row * D + kb * 32 + g * 8, r.a[2 * kb], r.a[2 * kb + 1]);
+        load8v<BF16>(b_par, row * D + kb * 32 + g * 8, r.bv[2 * kb], r.bv[2 * kb + 1]);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; j++) {
+        r.a[j] = zero_if(ok, r.a[j]);
+        r.bv[j] = zero_if(ok, r.bv[j]);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        const int64_t p = y0 + 4 * g + i;
+        const bool in = p < pend;
+        const uint32_t ei = pent[in ? p : y0];
+        r.code_r[i] = in ? static_cast<int>(ei >> 16) : -3;
+    }
+}
+
+__device__ __forceinline__ void split8v(const float4 &x, const float4 &y, float scale, half8 &hi, half8 &lo) {
+    const float v[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+    split8(v, scale, hi, lo);
+}
+
+// out^T += B_y^T S^T for one sub-tile held in r; ah/al are the row-side fragments.
+__device__ __forceinline__ void compute_partners(const PartnerRegs &r, const half8 ah[2], const half8 al[2],
+                                                 int rcode_c, float scale, float *tile, int g, int c,
+                                                 floatx4 outT[4]) {
+    // B_y through LDS: write row-major [partner][dim], read lane (g, c) <- partners 4g+i, dim 16dt + c
+#pragma unroll
+    for (int kb = 0; kb < 2; kb++) {
+        float4 *dst = reinterpret_cast<float4 *>(tile + c * kTileStride + kb * 32 + g * 8);
+        dst[0] = r.bv[2 * kb];
+        dst[1] = r.bv[2 * kb + 1];
+    }
+    // the tile is private to this wave and LDS executes a wave's accesses in order:
+    // only the compiler must keep the reads after the writes (and the next writes
+    // after these reads)
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    half4 bh[4], bl[4];
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++) {
+        float t[4];
+#pragma unroll
+        for (int i = 0; i < 4; i++) t[i] = tile[(4 * g + i) * kTileStride + dt * 16 + c];
+        split4(t, 256.0f, bh[dt], bl[dt]);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    // S^T[partner 4g+i][row c]
+    half8 ph[2], pl[2];
+    split8v(r.a[0], r.a[1], 1.0f, ph[0], pl[0]);
+    split8v(r.a[2], r.a[3], 1.0f, ph[1], pl[1]);
+    floatx4 st = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < 2; kb++) st = mfma3_16x16x32(ph[kb], pl[kb], ah[kb], al[kb], st);
+    float sv[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) sv[i] = (r.code_r[i] == rcode_c) ? st[i] * scale : 0.f;
+    half4 sh, sl;
+    split4(sv, 1.0f, sh, sl);
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++) outT[dt] = mfma3_16x16x16(bh[dt], bl[dt], sh, sl, outT[dt]);
+}
+
+template <bool BF16, bool STAGED>
 __global__ __launch_bounds__(kPassThreads) void pass_kernel(PassArgs a) {
+    extern __shared__ __align__(16) float smem[];
+    float *tile = smem + (threadIdx.x >> 6) * (16 * kTileStride);  // per-wave transpose tile
+    uint32_t *stage = reinterpret_cast<uint32_t *>(smem + kPassWaves * 16 * kTileStride);
+
     const int64_t units = a.bh * a.m;
     const int64_t id = xcd_remap(blockIdx.x, 2 * units);
     const int64_t unit = id >> 1;
     const bool kside = id & 1;
     const int64_t b = unit / a.m;
     const int h = static_cast<int>(unit - b * a.m);
-    if (!kside) {
-        // dQ: rows = queries (a = dY), partners = keys (a' = V, b = K)
-        pass_run<BF16>(a.q, a.k, a.dyv, a.vv, a.kv, a.pq, unit, b, h, a.m, a.tau, a.scale);
-    } else {
-        // dK: rows = keys (a = V), partners = queries (a' = dY, b = Q)
-        pass_run<BF16>(a.k, a.q, a.vv, a.dyv, a.qv, a.pk, unit, b, h, a.m, a.tau, a.scale);
+    // dQ: rows = queries (a = dY), partners = keys (a' = V, b = K)
+    // dK: rows = keys (a = V), partners = queries (a' = dY, b = Q)
+    // (fields are selected by value: a runtime choice between references into the
+    // kernel-argument struct would force a private copy of it)
+    const int64_t n_r = kside ? a.k.n : a.q.n;
+    const int64_t n_p = kside ? a.q.n : a.k.n;
+    const uint32_t *r_ent = kside ? a.k.ent : a.q.ent;
+    const uint32_t *p_ent = kside ? a.q.ent : a.k.ent;
+    const int32_t *p_off = kside ? a.q.off : a.k.off;
+    const void *a_row = kside ? a.vv : a.dyv;
+    const void *a_par = kside ? a.dyv : a.vv;
+    const void *b_par = kside ? a.qv : a.kv;
+    void *part = kside ? a.pk : a.pq;
+
+    const int nbk = (1 << a.tau) + 1;
+    const uint32_t *rent = r_ent + unit * n_r;
+    const uint32_t *pent = p_ent + unit * n_p;
+    const int32_t *poff = p_off + unit * nbk;
+    if constexpr (STAGED) {
+        uint32_t *s_ent = stage;
+        int32_t *s_off = reinterpret_cast<int32_t *>(stage + n_p);
+        for (int64_t i = threadIdx.x; i < n_p; i += kPassThreads) s_ent[i] = pent[i];
+        for (int i = threadIdx.x; i < nbk; i += kPassThreads) s_off[i] = poff[i];
+        __syncthreads();
+        pent = s_ent;
+        poff = s_off;
+    }
+    const int64_t rrow0 = b * n_r, prow0 = b * n_p;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int g = lane >> 4, c = lane & 15;
+    const int64_t tiles = (n_r + 15) >> 4;
+
+    uint32_t e_next = 0;
+    if (wave < tiles && static_cast<int64_t>(wave) * 16 + c < n_r) e_next = rent[static_cast<int64_t>(wave) * 16 + c];
+    for (int64_t t = wave; t < tiles; t += kPassWaves) {
+        const uint32_t e = e_next;
+        {
+            const int64_t tn = t + kPassWaves;
+            e_next = (tn < tiles && tn * 16 + c < n_r) ? rent[tn * 16 + c] : 0u;
+        }
+        const int64_t p0 = t * 16;
+        const int nrow = static_cast<int>(n_r - p0 < 16 ? n_r - p0 : 16);
+        const bool rv_c = c < nrow;
+        const int rcode_c = rv_c ? static_cast<int>(e >> 16) : -2;
+        const int64_t rrow_c = rrow0 + (e & 0xFFFFu);
+        const int cfirst = static_cast<int>(__builtin_amdgcn_readlane(e, 0) >> 16);
+        const int clast = static_cast<int>(__builtin_amdgcn_readlane(e, nrow - 1) >> 16);
+        const int64_t pbeg = poff[cfirst], pend = poff[clast + 1];
+
+        floatx4 outT[4];
+#pragma unroll
+        for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+        if (pbeg < pend) {
+            PartnerRegs A, B;
+            load_partners<BF16>(A, pent, pbeg, pend, prow0, a_par, b_par, g, c);
+            half8 ah[2], al[2];
+            {
+                float4 x[4];
+#pragma unroll
+                for (int kb = 0; kb < 2; kb++) load8v<BF16>(a_row, rrow_c * D + kb * 32 + g * 8, x[2 * kb], x[2 * kb + 1]);
+#pragma unroll
+                for (int j = 0; j < 4; j++) x[j] = zero_if(rv_c, x[j]);
+                split8v(x[0], x[1], 1.0f, ah[0], al[0]);
+                split8v(x[2], x[3], 1.0f, ah[1], al[1]);
+            }
+            for (int64_t y0 = pbeg;;) {
+                if (y0 + 16 < pend) load_partners<BF16>(B, pent, y0 + 16, pend, prow0, a_par, b_par, g, c);
+                compute_partners(A, ah, al, rcode_c, a.scale, tile, g, c, outT);
+                y0 += 16;
+                if (y0 >= pend) break;
+                if (y0 + 16 < pend) load_partners<BF16>(A, pent, y0 + 16, pend, prow0, a_par, b_par, g, c);
+                compute_partners(B, ah, al, rcode_c, a.scale, tile, g, c, outT);
+                y0 += 16;
+                if (y0 >= pend) break;
+            }
+        }
+        // lane (g, c) holds out[row c][dims 16dt + 4g + (0..3)] * 256
+        if (rv_c) {
+            const int64_t base = ((rrow_c * a.m) + h) * D + 4 * g;
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) {
+                const float4 o = make_float4(outT[dt][0] * (1.0f / 256.0f), outT[dt][1] * (1.0f / 256.0f),
+                                             outT[dt][2] * (1.0f / 256.0f), outT[dt][3] * (1.0f / 256.0f));
+                if constexpr (BF16) {
+                    uint2 w;
+                    w.x = static_cast<uint32_t>(f32_to_bf16(o.x)) | (static_cast<uint32_t>(f32_to_bf16(o.y)) << 16);
+                    w.y = static_cast<uint32_t>(f32_to_bf16(o.z)) | (static_cast<uint32_t>(f32_to_bf16(o.w)) << 16);
+                    *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(part) + base + dt * 16) = w;
+                } else {
+                    *reinterpret_cast<float4 *>(static_cast<float *>(part) + base + dt * 16) = o;
+                }
+            }
+        }
     }
 }
 
-// out[r][:] = sum_h part[r][h][:]; 16 lanes per row, 4 floats each.
+// out[r][:] = sum_h part[r][h][:]; 16 lanes per row, 4 values each.
 template <bool BF16>
-__global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const float *__restrict__ part, void *__restrict__ out,
+__global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const void *__restrict__ part, void *__restrict__ out,
                                                                 int64_t rows, int m) {
     const int64_t r = (static_cast<int64_t>(blockIdx.x) * kReduceThreads + threadIdx.x) >> 4;
     const int q = threadIdx.x & 15;
     if (r >= rows) return;
-    const float4 *src = reinterpret_cast<const float4 *>(part + r * m * D) + q;
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int h = 0; h < m; h++) {
-        const float4 v = src[h * (D / 4)];
-        s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-    }
     if constexpr (BF16) {
+        const uint2 *src = reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(part) + r * m * D) + q;
+        for (int h = 0; h < m; h++) {
+            const uint2 v = src[h * (D / 4)];
+            s.x += __uint_as_float(v.x << 16);
+            s.y += __uint_as_float(v.x & 0xFFFF0000u);
+            s.z += __uint_as_float(v.y << 16);
+            s.w += __uint_as_float(v.y & 0xFFFF0000u);
+        }
         uint2 o;
         o.x = static_cast<uint32_t>(f32_to_bf16(s.x)) | (static_cast<uint32_t>(f32_to_bf16(s.y)) << 16);
         o.y = static_cast<uint32_t>(f32_to_bf16(s.z)) | (static_cast<uint32_t>(f32_to_bf16(s.w)) << 16);
         reinterpret_cast<uint2 *>(static_cast<uint16_t *>(out) + r * D)[q] = o;
     } else {
+        const float4 *src = reinterpret_cast<const float4 *>(static_cast<const float *>(part) + r * m * D) + q;
+        for (int h = 0; h < m; h++) {
+            const float4 v = src[h * (D / 4)];
+            s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+        }
         reinterpret_cast<float4 *>(static_cast<float *>(out) + r * D)[q] = s;
     }
 }
 
-__global__ void zero_kernel(float *__restrict__ p, int64_t count) {
+__global__ void zero_kernel(uint32_t *__restrict__ p, int64_t count) {
     for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < count;
          e += static_cast<int64_t>(gridDim.x) * blockDim.x)
-        p[e] = 0.f;
-}
-
-__global__ void zero_bf16_kernel(uint16_t *__restrict__ p, int64_t count) {
-    for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < count;
-         e += static_cast<int64_t>(gridDim.x) * blockDim.x)
-        p[e] = 0;
+        p[e] = 0u;
 }
 
 unsigned elementwise_grid(int64_t count) {
@@ -289,7 +375,7 @@ unsigned elementwise_grid(int64_t count) {
 size_t align_up(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 template <bool BF16>
-hipError_t launch_reduce(const float *part, void *out, int64_t rows, int m, hipStream_t stream) {
+hipError_t launch_reduce(const void *part, void *out, int64_t rows, int m, hipStream_t stream) {
     if (rows == 0) return hipSuccess;
     const int64_t blocks = (rows * 16 + kReduceThreads - 1) / kReduceThreads;
     KernelTimer timer("reduce_kernel", stream);
@@ -298,16 +384,29 @@ hipError_t launch_reduce(const float *part, void *out, int64_t rows, int m, hipS
     return hipGetLastError();
 }
 
-// Zero an output that no pair can reach (the other side is empty).
-hipError_t zero_output(void *out, bool bf16, int64_t count, hipStream_t stream) {
-    if (count == 0) return hipSuccess;
+// Zero an output that no pair can reach (the other side is empty).  `bytes` is a
+// multiple of 4 (rows of 64 fp32 or bf16 values).
+hipError_t zero_output(void *out, int64_t bytes, hipStream_t stream) {
+    const int64_t words = bytes / 4;
+    if (words == 0) return hipSuccess;
     KernelTimer timer("zero_kernel", stream);
-    if (bf16)
-        hipLaunchKernelGGL(zero_bf16_kernel, dim3(elementwise_grid(count)), dim3(256), 0, stream,
-                           static_cast<uint16_t *>(out), count);
+    hipLaunchKernelGGL(zero_kernel, dim3(elementwise_grid(words)), dim3(256), 0, stream, static_cast<uint32_t *>(out),
+                       words);
+    return hipGetLastError();
+}
+
+template <bool BF16>
+hipError_t launch_pass(const PassArgs &a, int64_t units, hipStream_t stream) {
+    const int64_t nmax = a.q.n > a.k.n ? a.q.n : a.k.n;
+    const size_t stage = (static_cast<size_t>(nmax) + (static_cast<size_t>(1) << a.tau) + 1) * 4;
+    const size_t tiles = static_cast<size_t>(kPassWaves) * 16 * kTileStride * 4;
+    KernelTimer timer("pass_kernel", stream);
+    if (stage <= kPassStageBudget)
+        hipLaunchKernelGGL((pass_kernel<BF16, true>), dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads),
+                           tiles + stage, stream, a);
     else
-        hipLaunchKernelGGL(zero_kernel, dim3(elementwise_grid(count)), dim3(256), 0, stream, static_cast<float *>(out),
-                           count);
+        hipLaunchKernelGGL((pass_kernel<BF16, false>), dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads),
+                           tiles, stream, a);
     return hipGetLastError();
 }
 
@@ -317,15 +416,14 @@ BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, 
     BackwardLayout L;
     const int64_t units = bh * m;
     const size_t nb = (static_cast<size_t>(1) << tau) + 1;
+    const size_t pbytes = bf16 ? 2 : 4;
     size_t o = 0;
     L.qoff = o; o = align_up(o + units * nb * 4);
     L.koff = o; o = align_up(o + units * nb * 4);
-    L.qperm = o; o = align_up(o + units * n_q * 2);
-    L.kperm = o; o = align_up(o + units * n_k * 2);
-    L.qsorted = o; o = align_up(o + units * n_q * 2);
-    L.ksorted = o; o = align_up(o + units * n_k * 2);
-    L.pq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m * D * 4);
-    L.pk = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m * D * 4);
+    L.qent = o; o = align_up(o + units * n_q * 4);
+    L.kent = o; o = align_up(o + units * n_k * 4);
+    L.pq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m * D * pbytes);
+    L.pk = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m * D * pbytes);
     L.table = o; o = align_up(o + table_workspace_bytes(bf16, bh, n_k, m, tau));
     L.total = o;
     return L;
@@ -344,10 +442,11 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
 
     const int64_t units = bh * m;
     if (units == 0) return hipSuccess;
+    const int64_t ebytes = bf16 ? 2 : 4;
     if (n_q == 0 || n_k == 0) {
         // no pairs: dq and dk are zero
-        if ((e = zero_output(dq, bf16, bh * n_q * D, stream)) != hipSuccess) return e;
-        return zero_output(dk, bf16, bh * n_k * D, stream);
+        if ((e = zero_output(dq, bh * n_q * D * ebytes, stream)) != hipSuccess) return e;
+        return zero_output(dk, bh * n_k * D * ebytes, stream);
     }
 
     {
@@ -355,32 +454,21 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
         KernelTimer timer("sort_kernel", stream);
         hipLaunchKernelGGL(sort_kernel, dim3(static_cast<unsigned>(2 * units)), dim3(kSortThreads), sort_lds, stream,
                            qcodes, kcodes, m, n_q, n_k, tau, reinterpret_cast<int32_t *>(ws + L.qoff),
-                           reinterpret_cast<int32_t *>(ws + L.koff), reinterpret_cast<uint16_t *>(ws + L.qperm),
-                           reinterpret_cast<uint16_t *>(ws + L.kperm), reinterpret_cast<uint16_t *>(ws + L.qsorted),
-                           reinterpret_cast<uint16_t *>(ws + L.ksorted));
+                           reinterpret_cast<int32_t *>(ws + L.koff), reinterpret_cast<uint32_t *>(ws + L.qent),
+                           reinterpret_cast<uint32_t *>(ws + L.kent));
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     PassArgs a;
-    a.q = Side{reinterpret_cast<const uint16_t *>(ws + L.qperm), reinterpret_cast<const uint16_t *>(ws + L.qsorted),
-               reinterpret_cast<const int32_t *>(ws + L.qoff), n_q};
-    a.k = Side{reinterpret_cast<const uint16_t *>(ws + L.kperm), reinterpret_cast<const uint16_t *>(ws + L.ksorted),
-               reinterpret_cast<const int32_t *>(ws + L.koff), n_k};
+    a.q = Side{reinterpret_cast<const uint32_t *>(ws + L.qent), reinterpret_cast<const int32_t *>(ws + L.qoff), n_q};
+    a.k = Side{reinterpret_cast<const uint32_t *>(ws + L.kent), reinterpret_cast<const int32_t *>(ws + L.koff), n_k};
     a.qv = q; a.kv = k; a.vv = v; a.dyv = dy;
-    a.pq = reinterpret_cast<float *>(ws + L.pq);
-    a.pk = reinterpret_cast<float *>(ws + L.pk);
+    a.pq = ws + L.pq;
+    a.pk = ws + L.pk;
     a.bh = bh; a.m = m; a.tau = tau;
     a.scale = static_cast<float>(tau) / (2.0f * static_cast<float>(m));
-    {
-        KernelTimer timer("pass_kernel", stream);
-        if (bf16)
-            hipLaunchKernelGGL(pass_kernel<true>, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0,
-                               stream, a);
-        else
-            hipLaunchKernelGGL(pass_kernel<false>, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0,
-                               stream, a);
-    }
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    e = bf16 ? launch_pass<true>(a, units, stream) : launch_pass<false>(a, units, stream);
+    if (e != hipSuccess) return e;
     if (bf16) {
         if ((e = launch_reduce<true>(a.pq, dq, bh * n_q, m, stream)) != hipSuccess) return e;
         return launch_reduce<true>(a.pk, dk, bh * n_k, m, stream);
