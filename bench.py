@@ -135,7 +135,8 @@ def main() -> int:
     ms_per_step = ms_total / args.steps
 
     kernels = {}
-    for name in ("hash_kernel", "table_kernel", "sort_kernel", "pass_kernel", "reduce_kernel", "zero_kernel"):
+    for name in ("hash_kernel", "table_kernel", "sort_kernel", "split_kernel", "pass_kernel", "reduce_kernel",
+                 "zero_kernel"):
         tot, n = Y.yoso_timing_query(name)
         if n:
             kernels[name] = {"launches_per_step": n / args.steps, "avg_us": 1000.0 * tot / n,

@@ -142,7 +142,8 @@ const char *yoso_last_error(void);
  * first launch and live until the next yoso_timing_enable call; 0 disables and
  * frees them).  yoso_timing_reset() forgets the launches recorded so far.
  * yoso_timing_query() waits for the recorded events of `kernel` ("hash_kernel",
- * "table_kernel", "sort_kernel", "pass_kernel", "reduce_kernel", "zero_kernel")
+ * "table_kernel", "sort_kernel", "split_kernel", "pass_kernel", "reduce_kernel",
+ * "zero_kernel")
  * and returns the summed duration and the launch count.
  * Not thread-safe with respect to concurrent launches on other threads' streams
  * beyond the pool bookkeeping, which is locked.

@@ -47,7 +47,7 @@ constexpr int kSortThreads = 256;
 constexpr int kPassThreads = 256;
 constexpr int kPassWaves = kPassThreads / 64;
 constexpr int kReduceThreads = 256;
-constexpr int kTileStride = 68;        // floats per row of the per-wave transpose tile (bank-conflict padding)
+constexpr int kTileStride = 2 * 64 + 8;  // halves per row of the per-wave transpose tile ([hi 64 | lo 64] + pad)
 constexpr size_t kPassStageBudget = 24 * 1024;  // LDS bytes for staged partner entries + offsets
 
 // ---------------------------------------------------------------- counting sort
@@ -115,58 +115,42 @@ struct Side {
 
 struct PassArgs {
     Side q, k;
-    const void *qv, *kv, *vv, *dyv;  // Q, K, V, dY [bh][n][64]
+    // Q, K, V, dY split into fp16 (hi, lo) pairs by split_kernel: row r holds 64 hi
+    // halves then 64 lo halves; Q and K are scaled by 2^8 first
+    const _Float16 *qs, *ks, *vs, *dys;
     void *pq, *pk;                   // partials [bh][n][m][64] (fp32, or bf16 for bf16 storage)
     int64_t bh;
     int m, tau;
     float scale;                     // tau / (2m)
 };
 
-// 8 consecutive values of a row (fp32 or bf16 storage) as two float4.
-template <bool BF16>
-__device__ __forceinline__ void load8v(const void *base, int64_t off, float4 &lo, float4 &hi) {
-    if constexpr (BF16) {
-        const uint4 w = *reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(base) + off);
-        lo = make_float4(__uint_as_float(w.x << 16), __uint_as_float(w.x & 0xFFFF0000u), __uint_as_float(w.y << 16),
-                         __uint_as_float(w.y & 0xFFFF0000u));
-        hi = make_float4(__uint_as_float(w.z << 16), __uint_as_float(w.z & 0xFFFF0000u), __uint_as_float(w.w << 16),
-                         __uint_as_float(w.w & 0xFFFF0000u));
-    } else {
-        const float4 *p = reinterpret_cast<const float4 *>(static_cast<const float *>(base) + off);
-        lo = p[0];
-        hi = p[1];
-    }
-}
-
-__device__ __forceinline__ float4 zero_if(bool keep, float4 v) {
-    return keep ? v : make_float4(0.f, 0.f, 0.f, 0.f);
-}
-
-// Operands of one 16-partner sub-tile, as loaded (fp32).
+// Operands of one 16-partner sub-tile (fp16 hi/lo halves).
 struct PartnerRegs {
-    float4 a[4];      // a'_y of partner c: dims kb*32 + g*8 + [0,8) as a[2kb], a[2kb+1]
-    float4 bv[4];     // b_y of partner c, same dims (transposed through LDS before use)
-    int code_r[4];    // codes of partners 4g + i (negative past the range)
+    half8 ah[2], al[2];  // a'_y of partner c: dims kb*32 + g*8 + [0,8), kb = 0, 1
+    half8 bh[2], bl[2];  // b_y of partner c, same dims (transposed through LDS before use)
+    int code_r[4];       // codes of partners 4g + i (negative past the range)
 };
+
+__device__ __forceinline__ half8 zero_if8(bool keep, half8 v) {
+    return keep ? v : half8{0, 0, 0, 0, 0, 0, 0, 0};
+}
 
 // Loads are unconditional (a row of this head is always valid memory) and the
 // values past the range are zeroed afterwards, so no branch sits between the
 // issue of the loads and their use.
-template <bool BF16>
 __device__ __forceinline__ void load_partners(PartnerRegs &r, const uint32_t *pent, int64_t y0, int64_t pend,
-                                              int64_t prow0, const void *a_par, const void *b_par, int g, int c) {
+                                              int64_t prow0, const _Float16 *a_par, const _Float16 *b_par, int g,
+                                              int c) {
     const bool ok = y0 + c < pend;
     const uint32_t e = pent[ok ? y0 + c : y0];
-    const int64_t row = prow0 + (e & 0xFFFFu);
+    const int64_t row = (prow0 + (e & 0xFFFFu)) * (2 * D);
 #pragma unroll
     for (int kb = 0; kb < 2; kb++) {
-        load8v<BF16>(a_par, row * D + kb * 32 + g * 8, r.a[2 * kb], r.a[2 * kb + 1]);
-        load8v<BF16>(b_par, row * D + kb * 32 + g * 8, r.bv[2 * kb], r.bv[2 * kb + 1]);
-    }
-#pragma unroll
-    for (int j = 0; j < 4; j++) {
-        r.a[j] = zero_if(ok, r.a[j]);
-        r.bv[j] = zero_if(ok, r.bv[j]);
+        const int o = kb * 32 + g * 8;
+        r.ah[kb] = zero_if8(ok, *reinterpret_cast<const half8 *>(a_par + row + o));
+        r.al[kb] = zero_if8(ok, *reinterpret_cast<const half8 *>(a_par + row + D + o));
+        r.bh[kb] = zero_if8(ok, *reinterpret_cast<const half8 *>(b_par + row + o));
+        r.bl[kb] = zero_if8(ok, *reinterpret_cast<const half8 *>(b_par + row + D + o));
     }
 #pragma unroll
     for (int i = 0; i < 4; i++) {
@@ -177,21 +161,16 @@ __device__ __forceinline__ void load_partners(PartnerRegs &r, const uint32_t *pe
     }
 }
 
-__device__ __forceinline__ void split8v(const float4 &x, const float4 &y, float scale, half8 &hi, half8 &lo) {
-    const float v[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
-    split8(v, scale, hi, lo);
-}
-
 // out^T += B_y^T S^T for one sub-tile held in r; ah/al are the row-side fragments.
 __device__ __forceinline__ void compute_partners(const PartnerRegs &r, const half8 ah[2], const half8 al[2],
-                                                 int rcode_c, float scale, float *tile, int g, int c,
+                                                 int rcode_c, float scale, _Float16 *tile, int g, int c,
                                                  floatx4 outT[4]) {
-    // B_y through LDS: write row-major [partner][dim], read lane (g, c) <- partners 4g+i, dim 16dt + c
+    // B_y through LDS: rows [partner][hi 64 | lo 64] halves; lane (g, c) then reads
+    // partners 4g + i of dim 16dt + c
 #pragma unroll
     for (int kb = 0; kb < 2; kb++) {
-        float4 *dst = reinterpret_cast<float4 *>(tile + c * kTileStride + kb * 32 + g * 8);
-        dst[0] = r.bv[2 * kb];
-        dst[1] = r.bv[2 * kb + 1];
+        *reinterpret_cast<half8 *>(tile + c * kTileStride + kb * 32 + g * 8) = r.bh[kb];
+        *reinterpret_cast<half8 *>(tile + c * kTileStride + D + kb * 32 + g * 8) = r.bl[kb];
     }
     // the tile is private to this wave and LDS executes a wave's accesses in order:
     // only the compiler must keep the reads after the writes (and the next writes
@@ -200,19 +179,17 @@ __device__ __forceinline__ void compute_partners(const PartnerRegs &r, const hal
     half4 bh[4], bl[4];
 #pragma unroll
     for (int dt = 0; dt < 4; dt++) {
-        float t[4];
 #pragma unroll
-        for (int i = 0; i < 4; i++) t[i] = tile[(4 * g + i) * kTileStride + dt * 16 + c];
-        split4(t, 256.0f, bh[dt], bl[dt]);
+        for (int i = 0; i < 4; i++) {
+            bh[dt][i] = tile[(4 * g + i) * kTileStride + dt * 16 + c];
+            bl[dt][i] = tile[(4 * g + i) * kTileStride + D + dt * 16 + c];
+        }
     }
     asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     // S^T[partner 4g+i][row c]
-    half8 ph[2], pl[2];
-    split8v(r.a[0], r.a[1], 1.0f, ph[0], pl[0]);
-    split8v(r.a[2], r.a[3], 1.0f, ph[1], pl[1]);
     floatx4 st = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < 2; kb++) st = mfma3_16x16x32(ph[kb], pl[kb], ah[kb], al[kb], st);
+    for (int kb = 0; kb < 2; kb++) st = mfma3_16x16x32(r.ah[kb], r.al[kb], ah[kb], al[kb], st);
     float sv[4];
 #pragma unroll
     for (int i = 0; i < 4; i++) sv[i] = (r.code_r[i] == rcode_c) ? st[i] * scale : 0.f;
@@ -224,8 +201,8 @@ __device__ __forceinline__ void compute_partners(const PartnerRegs &r, const hal
 
 template <bool BF16, bool STAGED>
 __global__ __launch_bounds__(kPassThreads) void pass_kernel(PassArgs a) {
-    extern __shared__ __align__(16) float smem[];
-    float *tile = smem + (threadIdx.x >> 6) * (16 * kTileStride);  // per-wave transpose tile
+    extern __shared__ __align__(16) _Float16 smem[];
+    _Float16 *tile = smem + (threadIdx.x >> 6) * (16 * kTileStride);  // per-wave transpose tile
     uint32_t *stage = reinterpret_cast<uint32_t *>(smem + kPassWaves * 16 * kTileStride);
 
     const int64_t units = a.bh * a.m;
@@ -243,9 +220,9 @@ __global__ __launch_bounds__(kPassThreads) void pass_kernel(PassArgs a) {
     const uint32_t *r_ent = kside ? a.k.ent : a.q.ent;
     const uint32_t *p_ent = kside ? a.q.ent : a.k.ent;
     const int32_t *p_off = kside ? a.q.off : a.k.off;
-    const void *a_row = kside ? a.vv : a.dyv;
-    const void *a_par = kside ? a.dyv : a.vv;
-    const void *b_par = kside ? a.qv : a.kv;
+    const _Float16 *a_row = kside ? a.vs : a.dys;
+    const _Float16 *a_par = kside ? a.dys : a.vs;
+    const _Float16 *b_par = kside ? a.qs : a.ks;
     void *part = kside ? a.pk : a.pq;
 
     const int nbk = (1 << a.tau) + 1;
@@ -288,23 +265,20 @@ __global__ __launch_bounds__(kPassThreads) void pass_kernel(PassArgs a) {
         for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
         if (pbeg < pend) {
             PartnerRegs A, B;
-            load_partners<BF16>(A, pent, pbeg, pend, prow0, a_par, b_par, g, c);
+            load_partners(A, pent, pbeg, pend, prow0, a_par, b_par, g, c);
             half8 ah[2], al[2];
-            {
-                float4 x[4];
 #pragma unroll
-                for (int kb = 0; kb < 2; kb++) load8v<BF16>(a_row, rrow_c * D + kb * 32 + g * 8, x[2 * kb], x[2 * kb + 1]);
-#pragma unroll
-                for (int j = 0; j < 4; j++) x[j] = zero_if(rv_c, x[j]);
-                split8v(x[0], x[1], 1.0f, ah[0], al[0]);
-                split8v(x[2], x[3], 1.0f, ah[1], al[1]);
+            for (int kb = 0; kb < 2; kb++) {
+                const int o = kb * 32 + g * 8;
+                ah[kb] = zero_if8(rv_c, *reinterpret_cast<const half8 *>(a_row + rrow_c * (2 * D) + o));
+                al[kb] = zero_if8(rv_c, *reinterpret_cast<const half8 *>(a_row + rrow_c * (2 * D) + D + o));
             }
             for (int64_t y0 = pbeg;;) {
-                if (y0 + 16 < pend) load_partners<BF16>(B, pent, y0 + 16, pend, prow0, a_par, b_par, g, c);
+                if (y0 + 16 < pend) load_partners(B, pent, y0 + 16, pend, prow0, a_par, b_par, g, c);
                 compute_partners(A, ah, al, rcode_c, a.scale, tile, g, c, outT);
                 y0 += 16;
                 if (y0 >= pend) break;
-                if (y0 + 16 < pend) load_partners<BF16>(A, pent, y0 + 16, pend, prow0, a_par, b_par, g, c);
+                if (y0 + 16 < pend) load_partners(A, pent, y0 + 16, pend, prow0, a_par, b_par, g, c);
                 compute_partners(B, ah, al, rcode_c, a.scale, tile, g, c, outT);
                 y0 += 16;
                 if (y0 >= pend) break;
@@ -327,6 +301,40 @@ __global__ __launch_bounds__(kPassThreads) void pass_kernel(PassArgs a) {
                 }
             }
         }
+    }
+}
+
+// Q, K, V, dY -> fp16 (hi, lo) rows [hi 64 | lo 64] for the pair passes; Q and K
+// (the vectors that multiply S) are scaled by 2^8 so that their lo parts stay
+// normal fp16 numbers.  One thread per 8 values.
+template <bool BF16>
+__global__ __launch_bounds__(256) void split_kernel(const void *__restrict__ q, const void *__restrict__ k,
+                                                    const void *__restrict__ v, const void *__restrict__ dy,
+                                                    _Float16 *__restrict__ qs, _Float16 *__restrict__ ks,
+                                                    _Float16 *__restrict__ vs, _Float16 *__restrict__ dys,
+                                                    int64_t rows_q, int64_t rows_k) {
+    const int64_t per_q = rows_q * (D / 8), per_k = rows_k * (D / 8);
+    const int64_t total = 2 * (per_q + per_k);
+    for (int64_t tid = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; tid < total;
+         tid += static_cast<int64_t>(gridDim.x) * 256) {
+        // which: 0 = Q, 1 = dY (query side), 2 = K, 3 = V (key side)
+        int which;
+        int64_t t;
+        if (tid < per_q) { which = 0; t = tid; }
+        else if (tid < 2 * per_q) { which = 1; t = tid - per_q; }
+        else if (tid < 2 * per_q + per_k) { which = 2; t = tid - 2 * per_q; }
+        else { which = 3; t = tid - 2 * per_q - per_k; }
+        const void *src = which == 0 ? q : which == 1 ? dy : which == 2 ? k : v;
+        _Float16 *dst = which == 0 ? qs : which == 1 ? dys : which == 2 ? ks : vs;
+        const float scale = (which == 0 || which == 2) ? 256.0f : 1.0f;
+        const int64_t row = t / (D / 8);
+        const int o = static_cast<int>(t - row * (D / 8)) * 8;
+        float x[8];
+        load8<BF16>(src, row * D + o, x);
+        half8 hi, lo;
+        split8(x, scale, hi, lo);
+        *reinterpret_cast<half8 *>(dst + row * (2 * D) + o) = hi;
+        *reinterpret_cast<half8 *>(dst + row * (2 * D) + D + o) = lo;
     }
 }
 
@@ -399,7 +407,7 @@ template <bool BF16>
 hipError_t launch_pass(const PassArgs &a, int64_t units, hipStream_t stream) {
     const int64_t nmax = a.q.n > a.k.n ? a.q.n : a.k.n;
     const size_t stage = (static_cast<size_t>(nmax) + (static_cast<size_t>(1) << a.tau) + 1) * 4;
-    const size_t tiles = static_cast<size_t>(kPassWaves) * 16 * kTileStride * 4;
+    const size_t tiles = static_cast<size_t>(kPassWaves) * 16 * kTileStride * 2;
     KernelTimer timer("pass_kernel", stream);
     if (stage <= kPassStageBudget)
         hipLaunchKernelGGL((pass_kernel<BF16, true>), dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads),
@@ -422,6 +430,10 @@ BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, 
     L.koff = o; o = align_up(o + units * nb * 4);
     L.qent = o; o = align_up(o + units * n_q * 4);
     L.kent = o; o = align_up(o + units * n_k * 4);
+    L.qs = o; o = align_up(o + static_cast<size_t>(bh) * n_q * D * 4);
+    L.dys = o; o = align_up(o + static_cast<size_t>(bh) * n_q * D * 4);
+    L.ks = o; o = align_up(o + static_cast<size_t>(bh) * n_k * D * 4);
+    L.vs = o; o = align_up(o + static_cast<size_t>(bh) * n_k * D * 4);
     L.pq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m * D * pbytes);
     L.pk = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m * D * pbytes);
     L.table = o; o = align_up(o + table_workspace_bytes(bf16, bh, n_k, m, tau));
@@ -459,10 +471,25 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
+    _Float16 *qs = reinterpret_cast<_Float16 *>(ws + L.qs), *ks = reinterpret_cast<_Float16 *>(ws + L.ks);
+    _Float16 *vs = reinterpret_cast<_Float16 *>(ws + L.vs), *dys = reinterpret_cast<_Float16 *>(ws + L.dys);
+    {
+        const int64_t threads = 2 * bh * (n_q + n_k) * (D / 8);
+        const int64_t blocks = (threads + 255) / 256 < 65536 ? (threads + 255) / 256 : 65536;
+        KernelTimer timer("split_kernel", stream);
+        if (bf16)
+            hipLaunchKernelGGL(split_kernel<true>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, q, k, v,
+                               dy, qs, ks, vs, dys, bh * n_q, bh * n_k);
+        else
+            hipLaunchKernelGGL(split_kernel<false>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, q, k,
+                               v, dy, qs, ks, vs, dys, bh * n_q, bh * n_k);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+
     PassArgs a;
     a.q = Side{reinterpret_cast<const uint32_t *>(ws + L.qent), reinterpret_cast<const int32_t *>(ws + L.qoff), n_q};
     a.k = Side{reinterpret_cast<const uint32_t *>(ws + L.kent), reinterpret_cast<const int32_t *>(ws + L.koff), n_k};
-    a.qv = q; a.kv = k; a.vv = v; a.dyv = dy;
+    a.qs = qs; a.ks = ks; a.vs = vs; a.dys = dys;
     a.pq = ws + L.pq;
     a.pk = ws + L.pk;
     a.bh = bh; a.m = m; a.tau = tau;

@@ -40,7 +40,7 @@ namespace yoso {
 
 namespace {
 
-constexpr int kTableThreads = 1024;
+constexpr int kTableThreads = 512;
 constexpr int kTableWaves = kTableThreads / 64;
 
 template <bool BF16, int DS>
@@ -95,13 +95,16 @@ struct TableArgs {
     int e_n;                    // ceil(log2(n_src)): bucket populations are < 2^e_n + 1
 };
 
-// (lo, hi) of a packed word whose fields are signed and |field sums| < 2^31.
+// (lo, hi) of a packed word whose fields are signed and |field sums| < 2^31:
+// the low dword is lo itself; the high dword is hi minus the borrow of a negative lo.
 __device__ __forceinline__ void unpack(unsigned long long w, int &lo, int &hi) {
     lo = static_cast<int>(static_cast<uint32_t>(w));
-    hi = static_cast<int>(static_cast<long long>(w - static_cast<unsigned long long>(static_cast<long long>(lo))) >> 32);
+    hi = static_cast<int>(static_cast<uint32_t>(w >> 32)) + static_cast<int>(static_cast<uint32_t>(lo) >> 31);
 }
 
-template <bool BF16, int DS>
+// KM: how a step broadcasts key values to the lanes: 0 -> one key per step
+// (readlane), 1 -> two keys per step (two readlanes), 2 -> more (ds_bpermute).
+template <bool BF16, int DS, int KM>
 __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
     constexpr int P = DS / 2;   // packed words per table row
     constexpr int S = D / DS;   // slices per head
@@ -178,73 +181,127 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
         __syncthreads();
 
         // ---- scatter
-        for (int64_t j0 = static_cast<int64_t>(wave) * 64; j0 < a.n_src; j0 += static_cast<int64_t>(kTableWaves) * 64) {
-            // lane = key j0 + lane: quantised, packed words of its DS values
-            uint32_t pw[2 * P];
-            {
-                const int64_t j = j0 + lane;
-                float v[DS];
-                if (j < a.n_src) {
-                    load_slice<BF16, DS>(a.values, vbase + j * D, v);
-                } else {
+        // A wave owns 64-key chunks wave, wave+16, ...  Lane = key first loads and
+        // quantises the chunk's values; then each step adds one (KM 0) or two (KM 1)
+        // keys into the tables, every lane taking its (hash, word) combo and reading
+        // the key's packed word from the lane that holds it (readlane).  The codes a
+        // lane needs for a whole chunk are fetched one chunk ahead (packed two per
+        // register) and so are the values, so load latency overlaps the atomics.
+        // Lanes without a valid (key, hash) add into a private dummy slot instead of
+        // branching.
+        if constexpr (KM < 2) {
+            constexpr int KPI_C = KM == 0 ? 1 : 2;
+            constexpr int SPC = 64 / KPI_C;  // steps per chunk
+            const int64_t nchunks = (a.n_src + 63) / 64;
+            const int mychunks = wave < nchunks ? static_cast<int>((nchunks - wave + kTableWaves - 1) / kTableWaves) : 0;
+            const int hh = sh[0], pp = sp[0];
+            const bool hok = hh < gcount;
+            // uniform base + 32-bit per-lane offsets (n*m < 2^22)
+            const uint16_t *cbase = a.src_codes + src_row0 * a.m + h0;
+            const int nsrc = static_cast<int>(a.n_src);
+            const int tab_words = (cmask + 1) * G * P;
+            const int dummy = tab_words + lane;
+            const int lane_off = hh * P + pp;
+            // codes are fetched kAhead steps ahead of their use, from a clamped (always
+            // valid) row, into a ring of registers; validity is decided at use
+            constexpr int kAhead = 16;
+            static_assert(SPC % kAhead == 0, "prefetch distance must divide the chunk");
+            const uint32_t last = static_cast<uint32_t>(nsrc - 1), mm = static_cast<uint32_t>(a.m);
+            const uint32_t hcl = hok ? static_cast<uint32_t>(hh) : 0u;
+            auto code_at = [&](int tc, int st) -> int {
+                const uint32_t row = static_cast<uint32_t>((wave + kTableWaves * tc) * 64 + st * KPI_C + slot);
+                return cbase[min(row, last) * mm + hcl];
+            };
+            // values of the chunk, lane = key (loaded from a clamped row, zeroed past the end,
+            // so no branch separates the load from its use)
+            auto load_vals = [&](float v[DS], int tc) {
+                const int j = (wave + kTableWaves * tc) * 64 + lane;
+                load_slice<BF16, DS>(a.values, vbase + static_cast<int64_t>(min(j, nsrc - 1)) * D, v);
 #pragma unroll
-                    for (int d = 0; d < DS; d++) v[d] = 0.f;
-                }
+                for (int d = 0; d < DS; d++) v[d] = j < nsrc ? v[d] : 0.f;
+            };
+            int cr[kAhead];
+            float vr[DS];
+            // this wave's staging area: the packed words of its chunk, [key][P]
+            unsigned long long *wstage = tab + tab_words + 64 + wave * 64 * P;
+            if (mychunks > 0) {
+#pragma unroll
+                for (int st = 0; st < kAhead; st++) cr[st] = code_at(0, st);
+                load_vals(vr, 0);
+            }
+            for (int tc = 0; tc < mychunks; tc++) {
+                // keys of this chunk that exist: step st is valid for this lane iff
+                // st*KPI_C + slot < nvalid and the lane's hash exists
+                const int nvalid = hok ? min(64, nsrc - (wave + kTableWaves * tc) * 64) - slot : 0;
+                // quantise and publish this chunk's words (lane = key), then start
+                // fetching the next chunk's values
 #pragma unroll
                 for (int p = 0; p < P; p++) {
-                    const int lo = __float2int_rn(ldexpf(v[2 * p], k));
-                    const int hi = __float2int_rn(ldexpf(v[2 * p + 1], k));
-                    const unsigned long long w = (static_cast<unsigned long long>(static_cast<uint32_t>(hi)) << 32) +
-                                                 static_cast<unsigned long long>(static_cast<long long>(lo));
-                    pw[2 * p] = static_cast<uint32_t>(w);
-                    pw[2 * p + 1] = static_cast<uint32_t>(w >> 32);
+                    const int lo = __float2int_rn(ldexpf(vr[2 * p], k));
+                    const int hi = __float2int_rn(ldexpf(vr[2 * p + 1], k));
+                    wstage[lane * P + p] = (static_cast<unsigned long long>(static_cast<uint32_t>(hi)) << 32) +
+                                           static_cast<unsigned long long>(static_cast<long long>(lo));
                 }
+                // the staging area is private to this wave and LDS executes a wave's
+                // accesses in order: only the compiler must keep the reads below after
+                // these writes (and the next chunk's writes after the reads)
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                if (tc + 1 < mychunks) load_vals(vr, tc + 1);
+#pragma unroll
+                for (int st = 0; st < SPC; st++) {
+                    const unsigned long long word = wstage[(st * KPI_C + slot) * P + pp];
+                    const int c = cr[st % kAhead] & cmask;
+                    const int idx = st * KPI_C < nvalid ? c * (G * P) + lane_off : dummy;
+                    atomicAdd(&tab[idx], word);
+                    cr[st % kAhead] = st + kAhead < SPC ? code_at(tc, st + kAhead) : code_at(tc + 1, st + kAhead - SPC);
+                    // keep the scheduler from hoisting the unrolled chunk (register pressure)
+                    if ((st & 7) == 7) __builtin_amdgcn_sched_barrier(0);
+                }
+                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
             }
-            const int nk = static_cast<int>(a.n_src - j0 < 64 ? a.n_src - j0 : 64);
-            const int nsteps = (nk + KPI - 1) / KPI;
-            constexpr int B = 4;  // steps whose codes are fetched together
-            for (int s0 = 0; s0 < nsteps; s0 += B) {
-                int cc[B][2];
+        } else {
+            // general case (few hashes, wide slices): one step at a time, combos in NI passes
+            for (int ii = 0; ii < NI; ii++) {
+                const int hh = sh[ii], pp = sp[ii];
+                const bool hok = hh < gcount;
+                for (int64_t j0 = static_cast<int64_t>(wave) * 64; j0 < a.n_src;
+                     j0 += static_cast<int64_t>(kTableWaves) * 64) {
+                    uint32_t pw[2 * P];
+                    {
+                        const int64_t j = j0 + lane;
+                        float v[DS];
+                        if (j < a.n_src) {
+                            load_slice<BF16, DS>(a.values, vbase + j * D, v);
+                        } else {
 #pragma unroll
-                for (int t = 0; t < B; t++) {
-#pragma unroll
-                    for (int ii = 0; ii < 2; ii++) {
-                        const int key = (s0 + t) * KPI + slot;
-                        const bool ok = ii < NI && s0 + t < nsteps && key < nk && sh[ii] < gcount;
-                        cc[t][ii] = ok ? (a.src_codes[(src_row0 + j0 + key) * a.m + h0 + sh[ii]] & cmask) : -1;
-                    }
-                }
-#pragma unroll
-                for (int t = 0; t < B; t++) {
-                    if (s0 + t >= nsteps) break;
-                    const int kk = (s0 + t) * KPI;
-                    uint32_t w[2 * P];
-                    if (KPI == 1) {
-#pragma unroll
-                        for (int d = 0; d < 2 * P; d++) w[d] = __builtin_amdgcn_readlane(pw[d], kk);
-                    } else if (KPI == 2) {
-#pragma unroll
-                        for (int d = 0; d < 2 * P; d++) {
-                            const uint32_t w0 = __builtin_amdgcn_readlane(pw[d], kk);
-                            const uint32_t w1 = __builtin_amdgcn_readlane(pw[d], kk + 1 < 64 ? kk + 1 : 63);
-                            w[d] = slot ? w1 : w0;
+                            for (int d = 0; d < DS; d++) v[d] = 0.f;
                         }
-                    } else {
+#pragma unroll
+                        for (int p = 0; p < P; p++) {
+                            const int lo = __float2int_rn(ldexpf(v[2 * p], k));
+                            const int hi = __float2int_rn(ldexpf(v[2 * p + 1], k));
+                            const unsigned long long w =
+                                (static_cast<unsigned long long>(static_cast<uint32_t>(hi)) << 32) +
+                                static_cast<unsigned long long>(static_cast<long long>(lo));
+                            pw[2 * p] = static_cast<uint32_t>(w);
+                            pw[2 * p + 1] = static_cast<uint32_t>(w >> 32);
+                        }
+                    }
+                    const int nk = static_cast<int>(a.n_src - j0 < 64 ? a.n_src - j0 : 64);
+                    for (int kk = 0; kk < nk; kk += KPI) {
+                        uint32_t w[2 * P];
 #pragma unroll
                         for (int d = 0; d < 2 * P; d++) w[d] = __shfl(pw[d], (kk + slot) & 63);
-                    }
-#pragma unroll
-                    for (int ii = 0; ii < 2; ii++) {
-                        const int c = cc[t][ii];
-                        if (c >= 0) {
+                        const int key = kk + slot;
+                        if (key < nk && hok) {
                             uint32_t lo = w[0], hi = w[1];
 #pragma unroll
                             for (int p = 1; p < P; p++) {
-                                lo = sp[ii] == p ? w[2 * p] : lo;
-                                hi = sp[ii] == p ? w[2 * p + 1] : hi;
+                                lo = pp == p ? w[2 * p] : lo;
+                                hi = pp == p ? w[2 * p + 1] : hi;
                             }
-                            const unsigned long long word = (static_cast<unsigned long long>(hi) << 32) | lo;
-                            atomicAdd(&tab[(c * G + sh[ii]) * P + sp[ii]], word);
+                            const int c = a.src_codes[(src_row0 + j0 + key) * a.m + h0 + hh] & cmask;
+                            atomicAdd(&tab[(c * G + hh) * P + pp], (static_cast<unsigned long long>(hi) << 32) | lo);
                         }
                     }
                 }
@@ -252,86 +309,130 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
         }
         __syncthreads();
 
-        // ---- gather: out[i][slice*DS + d] (+)= 2^-k / m * sum_h table[code_h(i)][h][d]
-        for (int64_t i0 = static_cast<int64_t>(wave) * QPI; i0 < a.n_dst; i0 += static_cast<int64_t>(kTableWaves) * QPI) {
-            const int64_t i = i0 + gq;
-            const bool qok = i < a.n_dst;
-            int cc[8], hh[8];
-#pragma unroll
-            for (int t = 0; t < 8; t++) {
-                hh[t] = gr + L * ((t + gq) % (HL > 0 ? HL : 1));
-                const bool ok = t < HL && qok && hh[t] < gcount;
-                cc[t] = ok ? (a.dst_codes[(dst_row0 + i) * a.m + h0 + hh[t]] & cmask) : -1;
+        // ---- integer sums -> floats scaled by 2^-k / m, in place (a packed word and
+        // its two floats have the same 8 bytes)
+        {
+            const int words = (cmask + 1) * G * P;
+            float2 *tf = reinterpret_cast<float2 *>(tab);
+            for (int e = tid; e < words; e += kTableThreads) {
+                int lo, hi;
+                unpack(tab[e], lo, hi);
+                tf[e] = make_float2(ldexpf(static_cast<float>(lo), -k) * inv_m, ldexpf(static_cast<float>(hi), -k) * inv_m);
             }
-            float acc[DS];
+        }
+        __syncthreads();
+
+        // ---- gather: out[i][slice*DS + d] (+)= sum_h table[code_h(i)][h][d]
+        // (the codes of the wave's next query group are fetched before this one is summed)
+        {
+            int hh[8];
 #pragma unroll
-            for (int d = 0; d < DS; d++) acc[d] = 0.f;
+            for (int t = 0; t < 8; t++) hh[t] = gr + L * ((t + gq) % (HL > 0 ? HL : 1));
+            // codes of a query group: loads from clamped (always valid) positions,
+            // validity applied afterwards, so the loads stay in flight
+            const uint16_t *qbase = a.dst_codes + dst_row0 * a.m + h0;
+            const uint32_t qlast = static_cast<uint32_t>(a.n_dst - 1), mm = static_cast<uint32_t>(a.m);
+            auto fetch = [&](int cc[8], int64_t i0) {
+                const int64_t i = i0 + gq;
+                const uint32_t icl = i < a.n_dst ? static_cast<uint32_t>(i) : qlast;
 #pragma unroll
-            for (int t = 0; t < 8; t++) {
-                if (cc[t] >= 0) {
-                    const unsigned long long *row = tab + (cc[t] * G + hh[t]) * P;
-                    unsigned long long wv[P];
-                    if constexpr (P == 1) {
-                        wv[0] = row[0];
+                for (int t = 0; t < 8; t++) {
+                    if (t < HL) {
+                        const bool ok = i < a.n_dst && hh[t] < gcount;
+                        const uint32_t hcl = hh[t] < gcount ? static_cast<uint32_t>(hh[t]) : 0u;
+                        const int v = qbase[icl * mm + hcl];
+                        cc[t] = ok ? (v & cmask) : -1;
                     } else {
+                        cc[t] = -1;
+                    }
+                }
+            };
+            const int64_t step = static_cast<int64_t>(kTableWaves) * QPI;
+            int cA[8], cB[8];
+            fetch(cA, static_cast<int64_t>(wave) * QPI);
+            for (int64_t i0 = static_cast<int64_t>(wave) * QPI; i0 < a.n_dst; i0 += step) {
+                fetch(cB, i0 + step);
+                const int64_t i = i0 + gq;
+                const bool qok = i < a.n_dst;
+                float acc[DS];
 #pragma unroll
-                        for (int p = 0; p < P; p += 2) {
-                            const ulonglong2 x = reinterpret_cast<const ulonglong2 *>(row)[p / 2];
-                            wv[p] = x.x;
-                            wv[p + 1] = x.y;
+                for (int d = 0; d < DS; d++) acc[d] = 0.f;
+#pragma unroll
+                for (int t = 0; t < 8; t++) {
+                    if (cA[t] >= 0) {
+                        const float *row = reinterpret_cast<const float *>(tab) + (cA[t] * G + hh[t]) * DS;
+                        if constexpr (DS == 2) {
+                            const float2 x = *reinterpret_cast<const float2 *>(row);
+                            acc[0] += x.x;
+                            acc[1] += x.y;
+                        } else {
+#pragma unroll
+                            for (int d = 0; d < DS; d += 4) {
+                                const float4 x = *reinterpret_cast<const float4 *>(row + d);
+                                acc[d] += x.x;
+                                acc[d + 1] += x.y;
+                                acc[d + 2] += x.z;
+                                acc[d + 3] += x.w;
+                            }
                         }
                     }
+                }
 #pragma unroll
-                    for (int p = 0; p < P; p++) {
-                        int lo, hi;
-                        unpack(wv[p], lo, hi);
-                        acc[2 * p] += static_cast<float>(lo);
-                        acc[2 * p + 1] += static_cast<float>(hi);
+                for (int d = 0; d < DS; d++) acc[d] = group_sum(acc[d], L);
+                if (qok) {
+                    const int64_t obase = (dst_row0 + i) * D + slice * DS;
+#pragma unroll
+                    for (int d = 0; d < DS; d++) {
+                        if (d % L != gr) continue;
+                        const float v = acc[d];
+                        if (ngroups == 1) {
+                            if constexpr (BF16)
+                                static_cast<uint16_t *>(a.out)[obase + d] = f32_to_bf16(v);
+                            else
+                                static_cast<float *>(a.out)[obase + d] = v;
+                        } else {
+                            // the same lane owns this element in every group
+                            const float prev = grp == 0 ? 0.f : a.acc[obase + d];
+                            if (grp == ngroups - 1 && BF16)
+                                static_cast<uint16_t *>(a.out)[obase + d] = f32_to_bf16(prev + v);
+                            else
+                                a.acc[obase + d] = prev + v;
+                        }
                     }
                 }
-            }
 #pragma unroll
-            for (int d = 0; d < DS; d++) acc[d] = group_sum(acc[d], L);
-            if (qok) {
-                const int64_t obase = (dst_row0 + i) * D + slice * DS;
-#pragma unroll
-                for (int d = 0; d < DS; d++) {
-                    if (d % L != gr) continue;
-                    const float v = ldexpf(acc[d], -k) * inv_m;
-                    if (ngroups == 1) {
-                        if constexpr (BF16)
-                            static_cast<uint16_t *>(a.out)[obase + d] = f32_to_bf16(v);
-                        else
-                            static_cast<float *>(a.out)[obase + d] = v;
-                    } else {
-                        // the same lane owns this element in every group
-                        const float prev = grp == 0 ? 0.f : a.acc[obase + d];
-                        if (grp == ngroups - 1 && BF16)
-                            static_cast<uint16_t *>(a.out)[obase + d] = f32_to_bf16(prev + v);
-                        else
-                            a.acc[obase + d] = prev + v;
-                    }
-                }
+                for (int t = 0; t < 8; t++) cA[t] = cB[t];
             }
         }
         __syncthreads();
     }
 }
 
+template <bool BF16, int DS>
+void launch_table_km(int km, const TableArgs &a, size_t lds, hipStream_t stream) {
+    const int64_t blocks = a.bh * (D / DS);
+    const dim3 grid(static_cast<unsigned>(blocks)), block(kTableThreads);
+    if (km == 0)
+        hipLaunchKernelGGL((table_kernel<BF16, DS, 0>), grid, block, lds, stream, a);
+    else if (km == 1)
+        hipLaunchKernelGGL((table_kernel<BF16, DS, 1>), grid, block, lds, stream, a);
+    else
+        hipLaunchKernelGGL((table_kernel<BF16, DS, 2>), grid, block, lds, stream, a);
+}
+
 template <bool BF16>
 hipError_t launch_table_ds(int ds, const TableArgs &a, size_t lds, hipStream_t stream) {
-    const int64_t blocks = a.bh * (D / ds);
-    const dim3 grid(static_cast<unsigned>(blocks)), block(kTableThreads);
+    int gp = 1;
+    while (gp < a.G) gp <<= 1;
+    const int cpk = gp * (ds / 2);
+    const int km = (ds > 8) ? 2 : (cpk == 64 ? 0 : (cpk == 32 ? 1 : 2));
     KernelTimer timer("table_kernel", stream);
     switch (ds) {
-#define YOSO_CASE(X)                                                              \
-    case X:                                                                       \
-        hipLaunchKernelGGL((table_kernel<BF16, X>), grid, block, lds, stream, a); \
-        break;
-        YOSO_CASE(2) YOSO_CASE(4) YOSO_CASE(8) YOSO_CASE(16)
-#undef YOSO_CASE
-        default:
-            return hipErrorInvalidValue;
+        case 2: launch_table_km<BF16, 2>(km, a, lds, stream); break;
+        case 4: launch_table_km<BF16, 4>(km, a, lds, stream); break;
+        case 8: launch_table_km<BF16, 8>(km, a, lds, stream); break;
+        case 16: launch_table_km<BF16, 16>(km, a, lds, stream); break;
+        default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
@@ -389,7 +490,11 @@ hipError_t launch_table(const uint16_t *src_codes, const void *values, const uin
     a.tau = tau;
     a.G = p.G;
     a.e_n = ceil_log2(n_src);
-    return bf16 ? launch_table_ds<true>(p.DS, a, p.lds, stream) : launch_table_ds<false>(p.DS, a, p.lds, stream);
+    // + one private dummy word per lane (targets of lanes without a valid key)
+    // + per-wave staging of a chunk's packed words (64 keys x DS/2 words)
+    const size_t lds = p.lds + 64 * sizeof(unsigned long long) +
+                       static_cast<size_t>(kTableWaves) * 64 * (p.DS / 2) * sizeof(unsigned long long);
+    return bf16 ? launch_table_ds<true>(p.DS, a, lds, stream) : launch_table_ds<false>(p.DS, a, lds, stream);
 }
 
 }  // namespace yoso
