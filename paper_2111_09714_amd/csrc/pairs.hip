@@ -47,8 +47,10 @@ constexpr int kSortThreads = 256;
 constexpr int kPassThreads = 256;
 constexpr int kPassWaves = kPassThreads / 64;
 constexpr int kReduceThreads = 256;
-constexpr int kTileStride = 2 * 64 + 8;  // halves per row of the per-wave transpose tile ([hi 64 | lo 64] + pad)
-constexpr size_t kPassStageBudget = 24 * 1024;  // LDS bytes for staged partner entries + offsets
+constexpr int kTileBytes = 16 * 512;   // LDS bytes of one wave's operand tile
+constexpr int kPlanTiles = 1024;       // row tiles planned per run (multiple of kPassThreads)
+constexpr int kEntPad = 16;            // sentinel entries after each unit's sorted entries
+constexpr uint32_t kSentinel = 0xFFFF0000u;  // code 0xFFFF (no real code), row 0
 
 // ---------------------------------------------------------------- counting sort
 // codes are [bh][n][m]; unit = b*m + h reads column h with stride m.
@@ -67,7 +69,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
     const int64_t n = kside ? n_k : n_q;
     const uint16_t *codes = (kside ? kcodes : qcodes) + b * n * m + h;
     int32_t *off = (kside ? koff : qoff) + unit * ((1 << tau) + 1);
-    uint32_t *ent = (kside ? kent : qent) + unit * n;
+    uint32_t *ent = (kside ? kent : qent) + unit * (n + kEntPad);
     const int B = 1 << tau;
     const int tid = threadIdx.x;
 
@@ -104,11 +106,12 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
         const int32_t pos = atomicAdd(&cnt[c], 1);
         ent[pos] = (c << 16) | static_cast<uint32_t>(i);
     }
+    if (tid < kEntPad) ent[n + tid] = kSentinel;
 }
 
 // ---------------------------------------------------------------- pair passes
 struct Side {
-    const uint32_t *ent;  // [units][n] (code << 16 | row) in bucket order
+    const uint32_t *ent;  // [units][n + kEntPad]: (code << 16 | row) in bucket order, then sentinels
     const int32_t *off;   // [units][2^tau + 1] bucket offsets
     int64_t n;
 };
@@ -124,86 +127,173 @@ struct PassArgs {
     float scale;                     // tau / (2m)
 };
 
-// Operands of one 16-partner sub-tile (fp16 hi/lo halves).
-struct PartnerRegs {
-    half8 ah[2], al[2];  // a'_y of partner c: dims kb*32 + g*8 + [0,8), kb = 0, 1
-    half8 bh[2], bl[2];  // b_y of partner c, same dims (transposed through LDS before use)
-    int code_r[4];       // codes of partners 4g + i (negative past the range)
+// Load a T at `byte_off` bytes past `base` (a wave-uniform pointer): keeps the
+// per-lane part of the address in one 32-bit register.
+template <typename T>
+__device__ __forceinline__ T ld(const void *base, uint32_t byte_off) {
+    return *reinterpret_cast<const T *>(static_cast<const char *>(base) + byte_off);
+}
+
+// ---- the wave's LDS tile
+// Operands reach the MFMA layouts through one 8 KiB LDS tile per wave.  Global
+// loads are coalesced: the 16 lanes of a quarter-wave read 256 contiguous bytes
+// of one row (where an MFMA-layout load would touch 16 rows per quarter-wave and
+// make 4x as many cache requests).  16-byte chunks are XOR-swizzled within a row
+// so that both the MFMA-layout reads (16 rows, one chunk each) and the transpose
+// reads (8 rows x 32 bytes) hit distinct banks.
+//   partner tile: 16 rows x 512 B  [a' hi | a' lo | b hi | b lo], 128 B each
+//   row tile:     16 rows x 256 B  [a hi | a lo]
+//   out tile:     16 rows x 256 B  (64 fp32)
+__device__ __forceinline__ uint32_t swz(int row, int chunk, int row_bytes) {
+    const int f = ((row & 7) << 1) | ((row >> 3) & 1);
+    return static_cast<uint32_t>(row * row_bytes + ((chunk ^ f) << 4));
+}
+
+template <typename T>
+__device__ __forceinline__ T lds_ld(const unsigned char *base, uint32_t off) {
+    return *reinterpret_cast<const T *>(base + off);
+}
+template <typename T>
+__device__ __forceinline__ void lds_st(unsigned char *base, uint32_t off, const T &v) {
+    *reinterpret_cast<T *>(base + off) = v;
+}
+
+// One 16-partner sub-tile as loaded: lane l holds 16-byte chunk (l & 15) of
+// partner 4i + (l >> 4) of a' (a[i]) and of b (b[i]).
+struct Sub {
+    uint4 a[4], b[4];
 };
 
-__device__ __forceinline__ half8 zero_if8(bool keep, half8 v) {
-    return keep ? v : half8{0, 0, 0, 0, 0, 0, 0, 0};
-}
-
-// Loads are unconditional (a row of this head is always valid memory) and the
-// values past the range are zeroed afterwards, so no branch sits between the
-// issue of the loads and their use.
-__device__ __forceinline__ void load_partners(PartnerRegs &r, const uint32_t *pent, int64_t y0, int64_t pend,
-                                              int64_t prow0, const _Float16 *a_par, const _Float16 *b_par, int g,
-                                              int c) {
-    const bool ok = y0 + c < pend;
-    const uint32_t e = pent[ok ? y0 + c : y0];
-    const int64_t row = (prow0 + (e & 0xFFFFu)) * (2 * D);
-#pragma unroll
-    for (int kb = 0; kb < 2; kb++) {
-        const int o = kb * 32 + g * 8;
-        r.ah[kb] = zero_if8(ok, *reinterpret_cast<const half8 *>(a_par + row + o));
-        r.al[kb] = zero_if8(ok, *reinterpret_cast<const half8 *>(a_par + row + D + o));
-        r.bh[kb] = zero_if8(ok, *reinterpret_cast<const half8 *>(b_par + row + o));
-        r.bl[kb] = zero_if8(ok, *reinterpret_cast<const half8 *>(b_par + row + D + o));
-    }
+// `pe` is this lane's entry of partner (l & 15) (code << 16 | row); entries past
+// the unit's end are sentinels (row 0, an impossible code), so every load is in
+// bounds and a partner outside the tile's buckets is masked by its code.
+__device__ __forceinline__ void load_sub(Sub &s, uint32_t pe, const _Float16 *apar, const _Float16 *bpar, int q,
+                                         int cl) {
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-        const int64_t p = y0 + 4 * g + i;
-        const bool in = p < pend;
-        const uint32_t ei = pent[in ? p : y0];
-        r.code_r[i] = in ? static_cast<int>(ei >> 16) : -3;
+        const uint32_t e = static_cast<uint32_t>(__shfl(static_cast<int>(pe), 4 * i + q));
+        const uint32_t off = (e & 0xFFFFu) * (4 * D) + 16 * cl;
+        s.a[i] = ld<uint4>(apar, off);
+        s.b[i] = ld<uint4>(bpar, off);
     }
 }
 
-// out^T += B_y^T S^T for one sub-tile held in r; ah/al are the row-side fragments.
-__device__ __forceinline__ void compute_partners(const PartnerRegs &r, const half8 ah[2], const half8 al[2],
-                                                 int rcode_c, float scale, _Float16 *tile, int g, int c,
-                                                 floatx4 outT[4]) {
-    // B_y through LDS: rows [partner][hi 64 | lo 64] halves; lane (g, c) then reads
-    // partners 4g + i of dim 16dt + c
+// The 16 rows of a tile (row entry `re` of row (l & 15)) as loaded.
+__device__ __forceinline__ void load_row_tile(uint4 r[4], uint32_t re, const _Float16 *arow, int q, int cl) {
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        const uint32_t e = static_cast<uint32_t>(__shfl(static_cast<int>(re), 4 * i + q));
+        r[i] = ld<uint4>(arow, (e & 0xFFFFu) * (4 * D) + 16 * cl);
+    }
+}
+
+// Rows through the tile into the MFMA B-operand layout of S^T: lane (g, c) gets
+// row c, dims kb*32 + 8g + [0, 8) (hi and lo).
+__device__ __forceinline__ void stage_rows(const uint4 r[4], unsigned char *tile, int q, int cl, int g, int c,
+                                           half8 rh[2], half8 rl[2]) {
+#pragma unroll
+    for (int i = 0; i < 4; i++) lds_st(tile, swz(4 * i + q, cl, 256), r[i]);
 #pragma unroll
     for (int kb = 0; kb < 2; kb++) {
-        *reinterpret_cast<half8 *>(tile + c * kTileStride + kb * 32 + g * 8) = r.bh[kb];
-        *reinterpret_cast<half8 *>(tile + c * kTileStride + D + kb * 32 + g * 8) = r.bl[kb];
+        rh[kb] = lds_ld<half8>(tile, swz(c, kb * 4 + g, 256));
+        rl[kb] = lds_ld<half8>(tile, swz(c, 8 + kb * 4 + g, 256));
     }
-    // the tile is private to this wave and LDS executes a wave's accesses in order:
-    // only the compiler must keep the reads after the writes (and the next writes
-    // after these reads)
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    half4 bh[4], bl[4];
+}
+
+__device__ __forceinline__ half4 tr_load(const unsigned char *p) {
+    typedef short short4v __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) short4v lds_short4;
+    return __builtin_bit_cast(half4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4 *)(p)));
+}
+
+// Sub-tile into the tile (LDS executes one wave's accesses in order, so the reads
+// of compute_sub see these writes; the tile is private to the wave).
+__device__ __forceinline__ void publish_sub(const Sub &s, unsigned char *tile, int q, int cl) {
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        lds_st(tile, swz(4 * i + q, cl, 512), s.a[i]);
+        lds_st(tile, swz(4 * i + q, 16 + cl, 512), s.b[i]);
+    }
+}
+
+// out^T += B_y^T S^T for the sub-tile in the tile: S^T = A'_y A_x^T masked by
+// code equality.  `pe` as in load_sub.
+__device__ __forceinline__ void compute_sub(const unsigned char *tile, uint32_t pe, const half8 rh[2],
+                                            const half8 rl[2], int rcode, int g, int c, floatx4 outT[4]) {
+    // A'_y in the A-operand layout: lane (g, c) = partner c, dims kb*32 + 8g + [0, 8)
+    half8 ah[2], al[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; kb++) {
+        ah[kb] = lds_ld<half8>(tile, swz(c, kb * 4 + g, 512));
+        al[kb] = lds_ld<half8>(tile, swz(c, 8 + kb * 4 + g, 512));
+    }
+    // B_y^T as the A operand of a 16x16x16 MFMA: lane (g, c) needs partners 4g+i of
+    // dim 16dt+c.  ds_read_b64_tr_b16 gives destination lane 4a+b of a 16-lane
+    // group element b of the 8 bytes addressed by source lanes 4i+a (i = 0..3), so
+    // source lane 4i+a addresses partner 4g+i, dims 16dt + 4a .. +3 (chunk 2dt +
+    // a/2 of the b hi or lo part, half a%2 of it).
+    const int pr = 4 * g + (c >> 2), a4 = c & 3;
+    half4 bth[4], btl[4];
 #pragma unroll
     for (int dt = 0; dt < 4; dt++) {
-#pragma unroll
-        for (int i = 0; i < 4; i++) {
-            bh[dt][i] = tile[(4 * g + i) * kTileStride + dt * 16 + c];
-            bl[dt][i] = tile[(4 * g + i) * kTileStride + D + dt * 16 + c];
-        }
+        bth[dt] = tr_load(tile + swz(pr, 16 + 2 * dt + (a4 >> 1), 512) + 8 * (a4 & 1));
+        btl[dt] = tr_load(tile + swz(pr, 24 + 2 * dt + (a4 >> 1), 512) + 8 * (a4 & 1));
     }
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     // S^T[partner 4g+i][row c]
     floatx4 st = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < 2; kb++) st = mfma3_16x16x32(r.ah[kb], r.al[kb], ah[kb], al[kb], st);
+    for (int kb = 0; kb < 2; kb++) st = mfma3_16x16x32(ah[kb], al[kb], rh[kb], rl[kb], st);
+    // codes of partners 4g+i from the lanes holding their entries
     float sv[4];
 #pragma unroll
-    for (int i = 0; i < 4; i++) sv[i] = (r.code_r[i] == rcode_c) ? st[i] * scale : 0.f;
+    for (int i = 0; i < 4; i++) {
+        const int code = static_cast<int>(static_cast<uint32_t>(__shfl(static_cast<int>(pe), 4 * g + i)) >> 16);
+        sv[i] = code == rcode ? st[i] : 0.f;
+    }
     half4 sh, sl;
     split4(sv, 1.0f, sh, sl);
 #pragma unroll
-    for (int dt = 0; dt < 4; dt++) outT[dt] = mfma3_16x16x16(bh[dt], bl[dt], sh, sl, outT[dt]);
+    for (int dt = 0; dt < 4; dt++) outT[dt] = mfma3_16x16x16(bth[dt], btl[dt], sh, sl, outT[dt]);
 }
 
-template <bool BF16, bool STAGED>
-__global__ __launch_bounds__(kPassThreads) void pass_kernel(PassArgs a) {
-    extern __shared__ __align__(16) _Float16 smem[];
-    _Float16 *tile = smem + (threadIdx.x >> 6) * (16 * kTileStride);  // per-wave transpose tile
-    uint32_t *stage = reinterpret_cast<uint32_t *>(smem + kPassWaves * 16 * kTileStride);
+// Write the partial rows of a finished tile: lane (g, c) holds out[row c][16dt +
+// 4g + (0..3)] / oscale.  The tile goes through LDS so that each quarter-wave then
+// stores one whole partial row; the stores are non-temporal (the partials are
+// read once, by the reduction, and should not evict the operands from L2).
+template <bool BF16>
+__device__ __forceinline__ void store_tile(unsigned char *tile, char *part, int m, uint32_t re, int nvalid,
+                                           int q, int cl, int g, int c, const floatx4 outT[4], float oscale) {
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++) lds_st(tile, swz(c, 4 * dt + g, 256), outT[dt]);
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        const int r = 4 * i + q;
+        const uint32_t e = static_cast<uint32_t>(__shfl(static_cast<int>(re), r));
+        floatx4 o = lds_ld<floatx4>(tile, swz(r, cl, 256));
+        if (r < nvalid) {
+            o = o * oscale;
+            const uint32_t row = (e & 0xFFFFu) * static_cast<uint32_t>(m);
+            if constexpr (BF16) {
+                typedef unsigned int uint2v __attribute__((ext_vector_type(2)));
+                uint2v w;
+                w.x = static_cast<uint32_t>(f32_to_bf16(o.x)) | (static_cast<uint32_t>(f32_to_bf16(o.y)) << 16);
+                w.y = static_cast<uint32_t>(f32_to_bf16(o.z)) | (static_cast<uint32_t>(f32_to_bf16(o.w)) << 16);
+                __builtin_nontemporal_store(w, reinterpret_cast<uint2v *>(part + row * (2 * D) + 8 * cl));
+            } else {
+                __builtin_nontemporal_store(o, reinterpret_cast<floatx4 *>(part + row * (4 * D) + 16 * cl));
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+template <bool BF16>
+__global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
+    __shared__ __align__(16) unsigned char tiles_lds[kPassWaves * kTileBytes];
+    __shared__ int32_t plan_beg[kPlanTiles];      // first partner of each row tile's bucket range
+    __shared__ int32_t plan_x[kPlanTiles + 1];    // exclusive prefix of the tiles' sub-tile counts
+    __shared__ int32_t scan_tmp[kPassThreads];
 
     const int64_t units = a.bh * a.m;
     const int64_t id = xcd_remap(blockIdx.x, 2 * units);
@@ -215,92 +305,151 @@ __global__ __launch_bounds__(kPassThreads) void pass_kernel(PassArgs a) {
     // dK: rows = keys (a = V), partners = queries (a' = dY, b = Q)
     // (fields are selected by value: a runtime choice between references into the
     // kernel-argument struct would force a private copy of it)
-    const int64_t n_r = kside ? a.k.n : a.q.n;
-    const int64_t n_p = kside ? a.q.n : a.k.n;
-    const uint32_t *r_ent = kside ? a.k.ent : a.q.ent;
-    const uint32_t *p_ent = kside ? a.q.ent : a.k.ent;
-    const int32_t *p_off = kside ? a.q.off : a.k.off;
-    const _Float16 *a_row = kside ? a.vs : a.dys;
-    const _Float16 *a_par = kside ? a.dys : a.vs;
-    const _Float16 *b_par = kside ? a.qs : a.ks;
-    void *part = kside ? a.pk : a.pq;
+    const int n_r = static_cast<int>(kside ? a.k.n : a.q.n);
+    const int n_p = static_cast<int>(kside ? a.q.n : a.k.n);
+    const uint32_t *rent = (kside ? a.k.ent : a.q.ent) + unit * (n_r + kEntPad);
+    const uint32_t *pent = (kside ? a.q.ent : a.k.ent) + unit * (n_p + kEntPad);
+    const int32_t *poff = (kside ? a.q.off : a.k.off) + unit * ((1 << a.tau) + 1);
+    const _Float16 *arow = (kside ? a.vs : a.dys) + b * n_r * (2 * D);
+    const _Float16 *apar = (kside ? a.dys : a.vs) + b * n_p * (2 * D);
+    const _Float16 *bpar = (kside ? a.qs : a.ks) + b * n_p * (2 * D);
+    // partial row (row r, hash h) starts r*m*64 elements past this base
+    char *part = static_cast<char *>(kside ? a.pk : a.pq) + ((b * n_r) * a.m + h) * D * (BF16 ? 2 : 4);
 
-    const int nbk = (1 << a.tau) + 1;
-    const uint32_t *rent = r_ent + unit * n_r;
-    const uint32_t *pent = p_ent + unit * n_p;
-    const int32_t *poff = p_off + unit * nbk;
-    if constexpr (STAGED) {
-        uint32_t *s_ent = stage;
-        int32_t *s_off = reinterpret_cast<int32_t *>(stage + n_p);
-        for (int64_t i = threadIdx.x; i < n_p; i += kPassThreads) s_ent[i] = pent[i];
-        for (int i = threadIdx.x; i < nbk; i += kPassThreads) s_off[i] = poff[i];
-        __syncthreads();
-        pent = s_ent;
-        poff = s_off;
-    }
-    const int64_t rrow0 = b * n_r, prow0 = b * n_p;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int g = lane >> 4, c = lane & 15;
-    const int64_t tiles = (n_r + 15) >> 4;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = uni(tid >> 6);  // wave-uniform, so the scheduling below stays scalar
+    const int g = lane >> 4, c = lane & 15;  // MFMA layout
+    const int q = lane >> 4, cl = lane & 15; // coalesced layout: quarter q, 16-byte chunk cl
+    unsigned char *tile = tiles_lds + wave * kTileBytes;
+    const int tiles = (n_r + 15) >> 4;
+    const float oscale = a.scale * (1.0f / 256.0f);
 
-    uint32_t e_next = 0;
-    if (wave < tiles && static_cast<int64_t>(wave) * 16 + c < n_r) e_next = rent[static_cast<int64_t>(wave) * 16 + c];
-    for (int64_t t = wave; t < tiles; t += kPassWaves) {
-        const uint32_t e = e_next;
+    for (int T0 = 0; T0 < tiles; T0 += kPlanTiles) {
+        const int nt = min(kPlanTiles, tiles - T0);
+        // ---- plan: the bucket range of every row tile and its number of 16-partner sub-tiles
         {
-            const int64_t tn = t + kPassWaves;
-            e_next = (tn < tiles && tn * 16 + c < n_r) ? rent[tn * 16 + c] : 0u;
-        }
-        const int64_t p0 = t * 16;
-        const int nrow = static_cast<int>(n_r - p0 < 16 ? n_r - p0 : 16);
-        const bool rv_c = c < nrow;
-        const int rcode_c = rv_c ? static_cast<int>(e >> 16) : -2;
-        const int64_t rrow_c = rrow0 + (e & 0xFFFFu);
-        const int cfirst = static_cast<int>(__builtin_amdgcn_readlane(e, 0) >> 16);
-        const int clast = static_cast<int>(__builtin_amdgcn_readlane(e, nrow - 1) >> 16);
-        const int64_t pbeg = poff[cfirst], pend = poff[clast + 1];
-
-        floatx4 outT[4];
+            constexpr int PER = kPlanTiles / kPassThreads;
+            int cnt[PER];
+            int local = 0;
 #pragma unroll
-        for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-        if (pbeg < pend) {
-            PartnerRegs A, B;
-            load_partners(A, pent, pbeg, pend, prow0, a_par, b_par, g, c);
-            half8 ah[2], al[2];
-#pragma unroll
-            for (int kb = 0; kb < 2; kb++) {
-                const int o = kb * 32 + g * 8;
-                ah[kb] = zero_if8(rv_c, *reinterpret_cast<const half8 *>(a_row + rrow_c * (2 * D) + o));
-                al[kb] = zero_if8(rv_c, *reinterpret_cast<const half8 *>(a_row + rrow_c * (2 * D) + D + o));
-            }
-            for (int64_t y0 = pbeg;;) {
-                if (y0 + 16 < pend) load_partners(B, pent, y0 + 16, pend, prow0, a_par, b_par, g, c);
-                compute_partners(A, ah, al, rcode_c, a.scale, tile, g, c, outT);
-                y0 += 16;
-                if (y0 >= pend) break;
-                if (y0 + 16 < pend) load_partners(A, pent, y0 + 16, pend, prow0, a_par, b_par, g, c);
-                compute_partners(B, ah, al, rcode_c, a.scale, tile, g, c, outT);
-                y0 += 16;
-                if (y0 >= pend) break;
-            }
-        }
-        // lane (g, c) holds out[row c][dims 16dt + 4g + (0..3)] * 256
-        if (rv_c) {
-            const int64_t base = ((rrow_c * a.m) + h) * D + 4 * g;
-#pragma unroll
-            for (int dt = 0; dt < 4; dt++) {
-                const float4 o = make_float4(outT[dt][0] * (1.0f / 256.0f), outT[dt][1] * (1.0f / 256.0f),
-                                             outT[dt][2] * (1.0f / 256.0f), outT[dt][3] * (1.0f / 256.0f));
-                if constexpr (BF16) {
-                    uint2 w;
-                    w.x = static_cast<uint32_t>(f32_to_bf16(o.x)) | (static_cast<uint32_t>(f32_to_bf16(o.y)) << 16);
-                    w.y = static_cast<uint32_t>(f32_to_bf16(o.z)) | (static_cast<uint32_t>(f32_to_bf16(o.w)) << 16);
-                    *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(part) + base + dt * 16) = w;
-                } else {
-                    *reinterpret_cast<float4 *>(static_cast<float *>(part) + base + dt * 16) = o;
+            for (int j = 0; j < PER; j++) {
+                const int i = tid * PER + j;
+                cnt[j] = 0;
+                if (i < nt) {
+                    const int r0 = (T0 + i) * 16;
+                    const int nrow = min(16, n_r - r0);
+                    const int cf = static_cast<int>(rent[r0] >> 16), cl2 = static_cast<int>(rent[r0 + nrow - 1] >> 16);
+                    const int pb = poff[cf], pe = poff[cl2 + 1];
+                    plan_beg[i] = pb;
+                    cnt[j] = (pe - pb + 15) >> 4;
                 }
+                local += cnt[j];
+            }
+            scan_tmp[tid] = local;
+            __syncthreads();
+            for (int s = 1; s < kPassThreads; s <<= 1) {
+                const int v = tid >= s ? scan_tmp[tid - s] : 0;
+                __syncthreads();
+                scan_tmp[tid] += v;
+                __syncthreads();
+            }
+            int run = scan_tmp[tid] - local;
+#pragma unroll
+            for (int j = 0; j < PER; j++) {
+                const int i = tid * PER + j;
+                if (i < nt) plan_x[i] = run;
+                run += cnt[j];
+            }
+            if (tid == kPassThreads - 1) plan_x[nt] = scan_tmp[tid];
+            __syncthreads();
+        }
+        // ---- this wave's tiles: a contiguous run holding about a quarter of the sub-tiles
+        const int total = uni(plan_x[nt]);
+        auto lower = [&](int64_t target4) {  // smallest i in [0, nt] with 4 x[i] >= target4
+            int lo = 0, hi = nt;
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (4 * static_cast<int64_t>(uni(plan_x[mid])) >= target4) hi = mid; else lo = mid + 1;
+            }
+            return lo;
+        };
+        const int tlo = wave == 0 ? 0 : lower(static_cast<int64_t>(wave) * total);
+        const int thi = wave == kPassWaves - 1 ? nt : lower(static_cast<int64_t>(wave + 1) * total);
+        const int jbeg = uni(plan_x[tlo]), jend = uni(plan_x[thi]);
+
+        auto row_entry = [&](int t) { return ld<uint32_t>(rent, static_cast<uint32_t>((T0 + t) * 16 + c) * 4); };
+        auto row_count = [&](int t) { return min(16, n_r - (T0 + t) * 16); };
+        // tiles with no partner at all still own partial rows: they are zero
+        auto zero_tiles = [&](int ta, int tb) {
+            const floatx4 z[4] = {};
+            for (int t = ta; t < tb; t++)
+                store_tile<BF16>(tile, part, a.m, row_entry(t), row_count(t), q, cl, g, c, z, 0.f);
+        };
+        // sub-tile j of the run: its tile (searched forward from t) and first partner
+        auto tile_of = [&](int j, int t) {
+            while (uni(plan_x[t + 1]) <= j) t++;
+            return t;
+        };
+        auto first_partner = [&](int j, int t) { return uni(plan_beg[t]) + 16 * (j - uni(plan_x[t])); };
+        auto pent_at = [&](int y) { return ld<uint32_t>(pent, static_cast<uint32_t>(y + c) * 4); };
+
+        if (jbeg == jend) {
+            zero_tiles(tlo, thi);
+        } else {
+            // pipeline: partner entries two sub-tiles ahead, operands one sub-tile ahead
+            // (sub-tiles past the run load from partner 0 and are never computed)
+            int t0 = tile_of(jbeg, tlo);
+            zero_tiles(tlo, t0);
+            const int y0 = first_partner(jbeg, t0);
+            int t1 = t0, y1 = 0;
+            if (jbeg + 1 < jend) { t1 = tile_of(jbeg + 1, t0); y1 = first_partner(jbeg + 1, t1); }
+            uint32_t re0 = row_entry(t0), re1 = row_entry(t1);
+            uint32_t pe0 = pent_at(y0), pe1 = pent_at(y1);
+            half8 rh[2], rl[2];
+            uint4 rn[4];
+            load_row_tile(rn, re0, arow, q, cl);
+            stage_rows(rn, tile, q, cl, g, c, rh, rl);
+            Sub A, B;
+            load_sub(A, pe0, apar, bpar, q, cl);
+            floatx4 outT[4];
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+            // one step: compute sub-tile j from `cur` while loading sub-tile j+1 into
+            // `nxt` and the entries of sub-tile j+2
+            auto step = [&](int j, Sub &cur, Sub &nxt) -> bool {
+                const bool has1 = j + 1 < jend, has2 = j + 2 < jend;
+                int t2 = t1, y2 = 0;
+                if (has2) { t2 = tile_of(j + 2, t1); y2 = first_partner(j + 2, t2); }
+                publish_sub(cur, tile, q, cl);
+                const uint32_t pe2 = pent_at(y2);
+                const uint32_t re2 = row_entry(t2);
+                const bool newtile = !has1 || t1 != t0;
+                if (has1) {
+                    load_sub(nxt, pe1, apar, bpar, q, cl);
+                    if (t1 != t0) load_row_tile(rn, re1, arow, q, cl);
+                }
+                compute_sub(tile, pe0, rh, rl, static_cast<int>(re0 >> 16), g, c, outT);
+                if (newtile) {
+                    store_tile<BF16>(tile, part, a.m, re0, row_count(t0), q, cl, g, c, outT, oscale);
+#pragma unroll
+                    for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+                    zero_tiles(t0 + 1, has1 ? t1 : thi);
+                    if (has1) {
+                        stage_rows(rn, tile, q, cl, g, c, rh, rl);
+                        re0 = re1;
+                    }
+                }
+                t0 = t1;
+                t1 = t2; pe0 = pe1; pe1 = pe2; re1 = re2;
+                return has1;
+            };
+            for (int j = jbeg;; j += 2) {
+                if (!step(j, A, B)) break;
+                if (!step(j + 1, B, A)) break;
             }
         }
+        __syncthreads();  // the plan arrays are rewritten for the next run of tiles
     }
 }
 
@@ -405,16 +554,8 @@ hipError_t zero_output(void *out, int64_t bytes, hipStream_t stream) {
 
 template <bool BF16>
 hipError_t launch_pass(const PassArgs &a, int64_t units, hipStream_t stream) {
-    const int64_t nmax = a.q.n > a.k.n ? a.q.n : a.k.n;
-    const size_t stage = (static_cast<size_t>(nmax) + (static_cast<size_t>(1) << a.tau) + 1) * 4;
-    const size_t tiles = static_cast<size_t>(kPassWaves) * 16 * kTileStride * 2;
     KernelTimer timer("pass_kernel", stream);
-    if (stage <= kPassStageBudget)
-        hipLaunchKernelGGL((pass_kernel<BF16, true>), dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads),
-                           tiles + stage, stream, a);
-    else
-        hipLaunchKernelGGL((pass_kernel<BF16, false>), dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads),
-                           tiles, stream, a);
+    hipLaunchKernelGGL((pass_kernel<BF16>), dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -428,8 +569,8 @@ BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, 
     size_t o = 0;
     L.qoff = o; o = align_up(o + units * nb * 4);
     L.koff = o; o = align_up(o + units * nb * 4);
-    L.qent = o; o = align_up(o + units * n_q * 4);
-    L.kent = o; o = align_up(o + units * n_k * 4);
+    L.qent = o; o = align_up(o + units * (n_q + kEntPad) * 4);
+    L.kent = o; o = align_up(o + units * (n_k + kEntPad) * 4);
     L.qs = o; o = align_up(o + static_cast<size_t>(bh) * n_q * D * 4);
     L.dys = o; o = align_up(o + static_cast<size_t>(bh) * n_q * D * 4);
     L.ks = o; o = align_up(o + static_cast<size_t>(bh) * n_k * D * 4);
