@@ -49,7 +49,11 @@ constexpr int kPassWaves = kPassThreads / 64;
 constexpr int kReduceThreads = 256;
 constexpr int kTileBytes = 16 * 512;   // LDS bytes of one wave's operand tile
 constexpr int kPlanTiles = 1024;       // row tiles planned per run (multiple of kPassThreads)
-constexpr int kEntPad = 16;            // sentinel entries after each unit's sorted entries
+constexpr int kEntPad = 16;            // at least this many sentinel entries after each unit's sorted entries
+
+// Entries per unit: n rounded up to a multiple of 4 (16-byte aligned units), then
+// at least kEntPad sentinels.
+__host__ __device__ constexpr int64_t ent_stride(int64_t n) { return ((n + 3) & ~int64_t{3}) + kEntPad; }
 constexpr uint32_t kSentinel = 0xFFFF0000u;  // code 0xFFFF (no real code), row 0
 
 // ---------------------------------------------------------------- counting sort
@@ -69,7 +73,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
     const int64_t n = kside ? n_k : n_q;
     const uint16_t *codes = (kside ? kcodes : qcodes) + b * n * m + h;
     int32_t *off = (kside ? koff : qoff) + unit * ((1 << tau) + 1);
-    uint32_t *ent = (kside ? kent : qent) + unit * (n + kEntPad);
+    uint32_t *ent = (kside ? kent : qent) + unit * ent_stride(n);
     const int B = 1 << tau;
     const int tid = threadIdx.x;
 
@@ -106,12 +110,12 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
         const int32_t pos = atomicAdd(&cnt[c], 1);
         ent[pos] = (c << 16) | static_cast<uint32_t>(i);
     }
-    if (tid < kEntPad) ent[n + tid] = kSentinel;
+    for (int64_t i = n + tid; i < ent_stride(n); i += kSortThreads) ent[i] = kSentinel;
 }
 
 // ---------------------------------------------------------------- pair passes
 struct Side {
-    const uint32_t *ent;  // [units][n + kEntPad]: (code << 16 | row) in bucket order, then sentinels
+    const uint32_t *ent;  // [units][ent_stride(n)]: (code << 16 | row) in bucket order, then sentinels
     const int32_t *off;   // [units][2^tau + 1] bucket offsets
     int64_t n;
 };
@@ -139,13 +143,15 @@ __device__ __forceinline__ T ld(const void *base, uint32_t byte_off) {
 // loads are coalesced: the 16 lanes of a quarter-wave read 256 contiguous bytes
 // of one row (where an MFMA-layout load would touch 16 rows per quarter-wave and
 // make 4x as many cache requests).  16-byte chunks are XOR-swizzled within a row
-// so that both the MFMA-layout reads (16 rows, one chunk each) and the transpose
-// reads (8 rows x 32 bytes) hit distinct banks.
+// so that the MFMA-layout reads (16 rows, one chunk each), the transpose reads
+// (4 or 8 rows x 32 bytes) and the row writes all hit distinct banks.
 //   partner tile: 16 rows x 512 B  [a' hi | a' lo | b hi | b lo], 128 B each
 //   row tile:     16 rows x 256 B  [a hi | a lo]
 //   out tile:     16 rows x 256 B  (64 fp32)
 __device__ __forceinline__ uint32_t swz(int row, int chunk, int row_bytes) {
-    const int f = ((row & 7) << 1) | ((row >> 3) & 1);
+    // f permutes 0..15; f(r) mod 8 differs within every aligned group of 8 rows and
+    // f(r) >> 1 differs within every aligned group of 8 (so also of 4) rows
+    const int f = ((2 * row + ((row >> 2) & 1)) & 15) ^ ((row >> 3) & 1);
     return static_cast<uint32_t>(row * row_bytes + ((chunk ^ f) << 4));
 }
 
@@ -159,32 +165,32 @@ __device__ __forceinline__ void lds_st(unsigned char *base, uint32_t off, const 
 }
 
 // One 16-partner sub-tile as loaded: lane l holds 16-byte chunk (l & 15) of
-// partner 4i + (l >> 4) of a' (a[i]) and of b (b[i]).
+// partner 4(l >> 4) + i of a' (a[i]) and of b (b[i]).
 struct Sub {
     uint4 a[4], b[4];
 };
 
-// `pe` is this lane's entry of partner (l & 15) (code << 16 | row); entries past
-// the unit's end are sentinels (row 0, an impossible code), so every load is in
-// bounds and a partner outside the tile's buckets is masked by its code.
-__device__ __forceinline__ void load_sub(Sub &s, uint32_t pe, const _Float16 *apar, const _Float16 *bpar, int q,
+// `pe` holds this lane's entries of partners 4q .. 4q+3 (code << 16 | row), one
+// aligned 16-byte load.  Entries past the unit's end are sentinels (row 0, an
+// impossible code), so every load is in bounds and a partner outside the tile's
+// buckets is masked by its code.
+__device__ __forceinline__ void load_sub(Sub &s, const uint4 &pe, const _Float16 *apar, const _Float16 *bpar,
                                          int cl) {
+    const uint32_t e[4] = {pe.x, pe.y, pe.z, pe.w};
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-        const uint32_t e = static_cast<uint32_t>(__shfl(static_cast<int>(pe), 4 * i + q));
-        const uint32_t off = (e & 0xFFFFu) * (4 * D) + 16 * cl;
+        const uint32_t off = (e[i] & 0xFFFFu) * (4 * D) + 16 * cl;
         s.a[i] = ld<uint4>(apar, off);
         s.b[i] = ld<uint4>(bpar, off);
     }
 }
 
-// The 16 rows of a tile (row entry `re` of row (l & 15)) as loaded.
-__device__ __forceinline__ void load_row_tile(uint4 r[4], uint32_t re, const _Float16 *arow, int q, int cl) {
+// The 16 rows of a tile as loaded: lane l holds chunk (l & 15) of row 4(l >> 4) + i;
+// `re4` holds the entries of rows 4q .. 4q+3.
+__device__ __forceinline__ void load_row_tile(uint4 r[4], const uint4 &re4, const _Float16 *arow, int cl) {
+    const uint32_t e[4] = {re4.x, re4.y, re4.z, re4.w};
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-        const uint32_t e = static_cast<uint32_t>(__shfl(static_cast<int>(re), 4 * i + q));
-        r[i] = ld<uint4>(arow, (e & 0xFFFFu) * (4 * D) + 16 * cl);
-    }
+    for (int i = 0; i < 4; i++) r[i] = ld<uint4>(arow, (e[i] & 0xFFFFu) * (4 * D) + 16 * cl);
 }
 
 // Rows through the tile into the MFMA B-operand layout of S^T: lane (g, c) gets
@@ -192,7 +198,7 @@ __device__ __forceinline__ void load_row_tile(uint4 r[4], uint32_t re, const _Fl
 __device__ __forceinline__ void stage_rows(const uint4 r[4], unsigned char *tile, int q, int cl, int g, int c,
                                            half8 rh[2], half8 rl[2]) {
 #pragma unroll
-    for (int i = 0; i < 4; i++) lds_st(tile, swz(4 * i + q, cl, 256), r[i]);
+    for (int i = 0; i < 4; i++) lds_st(tile, swz(4 * q + i, cl, 256), r[i]);
 #pragma unroll
     for (int kb = 0; kb < 2; kb++) {
         rh[kb] = lds_ld<half8>(tile, swz(c, kb * 4 + g, 256));
@@ -211,14 +217,15 @@ __device__ __forceinline__ half4 tr_load(const unsigned char *p) {
 __device__ __forceinline__ void publish_sub(const Sub &s, unsigned char *tile, int q, int cl) {
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-        lds_st(tile, swz(4 * i + q, cl, 512), s.a[i]);
-        lds_st(tile, swz(4 * i + q, 16 + cl, 512), s.b[i]);
+        lds_st(tile, swz(4 * q + i, cl, 512), s.a[i]);
+        lds_st(tile, swz(4 * q + i, 16 + cl, 512), s.b[i]);
     }
 }
 
 // out^T += B_y^T S^T for the sub-tile in the tile: S^T = A'_y A_x^T masked by
-// code equality.  `pe` as in load_sub.
-__device__ __forceinline__ void compute_sub(const unsigned char *tile, uint32_t pe, const half8 rh[2],
+// code equality.  `pe` as in load_sub: in the MFMA layout it holds the entries of
+// exactly the partners 4g+i whose S^T values this lane computes.
+__device__ __forceinline__ void compute_sub(const unsigned char *tile, const uint4 &pe, const half8 rh[2],
                                             const half8 rl[2], int rcode, int g, int c, floatx4 outT[4]) {
     // A'_y in the A-operand layout: lane (g, c) = partner c, dims kb*32 + 8g + [0, 8)
     half8 ah[2], al[2];
@@ -243,13 +250,10 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, uint32_t 
     floatx4 st = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < 2; kb++) st = mfma3_16x16x32(ah[kb], al[kb], rh[kb], rl[kb], st);
-    // codes of partners 4g+i from the lanes holding their entries
+    const uint32_t e[4] = {pe.x, pe.y, pe.z, pe.w};
     float sv[4];
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-        const int code = static_cast<int>(static_cast<uint32_t>(__shfl(static_cast<int>(pe), 4 * g + i)) >> 16);
-        sv[i] = code == rcode ? st[i] : 0.f;
-    }
+    for (int i = 0; i < 4; i++) sv[i] = static_cast<int>(e[i] >> 16) == rcode ? st[i] : 0.f;
     half4 sh, sl;
     split4(sv, 1.0f, sh, sl);
 #pragma unroll
@@ -261,18 +265,18 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, uint32_t 
 // stores one whole partial row; the stores are non-temporal (the partials are
 // read once, by the reduction, and should not evict the operands from L2).
 template <bool BF16>
-__device__ __forceinline__ void store_tile(unsigned char *tile, char *part, int m, uint32_t re, int nvalid,
+__device__ __forceinline__ void store_tile(unsigned char *tile, char *part, int m, const uint4 &re4, int nvalid,
                                            int q, int cl, int g, int c, const floatx4 outT[4], float oscale) {
 #pragma unroll
     for (int dt = 0; dt < 4; dt++) lds_st(tile, swz(c, 4 * dt + g, 256), outT[dt]);
+    const uint32_t e[4] = {re4.x, re4.y, re4.z, re4.w};
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-        const int r = 4 * i + q;
-        const uint32_t e = static_cast<uint32_t>(__shfl(static_cast<int>(re), r));
+        const int r = 4 * q + i;
         floatx4 o = lds_ld<floatx4>(tile, swz(r, cl, 256));
         if (r < nvalid) {
             o = o * oscale;
-            const uint32_t row = (e & 0xFFFFu) * static_cast<uint32_t>(m);
+            const uint32_t row = (e[i] & 0xFFFFu) * static_cast<uint32_t>(m);
             if constexpr (BF16) {
                 typedef unsigned int uint2v __attribute__((ext_vector_type(2)));
                 uint2v w;
@@ -307,8 +311,8 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
     // kernel-argument struct would force a private copy of it)
     const int n_r = static_cast<int>(kside ? a.k.n : a.q.n);
     const int n_p = static_cast<int>(kside ? a.q.n : a.k.n);
-    const uint32_t *rent = (kside ? a.k.ent : a.q.ent) + unit * (n_r + kEntPad);
-    const uint32_t *pent = (kside ? a.q.ent : a.k.ent) + unit * (n_p + kEntPad);
+    const uint32_t *rent = (kside ? a.k.ent : a.q.ent) + unit * ent_stride(n_r);
+    const uint32_t *pent = (kside ? a.q.ent : a.k.ent) + unit * ent_stride(n_p);
     const int32_t *poff = (kside ? a.q.off : a.k.off) + unit * ((1 << a.tau) + 1);
     const _Float16 *arow = (kside ? a.vs : a.dys) + b * n_r * (2 * D);
     const _Float16 *apar = (kside ? a.dys : a.vs) + b * n_p * (2 * D);
@@ -339,7 +343,9 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
                     const int r0 = (T0 + i) * 16;
                     const int nrow = min(16, n_r - r0);
                     const int cf = static_cast<int>(rent[r0] >> 16), cl2 = static_cast<int>(rent[r0 + nrow - 1] >> 16);
-                    const int pb = poff[cf], pe = poff[cl2 + 1];
+                    // start at a multiple of 4 (aligned entry loads); the extra
+                    // partners belong to earlier buckets and are masked by their codes
+                    const int pb = poff[cf] & ~3, pe = poff[cl2 + 1];
                     plan_beg[i] = pb;
                     cnt[j] = (pe - pb + 15) >> 4;
                 }
@@ -378,12 +384,13 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
         const int jbeg = uni(plan_x[tlo]), jend = uni(plan_x[thi]);
 
         auto row_entry = [&](int t) { return ld<uint32_t>(rent, static_cast<uint32_t>((T0 + t) * 16 + c) * 4); };
+        auto row_entries4 = [&](int t) { return ld<uint4>(rent, static_cast<uint32_t>((T0 + t) * 16 + 4 * q) * 4); };
         auto row_count = [&](int t) { return min(16, n_r - (T0 + t) * 16); };
         // tiles with no partner at all still own partial rows: they are zero
         auto zero_tiles = [&](int ta, int tb) {
             const floatx4 z[4] = {};
             for (int t = ta; t < tb; t++)
-                store_tile<BF16>(tile, part, a.m, row_entry(t), row_count(t), q, cl, g, c, z, 0.f);
+                store_tile<BF16>(tile, part, a.m, row_entries4(t), row_count(t), q, cl, g, c, z, 0.f);
         };
         // sub-tile j of the run: its tile (searched forward from t) and first partner
         auto tile_of = [&](int j, int t) {
@@ -391,7 +398,7 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
             return t;
         };
         auto first_partner = [&](int j, int t) { return uni(plan_beg[t]) + 16 * (j - uni(plan_x[t])); };
-        auto pent_at = [&](int y) { return ld<uint32_t>(pent, static_cast<uint32_t>(y + c) * 4); };
+        auto pent4 = [&](int y) { return ld<uint4>(pent, static_cast<uint32_t>(y + 4 * q) * 4); };
 
         if (jbeg == jend) {
             zero_tiles(tlo, thi);
@@ -404,49 +411,49 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
             int t1 = t0, y1 = 0;
             if (jbeg + 1 < jend) { t1 = tile_of(jbeg + 1, t0); y1 = first_partner(jbeg + 1, t1); }
             uint32_t re0 = row_entry(t0), re1 = row_entry(t1);
-            uint32_t pe0 = pent_at(y0), pe1 = pent_at(y1);
+            uint4 r40 = row_entries4(t0), r41 = row_entries4(t1);
+            uint4 pe0 = pent4(y0), pe1 = pent4(y1);
             half8 rh[2], rl[2];
             uint4 rn[4];
-            load_row_tile(rn, re0, arow, q, cl);
+            load_row_tile(rn, r40, arow, cl);
             stage_rows(rn, tile, q, cl, g, c, rh, rl);
-            Sub A, B;
-            load_sub(A, pe0, apar, bpar, q, cl);
+            // one operand buffer: a sub-tile's registers are reloaded with the next
+            // sub-tile as soon as they have been written to the tile
+            Sub S;
+            load_sub(S, pe0, apar, bpar, cl);
             floatx4 outT[4];
 #pragma unroll
             for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-            // one step: compute sub-tile j from `cur` while loading sub-tile j+1 into
-            // `nxt` and the entries of sub-tile j+2
-            auto step = [&](int j, Sub &cur, Sub &nxt) -> bool {
+            for (int j = jbeg;; j++) {
                 const bool has1 = j + 1 < jend, has2 = j + 2 < jend;
                 int t2 = t1, y2 = 0;
                 if (has2) { t2 = tile_of(j + 2, t1); y2 = first_partner(j + 2, t2); }
-                publish_sub(cur, tile, q, cl);
-                const uint32_t pe2 = pent_at(y2);
-                const uint32_t re2 = row_entry(t2);
+                publish_sub(S, tile, q, cl);
+                const uint4 pe2 = pent4(y2);
+                uint32_t re2 = re1;
+                uint4 r42 = r41;
+                if (t2 != t1) { re2 = row_entry(t2); r42 = row_entries4(t2); }
                 const bool newtile = !has1 || t1 != t0;
                 if (has1) {
-                    load_sub(nxt, pe1, apar, bpar, q, cl);
-                    if (t1 != t0) load_row_tile(rn, re1, arow, q, cl);
+                    load_sub(S, pe1, apar, bpar, cl);
+                    if (t1 != t0) load_row_tile(rn, r41, arow, cl);
                 }
                 compute_sub(tile, pe0, rh, rl, static_cast<int>(re0 >> 16), g, c, outT);
                 if (newtile) {
-                    store_tile<BF16>(tile, part, a.m, re0, row_count(t0), q, cl, g, c, outT, oscale);
+                    store_tile<BF16>(tile, part, a.m, r40, row_count(t0), q, cl, g, c, outT, oscale);
 #pragma unroll
                     for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
                     zero_tiles(t0 + 1, has1 ? t1 : thi);
                     if (has1) {
                         stage_rows(rn, tile, q, cl, g, c, rh, rl);
                         re0 = re1;
+                        r40 = r41;
                     }
                 }
+                if (!has1) break;
                 t0 = t1;
-                t1 = t2; pe0 = pe1; pe1 = pe2; re1 = re2;
-                return has1;
-            };
-            for (int j = jbeg;; j += 2) {
-                if (!step(j, A, B)) break;
-                if (!step(j + 1, B, A)) break;
+                t1 = t2; pe0 = pe1; pe1 = pe2; re1 = re2; r41 = r42;
             }
         }
         __syncthreads();  // the plan arrays are rewritten for the next run of tiles
@@ -569,8 +576,8 @@ BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, 
     size_t o = 0;
     L.qoff = o; o = align_up(o + units * nb * 4);
     L.koff = o; o = align_up(o + units * nb * 4);
-    L.qent = o; o = align_up(o + units * (n_q + kEntPad) * 4);
-    L.kent = o; o = align_up(o + units * (n_k + kEntPad) * 4);
+    L.qent = o; o = align_up(o + units * ent_stride(n_q) * 4);
+    L.kent = o; o = align_up(o + units * ent_stride(n_k) * 4);
     L.qs = o; o = align_up(o + static_cast<size_t>(bh) * n_q * D * 4);
     L.dys = o; o = align_up(o + static_cast<size_t>(bh) * n_q * D * 4);
     L.ks = o; o = align_up(o + static_cast<size_t>(bh) * n_k * D * 4);
