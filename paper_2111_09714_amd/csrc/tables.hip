@@ -149,8 +149,15 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
     const int k = scale_exp;
 
     // lane roles
-    int GP = 1;
-    while (GP < G) GP <<= 1;               // hashes rounded up to a power of two
+    // hashes rounded up to a power of two: fixed by (DS, KM) for the one- and
+    // two-key step forms (the host picks them exactly for those products), so their
+    // lane roles below are compile-time constants
+    constexpr int GPC = KM == 0 ? 2 * 64 / DS : (KM == 1 ? 64 / DS : 0);
+    int GP = GPC;
+    if constexpr (GPC == 0) {
+        GP = 1;
+        while (GP < G) GP <<= 1;
+    }
     const int CPK = GP * P;                // (hash, word) combos per key
     const int KPI = CPK <= 64 ? 64 / CPK : 1;   // keys per instruction
     const int NI = CPK <= 64 ? 1 : CPK / 64;    // instructions per key (<= 2)
@@ -204,7 +211,7 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
             const int lane_off = hh * P + pp;
             // codes are fetched kAhead steps ahead of their use, from a clamped (always
             // valid) row, into a ring of registers; validity is decided at use
-            constexpr int kAhead = 16;
+            constexpr int kAhead = 32;
             static_assert(SPC % kAhead == 0, "prefetch distance must divide the chunk");
             const uint32_t last = static_cast<uint32_t>(nsrc - 1), mm = static_cast<uint32_t>(a.m);
             const uint32_t hcl = hok ? static_cast<uint32_t>(hh) : 0u;
@@ -323,7 +330,7 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
         __syncthreads();
 
         // ---- gather: out[i][slice*DS + d] (+)= sum_h table[code_h(i)][h][d]
-        // (the codes of the wave's next query group are fetched before this one is summed)
+        // (the codes of the wave's next few query groups are fetched ahead)
         {
             int hh[8];
 #pragma unroll
@@ -332,76 +339,93 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
             // validity applied afterwards, so the loads stay in flight
             const uint16_t *qbase = a.dst_codes + dst_row0 * a.m + h0;
             const uint32_t qlast = static_cast<uint32_t>(a.n_dst - 1), mm = static_cast<uint32_t>(a.m);
+            // (raw codes only: a per-lane select on a loaded value makes the compiler
+            // branch around the load and wait for it; validity is kept apart)
             auto fetch = [&](int cc[8], int64_t i0) {
                 const int64_t i = i0 + gq;
                 const uint32_t icl = i < a.n_dst ? static_cast<uint32_t>(i) : qlast;
 #pragma unroll
                 for (int t = 0; t < 8; t++) {
                     if (t < HL) {
-                        const bool ok = i < a.n_dst && hh[t] < gcount;
                         const uint32_t hcl = hh[t] < gcount ? static_cast<uint32_t>(hh[t]) : 0u;
-                        const int v = qbase[icl * mm + hcl];
-                        cc[t] = ok ? (v & cmask) : -1;
-                    } else {
-                        cc[t] = -1;
+                        cc[t] = qbase[icl * mm + hcl];
                     }
                 }
             };
+            // bit t: query i0+gq exists and its lane's hash t exists
+            auto valid = [&](int64_t i0) {
+                const bool qok = i0 + gq < a.n_dst;
+                uint32_t mask = 0;
+#pragma unroll
+                for (int t = 0; t < 8; t++) mask |= (qok && t < HL && hh[t] < gcount) ? (1u << t) : 0u;
+                return mask;
+            };
             const int64_t step = static_cast<int64_t>(kTableWaves) * QPI;
-            int cA[8], cB[8];
-            fetch(cA, static_cast<int64_t>(wave) * QPI);
-            for (int64_t i0 = static_cast<int64_t>(wave) * QPI; i0 < a.n_dst; i0 += step) {
-                fetch(cB, i0 + step);
-                const int64_t i = i0 + gq;
-                const bool qok = i < a.n_dst;
-                float acc[DS];
+            // codes of the next kGD query groups are in flight while one is summed
+            constexpr int kGD = 2;
+            int cR[kGD][8];
 #pragma unroll
-                for (int d = 0; d < DS; d++) acc[d] = 0.f;
+            for (int u = 0; u < kGD; u++) fetch(cR[u], static_cast<int64_t>(wave) * QPI + u * step);
+            for (int64_t ib = static_cast<int64_t>(wave) * QPI; ib < a.n_dst; ib += kGD * step) {
 #pragma unroll
-                for (int t = 0; t < 8; t++) {
-                    if (cA[t] >= 0) {
-                        const float *row = reinterpret_cast<const float *>(tab) + (cA[t] * G + hh[t]) * DS;
-                        if constexpr (DS == 2) {
-                            const float2 x = *reinterpret_cast<const float2 *>(row);
-                            acc[0] += x.x;
-                            acc[1] += x.y;
-                        } else {
+                for (int u = 0; u < kGD; u++) {
+                    const int64_t i0 = ib + u * step;
+                    if (i0 >= a.n_dst) break;
+                    const int64_t i = i0 + gq;
+                    const bool qok = i < a.n_dst;
+                    float acc[DS];
 #pragma unroll
-                            for (int d = 0; d < DS; d += 4) {
-                                const float4 x = *reinterpret_cast<const float4 *>(row + d);
-                                acc[d] += x.x;
-                                acc[d + 1] += x.y;
-                                acc[d + 2] += x.z;
-                                acc[d + 3] += x.w;
+                    for (int d = 0; d < DS; d++) acc[d] = 0.f;
+                    // every lane reads a row (invalid ones read a clamped row and weight
+                    // it by 0): no divergent branch between the reads
+                    const uint32_t vmask = valid(i0);
+#pragma unroll
+                    for (int t = 0; t < 8; t++) {
+                        if (t < HL) {
+                            const float w = ((vmask >> t) & 1u) ? 1.f : 0.f;
+                            const int hcl = min(hh[t], gcount - 1);
+                            const float *row = reinterpret_cast<const float *>(tab) + ((cR[u][t] & cmask) * G + hcl) * DS;
+                            if constexpr (DS == 2) {
+                                const float2 x = *reinterpret_cast<const float2 *>(row);
+                                acc[0] = fmaf(x.x, w, acc[0]);
+                                acc[1] = fmaf(x.y, w, acc[1]);
+                            } else {
+#pragma unroll
+                                for (int d = 0; d < DS; d += 4) {
+                                    const float4 x = *reinterpret_cast<const float4 *>(row + d);
+                                    acc[d] = fmaf(x.x, w, acc[d]);
+                                    acc[d + 1] = fmaf(x.y, w, acc[d + 1]);
+                                    acc[d + 2] = fmaf(x.z, w, acc[d + 2]);
+                                    acc[d + 3] = fmaf(x.w, w, acc[d + 3]);
+                                }
+                            }
+                        }
+                    }
+                    fetch(cR[u], i0 + kGD * step);
+#pragma unroll
+                    for (int d = 0; d < DS; d++) acc[d] = group_sum(acc[d], L);
+                    if (qok) {
+                        const int64_t obase = (dst_row0 + i) * D + slice * DS;
+#pragma unroll
+                        for (int d = 0; d < DS; d++) {
+                            if (d % L != gr) continue;
+                            const float v = acc[d];
+                            if (ngroups == 1) {
+                                if constexpr (BF16)
+                                    static_cast<uint16_t *>(a.out)[obase + d] = f32_to_bf16(v);
+                                else
+                                    static_cast<float *>(a.out)[obase + d] = v;
+                            } else {
+                                // the same lane owns this element in every group
+                                const float prev = grp == 0 ? 0.f : a.acc[obase + d];
+                                if (grp == ngroups - 1 && BF16)
+                                    static_cast<uint16_t *>(a.out)[obase + d] = f32_to_bf16(prev + v);
+                                else
+                                    a.acc[obase + d] = prev + v;
                             }
                         }
                     }
                 }
-#pragma unroll
-                for (int d = 0; d < DS; d++) acc[d] = group_sum(acc[d], L);
-                if (qok) {
-                    const int64_t obase = (dst_row0 + i) * D + slice * DS;
-#pragma unroll
-                    for (int d = 0; d < DS; d++) {
-                        if (d % L != gr) continue;
-                        const float v = acc[d];
-                        if (ngroups == 1) {
-                            if constexpr (BF16)
-                                static_cast<uint16_t *>(a.out)[obase + d] = f32_to_bf16(v);
-                            else
-                                static_cast<float *>(a.out)[obase + d] = v;
-                        } else {
-                            // the same lane owns this element in every group
-                            const float prev = grp == 0 ? 0.f : a.acc[obase + d];
-                            if (grp == ngroups - 1 && BF16)
-                                static_cast<uint16_t *>(a.out)[obase + d] = f32_to_bf16(prev + v);
-                            else
-                                a.acc[obase + d] = prev + v;
-                        }
-                    }
-                }
-#pragma unroll
-                for (int t = 0; t < 8; t++) cA[t] = cB[t];
             }
         }
         __syncthreads();
