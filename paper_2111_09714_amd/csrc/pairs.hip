@@ -48,7 +48,7 @@ constexpr int kPassThreads = 256;
 constexpr int kPassWaves = kPassThreads / 64;
 constexpr int kReduceThreads = 256;
 constexpr int kTileBytes = 16 * 512;   // LDS bytes of one wave's operand tile
-constexpr int kPlanTiles = 1024;       // row tiles planned per run (multiple of kPassThreads)
+constexpr int kPlanTiles = 256;        // row tiles planned per run (multiple of kPassThreads)
 constexpr int kEntPad = 16;            // at least this many sentinel entries after each unit's sorted entries
 
 // Entries per unit: n rounded up to a multiple of 4 (16-byte aligned units), then
@@ -125,7 +125,8 @@ struct PassArgs {
     // Q, K, V, dY split into fp16 (hi, lo) pairs by split_kernel: row r holds 64 hi
     // halves then 64 lo halves; Q and K are scaled by 2^8 first
     const _Float16 *qs, *ks, *vs, *dys;
-    void *pq, *pk;                   // partials [bh][n][m][64] (fp32, or bf16 for bf16 storage)
+    int16_t *pq, *pk;                // partials [bh][n][m][64] int16 mantissas
+    int8_t *eq, *ek;                 // their exponents [bh][m][n] (one block writes one n-byte run)
     int64_t bh;
     int m, tau;
     float scale;                     // tau / (2m)
@@ -260,44 +261,62 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uin
     for (int dt = 0; dt < 4; dt++) outT[dt] = mfma3_16x16x16(bth[dt], btl[dt], sh, sl, outT[dt]);
 }
 
+// Max over each aligned group of 16 lanes (one partial row in the coalesced layout).
+__device__ __forceinline__ float row16_max(float x) {
+    x = fmaxf(x, dpp_mov<0xB1>(x));   // quad_perm [1,0,3,2]
+    x = fmaxf(x, dpp_mov<0x4E>(x));   // quad_perm [2,3,0,1]
+    x = fmaxf(x, dpp_mov<0x141>(x));  // row_half_mirror
+    x = fmaxf(x, dpp_mov<0x140>(x));  // row_mirror
+    return x;
+}
+
 // Write the partial rows of a finished tile: lane (g, c) holds out[row c][16dt +
 // 4g + (0..3)] / oscale.  The tile goes through LDS so that each quarter-wave then
-// stores one whole partial row; the stores are non-temporal (the partials are
-// read once, by the reduction, and should not evict the operands from L2).
-template <bool BF16>
-__device__ __forceinline__ void store_tile(unsigned char *tile, char *part, int m, const uint4 &re4, int nvalid,
-                                           int q, int cl, int g, int c, const floatx4 outT[4], float oscale) {
+// stores one whole partial row.  A partial row is stored in block floating point:
+// 64 int16 mantissas and one exponent e with max|value| < 2^e, value = mantissa *
+// 2^(e-15) (rounding error at most 2^(e-16), i.e. 2^-15 of the row's largest
+// value).  The stores are non-temporal: the partials are read once, by the
+// reduction, and should not evict the operands from L2.
+__device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, int8_t *pexp, int m,
+                                           const uint4 &re4, int nvalid, int q, int cl, int g, int c,
+                                           const floatx4 outT[4], float oscale) {
 #pragma unroll
     for (int dt = 0; dt < 4; dt++) lds_st(tile, swz(c, 4 * dt + g, 256), outT[dt]);
-    const uint32_t e[4] = {re4.x, re4.y, re4.z, re4.w};
+    const uint32_t e4[4] = {re4.x, re4.y, re4.z, re4.w};
 #pragma unroll
     for (int i = 0; i < 4; i++) {
         const int r = 4 * q + i;
-        floatx4 o = lds_ld<floatx4>(tile, swz(r, cl, 256));
+        const floatx4 o = lds_ld<floatx4>(tile, swz(r, cl, 256)) * oscale;
+        const float mx = row16_max(fmaxf(fmaxf(fabsf(o.x), fabsf(o.y)), fmaxf(fabsf(o.z), fabsf(o.w))));
+        // e with mx < 2^e from the biased exponent field (mx is finite; 0 gives a tiny
+        // e whose mantissas are all 0), clamped so that 2^(15-e) stays a normal float
+        const int e = min(max(static_cast<int>((__float_as_uint(mx) >> 23) & 0xFFu) - 126, -100), 100);
+        const float sc = __uint_as_float(static_cast<uint32_t>(15 - e + 127) << 23);
+        // round to nearest, clamp (|x * sc| < 32768 rounds to at most 32768) and pack
+        auto q16 = [&](float x) { return min(max(static_cast<int>(rintf(x * sc)), -32767), 32767); };
+        auto pk = [&](float x0, float x1) {
+            return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pk_i16(q16(x0), q16(x1)));
+        };
+        typedef unsigned int uint2v __attribute__((ext_vector_type(2)));
+        uint2v w;
+        w.x = pk(o.x, o.y);
+        w.y = pk(o.z, o.w);
         if (r < nvalid) {
-            o = o * oscale;
-            const uint32_t row = (e[i] & 0xFFFFu) * static_cast<uint32_t>(m);
-            if constexpr (BF16) {
-                typedef unsigned int uint2v __attribute__((ext_vector_type(2)));
-                uint2v w;
-                w.x = static_cast<uint32_t>(f32_to_bf16(o.x)) | (static_cast<uint32_t>(f32_to_bf16(o.y)) << 16);
-                w.y = static_cast<uint32_t>(f32_to_bf16(o.z)) | (static_cast<uint32_t>(f32_to_bf16(o.w)) << 16);
-                __builtin_nontemporal_store(w, reinterpret_cast<uint2v *>(part + row * (2 * D) + 8 * cl));
-            } else {
-                __builtin_nontemporal_store(o, reinterpret_cast<floatx4 *>(part + row * (4 * D) + 16 * cl));
-            }
+            const uint32_t row = e4[i] & 0xFFFFu;
+            __builtin_nontemporal_store(w, reinterpret_cast<uint2v *>(part + (row * static_cast<uint32_t>(m)) * D) + cl);
+            if (cl == 0) pexp[row] = static_cast<int8_t>(e);
         }
     }
 }
 
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
-template <bool BF16>
 __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
     __shared__ __align__(16) unsigned char tiles_lds[kPassWaves * kTileBytes];
     __shared__ int32_t plan_beg[kPlanTiles];      // first partner of each row tile's bucket range
     __shared__ int32_t plan_x[kPlanTiles + 1];    // exclusive prefix of the tiles' sub-tile counts
     __shared__ int32_t scan_tmp[kPassThreads];
+    __shared__ __align__(16) uint32_t row_ent[kPlanTiles * 16];  // the run's sorted row entries
 
     const int64_t units = a.bh * a.m;
     const int64_t id = xcd_remap(blockIdx.x, 2 * units);
@@ -317,8 +336,10 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
     const _Float16 *arow = (kside ? a.vs : a.dys) + b * n_r * (2 * D);
     const _Float16 *apar = (kside ? a.dys : a.vs) + b * n_p * (2 * D);
     const _Float16 *bpar = (kside ? a.qs : a.ks) + b * n_p * (2 * D);
-    // partial row (row r, hash h) starts r*m*64 elements past this base
-    char *part = static_cast<char *>(kside ? a.pk : a.pq) + ((b * n_r) * a.m + h) * D * (BF16 ? 2 : 4);
+    // partial row (row r, hash h) starts r*m*64 elements past this base, its
+    // exponent r bytes past the other
+    int16_t *part = (kside ? a.pk : a.pq) + ((b * n_r) * a.m + h) * D;
+    int8_t *pexp = (kside ? a.ek : a.eq) + (b * a.m + h) * n_r;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = uni(tid >> 6);  // wave-uniform, so the scheduling below stays scalar
@@ -367,6 +388,9 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
                 run += cnt[j];
             }
             if (tid == kPassThreads - 1) plan_x[nt] = scan_tmp[tid];
+            // the run's row entries (16-byte copies; entries past n_r are sentinels)
+            for (int i = tid; i < nt * 4; i += kPassThreads)
+                reinterpret_cast<uint4 *>(row_ent)[i] = ld<uint4>(rent, static_cast<uint32_t>(T0 * 16 + 4 * i) * 4);
             __syncthreads();
         }
         // ---- this wave's tiles: a contiguous run holding about a quarter of the sub-tiles
@@ -383,14 +407,14 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
         const int thi = wave == kPassWaves - 1 ? nt : lower(static_cast<int64_t>(wave + 1) * total);
         const int jbeg = uni(plan_x[tlo]), jend = uni(plan_x[thi]);
 
-        auto row_entry = [&](int t) { return ld<uint32_t>(rent, static_cast<uint32_t>((T0 + t) * 16 + c) * 4); };
-        auto row_entries4 = [&](int t) { return ld<uint4>(rent, static_cast<uint32_t>((T0 + t) * 16 + 4 * q) * 4); };
+        auto row_entry = [&](int t) { return row_ent[t * 16 + c]; };
+        auto row_entries4 = [&](int t) { return reinterpret_cast<const uint4 *>(row_ent)[t * 4 + q]; };
         auto row_count = [&](int t) { return min(16, n_r - (T0 + t) * 16); };
         // tiles with no partner at all still own partial rows: they are zero
         auto zero_tiles = [&](int ta, int tb) {
             const floatx4 z[4] = {};
             for (int t = ta; t < tb; t++)
-                store_tile<BF16>(tile, part, a.m, row_entries4(t), row_count(t), q, cl, g, c, z, 0.f);
+                store_tile(tile, part, pexp, a.m, row_entries4(t), row_count(t), q, cl, g, c, z, 0.f);
         };
         // sub-tile j of the run: its tile (searched forward from t) and first partner
         auto tile_of = [&](int j, int t) {
@@ -403,57 +427,66 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
         if (jbeg == jend) {
             zero_tiles(tlo, thi);
         } else {
-            // pipeline: partner entries two sub-tiles ahead, operands one sub-tile ahead
-            // (sub-tiles past the run load from partner 0 and are never computed)
-            int t0 = tile_of(jbeg, tlo);
-            zero_tiles(tlo, t0);
-            const int y0 = first_partner(jbeg, t0);
-            int t1 = t0, y1 = 0;
-            if (jbeg + 1 < jend) { t1 = tile_of(jbeg + 1, t0); y1 = first_partner(jbeg + 1, t1); }
-            uint32_t re0 = row_entry(t0), re1 = row_entry(t1);
-            uint4 r40 = row_entries4(t0), r41 = row_entries4(t1);
-            uint4 pe0 = pent4(y0), pe1 = pent4(y1);
+            // pipeline: partner and row entries two sub-tiles ahead, operands one ahead
+            // (sub-tiles past the run load from partner 0 and are never computed).
+            // The per-sub-tile state rotates through three slots with the loop unrolled
+            // three times, so no register that a load is still filling is ever copied
+            // (a copy would make the compiler wait for that load).
+            struct Slot {
+                int t;       // its tile (wave-uniform)
+                uint4 pe;    // entries of its partners 4q .. 4q+3
+            };
+            auto fill = [&](Slot &sl, int t, int y) {
+                sl.t = t;
+                sl.pe = pent4(y);
+            };
+            Slot A, B, C;
+            {
+                const int t0 = tile_of(jbeg, tlo);
+                zero_tiles(tlo, t0);
+                fill(A, t0, first_partner(jbeg, t0));
+                int t1 = t0, y1 = 0;
+                if (jbeg + 1 < jend) { t1 = tile_of(jbeg + 1, t0); y1 = first_partner(jbeg + 1, t1); }
+                fill(B, t1, y1);
+            }
             half8 rh[2], rl[2];
             uint4 rn[4];
-            load_row_tile(rn, r40, arow, cl);
+            load_row_tile(rn, row_entries4(A.t), arow, cl);
             stage_rows(rn, tile, q, cl, g, c, rh, rl);
             // one operand buffer: a sub-tile's registers are reloaded with the next
             // sub-tile as soon as they have been written to the tile
             Sub S;
-            load_sub(S, pe0, apar, bpar, cl);
+            load_sub(S, A.pe, apar, bpar, cl);
             floatx4 outT[4];
 #pragma unroll
             for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-            for (int j = jbeg;; j++) {
+            // step j: `cur` is sub-tile j (in S), `nxt` sub-tile j+1, `nn` receives j+2
+            auto step = [&](int j, Slot &cur, Slot &nxt, Slot &nn) -> bool {
                 const bool has1 = j + 1 < jend, has2 = j + 2 < jend;
-                int t2 = t1, y2 = 0;
-                if (has2) { t2 = tile_of(j + 2, t1); y2 = first_partner(j + 2, t2); }
+                int t2 = nxt.t, y2 = 0;
+                if (has2) { t2 = tile_of(j + 2, nxt.t); y2 = first_partner(j + 2, t2); }
                 publish_sub(S, tile, q, cl);
-                const uint4 pe2 = pent4(y2);
-                uint32_t re2 = re1;
-                uint4 r42 = r41;
-                if (t2 != t1) { re2 = row_entry(t2); r42 = row_entries4(t2); }
-                const bool newtile = !has1 || t1 != t0;
+                fill(nn, t2, y2);
+                const bool newtile = !has1 || nxt.t != cur.t;
                 if (has1) {
-                    load_sub(S, pe1, apar, bpar, cl);
-                    if (t1 != t0) load_row_tile(rn, r41, arow, cl);
+                    load_sub(S, nxt.pe, apar, bpar, cl);
+                    if (nxt.t != cur.t) load_row_tile(rn, row_entries4(nxt.t), arow, cl);
                 }
-                compute_sub(tile, pe0, rh, rl, static_cast<int>(re0 >> 16), g, c, outT);
+                compute_sub(tile, cur.pe, rh, rl, static_cast<int>(row_entry(cur.t) >> 16), g, c, outT);
                 if (newtile) {
-                    store_tile<BF16>(tile, part, a.m, r40, row_count(t0), q, cl, g, c, outT, oscale);
+                    store_tile(tile, part, pexp, a.m, row_entries4(cur.t), row_count(cur.t), q, cl, g, c, outT, oscale);
 #pragma unroll
                     for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-                    zero_tiles(t0 + 1, has1 ? t1 : thi);
-                    if (has1) {
-                        stage_rows(rn, tile, q, cl, g, c, rh, rl);
-                        re0 = re1;
-                        r40 = r41;
-                    }
+                    zero_tiles(cur.t + 1, has1 ? nxt.t : thi);
+                    if (has1) stage_rows(rn, tile, q, cl, g, c, rh, rl);
                 }
-                if (!has1) break;
-                t0 = t1;
-                t1 = t2; pe0 = pe1; pe1 = pe2; re1 = re2; r41 = r42;
+                return has1;
+            };
+            for (int j = jbeg;; j += 3) {
+                if (!step(j, A, B, C)) break;
+                if (!step(j + 1, B, C, A)) break;
+                if (!step(j + 2, C, A, B)) break;
             }
         }
         __syncthreads();  // the plan arrays are rewritten for the next run of tiles
@@ -494,33 +527,35 @@ __global__ __launch_bounds__(256) void split_kernel(const void *__restrict__ q, 
     }
 }
 
-// out[r][:] = sum_h part[r][h][:]; 16 lanes per row, 4 values each.
+// out[r][:] = sum_h part[r][h][:] * 2^(e[r][h] - 15), in hash order; 16 lanes per
+// row, 4 values each.
 template <bool BF16>
-__global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const void *__restrict__ part, void *__restrict__ out,
-                                                                int64_t rows, int m) {
+__global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *__restrict__ part,
+                                                                const int8_t *__restrict__ pexp,
+                                                                void *__restrict__ out, int64_t rows, int64_t n,
+                                                                int m) {
     const int64_t r = (static_cast<int64_t>(blockIdx.x) * kReduceThreads + threadIdx.x) >> 4;
     const int q = threadIdx.x & 15;
     if (r >= rows) return;
+    typedef unsigned int uint2v __attribute__((ext_vector_type(2)));
+    const uint2v *src = reinterpret_cast<const uint2v *>(part + r * m * D) + q;
+    const int64_t b = r / n;
+    const int8_t *ex = pexp + b * m * n + (r - b * n);
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int h = 0; h < m; h++) {
+        const uint2v v = __builtin_nontemporal_load(src + h * (D / 4));
+        const float sc = ldexpf(1.0f, static_cast<int>(ex[h * n]) - 15);
+        s.x = fmaf(static_cast<float>(static_cast<int16_t>(v.x & 0xFFFFu)), sc, s.x);
+        s.y = fmaf(static_cast<float>(static_cast<int16_t>(v.x >> 16)), sc, s.y);
+        s.z = fmaf(static_cast<float>(static_cast<int16_t>(v.y & 0xFFFFu)), sc, s.z);
+        s.w = fmaf(static_cast<float>(static_cast<int16_t>(v.y >> 16)), sc, s.w);
+    }
     if constexpr (BF16) {
-        const uint2 *src = reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(part) + r * m * D) + q;
-        for (int h = 0; h < m; h++) {
-            const uint2 v = src[h * (D / 4)];
-            s.x += __uint_as_float(v.x << 16);
-            s.y += __uint_as_float(v.x & 0xFFFF0000u);
-            s.z += __uint_as_float(v.y << 16);
-            s.w += __uint_as_float(v.y & 0xFFFF0000u);
-        }
         uint2 o;
         o.x = static_cast<uint32_t>(f32_to_bf16(s.x)) | (static_cast<uint32_t>(f32_to_bf16(s.y)) << 16);
         o.y = static_cast<uint32_t>(f32_to_bf16(s.z)) | (static_cast<uint32_t>(f32_to_bf16(s.w)) << 16);
         reinterpret_cast<uint2 *>(static_cast<uint16_t *>(out) + r * D)[q] = o;
     } else {
-        const float4 *src = reinterpret_cast<const float4 *>(static_cast<const float *>(part) + r * m * D) + q;
-        for (int h = 0; h < m; h++) {
-            const float4 v = src[h * (D / 4)];
-            s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
-        }
         reinterpret_cast<float4 *>(static_cast<float *>(out) + r * D)[q] = s;
     }
 }
@@ -539,12 +574,13 @@ unsigned elementwise_grid(int64_t count) {
 size_t align_up(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 template <bool BF16>
-hipError_t launch_reduce(const void *part, void *out, int64_t rows, int m, hipStream_t stream) {
+hipError_t launch_reduce(const int16_t *part, const int8_t *pexp, void *out, int64_t rows, int64_t n, int m,
+                         hipStream_t stream) {
     if (rows == 0) return hipSuccess;
     const int64_t blocks = (rows * 16 + kReduceThreads - 1) / kReduceThreads;
     KernelTimer timer("reduce_kernel", stream);
     hipLaunchKernelGGL(reduce_kernel<BF16>, dim3(static_cast<unsigned>(blocks)), dim3(kReduceThreads), 0, stream,
-                       part, out, rows, m);
+                       part, pexp, out, rows, n, m);
     return hipGetLastError();
 }
 
@@ -559,10 +595,9 @@ hipError_t zero_output(void *out, int64_t bytes, hipStream_t stream) {
     return hipGetLastError();
 }
 
-template <bool BF16>
 hipError_t launch_pass(const PassArgs &a, int64_t units, hipStream_t stream) {
     KernelTimer timer("pass_kernel", stream);
-    hipLaunchKernelGGL((pass_kernel<BF16>), dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0, stream, a);
+    hipLaunchKernelGGL(pass_kernel, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -572,7 +607,6 @@ BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, 
     BackwardLayout L;
     const int64_t units = bh * m;
     const size_t nb = (static_cast<size_t>(1) << tau) + 1;
-    const size_t pbytes = bf16 ? 2 : 4;
     size_t o = 0;
     L.qoff = o; o = align_up(o + units * nb * 4);
     L.koff = o; o = align_up(o + units * nb * 4);
@@ -582,8 +616,10 @@ BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, 
     L.dys = o; o = align_up(o + static_cast<size_t>(bh) * n_q * D * 4);
     L.ks = o; o = align_up(o + static_cast<size_t>(bh) * n_k * D * 4);
     L.vs = o; o = align_up(o + static_cast<size_t>(bh) * n_k * D * 4);
-    L.pq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m * D * pbytes);
-    L.pk = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m * D * pbytes);
+    L.pq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m * D * 2);
+    L.pk = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m * D * 2);
+    L.eq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m);
+    L.ek = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m);
     L.table = o; o = align_up(o + table_workspace_bytes(bf16, bh, n_k, m, tau));
     L.total = o;
     return L;
@@ -638,18 +674,20 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
     a.q = Side{reinterpret_cast<const uint32_t *>(ws + L.qent), reinterpret_cast<const int32_t *>(ws + L.qoff), n_q};
     a.k = Side{reinterpret_cast<const uint32_t *>(ws + L.kent), reinterpret_cast<const int32_t *>(ws + L.koff), n_k};
     a.qs = qs; a.ks = ks; a.vs = vs; a.dys = dys;
-    a.pq = ws + L.pq;
-    a.pk = ws + L.pk;
+    a.pq = reinterpret_cast<int16_t *>(ws + L.pq);
+    a.pk = reinterpret_cast<int16_t *>(ws + L.pk);
+    a.eq = reinterpret_cast<int8_t *>(ws + L.eq);
+    a.ek = reinterpret_cast<int8_t *>(ws + L.ek);
     a.bh = bh; a.m = m; a.tau = tau;
     a.scale = static_cast<float>(tau) / (2.0f * static_cast<float>(m));
-    e = bf16 ? launch_pass<true>(a, units, stream) : launch_pass<false>(a, units, stream);
+    e = launch_pass(a, units, stream);
     if (e != hipSuccess) return e;
     if (bf16) {
-        if ((e = launch_reduce<true>(a.pq, dq, bh * n_q, m, stream)) != hipSuccess) return e;
-        return launch_reduce<true>(a.pk, dk, bh * n_k, m, stream);
+        if ((e = launch_reduce<true>(a.pq, a.eq, dq, bh * n_q, n_q, m, stream)) != hipSuccess) return e;
+        return launch_reduce<true>(a.pk, a.ek, dk, bh * n_k, n_k, m, stream);
     }
-    if ((e = launch_reduce<false>(a.pq, dq, bh * n_q, m, stream)) != hipSuccess) return e;
-    return launch_reduce<false>(a.pk, dk, bh * n_k, m, stream);
+    if ((e = launch_reduce<false>(a.pq, a.eq, dq, bh * n_q, n_q, m, stream)) != hipSuccess) return e;
+    return launch_reduce<false>(a.pk, a.ek, dk, bh * n_k, n_k, m, stream);
 }
 
 }  // namespace yoso

@@ -130,15 +130,19 @@ def test_empty_tensors_need_no_pointers(L):
 
 
 def test_workspace_sizes():
-    # backward workspace: bucket offsets + sorted entries + one partial row per (row, hash)
-    # for dq and dk (fp32 partials for fp32 storage, bf16 partials for bf16 storage)
+    # backward workspace: bucket offsets + sorted entries, the fp16 (hi, lo) copies of
+    # Q, K, V, dY (4 bytes per element) and one partial row per (row, hash) for dq and
+    # dk in block floating point (64 int16 mantissas + one exponent byte), the same
+    # for both storage types
     f32 = Y.yoso_workspace_size(Y.OP_BACKWARD, Y.F32, 32, 4096, 4096, 64, 32, 8)
     bf = Y.yoso_workspace_size(Y.OP_BACKWARD, Y.BF16, 32, 4096, 4096, 64, 32, 8)
     units = 32 * 32
     index = units * (2 * 257 * 4 + 2 * 4096 * 4)
-    assert f32 >= index + 2 * 32 * 4096 * 32 * 64 * 4
-    assert bf >= index + 2 * 32 * 4096 * 32 * 64 * 2
-    assert bf < f32
+    split = 4 * 32 * 4096 * 64 * 4
+    partials = 2 * 32 * 4096 * 32 * (64 * 2 + 1)
+    assert f32 >= index + split + partials
+    assert f32 < 1.05 * (index + split + partials) + (1 << 20)
+    assert bf == f32
     assert Y.yoso_workspace_size(Y.OP_HASH, Y.F32, 32, 4096, 4096, 64, 32, 8) == 0
     assert Y.yoso_workspace_size(Y.OP_FORWARD, Y.F32, 32, 4096, 4096, 64, 32, 8) == 0
     with pytest.raises(Y.YosoError):

@@ -162,7 +162,15 @@ def test_golden_worked_example(golden):
     torch.cuda.synchronize()
     for t, key in ((y, "y"), (dq, "dq"), (dk, "dk"), (dv, "dv")):
         got = t.cpu().numpy()[0]
-        np.testing.assert_allclose(got[:, :2], g[key], rtol=1e-5, atol=1e-5)
+        ref = np.array(g[key])
+        if key in ("dq", "dk"):
+            # per-hash partial rows are stored with 16-bit mantissas and one exponent per
+            # row: each is exact to 2^-15 of the row's largest value, so the sum of m of
+            # them to m * 2^-15 of the largest |value|
+            tol = m * 2.0 ** -15 * np.abs(ref).max()
+            np.testing.assert_allclose(got[:, :2], ref, rtol=0, atol=tol)
+        else:
+            np.testing.assert_allclose(got[:, :2], ref, rtol=1e-5, atol=1e-5)
         assert not got[:, 2:].any()
 
 
