@@ -274,8 +274,8 @@ __device__ __forceinline__ float row16_max(float x) {
 // 4g + (0..3)] / oscale.  The tile goes through LDS so that each quarter-wave then
 // stores one whole partial row.  A partial row is stored in block floating point:
 // 64 int16 mantissas and one exponent e with max|value| < 2^e, value = mantissa *
-// 2^(e-15) (rounding error at most 2^(e-16), i.e. 2^-15 of the row's largest
-// value).  The stores are non-temporal: the partials are read once, by the
+// 2^e / 32767 (rounding error at most 2^e / 65534, i.e. about 2^-15 of the row's
+// largest value).  The stores are non-temporal: the partials are read once, by the
 // reduction, and should not evict the operands from L2.
 __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, int8_t *pexp, int m,
                                            const uint4 &re4, int nvalid, int q, int cl, int g, int c,
@@ -286,16 +286,17 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, i
 #pragma unroll
     for (int i = 0; i < 4; i++) {
         const int r = 4 * q + i;
-        const floatx4 o = lds_ld<floatx4>(tile, swz(r, cl, 256)) * oscale;
-        const float mx = row16_max(fmaxf(fmaxf(fabsf(o.x), fabsf(o.y)), fmaxf(fabsf(o.z), fabsf(o.w))));
-        // e with mx < 2^e from the biased exponent field (mx is finite; 0 gives a tiny
-        // e whose mantissas are all 0), clamped so that 2^(15-e) stays a normal float
+        const floatx4 o = lds_ld<floatx4>(tile, swz(r, cl, 256));
+        // e with max|value| < 2^e, from the biased exponent field of the scaled row
+        // maximum (0 gives a tiny e whose mantissas are all 0), clamped so that 2^-e
+        // stays a normal float
+        const float mx = row16_max(fmaxf(fmaxf(fabsf(o.x), fabsf(o.y)), fmaxf(fabsf(o.z), fabsf(o.w)))) * oscale;
         const int e = min(max(static_cast<int>((__float_as_uint(mx) >> 23) & 0xFFu) - 126, -100), 100);
-        const float sc = __uint_as_float(static_cast<uint32_t>(15 - e + 127) << 23);
-        // round to nearest, clamp (|x * sc| < 32768 rounds to at most 32768) and pack
-        auto q16 = [&](float x) { return min(max(static_cast<int>(rintf(x * sc)), -32767), 32767); };
+        // value * 2^-e lies in (-1, 1); the snorm conversion rounds it to a multiple
+        // of 1/32767 (mantissa = round(value * 2^-e * 32767))
+        const float sc = __uint_as_float(static_cast<uint32_t>(127 - e) << 23) * oscale;
         auto pk = [&](float x0, float x1) {
-            return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pk_i16(q16(x0), q16(x1)));
+            return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pknorm_i16(x0 * sc, x1 * sc));
         };
         typedef unsigned int uint2v __attribute__((ext_vector_type(2)));
         uint2v w;
@@ -527,7 +528,7 @@ __global__ __launch_bounds__(256) void split_kernel(const void *__restrict__ q, 
     }
 }
 
-// out[r][:] = sum_h part[r][h][:] * 2^(e[r][h] - 15), in hash order; 16 lanes per
+// out[r][:] = sum_h part[r][h][:] * 2^e[r][h] / 32767, in hash order; 16 lanes per
 // row, 4 values each.
 template <bool BF16>
 __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *__restrict__ part,
@@ -544,7 +545,7 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *_
     float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int h = 0; h < m; h++) {
         const uint2v v = __builtin_nontemporal_load(src + h * (D / 4));
-        const float sc = ldexpf(1.0f, static_cast<int>(ex[h * n]) - 15);
+        const float sc = ldexpf(1.0f / 32767.0f, static_cast<int>(ex[h * n]));
         s.x = fmaf(static_cast<float>(static_cast<int16_t>(v.x & 0xFFFFu)), sc, s.x);
         s.y = fmaf(static_cast<float>(static_cast<int16_t>(v.x >> 16)), sc, s.y);
         s.z = fmaf(static_cast<float>(static_cast<int16_t>(v.y & 0xFFFFu)), sc, s.z);
