@@ -247,27 +247,34 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uin
         bth[dt] = tr_load(tile + swz(pr, 16 + 2 * dt + (a4 >> 1), 512) + 8 * (a4 & 1));
         btl[dt] = tr_load(tile + swz(pr, 24 + 2 * dt + (a4 >> 1), 512) + 8 * (a4 & 1));
     }
-    // S^T[partner 4g+i][row c]
-    floatx4 st = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < 2; kb++) st = mfma3_16x16x32(ah[kb], al[kb], rh[kb], rl[kb], st);
+    // S^T[partner 4g+i][row c]: two independent accumulation chains (one per 32
+    // dims) interleaved, so consecutive MFMAs do not wait on each other
+    const floatx4 z = {0.f, 0.f, 0.f, 0.f};
+    floatx4 s0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[0], rh[0], z, 0, 0, 0);
+    floatx4 s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[1], rh[1], z, 0, 0, 0);
+    s0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[0], rl[0], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[1], rl[1], s1, 0, 0, 0);
+    s0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[0], rh[0], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[1], rh[1], s1, 0, 0, 0);
+    const floatx4 st = s0 + s1;
     const uint32_t e[4] = {pe.x, pe.y, pe.z, pe.w};
     float sv[4];
 #pragma unroll
     for (int i = 0; i < 4; i++) sv[i] = static_cast<int>(e[i] >> 16) == rcode ? st[i] : 0.f;
     half4 sh, sl;
     split4(sv, 1.0f, sh, sl);
+    // out^T += B_y^T S^T (hi*hi + hi*lo + lo*hi), the four dim blocks interleaved
 #pragma unroll
-    for (int dt = 0; dt < 4; dt++) outT[dt] = mfma3_16x16x16(bth[dt], btl[dt], sh, sl, outT[dt]);
+    for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(bth[dt], sh, outT[dt], 0, 0, 0);
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(bth[dt], sl, outT[dt], 0, 0, 0);
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(btl[dt], sh, outT[dt], 0, 0, 0);
 }
 
-// Max over each aligned group of 16 lanes (one partial row in the coalesced layout).
-__device__ __forceinline__ float row16_max(float x) {
-    x = fmaxf(x, dpp_mov<0xB1>(x));   // quad_perm [1,0,3,2]
-    x = fmaxf(x, dpp_mov<0x4E>(x));   // quad_perm [2,3,0,1]
-    x = fmaxf(x, dpp_mov<0x141>(x));  // row_half_mirror
-    x = fmaxf(x, dpp_mov<0x140>(x));  // row_mirror
-    return x;
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), CTRL, 0xF, 0xF, false));
 }
 
 // Write the partial rows of a finished tile: lane (g, c) holds out[row c][16dt +
@@ -283,25 +290,42 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, i
 #pragma unroll
     for (int dt = 0; dt < 4; dt++) lds_st(tile, swz(c, 4 * dt + g, 256), outT[dt]);
     const uint32_t e4[4] = {re4.x, re4.y, re4.z, re4.w};
+    // rows 4q + i: all four reads first, then the four exponent reductions side by side
+    // (max over the 16 lanes of a row, on |x| bit patterns, whose integer order is
+    // their order)
+    floatx4 o[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) o[i] = lds_ld<floatx4>(tile, swz(4 * q + i, cl, 256));
+    uint32_t mb[4];
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        const uint32_t a0 = max(__float_as_uint(o[i].x) & 0x7FFFFFFFu, __float_as_uint(o[i].y) & 0x7FFFFFFFu);
+        const uint32_t a1 = max(__float_as_uint(o[i].z) & 0x7FFFFFFFu, __float_as_uint(o[i].w) & 0x7FFFFFFFu);
+        mb[i] = max(a0, a1);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; i++) mb[i] = max(mb[i], dpp_u32<0xB1>(mb[i]));
+#pragma unroll
+    for (int i = 0; i < 4; i++) mb[i] = max(mb[i], dpp_u32<0x4E>(mb[i]));
+#pragma unroll
+    for (int i = 0; i < 4; i++) mb[i] = max(mb[i], dpp_u32<0x141>(mb[i]));
+#pragma unroll
+    for (int i = 0; i < 4; i++) mb[i] = max(mb[i], dpp_u32<0x140>(mb[i]));
 #pragma unroll
     for (int i = 0; i < 4; i++) {
         const int r = 4 * q + i;
-        const floatx4 o = lds_ld<floatx4>(tile, swz(r, cl, 256));
         // e with max|value| < 2^e, from the biased exponent field of the scaled row
         // maximum (0 gives a tiny e whose mantissas are all 0), clamped so that 2^-e
         // stays a normal float
-        const float mx = row16_max(fmaxf(fmaxf(fabsf(o.x), fabsf(o.y)), fmaxf(fabsf(o.z), fabsf(o.w)))) * oscale;
+        const float mx = __uint_as_float(mb[i]) * oscale;
         const int e = min(max(static_cast<int>((__float_as_uint(mx) >> 23) & 0xFFu) - 126, -100), 100);
         // value * 2^-e lies in (-1, 1); the snorm conversion rounds it to a multiple
         // of 1/32767 (mantissa = round(value * 2^-e * 32767))
         const float sc = __uint_as_float(static_cast<uint32_t>(127 - e) << 23) * oscale;
-        auto pk = [&](float x0, float x1) {
-            return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pknorm_i16(x0 * sc, x1 * sc));
-        };
         typedef unsigned int uint2v __attribute__((ext_vector_type(2)));
         uint2v w;
-        w.x = pk(o.x, o.y);
-        w.y = pk(o.z, o.w);
+        w.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pknorm_i16(o[i].x * sc, o[i].y * sc));
+        w.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pknorm_i16(o[i].z * sc, o[i].w * sc));
         if (r < nvalid) {
             const uint32_t row = e4[i] & 0xFFFFu;
             __builtin_nontemporal_store(w, reinterpret_cast<uint2v *>(part + (row * static_cast<uint32_t>(m)) * D) + cl);
@@ -442,6 +466,14 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
                 sl.pe = pent4(y);
             };
             Slot A, B, C;
+            // the prefetch cursor: tile pt holds sub-tiles [plan_x[pt], pxe); sub-tile j
+            // of it starts at partner pbase + 16 j (LDS is read only when it changes tile)
+            int pt, pxe, pbase;
+            auto cursor_at = [&](int t) {
+                pt = t;
+                pxe = uni(plan_x[t + 1]);
+                pbase = uni(plan_beg[t]) - 16 * uni(plan_x[t]);
+            };
             {
                 const int t0 = tile_of(jbeg, tlo);
                 zero_tiles(tlo, t0);
@@ -449,6 +481,7 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
                 int t1 = t0, y1 = 0;
                 if (jbeg + 1 < jend) { t1 = tile_of(jbeg + 1, t0); y1 = first_partner(jbeg + 1, t1); }
                 fill(B, t1, y1);
+                cursor_at(t1);
             }
             half8 rh[2], rl[2];
             uint4 rn[4];
@@ -466,7 +499,11 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
             auto step = [&](int j, Slot &cur, Slot &nxt, Slot &nn) -> bool {
                 const bool has1 = j + 1 < jend, has2 = j + 2 < jend;
                 int t2 = nxt.t, y2 = 0;
-                if (has2) { t2 = tile_of(j + 2, nxt.t); y2 = first_partner(j + 2, t2); }
+                if (has2) {
+                    if (j + 2 >= pxe) cursor_at(tile_of(j + 2, pt + 1));
+                    t2 = pt;
+                    y2 = pbase + 16 * (j + 2);
+                }
                 publish_sub(S, tile, q, cl);
                 fill(nn, t2, y2);
                 const bool newtile = !has1 || nxt.t != cur.t;
