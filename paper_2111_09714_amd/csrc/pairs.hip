@@ -458,12 +458,14 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
             // three times, so no register that a load is still filling is ever copied
             // (a copy would make the compiler wait for that load).
             struct Slot {
-                int t;       // its tile (wave-uniform)
-                uint4 pe;    // entries of its partners 4q .. 4q+3
+                int t;        // its tile (wave-uniform)
+                uint4 pe;     // entries of its partners 4q .. 4q+3
+                uint4 rw[4];  // its tile's rows, loaded when the tile starts here
             };
-            auto fill = [&](Slot &sl, int t, int y) {
+            auto fill = [&](Slot &sl, int t, int y, bool new_tile) {
                 sl.t = t;
                 sl.pe = pent4(y);
+                if (new_tile) load_row_tile(sl.rw, row_entries4(t), arow, cl);
             };
             Slot A, B, C;
             // the prefetch cursor: tile pt holds sub-tiles [plan_x[pt], pxe); sub-tile j
@@ -477,16 +479,14 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
             {
                 const int t0 = tile_of(jbeg, tlo);
                 zero_tiles(tlo, t0);
-                fill(A, t0, first_partner(jbeg, t0));
+                fill(A, t0, first_partner(jbeg, t0), true);
                 int t1 = t0, y1 = 0;
                 if (jbeg + 1 < jend) { t1 = tile_of(jbeg + 1, t0); y1 = first_partner(jbeg + 1, t1); }
-                fill(B, t1, y1);
+                fill(B, t1, y1, t1 != t0);
                 cursor_at(t1);
             }
             half8 rh[2], rl[2];
-            uint4 rn[4];
-            load_row_tile(rn, row_entries4(A.t), arow, cl);
-            stage_rows(rn, tile, q, cl, g, c, rh, rl);
+            stage_rows(A.rw, tile, q, cl, g, c, rh, rl);
             // one operand buffer: a sub-tile's registers are reloaded with the next
             // sub-tile as soon as they have been written to the tile
             Sub S;
@@ -505,19 +505,16 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
                     y2 = pbase + 16 * (j + 2);
                 }
                 publish_sub(S, tile, q, cl);
-                fill(nn, t2, y2);
+                fill(nn, t2, y2, has2 && t2 != nxt.t);
                 const bool newtile = !has1 || nxt.t != cur.t;
-                if (has1) {
-                    load_sub(S, nxt.pe, apar, bpar, cl);
-                    if (nxt.t != cur.t) load_row_tile(rn, row_entries4(nxt.t), arow, cl);
-                }
+                if (has1) load_sub(S, nxt.pe, apar, bpar, cl);
                 compute_sub(tile, cur.pe, rh, rl, static_cast<int>(row_entry(cur.t) >> 16), g, c, outT);
                 if (newtile) {
                     store_tile(tile, part, pexp, a.m, row_entries4(cur.t), row_count(cur.t), q, cl, g, c, outT, oscale);
 #pragma unroll
                     for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
                     zero_tiles(cur.t + 1, has1 ? nxt.t : thi);
-                    if (has1) stage_rows(rn, tile, q, cl, g, c, rh, rl);
+                    if (has1) stage_rows(nxt.rw, tile, q, cl, g, c, rh, rl);
                 }
                 return has1;
             };
