@@ -49,6 +49,46 @@ def kernel_algorithmic(w, kernel: str):
     return per_head * w.bh
 
 
+COPY_BYTES = 256 << 20
+
+
+def source_digest(files) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+# Kernel -> the sources its code comes from (the traffic figure is void once they change).
+KERNEL_SOURCES = {
+    "pass_kernel": ["paper_2111_09714_amd/csrc/pairs.hip", "paper_2111_09714_amd/csrc/common.h"],
+    "table_kernel": ["paper_2111_09714_amd/csrc/tables.hip", "paper_2111_09714_amd/csrc/common.h"],
+}
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from its committed counter summary
+    (profiles/<kernel>_<workload>_traffic.md), or None when there is none or the
+    kernel's sources have changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.md")
+    if not os.path.exists(path) or kernel not in KERNEL_SOURCES:
+        return None
+    fields = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and line.startswith("- `"):
+                key, _, val = line[3:].partition("`:")
+                fields[key.strip()] = val.strip().strip("`")
+    if fields.get("source_digest") != source_digest(KERNEL_SOURCES[kernel]):
+        return None
+    try:
+        return int(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(w, inp, heads):
     """Time the oracle (hash + forward + backward) on `heads`, one head per thread."""
     import oracle
@@ -58,18 +98,22 @@ def cpu_baseline(w, inp, heads):
     def one(h):
         oracle.run_all(inp, w.m, w.tau, heads=slice(h, h + 1))
 
-    t0 = time.perf_counter()
+    # repeat the sample until about 10 s of wall time have been spent (at most 30 s)
+    reps, wall = 0, 0.0
     with concurrent.futures.ThreadPoolExecutor(max_workers=threads) as ex:
-        list(ex.map(one, heads))
-    wall = time.perf_counter() - t0
-    step_equiv = wall * w.bh / len(heads)
+        while reps == 0 or (wall < 10.0 and wall * (reps + 1) / reps < 30.0):
+            t0 = time.perf_counter()
+            list(ex.map(one, heads))
+            wall += time.perf_counter() - t0
+            reps += 1
+    step_equiv = wall / reps * w.bh / len(heads)
     return {
         "value": w.tokens / step_equiv,
         "unit": "tokens/s",
         "cores": threads,
         "kind": "oracle",
         "sample": f"{len(heads)} of {w.bh} heads of the same workload (hash+forward+backward, fp64 C oracle, "
-                  f"one head per thread); {wall:.2f} s wall, scaled by {w.bh}/{len(heads)}",
+                  f"one head per thread), {reps} repetitions in {wall:.2f} s wall, scaled by {w.bh}/{len(heads)}",
     }
 
 
@@ -81,6 +125,9 @@ def main() -> int:
     ap.add_argument("--workload", default="lra_n4096")
     ap.add_argument("--cpu-heads", type=int, default=-1, help="heads in the oracle sample (-1: all)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed steps, run a plain 256 MiB device copy (read + write) three times, "
+                         "so that a counter run sees a kernel of known traffic")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -151,6 +198,17 @@ def main() -> int:
         roofline = {"kernel": dominant, "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                     "algorithmic_bytes_per_launch": alg, "avg_launch_us": round(kernels[dominant]["avg_us"], 2)}
+
+    if roofline is not None:
+        roofline["traffic"] = measured_traffic(dominant, w.name)
+
+    if args.copy_calibration:
+        # elementwise multiply by 1: one kernel reading and writing COPY_BYTES each
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
 
     tokens_per_s = w.tokens / (ms_per_step * 1e-3)
     alg_step_bytes = 11 * w.n * w.d * w.elem_bytes * w.bh

@@ -17,7 +17,9 @@
 // Kernels:
 //   sort_kernel    one workgroup per (head, hash, side): histogram of the codes,
 //                  exclusive scan -> bucket offsets, then the rows in bucket order
-//                  as packed entries (code << 16 | row) (a counting sort in LDS).
+//                  as packed entries (code << 16 | row): a stable counting sort in
+//                  LDS (rows of a bucket in increasing index), so the order in which
+//                  the pair passes accumulate, and hence every result, is reproducible.
 //   pass_kernel    one workgroup per (head, hash, side).  Each wave walks 16-row
 //                  tiles of sorted rows; the partners that can collide with a tile
 //                  form one contiguous range of sorted partners, visited 16 at a
@@ -44,6 +46,10 @@ namespace yoso {
 namespace {
 
 constexpr int kSortThreads = 256;
+constexpr int kSortWaves = kSortThreads / 64;
+
+// Waves of a sort workgroup that place rows: each needs a 64-bit lane mask per bucket.
+__host__ __device__ constexpr int sort_placing_waves(int tau) { return tau <= 10 ? kSortWaves : 1; }
 constexpr int kPassThreads = 256;
 constexpr int kPassWaves = kPassThreads / 64;
 constexpr int kReduceThreads = 256;
@@ -64,29 +70,41 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
                                                             int32_t *__restrict__ qoff, int32_t *__restrict__ koff,
                                                             uint32_t *__restrict__ qent,
                                                             uint32_t *__restrict__ kent) {
-    extern __shared__ int32_t cnt[];  // [buckets] counts, then cursors; + [kSortThreads] scan scratch
-    int32_t *scan = cnt + (1 << tau);
+    // [kSortWaves][buckets] per-wave counts, then per-wave cursors; + [kSortThreads]
+    // scan scratch; + [placing waves][buckets] 64-bit lane masks
+    extern __shared__ int32_t hist[];
+    const int B = 1 << tau;
+    int32_t *scan = hist + kSortWaves * B;
+    unsigned long long *masks = reinterpret_cast<unsigned long long *>(scan + kSortThreads);
+    const int pw = sort_placing_waves(tau);
     const int64_t unit = blockIdx.x >> 1;
     const bool kside = blockIdx.x & 1;
     const int64_t b = unit / m;
     const int h = static_cast<int>(unit - b * m);
     const int64_t n = kside ? n_k : n_q;
     const uint16_t *codes = (kside ? kcodes : qcodes) + b * n * m + h;
-    int32_t *off = (kside ? koff : qoff) + unit * ((1 << tau) + 1);
+    int32_t *off = (kside ? koff : qoff) + unit * (B + 1);
     uint32_t *ent = (kside ? kent : qent) + unit * ent_stride(n);
-    const int B = 1 << tau;
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // placing wave w owns the contiguous rows [r0, r1); the order is then rows in
+    // increasing index within each bucket, independent of any timing
+    const int64_t seg = (n + pw - 1) / pw;
+    const int64_t r0 = wave < pw ? min(n, wave * seg) : n, r1 = wave < pw ? min(n, r0 + seg) : n;
 
-    for (int c = tid; c < B; c += kSortThreads) cnt[c] = 0;
+    for (int c = tid; c < kSortWaves * B; c += kSortThreads) hist[c] = 0;
+    for (int c = tid; c < pw * B; c += kSortThreads) masks[c] = 0ull;
     __syncthreads();
-    for (int64_t i = tid; i < n; i += kSortThreads) atomicAdd(&cnt[codes[i * m] & (B - 1)], 1);
+    for (int64_t i = r0 + lane; i < r1; i += 64) atomicAdd(&hist[wave * B + (codes[i * m] & (B - 1))], 1);
     __syncthreads();
 
-    // exclusive scan: thread t owns buckets [t*per, (t+1)*per)
+    // bucket offsets (exclusive scan of the totals; thread t owns buckets
+    // [t*per, (t+1)*per)), and each wave's first position in each bucket
     const int per = (B + kSortThreads - 1) / kSortThreads;
     const int c0 = tid * per;
     int32_t local = 0;
-    for (int c = c0; c < c0 + per && c < B; c++) local += cnt[c];
+    for (int c = c0; c < c0 + per && c < B; c++)
+        for (int w = 0; w < kSortWaves; w++) local += hist[w * B + c];
     scan[tid] = local;
     __syncthreads();
     for (int s = 1; s < kSortThreads; s <<= 1) {
@@ -95,20 +113,42 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
         scan[tid] += v;
         __syncthreads();
     }
-    int32_t run = scan[tid] - local;  // exclusive prefix of this thread's first bucket
+    int32_t run = scan[tid] - local;
     for (int c = c0; c < c0 + per && c < B; c++) {
-        const int32_t k = cnt[c];
         off[c] = run;
-        cnt[c] = run;  // becomes the cursor
-        run += k;
+        for (int w = 0; w < kSortWaves; w++) {
+            const int32_t k = hist[w * B + c];
+            hist[w * B + c] = run;  // becomes wave w's cursor in bucket c
+            run += k;
+        }
     }
     if (tid == 0) off[B] = static_cast<int32_t>(n);
     __syncthreads();
 
-    for (int64_t i = tid; i < n; i += kSortThreads) {
-        const uint32_t c = codes[i * m] & (B - 1);
-        const int32_t pos = atomicAdd(&cnt[c], 1);
-        ent[pos] = (c << 16) | static_cast<uint32_t>(i);
+    // each placing wave places its rows 64 at a time, in order.  Every lane sets its
+    // bit in its bucket's lane mask; the mask then gives the lane its rank among the
+    // lanes of its bucket (bits below its own) and the bucket's count; the lowest
+    // such lane advances the cursor and clears the mask.  (The mask and cursor
+    // arrays are private to the wave and LDS executes one wave's accesses in order.)
+    if (wave < pw) {
+        int32_t *cur = hist + wave * B;
+        unsigned long long *mk = masks + wave * B;
+        for (int64_t base = r0; base < r1; base += 64) {
+            const int64_t i = base + lane;
+            const bool valid = i < r1;
+            const uint32_t c = codes[(valid ? i : r1 - 1) * m] & (B - 1);
+            if (valid) atomicOr(&mk[c], 1ull << lane);
+            const unsigned long long mask = mk[c];
+            const int32_t first = cur[c];
+            const int rank = __popcll(mask & ((1ull << lane) - 1ull));
+            if (valid) {
+                ent[first + rank] = (c << 16) | static_cast<uint32_t>(i);
+                if (rank == 0) {
+                    cur[c] = first + __popcll(mask);
+                    mk[c] = 0ull;
+                }
+            }
+        }
     }
     for (int64_t i = n + tid; i < ent_stride(n); i += kSortThreads) ent[i] = kSentinel;
 }
@@ -681,7 +721,8 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
     }
 
     {
-        const size_t sort_lds = (static_cast<size_t>(1 << tau) + kSortThreads) * 4;
+        const size_t sort_lds = (static_cast<size_t>(kSortWaves) * (1 << tau) + kSortThreads) * 4 +
+                                static_cast<size_t>(sort_placing_waves(tau)) * (1 << tau) * 8;
         KernelTimer timer("sort_kernel", stream);
         hipLaunchKernelGGL(sort_kernel, dim3(static_cast<unsigned>(2 * units)), dim3(kSortThreads), sort_lds, stream,
                            qcodes, kcodes, m, n_q, n_k, tau, reinterpret_cast<int32_t *>(ws + L.qoff),

@@ -194,5 +194,7 @@ def test_repeatable_and_side_stream():
         b = run_gpu(inp, w.m, w.tau, w.dtype)
     np.testing.assert_array_equal(a["qc"], b["qc"])
     np.testing.assert_array_equal(a["kc"], b["kc"])
+    # every accumulation order is fixed (integer tables; stable bucket order; partial
+    # rows summed in hash order), so a repeat is bitwise identical
     for key in ("y", "dq", "dk", "dv"):
-        assert rel_err(b[key], a[key]) <= 1e-6, key
+        np.testing.assert_array_equal(b[key], a[key], err_msg=key)
