@@ -34,10 +34,15 @@
  *   - Precision.  Y and dV are accumulated as exact fixed-point integers: each
  *     value of a 2-16 wide feature slice is rounded to a multiple of 2^-k, where
  *     2^k is the largest power of two keeping n_src * max|slice value| * 2^k
- *     below 2^30; everything after that rounding is exact, so Y and dV are
- *     bitwise reproducible.  dQ and dK use fp32 accumulation of products formed
- *     from fp16 (hi, lo) pairs (about 22 significant bits) and are reproducible
- *     too: every partial is written once and summed in hash order.
+ *     below 2^30; everything after that rounding is exact.  dQ and dK use fp32
+ *     accumulation of products formed from fp16 (hi, lo) pairs (about 22
+ *     significant bits); the contribution of each hash to a row is kept in block
+ *     floating point (16-bit mantissas, one power-of-two exponent per row), exact
+ *     to about 2^-15 of that row's largest value, and the m contributions are
+ *     summed in hash order in fp32 (about 3e-5 relative at unit-norm Q, K).
+ *   - Reproducibility.  Every accumulation order is fixed (integer tables, a
+ *     stable bucket order, partial rows summed in hash order), so repeating a
+ *     call on the same inputs gives bitwise identical outputs on any stream.
  */
 #ifndef YOSO_H
 #define YOSO_H
@@ -114,8 +119,9 @@ yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const v
  *
  * q, dy, dq [bh][n_q][d];  k, v, dk, dv [bh][n_k][d]  (dtype).
  * workspace: yoso_workspace_size(YOSO_OP_BACKWARD, ...) bytes of scratch: the
- * per-hash bucket orders and one fp32 partial row per (row, hash) for dq and dk,
- * about 4*m*d*(n_q + n_k)*bh bytes.
+ * per-hash bucket orders, fp16 (hi, lo) copies of q, k, v, dy, and one
+ * block-floating-point partial row per (row, hash) for dq and dk: about
+ * (2*m*d + 5*m + 8*d) * (n_q + n_k) * bh bytes.
  */
 yoso_status yoso_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q,
                           const void *k, const void *v, const void *dy, yoso_dtype dtype,
