@@ -32,6 +32,8 @@
 //   gather:  8 lanes per query, each reading the whole P-word rows of G/8
 //            hashes in a rotated order (the 16 lanes of a 16-byte access pass
 //            hit distinct bank groups), then a DPP butterfly sums the 8 lanes.
+#include <type_traits>
+
 #include "common.h"
 #include "launch.h"
 #include "timing.h"
@@ -331,6 +333,11 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
 
         // ---- gather: out[i][slice*DS + d] (+)= sum_h table[code_h(i)][h][d]
         // (the codes of the wave's next few query groups are fetched ahead)
+        // (the single-pass and multi-pass output paths are separate instantiations:
+        // sharing blocks with the accumulator loads of the multi-pass path would make
+        // every single-pass store wait for all outstanding loads)
+        auto gather = [&](auto single) {
+            constexpr bool SINGLE = decltype(single)::value;
         {
             int hh[8];
 #pragma unroll
@@ -362,7 +369,7 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
             };
             const int64_t step = static_cast<int64_t>(kTableWaves) * QPI;
             // codes of the next kGD query groups are in flight while one is summed
-            constexpr int kGD = 2;
+            constexpr int kGD = KM < 2 ? 8 : 2;
             int cR[kGD][8];
 #pragma unroll
             for (int u = 0; u < kGD; u++) fetch(cR[u], static_cast<int64_t>(wave) * QPI + u * step);
@@ -410,7 +417,7 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
                         for (int d = 0; d < DS; d++) {
                             if (d % L != gr) continue;
                             const float v = acc[d];
-                            if (ngroups == 1) {
+                            if constexpr (SINGLE) {
                                 if constexpr (BF16)
                                     static_cast<uint16_t *>(a.out)[obase + d] = f32_to_bf16(v);
                                 else
@@ -428,6 +435,11 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
                 }
             }
         }
+        };
+        if (ngroups == 1)
+            gather(std::true_type{});
+        else
+            gather(std::false_type{});
         __syncthreads();
     }
 }
