@@ -118,7 +118,8 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
     const int64_t logical = xcd_remap(blockIdx.x, blocks);
     const int64_t b = logical / S;
     const int slice = static_cast<int>(logical - b * S);
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar loops)
     const int G = a.G;
     const int cmask = (1 << a.tau) - 1;
     const int64_t vbase = b * a.n_src * D + slice * DS;
@@ -180,6 +181,10 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
     const int64_t src_row0 = b * a.n_src, dst_row0 = b * a.n_dst;
     const float inv_m = 1.0f / static_cast<float>(a.m);
     for (int grp = 0; grp < ngroups; grp++) {
+        // no loads in flight from the previous group's gather (its last prefetches are
+        // never used): otherwise the scatter below, whose registers they may occupy,
+        // would wait for them on every chunk (vmcnt(0), all other counters untouched)
+        __builtin_amdgcn_s_waitcnt(0x0F70);
         const int h0 = grp * G;
         const int gcount = min(G, a.m - h0);
         {
@@ -190,83 +195,98 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
         __syncthreads();
 
         // ---- scatter
-        // A wave owns 64-key chunks wave, wave+16, ...  Lane = key first loads and
-        // quantises the chunk's values; then each step adds one (KM 0) or two (KM 1)
-        // keys into the tables, every lane taking its (hash, word) combo and reading
-        // the key's packed word from the lane that holds it (readlane).  The codes a
-        // lane needs for a whole chunk are fetched one chunk ahead (packed two per
-        // register) and so are the values, so load latency overlaps the atomics.
-        // Lanes without a valid (key, hash) add into a private dummy slot instead of
-        // branching.
+        // A wave owns 64-key chunks wave, wave+8, ...  Lane = key first loads and
+        // quantises the chunk's values into the wave's staging area; then each step adds
+        // one (KM 0) or two (KM 1) keys into the tables, every lane taking its (hash,
+        // word) combo.  The words of eight steps are read from the staging area while the
+        // previous eight steps' atomics issue; the codes a lane needs are fetched 32 steps
+        // ahead and a chunk's values one chunk ahead, so no step waits for memory.
         if constexpr (KM < 2) {
             constexpr int KPI_C = KM == 0 ? 1 : 2;
             constexpr int SPC = 64 / KPI_C;  // steps per chunk
+            constexpr int NG = SPC / 8;      // groups of eight steps per chunk
             const int64_t nchunks = (a.n_src + 63) / 64;
             const int mychunks = wave < nchunks ? static_cast<int>((nchunks - wave + kTableWaves - 1) / kTableWaves) : 0;
             const int hh = sh[0], pp = sp[0];
             const bool hok = hh < gcount;
-            // uniform base + 32-bit per-lane offsets (n*m < 2^22)
-            const uint16_t *cbase = a.src_codes + src_row0 * a.m + h0;
+            // codes are read as the aligned 32-bit pair holding the lane's code (m is even
+            // and the codes 4-byte aligned for these forms), from a uniform per-head base
+            // with 32-bit per-lane offsets (n*m < 2^22); the pair's half is a lane constant
+            const uint32_t *cbase = reinterpret_cast<const uint32_t *>(a.src_codes + src_row0 * a.m);
             const int nsrc = static_cast<int>(a.n_src);
             const int tab_words = (cmask + 1) * G * P;
-            const int dummy = tab_words + lane;
-            const int lane_off = hh * P + pp;
+            // the lane's word index is code * cmul + loff; a lane whose hash does not exist
+            // adds into a private dummy slot.  Keys past the end add zero words into real
+            // slots (their values are zeroed, their codes read from a clamped row), so a
+            // step has no branch
+            const int cmul = hok ? G * P : 0;
+            const int loff = hok ? hh * P + pp : tab_words + lane;
             // codes are fetched kAhead steps ahead of their use, from a clamped (always
-            // valid) row, into a ring of registers; validity is decided at use
+            // valid) row, into a ring of full registers (a 16-bit ring gets packed, and
+            // packing at the chunk loop's back edge waits for every load in flight)
             constexpr int kAhead = 32;
             static_assert(SPC % kAhead == 0, "prefetch distance must divide the chunk");
             const uint32_t last = static_cast<uint32_t>(nsrc - 1), mm = static_cast<uint32_t>(a.m);
-            const uint32_t hcl = hok ? static_cast<uint32_t>(hh) : 0u;
-            auto code_at = [&](int tc, int st) -> int {
+            const uint32_t hcol = static_cast<uint32_t>(h0) + (hok ? static_cast<uint32_t>(hh) : 0u);
+            const uint32_t csh = (hcol & 1u) * 16u;
+            auto code_at = [&](int tc, int st) -> uint32_t {
                 const uint32_t row = static_cast<uint32_t>((wave + kTableWaves * tc) * 64 + st * KPI_C + slot);
-                return cbase[min(row, last) * mm + hcl];
+                return cbase[(min(row, last) * mm + hcol) >> 1];
             };
-            // values of the chunk, lane = key (loaded from a clamped row, zeroed past the end,
-            // so no branch separates the load from its use)
+            // values of a chunk, lane = key, from a clamped row; rows past the end are
+            // zeroed when the chunk is quantised (a select right after the load would
+            // make the load wait)
             auto load_vals = [&](float v[DS], int tc) {
                 const int j = (wave + kTableWaves * tc) * 64 + lane;
                 load_slice<BF16, DS>(a.values, vbase + static_cast<int64_t>(min(j, nsrc - 1)) * D, v);
-#pragma unroll
-                for (int d = 0; d < DS; d++) v[d] = j < nsrc ? v[d] : 0.f;
             };
-            int cr[kAhead];
+            uint32_t cr[kAhead];
             float vr[DS];
             // this wave's staging area: the packed words of its chunk, [key][P]
             unsigned long long *wstage = tab + tab_words + 64 + wave * 64 * P;
+            // (values before codes: at the top of the chunk loop the values are then
+            // older than every code load in flight, on entry as on the back edge)
             if (mychunks > 0) {
+                load_vals(vr, 0);
 #pragma unroll
                 for (int st = 0; st < kAhead; st++) cr[st] = code_at(0, st);
-                load_vals(vr, 0);
             }
             for (int tc = 0; tc < mychunks; tc++) {
-                // keys of this chunk that exist: step st is valid for this lane iff
-                // st*KPI_C + slot < nvalid and the lane's hash exists
-                const int nvalid = hok ? min(64, nsrc - (wave + kTableWaves * tc) * 64) - slot : 0;
+                const bool kok = (wave + kTableWaves * tc) * 64 + lane < nsrc;
                 // quantise and publish this chunk's words (lane = key), then start
-                // fetching the next chunk's values
+                // fetching the next chunk's values (the last chunk fetches itself again)
 #pragma unroll
                 for (int p = 0; p < P; p++) {
-                    const int lo = __float2int_rn(ldexpf(vr[2 * p], k));
-                    const int hi = __float2int_rn(ldexpf(vr[2 * p + 1], k));
+                    const int lo = kok ? __float2int_rn(ldexpf(vr[2 * p], k)) : 0;
+                    const int hi = kok ? __float2int_rn(ldexpf(vr[2 * p + 1], k)) : 0;
                     wstage[lane * P + p] = (static_cast<unsigned long long>(static_cast<uint32_t>(hi)) << 32) +
                                            static_cast<unsigned long long>(static_cast<long long>(lo));
                 }
                 // the staging area is private to this wave and LDS executes a wave's
                 // accesses in order: only the compiler must keep the reads below after
                 // these writes (and the next chunk's writes after the reads)
-                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-                if (tc + 1 < mychunks) load_vals(vr, tc + 1);
+                asm volatile("" ::: "memory");
+                load_vals(vr, min(tc + 1, mychunks - 1));
+                unsigned long long wd[2][8];
+                auto read_words = [&](unsigned long long w[8], int g) {
 #pragma unroll
-                for (int st = 0; st < SPC; st++) {
-                    const unsigned long long word = wstage[(st * KPI_C + slot) * P + pp];
-                    const int c = cr[st % kAhead] & cmask;
-                    const int idx = st * KPI_C < nvalid ? c * (G * P) + lane_off : dummy;
-                    atomicAdd(&tab[idx], word);
-                    cr[st % kAhead] = st + kAhead < SPC ? code_at(tc, st + kAhead) : code_at(tc + 1, st + kAhead - SPC);
+                    for (int u = 0; u < 8; u++) w[u] = wstage[((8 * g + u) * KPI_C + slot) * P + pp];
+                };
+                read_words(wd[0], 0);
+#pragma unroll
+                for (int g = 0; g < NG; g++) {
+                    if (g + 1 < NG) read_words(wd[(g + 1) & 1], g + 1);
+#pragma unroll
+                    for (int u = 0; u < 8; u++) {
+                        const int st = 8 * g + u;
+                        const int idx = static_cast<int>((cr[st % kAhead] >> csh) & cmask) * cmul + loff;
+                        atomicAdd(&tab[idx], wd[g & 1][u]);
+                        cr[st % kAhead] = st + kAhead < SPC ? code_at(tc, st + kAhead) : code_at(tc + 1, st + kAhead - SPC);
+                    }
                     // keep the scheduler from hoisting the unrolled chunk (register pressure)
-                    if ((st & 7) == 7) __builtin_amdgcn_sched_barrier(0);
+                    __builtin_amdgcn_sched_barrier(0);
                 }
-                asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+                asm volatile("" ::: "memory");
             }
         } else {
             // general case (few hashes, wide slices): one step at a time, combos in NI passes
@@ -344,18 +364,28 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
             for (int t = 0; t < 8; t++) hh[t] = gr + L * ((t + gq) % (HL > 0 ? HL : 1));
             // codes of a query group: loads from clamped (always valid) positions,
             // validity applied afterwards, so the loads stay in flight
-            const uint16_t *qbase = a.dst_codes + dst_row0 * a.m + h0;
-            const uint32_t qlast = static_cast<uint32_t>(a.n_dst - 1), mm = static_cast<uint32_t>(a.m);
             // (raw codes only: a per-lane select on a loaded value makes the compiler
-            // branch around the load and wait for it; validity is kept apart)
-            auto fetch = [&](int cc[8], int64_t i0) {
+            // branch around the load and wait for it; validity is kept apart.  The one-
+            // and two-key forms read the aligned 32-bit pair holding the code, so that the
+            // ring of codes in flight needs no widening copy at the loop's back edge)
+            const uint32_t qlast = static_cast<uint32_t>(a.n_dst - 1), mm = static_cast<uint32_t>(a.m);
+            uint32_t hcol[8], csh[8];
+#pragma unroll
+            for (int t = 0; t < 8; t++) {
+                hcol[t] = static_cast<uint32_t>(h0) + (hh[t] < gcount ? static_cast<uint32_t>(hh[t]) : 0u);
+                csh[t] = KM < 2 ? (hcol[t] & 1u) * 16u : 0u;
+            }
+            const uint16_t *qhead = a.dst_codes + dst_row0 * a.m;
+            auto fetch = [&](uint32_t cc[8], int64_t i0) {
                 const int64_t i = i0 + gq;
                 const uint32_t icl = i < a.n_dst ? static_cast<uint32_t>(i) : qlast;
 #pragma unroll
                 for (int t = 0; t < 8; t++) {
                     if (t < HL) {
-                        const uint32_t hcl = hh[t] < gcount ? static_cast<uint32_t>(hh[t]) : 0u;
-                        cc[t] = qbase[icl * mm + hcl];
+                        if constexpr (KM < 2)
+                            cc[t] = reinterpret_cast<const uint32_t *>(qhead)[(icl * mm + hcol[t]) >> 1];
+                        else
+                            cc[t] = qhead[icl * mm + hcol[t]];
                     }
                 }
             };
@@ -370,9 +400,13 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
             const int64_t step = static_cast<int64_t>(kTableWaves) * QPI;
             // codes of the next kGD query groups are in flight while one is summed
             constexpr int kGD = KM < 2 ? 8 : 2;
-            int cR[kGD][8];
+            uint32_t cR[kGD][8];
+            // (issued in ring order, which the first groups' waits assume)
 #pragma unroll
-            for (int u = 0; u < kGD; u++) fetch(cR[u], static_cast<int64_t>(wave) * QPI + u * step);
+            for (int u = 0; u < kGD; u++) {
+                fetch(cR[u], static_cast<int64_t>(wave) * QPI + u * step);
+                __builtin_amdgcn_sched_barrier(0);
+            }
             for (int64_t ib = static_cast<int64_t>(wave) * QPI; ib < a.n_dst; ib += kGD * step) {
 #pragma unroll
                 for (int u = 0; u < kGD; u++) {
@@ -391,7 +425,12 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
                         if (t < HL) {
                             const float w = ((vmask >> t) & 1u) ? 1.f : 0.f;
                             const int hcl = min(hh[t], gcount - 1);
-                            const float *row = reinterpret_cast<const float *>(tab) + ((cR[u][t] & cmask) * G + hcl) * DS;
+                            // (a 24-bit multiply: a 32-bit one becomes v_mad_u64_u32, whose unused
+                            // high addend half can be allocated to a load in flight, which then
+                            // has to be waited for)
+                            const uint32_t rw = __umul24((cR[u][t] >> csh[t]) & static_cast<uint32_t>(cmask),
+                                                         static_cast<uint32_t>(G)) + static_cast<uint32_t>(hcl);
+                            const float *row = reinterpret_cast<const float *>(tab) + rw * DS;
                             if constexpr (DS == 2) {
                                 const float2 x = *reinterpret_cast<const float2 *>(row);
                                 acc[0] = fmaf(x.x, w, acc[0]);
@@ -461,7 +500,10 @@ hipError_t launch_table_ds(int ds, const TableArgs &a, size_t lds, hipStream_t s
     int gp = 1;
     while (gp < a.G) gp <<= 1;
     const int cpk = gp * (ds / 2);
-    const int km = (ds > 8) ? 2 : (cpk == 64 ? 0 : (cpk == 32 ? 1 : 2));
+    // the one- and two-key forms read codes as aligned 32-bit pairs
+    const bool pairs = a.m % 2 == 0 && (reinterpret_cast<uintptr_t>(a.src_codes) & 3) == 0 &&
+                       (reinterpret_cast<uintptr_t>(a.dst_codes) & 3) == 0;
+    const int km = (ds > 8 || !pairs) ? 2 : (cpk == 64 ? 0 : (cpk == 32 ? 1 : 2));
     KernelTimer timer("table_kernel", stream);
     switch (ds) {
         case 2: launch_table_km<BF16, 2>(km, a, lds, stream); break;
