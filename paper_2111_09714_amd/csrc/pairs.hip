@@ -55,6 +55,7 @@ constexpr int kPassWaves = kPassThreads / 64;
 constexpr int kReduceThreads = 256;
 constexpr int kTileBytes = 16 * 512;   // LDS bytes of one wave's operand tile
 constexpr int kPlanTiles = 256;        // row tiles planned per run (multiple of kPassThreads)
+constexpr int kExpLds = 16384;         // rows whose exponents a pass block stages in LDS
 constexpr int kEntPad = 16;            // at least this many sentinel entries after each unit's sorted entries
 
 // Entries per unit: n rounded up to a multiple of 4 (16-byte aligned units), then
@@ -323,10 +324,13 @@ __device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
 // 64 int16 mantissas and one exponent e with max|value| < 2^e, value = mantissa *
 // 2^e / 32767 (rounding error at most 2^e / 65534, i.e. about 2^-15 of the row's
 // largest value).  The stores are non-temporal: the partials are read once, by the
-// reduction, and should not evict the operands from L2.
-__device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, int8_t *pexp, int m,
-                                           const uint4 &re4, int nvalid, int q, int cl, int g, int c,
-                                           const floatx4 outT[4], float oscale) {
+// reduction, and should not evict the operands from L2.  Exponents go to the block's
+// LDS copy of its exponent row when it fits (written out whole at the end: single-
+// byte stores scattered over the row would each cost a partial-line write), else
+// straight to memory.
+__device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, int8_t *pexp, int8_t *ex_lds,
+                                           bool ex_in_lds, int m, const uint4 &re4, int nvalid, int q, int cl,
+                                           int g, int c, const floatx4 outT[4], float oscale) {
 #pragma unroll
     for (int dt = 0; dt < 4; dt++) lds_st(tile, swz(c, 4 * dt + g, 256), outT[dt]);
     const uint32_t e4[4] = {re4.x, re4.y, re4.z, re4.w};
@@ -369,7 +373,10 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, i
         if (r < nvalid) {
             const uint32_t row = e4[i] & 0xFFFFu;
             __builtin_nontemporal_store(w, reinterpret_cast<uint2v *>(part + (row * static_cast<uint32_t>(m)) * D) + cl);
-            if (cl == 0) pexp[row] = static_cast<int8_t>(e);
+            if (cl == 0) {
+                if (ex_in_lds) ex_lds[row] = static_cast<int8_t>(e);
+                else pexp[row] = static_cast<int8_t>(e);
+            }
         }
     }
 }
@@ -382,6 +389,7 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
     __shared__ int32_t plan_x[kPlanTiles + 1];    // exclusive prefix of the tiles' sub-tile counts
     __shared__ int32_t scan_tmp[kPassThreads];
     __shared__ __align__(16) uint32_t row_ent[kPlanTiles * 16];  // the run's sorted row entries
+    __shared__ __align__(16) int8_t ex_lds[kExpLds];               // the block's exponent row
 
     const int64_t units = a.bh * a.m;
     const int64_t id = xcd_remap(blockIdx.x, 2 * units);
@@ -413,6 +421,7 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
     unsigned char *tile = tiles_lds + wave * kTileBytes;
     const int tiles = (n_r + 15) >> 4;
     const float oscale = a.scale * (1.0f / 256.0f);
+    const bool ex_in_lds = n_r <= kExpLds;
 
     for (int T0 = 0; T0 < tiles; T0 += kPlanTiles) {
         const int nt = min(kPlanTiles, tiles - T0);
@@ -479,7 +488,7 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
         auto zero_tiles = [&](int ta, int tb) {
             const floatx4 z[4] = {};
             for (int t = ta; t < tb; t++)
-                store_tile(tile, part, pexp, a.m, row_entries4(t), row_count(t), q, cl, g, c, z, 0.f);
+                store_tile(tile, part, pexp, ex_lds, ex_in_lds, a.m, row_entries4(t), row_count(t), q, cl, g, c, z, 0.f);
         };
         // sub-tile j of the run: its tile (searched forward from t) and first partner
         auto tile_of = [&](int j, int t) {
@@ -550,7 +559,7 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
                 if (has1) load_sub(S, nxt.pe, apar, bpar, cl);
                 compute_sub(tile, cur.pe, rh, rl, static_cast<int>(row_entry(cur.t) >> 16), g, c, outT);
                 if (newtile) {
-                    store_tile(tile, part, pexp, a.m, row_entries4(cur.t), row_count(cur.t), q, cl, g, c, outT, oscale);
+                    store_tile(tile, part, pexp, ex_lds, ex_in_lds, a.m, row_entries4(cur.t), row_count(cur.t), q, cl, g, c, outT, oscale);
 #pragma unroll
                     for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
                     zero_tiles(cur.t + 1, has1 ? nxt.t : thi);
@@ -565,6 +574,15 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
             }
         }
         __syncthreads();  // the plan arrays are rewritten for the next run of tiles
+    }
+    if (ex_in_lds) {
+        // every row's exponent is in LDS (the barrier above orders the writes): one
+        // coalesced copy of the row, 16 bytes per lane where aligned, else (and for
+        // the tail) byte by byte
+        const int n16 = (reinterpret_cast<uintptr_t>(pexp) & 15) == 0 ? n_r >> 4 : 0;
+        for (int e = tid; e < n16; e += kPassThreads)
+            reinterpret_cast<uint4 *>(pexp)[e] = reinterpret_cast<const uint4 *>(ex_lds)[e];
+        for (int e = (n16 << 4) + tid; e < n_r; e += kPassThreads) pexp[e] = ex_lds[e];
     }
 }
 
