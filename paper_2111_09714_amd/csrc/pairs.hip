@@ -620,36 +620,67 @@ __global__ __launch_bounds__(256) void split_kernel(const void *__restrict__ q, 
     }
 }
 
-// out[r][:] = sum_h part[r][h][:] * 2^e[r][h] / 32767, in hash order; 16 lanes per
-// row, 4 values each.
+// out[r][:] = sum_h part[r][h][:] * 2^e[r][h] / 32767, in hash order; 8 lanes per
+// row, 8 values each.  The hashes go in groups of eight, each group's loads issued
+// before the previous group is added, so that a lane keeps up to 256 bytes in flight.
 template <bool BF16>
 __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *__restrict__ part,
                                                                 const int8_t *__restrict__ pexp,
                                                                 void *__restrict__ out, int64_t rows, int64_t n,
                                                                 int m) {
-    const int64_t r = (static_cast<int64_t>(blockIdx.x) * kReduceThreads + threadIdx.x) >> 4;
-    const int q = threadIdx.x & 15;
+    const int64_t r = (static_cast<int64_t>(blockIdx.x) * kReduceThreads + threadIdx.x) >> 3;
+    const int q = threadIdx.x & 7;
     if (r >= rows) return;
-    typedef unsigned int uint2v __attribute__((ext_vector_type(2)));
-    const uint2v *src = reinterpret_cast<const uint2v *>(part + r * m * D) + q;
+    typedef unsigned int uint4v __attribute__((ext_vector_type(4)));
+    const uint4v *src = reinterpret_cast<const uint4v *>(part + r * m * D) + q;
     const int64_t b = r / n;
     const int8_t *ex = pexp + b * m * n + (r - b * n);
-    float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int h = 0; h < m; h++) {
-        const uint2v v = __builtin_nontemporal_load(src + h * (D / 4));
-        const float sc = ldexpf(1.0f / 32767.0f, static_cast<int>(ex[h * n]));
-        s.x = fmaf(static_cast<float>(static_cast<int16_t>(v.x & 0xFFFFu)), sc, s.x);
-        s.y = fmaf(static_cast<float>(static_cast<int16_t>(v.x >> 16)), sc, s.y);
-        s.z = fmaf(static_cast<float>(static_cast<int16_t>(v.y & 0xFFFFu)), sc, s.z);
-        s.w = fmaf(static_cast<float>(static_cast<int16_t>(v.y >> 16)), sc, s.w);
+    float s[8];
+#pragma unroll
+    for (int i = 0; i < 8; i++) s[i] = 0.f;
+    auto add = [&](const uint4v &v, int e) {
+        const float sc = ldexpf(1.0f / 32767.0f, e);
+        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            s[2 * i] = fmaf(static_cast<float>(static_cast<int16_t>(w[i] & 0xFFFFu)), sc, s[2 * i]);
+            s[2 * i + 1] = fmaf(static_cast<float>(static_cast<int16_t>(w[i] >> 16)), sc, s[2 * i + 1]);
+        }
+    };
+    // groups of eight hashes, double-buffered: group g+1 is loaded while g is added
+    uint4v v[2][8];
+    int e[2][8];
+    auto load = [&](uint4v w[8], int f[8], int h0) {
+#pragma unroll
+        for (int u = 0; u < 8; u++) w[u] = __builtin_nontemporal_load(src + (h0 + u) * (D / 8));
+#pragma unroll
+        for (int u = 0; u < 8; u++) f[u] = ex[(h0 + u) * n];
+    };
+    const int ng = m >> 3;
+    if (ng > 0) load(v[0], e[0], 0);
+    for (int g = 0; g < ng; g += 2) {
+        if (g + 1 < ng) load(v[1], e[1], 8 * (g + 1));
+#pragma unroll
+        for (int u = 0; u < 8; u++) add(v[0][u], e[0][u]);
+        if (g + 1 < ng) {
+            if (g + 2 < ng) load(v[0], e[0], 8 * (g + 2));
+#pragma unroll
+            for (int u = 0; u < 8; u++) add(v[1][u], e[1][u]);
+        }
     }
+    int h = 8 * ng;
+    for (; h < m; h++) add(__builtin_nontemporal_load(src + h * (D / 8)), ex[h * n]);
     if constexpr (BF16) {
-        uint2 o;
-        o.x = static_cast<uint32_t>(f32_to_bf16(s.x)) | (static_cast<uint32_t>(f32_to_bf16(s.y)) << 16);
-        o.y = static_cast<uint32_t>(f32_to_bf16(s.z)) | (static_cast<uint32_t>(f32_to_bf16(s.w)) << 16);
-        reinterpret_cast<uint2 *>(static_cast<uint16_t *>(out) + r * D)[q] = o;
+        uint4 o;
+        o.x = static_cast<uint32_t>(f32_to_bf16(s[0])) | (static_cast<uint32_t>(f32_to_bf16(s[1])) << 16);
+        o.y = static_cast<uint32_t>(f32_to_bf16(s[2])) | (static_cast<uint32_t>(f32_to_bf16(s[3])) << 16);
+        o.z = static_cast<uint32_t>(f32_to_bf16(s[4])) | (static_cast<uint32_t>(f32_to_bf16(s[5])) << 16);
+        o.w = static_cast<uint32_t>(f32_to_bf16(s[6])) | (static_cast<uint32_t>(f32_to_bf16(s[7])) << 16);
+        reinterpret_cast<uint4 *>(static_cast<uint16_t *>(out) + r * D)[q] = o;
     } else {
-        reinterpret_cast<float4 *>(static_cast<float *>(out) + r * D)[q] = s;
+        float4 *o = reinterpret_cast<float4 *>(static_cast<float *>(out) + r * D) + 2 * q;
+        o[0] = make_float4(s[0], s[1], s[2], s[3]);
+        o[1] = make_float4(s[4], s[5], s[6], s[7]);
     }
 }
 
@@ -670,7 +701,7 @@ template <bool BF16>
 hipError_t launch_reduce(const int16_t *part, const int8_t *pexp, void *out, int64_t rows, int64_t n, int m,
                          hipStream_t stream) {
     if (rows == 0) return hipSuccess;
-    const int64_t blocks = (rows * 16 + kReduceThreads - 1) / kReduceThreads;
+    const int64_t blocks = (rows * 8 + kReduceThreads - 1) / kReduceThreads;
     KernelTimer timer("reduce_kernel", stream);
     hipLaunchKernelGGL(reduce_kernel<BF16>, dim3(static_cast<unsigned>(blocks)), dim3(kReduceThreads), 0, stream,
                        part, pexp, out, rows, n, m);
