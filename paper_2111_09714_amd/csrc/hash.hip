@@ -46,18 +46,37 @@ __global__ __launch_bounds__(256) void hash_kernel(const void *__restrict__ x, i
     const int wave = tid >> 6;
 
     // R -> fp16 B-fragments.  Fragment (nt, kb) lane L holds rows
-    // k = kb*32 + (L>>4)*8 + [0,8) of column nt*16 + (L&15).
-    for (int s = tid; s < NT * 128; s += 256) {
-        const int nt = s >> 7, kb = (s >> 6) & 1, L = s & 63;
-        const int col = nt * 16 + (L & 15);
-        const int k0 = kb * 32 + (L >> 4) * 8;
-        float r[8];
+    // k = kb*32 + (L>>4)*8 + [0,8) of column nt*16 + (L&15).  Four fragments per
+    // thread at a time, all 32 loads issued before the first conversion (the
+    // conversion is latency-bound, and it is repeated by every workgroup).
+    for (int s0 = tid; s0 < NT * 128; s0 += 4 * 256) {
+        float r[4][8];
 #pragma unroll
-        for (int i = 0; i < 8; i++) r[i] = (col < N) ? R[(int64_t)(k0 + i) * N + col] : 0.f;
-        half8 hi, lo;
-        split8(r, 1.0f, hi, lo);
-        frag[((nt * 2 + kb) * 2 + 0) * 64 + L] = hi;
-        frag[((nt * 2 + kb) * 2 + 1) * 64 + L] = lo;
+        for (int u = 0; u < 4; u++) {
+            const int s = s0 + u * 256;
+            const int nt = s >> 7, kb = (s >> 6) & 1, L = s & 63;
+            const int col = nt * 16 + (L & 15);
+            const int k0 = kb * 32 + (L >> 4) * 8;
+            const bool ok = s < NT * 128 && col < N;
+            // (a clamped, always valid address; out-of-range values are zeroed below)
+            const float *src = R + (ok ? (int64_t)k0 * N + col : 0);
+#pragma unroll
+            for (int i = 0; i < 8; i++) r[u][i] = src[ok ? (int64_t)i * N : 0];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; u++) {
+            const int s = s0 + u * 256;
+            if (s >= NT * 128) break;
+            const int nt = s >> 7, kb = (s >> 6) & 1, L = s & 63;
+            const int col = nt * 16 + (L & 15);
+            float v[8];
+#pragma unroll
+            for (int i = 0; i < 8; i++) v[i] = col < N ? r[u][i] : 0.f;
+            half8 hi, lo;
+            split8(v, 1.0f, hi, lo);
+            frag[((nt * 2 + kb) * 2 + 0) * 64 + L] = hi;
+            frag[((nt * 2 + kb) * 2 + 1) * 64 + L] = lo;
+        }
     }
     __syncthreads();
 
@@ -149,7 +168,8 @@ hipError_t launch_hash(const void *x, bool bf16, int64_t bh, int64_t n, const fl
     const int64_t rows = bh * n;
     if (rows == 0) return hipSuccess;
     const int64_t tiles = (rows + kHashRowsPerTile - 1) / kHashRowsPerTile;
-    const int64_t grid = tiles < 1024 ? tiles : 1024;
+    // persistent workgroups (two per CU): each converts R once for several tiles
+    const int64_t grid = tiles < 512 ? tiles : 512;
     const size_t lds = hash_lds_bytes(m, tau);
     KernelTimer timer("hash_kernel", stream);
     if (bf16) {
