@@ -50,6 +50,7 @@ constexpr int kSortWaves = kSortThreads / 64;
 
 // Waves of a sort workgroup that place rows: each needs a 64-bit lane mask per bucket.
 __host__ __device__ constexpr int sort_placing_waves(int tau) { return tau <= 10 ? kSortWaves : 1; }
+constexpr size_t kSortStageLds = 120 * 1024;  // LDS bound of a sort workgroup that stages its column
 constexpr int kPassThreads = 256;
 constexpr int kPassWaves = kPassThreads / 64;
 constexpr int kReduceThreads = 256;
@@ -67,22 +68,27 @@ constexpr uint32_t kSentinel = 0xFFFF0000u;  // code 0xFFFF (no real code), row 
 // codes are [bh][n][m]; unit = b*m + h reads column h with stride m.
 __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__restrict__ qcodes,
                                                             const uint16_t *__restrict__ kcodes, int m,
-                                                            int64_t n_q, int64_t n_k, int tau,
+                                                            int64_t n_q, int64_t n_k, int tau, bool stage,
                                                             int32_t *__restrict__ qoff, int32_t *__restrict__ koff,
                                                             uint32_t *__restrict__ qent,
                                                             uint32_t *__restrict__ kent) {
     // [kSortWaves][buckets] per-wave counts, then per-wave cursors; + [kSortThreads]
-    // scan scratch; + [placing waves][buckets] 64-bit lane masks
+    // scan scratch; + [placing waves][buckets] 64-bit lane masks; when `stage`, the
+    // column's codes (read from memory once, with stride m) and the sorted entries,
+    // which are then written out whole (single scattered 4-byte stores would each
+    // cost a partial-line write)
     extern __shared__ int32_t hist[];
     const int B = 1 << tau;
     int32_t *scan = hist + kSortWaves * B;
-    unsigned long long *masks = reinterpret_cast<unsigned long long *>(scan + kSortThreads);
     const int pw = sort_placing_waves(tau);
+    unsigned long long *masks = reinterpret_cast<unsigned long long *>(scan + kSortThreads);
+    uint32_t *est = reinterpret_cast<uint32_t *>(masks + pw * B);
     const int64_t unit = blockIdx.x >> 1;
     const bool kside = blockIdx.x & 1;
     const int64_t b = unit / m;
     const int h = static_cast<int>(unit - b * m);
     const int64_t n = kside ? n_k : n_q;
+    uint16_t *cst = reinterpret_cast<uint16_t *>(est + (stage ? (kside ? n_k : n_q) : 0));
     const uint16_t *codes = (kside ? kcodes : qcodes) + b * n * m + h;
     int32_t *off = (kside ? koff : qoff) + unit * (B + 1);
     uint32_t *ent = (kside ? kent : qent) + unit * ent_stride(n);
@@ -96,7 +102,11 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
     for (int c = tid; c < kSortWaves * B; c += kSortThreads) hist[c] = 0;
     for (int c = tid; c < pw * B; c += kSortThreads) masks[c] = 0ull;
     __syncthreads();
-    for (int64_t i = r0 + lane; i < r1; i += 64) atomicAdd(&hist[wave * B + (codes[i * m] & (B - 1))], 1);
+    for (int64_t i = r0 + lane; i < r1; i += 64) {
+        const int c = codes[i * m] & (B - 1);
+        if (stage) cst[i] = static_cast<uint16_t>(c);
+        atomicAdd(&hist[wave * B + c], 1);
+    }
     __syncthreads();
 
     // bucket offsets (exclusive scan of the totals; thread t owns buckets
@@ -137,13 +147,18 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
         for (int64_t base = r0; base < r1; base += 64) {
             const int64_t i = base + lane;
             const bool valid = i < r1;
-            const uint32_t c = codes[(valid ? i : r1 - 1) * m] & (B - 1);
+            const int64_t ic = valid ? i : r1 - 1;
+            const uint32_t c = stage ? cst[ic] : codes[ic * m] & (B - 1);
             if (valid) atomicOr(&mk[c], 1ull << lane);
             const unsigned long long mask = mk[c];
             const int32_t first = cur[c];
             const int rank = __popcll(mask & ((1ull << lane) - 1ull));
             if (valid) {
-                ent[first + rank] = (c << 16) | static_cast<uint32_t>(i);
+                const uint32_t e = (c << 16) | static_cast<uint32_t>(i);
+                if (stage)
+                    est[first + rank] = e;
+                else
+                    ent[first + rank] = e;
                 if (rank == 0) {
                     cur[c] = first + __popcll(mask);
                     mk[c] = 0ull;
@@ -151,7 +166,27 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
             }
         }
     }
-    for (int64_t i = n + tid; i < ent_stride(n); i += kSortThreads) ent[i] = kSentinel;
+    if (stage) {
+        __syncthreads();
+        // the entries, then the sentinels, 16 bytes per thread (ent_stride is a
+        // multiple of 4 and the unit's entry array starts 16-byte aligned)
+        const int64_t n4 = n >> 2;
+        for (int64_t e = tid; e < ent_stride(n) / 4; e += kSortThreads) {
+            uint4 w;
+            if (e < n4) {
+                w = reinterpret_cast<const uint4 *>(est)[e];
+            } else {
+                const int64_t j = 4 * e;
+                w.x = j < n ? est[j] : kSentinel;
+                w.y = j + 1 < n ? est[j + 1] : kSentinel;
+                w.z = j + 2 < n ? est[j + 2] : kSentinel;
+                w.w = j + 3 < n ? est[j + 3] : kSentinel;
+            }
+            reinterpret_cast<uint4 *>(ent)[e] = w;
+        }
+    } else {
+        for (int64_t i = n + tid; i < ent_stride(n); i += kSortThreads) ent[i] = kSentinel;
+    }
 }
 
 // ---------------------------------------------------------------- pair passes
@@ -770,11 +805,15 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
     }
 
     {
-        const size_t sort_lds = (static_cast<size_t>(kSortWaves) * (1 << tau) + kSortThreads) * 4 +
-                                static_cast<size_t>(sort_placing_waves(tau)) * (1 << tau) * 8;
+        size_t sort_lds = (static_cast<size_t>(kSortWaves) * (1 << tau) + kSortThreads) * 4 +
+                          static_cast<size_t>(sort_placing_waves(tau)) * (1 << tau) * 8;
+        // stage the column's codes and entries in LDS when they fit (6 bytes per row)
+        const int64_t n_max = n_q > n_k ? n_q : n_k;
+        const bool stage = sort_lds + static_cast<size_t>(n_max) * 6 <= kSortStageLds;
+        if (stage) sort_lds += static_cast<size_t>(n_max) * 6;
         KernelTimer timer("sort_kernel", stream);
         hipLaunchKernelGGL(sort_kernel, dim3(static_cast<unsigned>(2 * units)), dim3(kSortThreads), sort_lds, stream,
-                           qcodes, kcodes, m, n_q, n_k, tau, reinterpret_cast<int32_t *>(ws + L.qoff),
+                           qcodes, kcodes, m, n_q, n_k, tau, stage, reinterpret_cast<int32_t *>(ws + L.qoff),
                            reinterpret_cast<int32_t *>(ws + L.koff), reinterpret_cast<uint32_t *>(ws + L.qent),
                            reinterpret_cast<uint32_t *>(ws + L.kent));
     }
