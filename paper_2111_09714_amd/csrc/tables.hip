@@ -125,13 +125,23 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
     const int64_t vbase = b * a.n_src * D + slice * DS;
 
     // ---- scale: largest |v| of this slice -> exponent k
+    // (eight rows per thread in flight at once: the pass is latency-bound; rows past
+    // the end re-read the last row, which cannot change the maximum)
     {
         float mx = 0.f;
-        for (int64_t j = tid; j < a.n_src; j += kTableThreads) {
-            float v[DS];
-            load_slice<BF16, DS>(a.values, vbase + j * D, v);
+        constexpr int U = 8;
+        const int64_t last = a.n_src - 1;
+        for (int64_t j0 = tid; j0 < a.n_src; j0 += U * kTableThreads) {
+            float v[U][DS];
 #pragma unroll
-            for (int d = 0; d < DS; d++) mx = fmaxf(mx, fabsf(v[d]));
+            for (int u = 0; u < U; u++) {
+                const int64_t j = j0 + u * kTableThreads;
+                load_slice<BF16, DS>(a.values, vbase + (j < last ? j : last) * D, v[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < U; u++)
+#pragma unroll
+                for (int d = 0; d < DS; d++) mx = fmaxf(mx, fabsf(v[u][d]));
         }
         mx = wave_max(mx);
         if (lane == 0) wave_red[wave] = mx;
@@ -414,16 +424,14 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
                     if (i0 >= a.n_dst) break;
                     const int64_t i = i0 + gq;
                     const bool qok = i < a.n_dst;
-                    float acc[DS];
-#pragma unroll
-                    for (int d = 0; d < DS; d++) acc[d] = 0.f;
                     // every lane reads a row (invalid ones read a clamped row and weight
-                    // it by 0): no divergent branch between the reads
+                    // it by 0): no divergent branch between the reads, and all of a
+                    // group's reads are issued before the first is used
                     const uint32_t vmask = valid(i0);
+                    float xs[8][DS];
 #pragma unroll
                     for (int t = 0; t < 8; t++) {
                         if (t < HL) {
-                            const float w = ((vmask >> t) & 1u) ? 1.f : 0.f;
                             const int hcl = min(hh[t], gcount - 1);
                             // (a 24-bit multiply: a 32-bit one becomes v_mad_u64_u32, whose unused
                             // high addend half can be allocated to a load in flight, which then
@@ -433,42 +441,78 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
                             const float *row = reinterpret_cast<const float *>(tab) + rw * DS;
                             if constexpr (DS == 2) {
                                 const float2 x = *reinterpret_cast<const float2 *>(row);
-                                acc[0] = fmaf(x.x, w, acc[0]);
-                                acc[1] = fmaf(x.y, w, acc[1]);
+                                xs[t][0] = x.x;
+                                xs[t][1] = x.y;
                             } else {
 #pragma unroll
                                 for (int d = 0; d < DS; d += 4) {
                                     const float4 x = *reinterpret_cast<const float4 *>(row + d);
-                                    acc[d] = fmaf(x.x, w, acc[d]);
-                                    acc[d + 1] = fmaf(x.y, w, acc[d + 1]);
-                                    acc[d + 2] = fmaf(x.z, w, acc[d + 2]);
-                                    acc[d + 3] = fmaf(x.w, w, acc[d + 3]);
+                                    xs[t][d] = x.x;
+                                    xs[t][d + 1] = x.y;
+                                    xs[t][d + 2] = x.z;
+                                    xs[t][d + 3] = x.w;
                                 }
                             }
                         }
                     }
                     fetch(cR[u], i0 + kGD * step);
+                    float acc[DS];
+#pragma unroll
+                    for (int d = 0; d < DS; d++) acc[d] = 0.f;
+#pragma unroll
+                    for (int t = 0; t < 8; t++) {
+                        if (t < HL) {
+                            const float w = ((vmask >> t) & 1u) ? 1.f : 0.f;
+#pragma unroll
+                            for (int d = 0; d < DS; d++) acc[d] = fmaf(xs[t][d], w, acc[d]);
+                        }
+                    }
+                    // every lane of the query's group holds the sums; lane c4 % L
+                    // stores dims [4 c4, 4 c4 + 4) (or the two dims of a 2-wide slice)
 #pragma unroll
                     for (int d = 0; d < DS; d++) acc[d] = group_sum(acc[d], L);
                     if (qok) {
                         const int64_t obase = (dst_row0 + i) * D + slice * DS;
+                        constexpr int CW = DS < 4 ? DS : 4;
 #pragma unroll
-                        for (int d = 0; d < DS; d++) {
-                            if (d % L != gr) continue;
-                            const float v = acc[d];
-                            if constexpr (SINGLE) {
-                                if constexpr (BF16)
-                                    static_cast<uint16_t *>(a.out)[obase + d] = f32_to_bf16(v);
-                                else
-                                    static_cast<float *>(a.out)[obase + d] = v;
-                            } else {
-                                // the same lane owns this element in every group
-                                const float prev = grp == 0 ? 0.f : a.acc[obase + d];
-                                if (grp == ngroups - 1 && BF16)
-                                    static_cast<uint16_t *>(a.out)[obase + d] = f32_to_bf16(prev + v);
-                                else
-                                    a.acc[obase + d] = prev + v;
+                        for (int c4 = 0; c4 < DS / CW; c4++) {
+                            if (gr != c4 % L) continue;
+                            float v[CW];
+#pragma unroll
+                            for (int e = 0; e < CW; e++) v[e] = acc[c4 * CW + e];
+                            const int64_t o = obase + c4 * CW;
+                            if constexpr (!SINGLE) {
+                                // the same lane owns this chunk in every group
+                                if (grp > 0) {
+                                    if constexpr (CW == 4) {
+                                        const float4 pv = *reinterpret_cast<const float4 *>(a.acc + o);
+                                        v[0] += pv.x; v[1] += pv.y; v[2] += pv.z; v[3] += pv.w;
+                                    } else {
+                                        const float2 pv = *reinterpret_cast<const float2 *>(a.acc + o);
+                                        v[0] += pv.x; v[1] += pv.y;
+                                    }
+                                }
                             }
+                            if (SINGLE || grp == ngroups - 1) {
+                                if constexpr (BF16) {
+                                    if constexpr (CW == 4) {
+                                        uint2 w2;
+                                        w2.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+                                        w2.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
+                                        *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(a.out) + o) = w2;
+                                    } else {
+                                        *reinterpret_cast<uint32_t *>(static_cast<uint16_t *>(a.out) + o) =
+                                            static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
+                                    }
+                                    continue;
+                                }
+                            }
+                            // fp32 output, or the fp32 running sums of a multi-pass bf16 run
+                            float *dst = (BF16 || !(SINGLE || grp == ngroups - 1)) ? a.acc : static_cast<float *>(a.out);
+                            if constexpr (CW == 4)
+                                *reinterpret_cast<float4 *>(dst + o) = make_float4(v[0], v[1], v[2], v[3]);
+                            else
+                                *reinterpret_cast<float2 *>(dst + o) = make_float2(v[0], v[1]);
                         }
                     }
                 }
