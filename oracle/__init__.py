@@ -46,10 +46,12 @@ def _load():
         lib.oracle_backward.argtypes = [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, P, P, P]
         lib.oracle_backward_d2.argtypes = [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, P, P]
         lib.oracle_expectation.argtypes = [P, P, P, P, I64, I64, I64, I32, I32, P, P, P, P, P]
+        lib.oracle_l2_normalize.argtypes = [P, I64, I32, P]
+        lib.oracle_l2_normalize_backward.argtypes = [P, P, I64, I32, P]
         lib.oracle_collision_prob.argtypes = [ctypes.c_double, I32]
         lib.oracle_collision_prob.restype = ctypes.c_double
         for fn in ("oracle_hash", "oracle_forward", "oracle_backward", "oracle_backward_d2",
-                   "oracle_expectation"):
+                   "oracle_expectation", "oracle_l2_normalize", "oracle_l2_normalize_backward"):
             getattr(lib, fn).restype = None
         _lib = lib
     return _lib
@@ -134,6 +136,25 @@ def expectation(q, k, v, dy, tau: int, true_grad: bool = False):
                                _ptr(tdq) if true_grad else None)
     out = (ey, edv, edq, edk)
     return out + (tdq,) if true_grad else out
+
+
+def l2_normalize(x) -> np.ndarray:
+    """Rows of x[..., d] divided by their Euclidean norms (zero rows stay zero)."""
+    x = _f64(x)
+    d = x.shape[-1]
+    y = np.zeros_like(x)
+    _load().oracle_l2_normalize(_ptr(x), x.size // d if d else 0, d, _ptr(y))
+    return y
+
+
+def l2_normalize_backward(x, dy) -> np.ndarray:
+    """Gradient w.r.t. x of <dy, l2_normalize(x)>, row by row, from the explicit Jacobian."""
+    x, dy = _f64(x), _f64(dy)
+    assert x.shape == dy.shape
+    d = x.shape[-1]
+    dx = np.zeros_like(x)
+    _load().oracle_l2_normalize_backward(_ptr(x), _ptr(dy), x.size // d if d else 0, d, _ptr(dx))
+    return dx
 
 
 def collision_prob(x: float, tau: int) -> float:

@@ -23,6 +23,11 @@
  *   expectation eq. (yoso-expectation): E[B_ij] = (1 - arccos(q_i.k_j)/pi)^tau,
  *               giving E[Y], E[dV], E[dQ], E[dK], and the true dQ of
  *               eq. (gradient-q) for reference.
+ *   l2_normalize          Sec. 3.1 "Normalizing Attention" (eq. normalized-yoso:
+ *               N-YOSO = l2(B V)) and Sec. 4 (Q, K l2-normalised before hashing):
+ *               each row divided by its Euclidean norm.
+ *   l2_normalize_backward the Jacobian of that map, built entry by entry and
+ *               applied to the incoming gradient (no simplification).
  *
  * Conventions (readings of points the paper leaves open):
  *   - bit b of hash h is [ sum_l x_l R[l][h*tau+b] > 0 ] (strict), code = sum_b bit_b 2^b;
@@ -30,6 +35,7 @@
  *     forward's codes;
  *   - m-hash averaging is the arithmetic mean, applied to Y, dV, dQ, dK;
  *   - empty buckets contribute 0 (no renormalisation);
+ *   - l2 normalisation maps the zero row to the zero row, with zero gradient;
  *   - tensors are row-major: x[bh][i][l], codes[bh][h][i].
  */
 #include <math.h>
@@ -276,6 +282,42 @@ void oracle_expectation(const double *q, const double *k, const double *v, const
                         tdq[(b * nq + i) * d + l] += g * w * kb[j * d + l];
                 }
             }
+        }
+    }
+}
+
+/* Row l2 normalisation: y[r] = x[r] / ||x[r]|| (the zero row stays zero).
+ * x, y: [rows][d]. */
+void oracle_l2_normalize(const double *x, int64_t rows, int d, double *y)
+{
+    for (int64_t r = 0; r < rows; r++) {
+        double ss = 0.0;
+        for (int l = 0; l < d; l++) ss += x[r * d + l] * x[r * d + l];
+        const double nrm = sqrt(ss);
+        for (int l = 0; l < d; l++) y[r * d + l] = nrm > 0.0 ? x[r * d + l] / nrm : 0.0;
+    }
+}
+
+/* Backward of the map above: dx[r][j] = sum_i dy[r][i] * dy_i/dx_j, with the
+ * Jacobian of y = x/||x|| written out entry by entry,
+ *   dy_i/dx_j = delta_ij / ||x|| - x_i x_j / ||x||^3,
+ * and 0 for the zero row.  x (the forward's input), dy, dx: [rows][d]. */
+void oracle_l2_normalize_backward(const double *x, const double *dy, int64_t rows, int d, double *dx)
+{
+    for (int64_t r = 0; r < rows; r++) {
+        const double *xr = x + r * d, *gr = dy + r * d;
+        double ss = 0.0;
+        for (int l = 0; l < d; l++) ss += xr[l] * xr[l];
+        const double nrm = sqrt(ss);
+        for (int j = 0; j < d; j++) {
+            double acc = 0.0;
+            if (nrm > 0.0) {
+                for (int i = 0; i < d; i++) {
+                    const double jac = (i == j ? 1.0 / nrm : 0.0) - xr[i] * xr[j] / (nrm * nrm * nrm);
+                    acc += gr[i] * jac;
+                }
+            }
+            dx[r * d + j] = acc;
         }
     }
 }

@@ -291,3 +291,84 @@ def test_true_gradient_matches_finite_difference_of_expectation():
     h = 1e-5
     fd = (loss(h) - loss(-h)) / (2 * h)
     assert abs(fd - tdq[0, i] @ t) < 1e-6 * max(1.0, abs(fd))
+
+
+# ---------------------------------------------------------------- l2 normalisation (N-YOSO, Q/K prologue)
+def _l2_inputs(seed, rows=7, d=64):
+    g = _rng(seed)
+    x = g.standard_normal((rows, d)) * g.uniform(1e-3, 1e3, size=(rows, 1))
+    x[2] = 0.0  # the zero row
+    return x
+
+
+def test_l2_normalize_unit_rows_and_zero_row():
+    x = _l2_inputs(11)
+    y = oracle.l2_normalize(x)
+    n = np.linalg.norm(y, axis=-1)
+    assert np.allclose(np.delete(n, 2), 1.0, atol=1e-14)
+    assert np.all(y[2] == 0.0)
+    # direction kept: y is a positive multiple of x
+    for r in (0, 1, 3):
+        assert np.allclose(y[r] * np.linalg.norm(x[r]), x[r], rtol=1e-12, atol=0)
+
+
+def test_l2_normalize_scale_and_sign_invariance():
+    x = _l2_inputs(12)
+    y = oracle.l2_normalize(x)
+    assert np.allclose(oracle.l2_normalize(3.7 * x), y, atol=1e-15)
+    assert np.allclose(oracle.l2_normalize(-x), -y, atol=1e-15)
+    # a basis vector and a two-hot vector have known normalisations
+    e = np.zeros((2, 64))
+    e[0, 5] = 4.0
+    e[1, [1, 2]] = 3.0, 4.0
+    ye = oracle.l2_normalize(e)
+    assert ye[0, 5] == 1.0 and np.count_nonzero(ye[0]) == 1
+    assert np.allclose(ye[1, [1, 2]], [0.6, 0.8], atol=1e-15)
+
+
+def test_l2_backward_matches_central_differences():
+    g = _rng(13)
+    x = g.standard_normal((3, 64))
+    dy = g.standard_normal((3, 64))
+    dx = oracle.l2_normalize_backward(x, dy)
+    h = 1e-6
+    fd = np.zeros_like(x)
+    for r in range(x.shape[0]):
+        for j in range(x.shape[1]):
+            xp, xm = x.copy(), x.copy()
+            xp[r, j] += h
+            xm[r, j] -= h
+            fd[r, j] = (np.sum(dy * oracle.l2_normalize(xp)) - np.sum(dy * oracle.l2_normalize(xm))) / (2 * h)
+    assert np.allclose(dx, fd, rtol=1e-6, atol=1e-8)
+
+
+def test_l2_backward_matches_autograd():
+    torch = pytest.importorskip("torch")
+    x = _l2_inputs(14)
+    g = _rng(15).standard_normal(x.shape)
+    xt = torch.tensor(x, dtype=torch.float64, requires_grad=True)
+    nz = xt.norm(dim=-1, keepdim=True)
+    yt = torch.where(nz > 0, xt / nz.clamp_min(1e-300), torch.zeros_like(xt))
+    (yt * torch.tensor(g)).sum().backward()
+    dx = oracle.l2_normalize_backward(x, g)
+    ref = xt.grad.numpy()
+    ref[2] = 0.0
+    assert np.allclose(dx, ref, rtol=1e-10, atol=1e-300)
+
+
+def test_l2_backward_invariants():
+    x = _l2_inputs(16)
+    g = _rng(17).standard_normal(x.shape)
+    dx = oracle.l2_normalize_backward(x, g)
+    # the gradient is orthogonal to x (moving along x does not change x/||x||) ...
+    dots = np.sum(dx * x, axis=-1) / (np.linalg.norm(x, axis=-1) * np.linalg.norm(dx, axis=-1) + 1e-300)
+    assert np.all(np.abs(np.delete(dots, 2)) < 1e-12)
+    # ... scales as 1/||x|| ...
+    assert np.allclose(oracle.l2_normalize_backward(2.0 * x, g), 0.5 * dx, rtol=1e-12, atol=0)
+    # ... passes a gradient orthogonal to x through scaled by 1/||x||, and kills one along x
+    r = 0
+    u = x[r] / np.linalg.norm(x[r])
+    gp = g[r] - u * np.dot(u, g[r])
+    assert np.allclose(oracle.l2_normalize_backward(x[r:r + 1], gp[None])[0], gp / np.linalg.norm(x[r]), rtol=1e-11)
+    assert np.allclose(oracle.l2_normalize_backward(x[r:r + 1], u[None])[0], 0.0, atol=1e-15)
+    assert np.all(dx[2] == 0.0)
