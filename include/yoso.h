@@ -129,6 +129,36 @@ yoso_status yoso_backward(const uint16_t *qcodes, const uint16_t *kcodes, const 
                           void *dq, void *dk, void *dv, void *workspace, size_t workspace_bytes,
                           void *stream);
 
+/*
+ * Row l2 normalisation: the output normalisation of N-YOSO (Sec. 3.1,
+ * "Normalizing Attention", eq. normalized-yoso: N-YOSO(Q, K, V) = l2(B(Q, K) V))
+ * and the normalisation of Q and K before hashing that the experiments use
+ * (Sec. 4, opening paragraph; Remark 1 assumes unit-length rows).
+ *
+ *   y[r] = x[r] / ||x[r]||_2        (y[r] = 0 where x[r] is the zero row)
+ *
+ * x, y [rows][d] (dtype), any number of rows (bh*n for Q, K or Y); y may be x.
+ * Arithmetic is fp32 (sum of squares, correctly rounded sqrt and division).
+ * Errors as for the calls above (YOSO_ERR_SHAPE for d != 64 or rows < 0).
+ */
+yoso_status yoso_l2_normalize(const void *x, yoso_dtype dtype, int64_t rows, int32_t d, void *y,
+                              void *stream);
+
+/*
+ * Backward of yoso_l2_normalize (the Jacobian of x -> x/||x|| applied to dy):
+ *
+ *   dx[r] = (dy[r] - y[r] (y[r] . dy[r])) / ||x[r]||,   y[r] = x[r] / ||x[r]||
+ *   (dx[r] = 0 where x[r] is the zero row)
+ *
+ * x is the forward's INPUT (the norm and y are recomputed from it); dy, dx
+ * [rows][d] (dtype).  dx may be dy; it must not be x.  Chaining it after
+ * yoso_backward gives the gradients of the normalised-input, normalised-output
+ * attention: dq = l2 backward(q, dq_hat), dk likewise, with yoso_backward run on
+ * the normalised q, k and on dy_hat = l2 backward(y_raw, dy).
+ */
+yoso_status yoso_l2_normalize_backward(const void *x, const void *dy, yoso_dtype dtype, int64_t rows,
+                                       int32_t d, void *dx, void *stream);
+
 /* Bytes of device workspace that `op` needs for these arguments (written to
  * *bytes).  Validates the arguments exactly as the call itself does. */
 yoso_status yoso_workspace_size(yoso_op op, yoso_dtype dtype, int64_t bh, int64_t n_q,
@@ -149,7 +179,7 @@ const char *yoso_last_error(void);
  * frees them).  yoso_timing_reset() forgets the launches recorded so far.
  * yoso_timing_query() waits for the recorded events of `kernel` ("hash_kernel",
  * "table_kernel", "sort_kernel", "split_kernel", "pass_kernel", "reduce_kernel",
- * "zero_kernel")
+ * "zero_kernel", "l2norm_kernel", "l2norm_bwd_kernel")
  * and returns the summed duration and the launch count.
  * Not thread-safe with respect to concurrent launches on other threads' streams
  * beyond the pool bookkeeping, which is locked.

@@ -57,6 +57,8 @@ def lib() -> ctypes.CDLL:
         L.yoso_forward.argtypes = [P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, SZ, P]
         L.yoso_backward.argtypes = [P, P, P, P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, P, P, SZ, P]
         L.yoso_workspace_size.argtypes = [I32, I32, I64, I64, I64, I32, I32, I32, ctypes.POINTER(SZ)]
+        L.yoso_l2_normalize.argtypes = [P, I32, I64, I32, P, P]
+        L.yoso_l2_normalize_backward.argtypes = [P, P, I32, I64, I32, P, P]
         for fn in ("yoso_hash", "yoso_forward", "yoso_backward", "yoso_workspace_size"):
             getattr(L, fn).restype = ctypes.c_int
         L.yoso_status_string.argtypes = [ctypes.c_int]
@@ -160,6 +162,27 @@ def yoso_backward(qcodes, kcodes, q, k, v, dy, m: int, tau: int, dq, dk, dv, ws,
     _check(lib().yoso_backward(_ptr(qcodes), _ptr(kcodes), _ptr(q), _ptr(k), _ptr(v), _ptr(dy), _dtype_code(q),
                                bh, n_q, n_k, d, m, tau, _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws), nbytes,
                                _stream(stream)))
+
+
+def yoso_l2_normalize(x, y, stream=None) -> None:
+    """y = x / ||x|| row by row over the last dimension (zero rows stay zero)."""
+    d = x.shape[-1]
+    _expect(y, x.shape, "y")
+    if y.dtype != x.dtype:
+        raise TypeError("y must have the dtype of x")
+    rows = x.numel() // d if d else 0
+    _check(lib().yoso_l2_normalize(_ptr(x), _dtype_code(x), rows, d, _ptr(y), _stream(stream)))
+
+
+def yoso_l2_normalize_backward(x, dy, dx, stream=None) -> None:
+    """dx = (dy - y (y . dy)) / ||x||, y = x / ||x||, row by row (x is the forward's input)."""
+    d = x.shape[-1]
+    _expect(dy, x.shape, "dy")
+    _expect(dx, x.shape, "dx")
+    if dy.dtype != x.dtype or dx.dtype != x.dtype:
+        raise TypeError("dy and dx must have the dtype of x")
+    rows = x.numel() // d if d else 0
+    _check(lib().yoso_l2_normalize_backward(_ptr(x), _ptr(dy), _dtype_code(x), rows, d, _ptr(dx), _stream(stream)))
 
 
 def yoso_timing_enable(capacity: int) -> None:

@@ -46,6 +46,14 @@ yoso_status check_shape(int64_t bh, int64_t n_q, int64_t n_k, int32_t d, int32_t
     return YOSO_OK;
 }
 
+// row operations: any number of 64-value rows (grid-stride kernels)
+yoso_status check_rows(int64_t rows, int32_t d) {
+    if (d != 64) return fail(YOSO_ERR_SHAPE, "d = %d; only d = 64 is supported", d);
+    if (rows < 0) return fail(YOSO_ERR_SHAPE, "rows = %lld < 0", (long long)rows);
+    if (rows > (int64_t{1} << 40)) return fail(YOSO_ERR_SHAPE, "rows = %lld too large", (long long)rows);
+    return YOSO_OK;
+}
+
 yoso_status check_hash(int32_t m, int32_t tau) {
     if (tau < 1 || tau > 12) return fail(YOSO_ERR_HASH, "tau = %d outside [1, 12]", tau);
     if (m < 1 || m > 64) return fail(YOSO_ERR_HASH, "m = %d outside [1, 64]", m);
@@ -171,6 +179,29 @@ yoso_status yoso_backward(const uint16_t *qcodes, const uint16_t *kcodes, const 
     return device_status(yoso::launch_backward(qcodes, kcodes, q, k, v, dy, bf16, bh, n_q, n_k, m, tau, dq, dk, dv,
                                                workspace, static_cast<hipStream_t>(stream)),
                          "yoso_backward");
+}
+
+yoso_status yoso_l2_normalize(const void *x, yoso_dtype dtype, int64_t rows, int32_t d, void *y, void *stream) {
+    g_last_error[0] = '\0';
+    YOSO_TRY(check_dtype(dtype));
+    YOSO_TRY(check_rows(rows, d));
+    YOSO_TRY(check_ptr(x, rows * d, "x"));
+    YOSO_TRY(check_ptr(y, rows * d, "y"));
+    return device_status(yoso::launch_l2norm(x, y, dtype == YOSO_BF16, rows, static_cast<hipStream_t>(stream)),
+                         "yoso_l2_normalize");
+}
+
+yoso_status yoso_l2_normalize_backward(const void *x, const void *dy, yoso_dtype dtype, int64_t rows, int32_t d,
+                                       void *dx, void *stream) {
+    g_last_error[0] = '\0';
+    YOSO_TRY(check_dtype(dtype));
+    YOSO_TRY(check_rows(rows, d));
+    YOSO_TRY(check_ptr(x, rows * d, "x"));
+    YOSO_TRY(check_ptr(dy, rows * d, "dy"));
+    YOSO_TRY(check_ptr(dx, rows * d, "dx"));
+    return device_status(
+        yoso::launch_l2norm_backward(x, dy, dx, dtype == YOSO_BF16, rows, static_cast<hipStream_t>(stream)),
+        "yoso_l2_normalize_backward");
 }
 
 }  // extern "C"
