@@ -202,6 +202,32 @@ def main() -> int:
     if roofline is not None:
         roofline["traffic"] = measured_traffic(dominant, w.name)
 
+    # the l2 row normalisation (N-YOSO output / Q, K prologue) on this workload's Q
+    # rows, outside the timed step: HBM-bound, algorithmic bytes = rows read + written
+    l2 = {}
+    qn, dqn = torch.empty_like(q), torch.empty_like(q)
+    Y.yoso_timing_enable(64)
+    for _ in range(3):
+        Y.yoso_l2_normalize(q, qn, stream)
+        Y.yoso_l2_normalize_backward(q, dy, dqn, stream)
+    torch.cuda.synchronize()
+    Y.yoso_timing_reset()
+    for _ in range(10):
+        Y.yoso_l2_normalize(q, qn, stream)
+        Y.yoso_l2_normalize_backward(q, dy, dqn, stream)
+    torch.cuda.synchronize()
+    row_bytes = w.d * w.elem_bytes
+    for name, per_row in (("l2norm_kernel", 2 * row_bytes), ("l2norm_bwd_kernel", 3 * row_bytes)):
+        tot, n = Y.yoso_timing_query(name)
+        if n:
+            avg_s = tot / n * 1e-3
+            gbs = per_row * w.bh * w.n / avg_s / 1e9
+            l2[name] = {"avg_us": round(avg_s * 1e6, 2), "bound": "hbm", "achieved": round(gbs, 1),
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                        "algorithmic_bytes_per_launch": per_row * w.bh * w.n}
+    Y.yoso_timing_enable(0)
+    del qn, dqn
+
     if args.copy_calibration:
         # elementwise multiply by 1: one kernel reading and writing COPY_BYTES each
         src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
@@ -239,6 +265,7 @@ def main() -> int:
         "roofline": roofline,
         "kernels": {kn: {kk: round(vv, 3) for kk, vv in kv.items()} for kn, kv in kernels.items()},
         "cpu_baseline": cpu,
+        "l2_normalize": l2,
     }
     print(json.dumps(out), flush=True)
     return 0
