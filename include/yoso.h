@@ -159,6 +159,30 @@ yoso_status yoso_l2_normalize(const void *x, yoso_dtype dtype, int64_t rows, int
 yoso_status yoso_l2_normalize_backward(const void *x, const void *dy, yoso_dtype dtype, int64_t rows,
                                        int32_t d, void *dx, void *stream);
 
+/*
+ * YOSO-E: the exact expectation of the forward and of the sampled surrogate
+ * backward over the hash functions, i.e. YOSO with infinitely many hashes (Sec. 4,
+ * "YOSO-E"; the collision probability of eq. yoso-expectation and the Fig. 2
+ * caption):
+ *
+ *   P[i][j] = (1 - arccos(q_i . k_j / (||q_i|| ||k_j||)) / pi)^tau
+ *   y  = P v
+ *   dv = P^T dy,  dq = (tau/2) [(dy v^T) .* P] k,  dk = (tau/2) [(dy v^T) .* P]^T q
+ *
+ * q, dy, y, dq [bh][n_q][d];  k, v, dk, dv [bh][n_k][d]  (dtype).  O(n_q n_k d)
+ * work per head, no workspace.  Rows of q and k must be nonzero; |entries| of
+ * q, k, v, dy below 4096.  Arithmetic: fp32 accumulation of products of fp16
+ * (hi, lo) pairs (three products per step, about 22 significant bits) and an
+ * fp32 arccos.
+ */
+yoso_status yoso_expectation_forward(const void *q, const void *k, const void *v, yoso_dtype dtype,
+                                     int64_t bh, int64_t n_q, int64_t n_k, int32_t d, int32_t tau,
+                                     void *y, void *stream);
+
+yoso_status yoso_expectation_backward(const void *q, const void *k, const void *v, const void *dy,
+                                      yoso_dtype dtype, int64_t bh, int64_t n_q, int64_t n_k, int32_t d,
+                                      int32_t tau, void *dq, void *dk, void *dv, void *stream);
+
 /* Bytes of device workspace that `op` needs for these arguments (written to
  * *bytes).  Validates the arguments exactly as the call itself does. */
 yoso_status yoso_workspace_size(yoso_op op, yoso_dtype dtype, int64_t bh, int64_t n_q,
@@ -179,7 +203,8 @@ const char *yoso_last_error(void);
  * frees them).  yoso_timing_reset() forgets the launches recorded so far.
  * yoso_timing_query() waits for the recorded events of `kernel` ("hash_kernel",
  * "table_kernel", "sort_kernel", "split_kernel", "pass_kernel", "reduce_kernel",
- * "zero_kernel", "l2norm_kernel", "l2norm_bwd_kernel")
+ * "zero_kernel", "l2norm_kernel", "l2norm_bwd_kernel", "expect_fwd_kernel",
+ * "expect_bwd_kv_kernel", "expect_bwd_q_kernel")
  * and returns the summed duration and the launch count.
  * Not thread-safe with respect to concurrent launches on other threads' streams
  * beyond the pool bookkeeping, which is locked.

@@ -58,6 +58,8 @@ def lib() -> ctypes.CDLL:
         L.yoso_backward.argtypes = [P, P, P, P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, P, P, SZ, P]
         L.yoso_workspace_size.argtypes = [I32, I32, I64, I64, I64, I32, I32, I32, ctypes.POINTER(SZ)]
         L.yoso_l2_normalize.argtypes = [P, I32, I64, I32, P, P]
+        L.yoso_expectation_forward.argtypes = [P, P, P, I32, I64, I64, I64, I32, I32, P, P]
+        L.yoso_expectation_backward.argtypes = [P, P, P, P, I32, I64, I64, I64, I32, I32, P, P, P, P]
         L.yoso_l2_normalize_backward.argtypes = [P, P, I32, I64, I32, P, P]
         for fn in ("yoso_hash", "yoso_forward", "yoso_backward", "yoso_workspace_size"):
             getattr(L, fn).restype = ctypes.c_int
@@ -183,6 +185,27 @@ def yoso_l2_normalize_backward(x, dy, dx, stream=None) -> None:
         raise TypeError("dy and dx must have the dtype of x")
     rows = x.numel() // d if d else 0
     _check(lib().yoso_l2_normalize_backward(_ptr(x), _ptr(dy), _dtype_code(x), rows, d, _ptr(dx), _stream(stream)))
+
+
+def yoso_expectation_forward(q, k, v, tau: int, y, stream=None) -> None:
+    """YOSO-E: y = P v with P_ij = (1 - arccos(cos(q_i, k_j))/pi)^tau."""
+    bh, n_q, d = q.shape
+    n_k = k.shape[1]
+    for t, shape, name in ((k, (bh, n_k, d), "k"), (v, (bh, n_k, d), "v"), (y, (bh, n_q, d), "y")):
+        _expect(t, shape, name)
+    _check(lib().yoso_expectation_forward(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), bh, n_q, n_k, d, tau, _ptr(y),
+                                          _stream(stream)))
+
+
+def yoso_expectation_backward(q, k, v, dy, tau: int, dq, dk, dv, stream=None) -> None:
+    """YOSO-E backward: dv = P^T dy, dq = (tau/2)[(dy v^T) .* P] k, dk = (tau/2)[(dy v^T) .* P]^T q."""
+    bh, n_q, d = q.shape
+    n_k = k.shape[1]
+    for t, shape, name in ((k, (bh, n_k, d), "k"), (v, (bh, n_k, d), "v"), (dy, (bh, n_q, d), "dy"),
+                           (dq, (bh, n_q, d), "dq"), (dk, (bh, n_k, d), "dk"), (dv, (bh, n_k, d), "dv")):
+        _expect(t, shape, name)
+    _check(lib().yoso_expectation_backward(_ptr(q), _ptr(k), _ptr(v), _ptr(dy), _dtype_code(q), bh, n_q, n_k, d, tau,
+                                           _ptr(dq), _ptr(dk), _ptr(dv), _stream(stream)))
 
 
 def yoso_timing_enable(capacity: int) -> None:

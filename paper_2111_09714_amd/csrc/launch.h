@@ -40,6 +40,12 @@ hipError_t launch_l2norm(const void *x, void *y, bool bf16, int64_t rows, hipStr
 hipError_t launch_l2norm_backward(const void *x, const void *dy, void *dx, bool bf16, int64_t rows,
                                   hipStream_t stream);
 
+hipError_t launch_expect_forward(const void *q, const void *k, const void *v, void *y, bool bf16, int64_t bh,
+                                 int64_t n_q, int64_t n_k, int tau, hipStream_t stream);
+hipError_t launch_expect_backward(const void *q, const void *k, const void *v, const void *dy, void *dq, void *dk,
+                                  void *dv, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int tau,
+                                  hipStream_t stream);
+
 hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
                            const void *v, const void *dy, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m,
                            int tau, void *dq, void *dk, void *dv, void *workspace, hipStream_t stream);

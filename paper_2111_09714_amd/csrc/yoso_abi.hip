@@ -204,4 +204,38 @@ yoso_status yoso_l2_normalize_backward(const void *x, const void *dy, yoso_dtype
         "yoso_l2_normalize_backward");
 }
 
+yoso_status yoso_expectation_forward(const void *q, const void *k, const void *v, yoso_dtype dtype, int64_t bh,
+                                     int64_t n_q, int64_t n_k, int32_t d, int32_t tau, void *y, void *stream) {
+    g_last_error[0] = '\0';
+    YOSO_TRY(check_dtype(dtype));
+    YOSO_TRY(check_shape(bh, n_q, n_k, d, 1));
+    YOSO_TRY(check_hash(1, tau));
+    YOSO_TRY(check_ptr(q, bh * n_q * d, "q"));
+    YOSO_TRY(check_ptr(k, bh * n_k * d, "k"));
+    YOSO_TRY(check_ptr(v, bh * n_k * d, "v"));
+    YOSO_TRY(check_ptr(y, bh * n_q * d, "y"));
+    return device_status(yoso::launch_expect_forward(q, k, v, y, dtype == YOSO_BF16, bh, n_q, n_k, tau,
+                                                     static_cast<hipStream_t>(stream)),
+                         "yoso_expectation_forward");
+}
+
+yoso_status yoso_expectation_backward(const void *q, const void *k, const void *v, const void *dy, yoso_dtype dtype,
+                                      int64_t bh, int64_t n_q, int64_t n_k, int32_t d, int32_t tau, void *dq,
+                                      void *dk, void *dv, void *stream) {
+    g_last_error[0] = '\0';
+    YOSO_TRY(check_dtype(dtype));
+    YOSO_TRY(check_shape(bh, n_q, n_k, d, 1));
+    YOSO_TRY(check_hash(1, tau));
+    YOSO_TRY(check_ptr(q, bh * n_q * d, "q"));
+    YOSO_TRY(check_ptr(k, bh * n_k * d, "k"));
+    YOSO_TRY(check_ptr(v, bh * n_k * d, "v"));
+    YOSO_TRY(check_ptr(dy, bh * n_q * d, "dy"));
+    YOSO_TRY(check_ptr(dq, bh * n_q * d, "dq"));
+    YOSO_TRY(check_ptr(dk, bh * n_k * d, "dk"));
+    YOSO_TRY(check_ptr(dv, bh * n_k * d, "dv"));
+    return device_status(yoso::launch_expect_backward(q, k, v, dy, dq, dk, dv, dtype == YOSO_BF16, bh, n_q, n_k, tau,
+                                                      static_cast<hipStream_t>(stream)),
+                         "yoso_expectation_backward");
+}
+
 }  // extern "C"
