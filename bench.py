@@ -31,6 +31,7 @@ if ROOT not in sys.path:
 METRIC = "YOSO attention fwd+bwd tokens/sec at n=4096,d=64,m=32,tau=8; % HBM roofline"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 FP16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense fp16/bf16 matrix peak
+FP32_PEAK_TFLOPS = 157.3        # MI355X fp32 (matrix or vector) peak
 
 
 def kernel_algorithmic(w, kernel: str):
@@ -228,6 +229,36 @@ def main() -> int:
     Y.yoso_timing_enable(0)
     del qn, dqn
 
+    # YOSO-E (exact expectation, O(n^2 d)) on the same inputs, outside the timed step:
+    # MFMA-bound dense tiles.  Algorithmic fp32 flops per head: forward 4 n_q n_k d (Q K^T
+    # and P V), backward 14 n_q n_k d (cosines and G twice, dV, dK, dQ); each is run as
+    # three fp16 products.
+    expect = {}
+    ye = torch.empty_like(q)
+    dqe, dke, dve = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    Y.yoso_timing_enable(64)
+    Y.yoso_expectation_forward(q, k, v, w.tau, ye, stream)
+    Y.yoso_expectation_backward(q, k, v, dy, w.tau, dqe, dke, dve, stream)
+    torch.cuda.synchronize()
+    Y.yoso_timing_reset()
+    for _ in range(3):
+        Y.yoso_expectation_forward(q, k, v, w.tau, ye, stream)
+        Y.yoso_expectation_backward(q, k, v, dy, w.tau, dqe, dke, dve, stream)
+    torch.cuda.synchronize()
+    nnd = float(w.n) * w.n * w.d * w.bh
+    for name, flops in (("expect_fwd_kernel", 4 * nnd), ("expect_bwd_kv_kernel", 8 * nnd),
+                        ("expect_bwd_q_kernel", 6 * nnd)):
+        tot, n = Y.yoso_timing_query(name)
+        if n:
+            avg_s = tot / n * 1e-3
+            tf = flops / avg_s / 1e12
+            expect[name] = {"avg_us": round(avg_s * 1e6, 1), "bound": "mfma", "achieved": round(tf, 1),
+                            "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(tf / FP32_PEAK_TFLOPS, 4),
+                            "fp16_mfma_util": round(3 * tf / FP16_MFMA_PEAK_TFLOPS, 4),
+                            "algorithmic_flops_per_launch": flops}
+    Y.yoso_timing_enable(0)
+    del ye, dqe, dke, dve
+
     if args.copy_calibration:
         # elementwise multiply by 1: one kernel reading and writing COPY_BYTES each
         src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
@@ -266,6 +297,7 @@ def main() -> int:
         "kernels": {kn: {kk: round(vv, 3) for kk, vv in kv.items()} for kn, kv in kernels.items()},
         "cpu_baseline": cpu,
         "l2_normalize": l2,
+        "yoso_e": expect,
     }
     print(json.dumps(out), flush=True)
     return 0
