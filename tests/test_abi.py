@@ -154,3 +154,80 @@ def test_binding_refuses_host_tensors():
     x = torch.zeros(1, 16, 64)
     with pytest.raises(ValueError):
         Y.yoso_hash(x, torch.zeros(64, 16), 2, 8, torch.zeros(1, 16, 2, dtype=torch.int16))
+
+
+def _l2(L, x=FAKE, dtype=0, rows=100, d=64, y=FAKE):
+    return L.yoso_l2_normalize(x, dtype, rows, d, y, None)
+
+
+def _l2b(L, x=FAKE, dy=FAKE, dtype=0, rows=100, d=64, dx=FAKE):
+    return L.yoso_l2_normalize_backward(x, dy, dtype, rows, d, dx, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=2), 4),
+    (dict(d=63), 2),
+    (dict(rows=-1), 2),
+    (dict(x=None), 1),
+    (dict(y=None), 1),
+    (dict(x=FAKE + 8), 5),
+    (dict(y=FAKE + 4), 5),
+])
+def test_l2_normalize_rejects(L, kw, status):
+    assert _l2(L, **kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=-1), 4),
+    (dict(d=128), 2),
+    (dict(rows=-5), 2),
+    (dict(dy=None), 1),
+    (dict(dx=None), 1),
+    (dict(dy=FAKE + 2), 5),
+])
+def test_l2_normalize_backward_rejects(L, kw, status):
+    assert _l2b(L, **kw) == status
+
+
+def test_l2_empty_is_a_no_op(L):
+    # zero rows: valid with NULL pointers, nothing launched
+    assert L.yoso_l2_normalize(None, 0, 0, 64, None, None) == 0
+    assert L.yoso_l2_normalize_backward(None, None, 1, 0, 64, None, None) == 0
+
+
+def _efwd(L, q=FAKE, k=FAKE, v=FAKE, dtype=0, bh=2, nq=64, nk=64, d=64, tau=8, y=FAKE):
+    return L.yoso_expectation_forward(q, k, v, dtype, bh, nq, nk, d, tau, y, None)
+
+
+def _ebwd(L, dtype=0, bh=2, nq=64, nk=64, d=64, tau=8, **ptrs):
+    p = dict(q=FAKE, k=FAKE, v=FAKE, dy=FAKE, dq=FAKE, dk=FAKE, dv=FAKE)
+    p.update(ptrs)
+    return L.yoso_expectation_backward(p["q"], p["k"], p["v"], p["dy"], dtype, bh, nq, nk, d, tau,
+                                       p["dq"], p["dk"], p["dv"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=3), 4),
+    (dict(d=16), 2),
+    (dict(bh=-2), 2),
+    (dict(nq=70000), 2),
+    (dict(tau=0), 3),
+    (dict(tau=13), 3),
+    (dict(q=None), 1),
+    (dict(y=None), 1),
+    (dict(v=FAKE + 4), 5),
+])
+def test_expectation_forward_rejects(L, kw, status):
+    assert _efwd(L, **kw) == status
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=9), 4),
+    (dict(nk=-1), 2),
+    (dict(tau=20), 3),
+    (dict(dy=None), 1),
+    (dict(dk=None), 1),
+    (dict(dq=FAKE + 12), 5),
+])
+def test_expectation_backward_rejects(L, kw, status):
+    assert _ebwd(L, **kw) == status
