@@ -48,10 +48,13 @@ def _load():
         lib.oracle_expectation.argtypes = [P, P, P, P, I64, I64, I64, I32, I32, P, P, P, P, P]
         lib.oracle_l2_normalize.argtypes = [P, I64, I32, P]
         lib.oracle_l2_normalize_backward.argtypes = [P, P, I64, I32, P]
+        lib.oracle_hadamard.argtypes = [I32, P]
+        lib.oracle_fast_hyperplanes.argtypes = [P, I32, I32, I32, P]
         lib.oracle_collision_prob.argtypes = [ctypes.c_double, I32]
         lib.oracle_collision_prob.restype = ctypes.c_double
         for fn in ("oracle_hash", "oracle_forward", "oracle_backward", "oracle_backward_d2",
-                   "oracle_expectation", "oracle_l2_normalize", "oracle_l2_normalize_backward"):
+                   "oracle_expectation", "oracle_l2_normalize", "oracle_l2_normalize_backward",
+                   "oracle_hadamard", "oracle_fast_hyperplanes"):
             getattr(lib, fn).restype = None
         _lib = lib
     return _lib
@@ -155,6 +158,33 @@ def l2_normalize_backward(x, dy) -> np.ndarray:
     dx = np.zeros_like(x)
     _load().oracle_l2_normalize_backward(_ptr(x), _ptr(dy), x.size // d if d else 0, d, _ptr(dx))
     return dx
+
+
+def hadamard(d: int) -> np.ndarray:
+    """Sylvester's Walsh-Hadamard matrix of order d (a power of two)."""
+    assert d >= 1 and d & (d - 1) == 0
+    H = np.zeros((d, d), np.float64)
+    _load().oracle_hadamard(d, _ptr(H))
+    return H
+
+
+def fast_hyperplanes(signs, d: int, m: int, tau: int) -> np.ndarray:
+    """R[d, m*tau] of the fast hash: the rows of the pseudo-random rotations
+    (1/d) H D3 H D2 H D1, rotation r giving columns r*d .. r*d+d-1.
+    ``signs``: uint64[ceil(m*tau/d), 3]; bit l of signs[r, i] negates coordinate l in D_{i+1}."""
+    assert d >= 1 and d & (d - 1) == 0 and d <= 64
+    nrot = (m * tau + d - 1) // d
+    signs = np.ascontiguousarray(signs, dtype=np.uint64).reshape(-1)
+    assert signs.size == 3 * nrot
+    R = np.zeros((d, m * tau), np.float64)
+    _load().oracle_fast_hyperplanes(_ptr(signs), d, m, tau, _ptr(R))
+    return R
+
+
+def fast_hash_codes(x, signs, m: int, tau: int, with_margin: bool = False):
+    """The fast hash: the sign hash of x under the hyperplanes of fast_hyperplanes."""
+    d = np.shape(x)[-1]
+    return hash_codes(x, fast_hyperplanes(signs, d, m, tau), m, tau, with_margin=with_margin)
 
 
 def collision_prob(x: float, tau: int) -> float:

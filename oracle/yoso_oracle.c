@@ -28,6 +28,11 @@
  *               each row divided by its Euclidean norm.
  *   l2_normalize_backward the Jacobian of that map, built entry by entry and
  *               applied to the incoming gradient (no simplification).
+ *   fast_hyperplanes  Sec. 3.2 "Speed-up": the approximate random projection of
+ *               Andoni et al. (2015), a pseudo-random rotation H D3 H D2 H D1 (H the
+ *               Walsh-Hadamard matrix, D_i random +-1 diagonals).  Its rows are the
+ *               hyperplanes of the fast hash; the routine writes them out as an
+ *               ordinary R for the hash routine above, by dense matrix products.
  *
  * Conventions (readings of points the paper leaves open):
  *   - bit b of hash h is [ sum_l x_l R[l][h*tau+b] > 0 ] (strict), code = sum_b bit_b 2^b;
@@ -36,7 +41,12 @@
  *   - m-hash averaging is the arithmetic mean, applied to Y, dV, dQ, dK;
  *   - empty buckets contribute 0 (no renormalisation);
  *   - l2 normalisation maps the zero row to the zero row, with zero gradient;
- *   - tensors are row-major: x[bh][i][l], codes[bh][h][i].
+ *   - tensors are row-major: x[bh][i][l], codes[bh][h][i];
+ *   - fast hash: rotation r supplies the hyperplanes of columns r*d .. r*d+d-1 of
+ *     R in order (column c = h*tau + b is row c mod d of rotation c / d), and
+ *     bit l of signs[3r + i] set means D_{i+1} of rotation r negates coordinate l;
+ *     the rotation is scaled by 1/d so that each row has length sqrt(d), as a
+ *     column of a standard Gaussian R has on average (signs do not depend on it).
  */
 #include <math.h>
 #include <stdint.h>
@@ -320,4 +330,60 @@ void oracle_l2_normalize_backward(const double *x, const double *dy, int64_t row
             dx[r * d + j] = acc;
         }
     }
+}
+
+/* Sylvester's Walsh-Hadamard matrix of order d (a power of two), built by the
+ * doubling H_1 = [1], H_2k = [[H_k, H_k], [H_k, -H_k]].  H: d*d row-major. */
+void oracle_hadamard(int d, double *H)
+{
+    H[0] = 1.0;
+    for (int k = 1; k < d; k *= 2) {
+        /* the k x k block in the top-left corner is H_k; fill the other three */
+        for (int i = 0; i < k; i++) {
+            for (int j = 0; j < k; j++) {
+                const double h = H[i * d + j];
+                H[i * d + j + k] = h;
+                H[(i + k) * d + j] = h;
+                H[(i + k) * d + j + k] = -h;
+            }
+        }
+    }
+}
+
+/* Hyperplanes of the fast hash (Sec. 3.2 "Speed-up"; the pseudo-random rotation of
+ * Andoni et al. 2015): for rotation r = 0 .. ceil(m*tau/d) - 1
+ *   M_r = (1/d) H D3 H D2 H D1,   D_i = diag(+-1 from signs[3r + i - 1]),
+ * and column c = r*d + l of R (c < m*tau) is row l of M_r:  R[j][c] = M_r[l][j].
+ * d is a power of two, at most 64.  R: d x (m*tau) row-major. */
+void oracle_fast_hyperplanes(const uint64_t *signs, int d, int m, int tau, double *R)
+{
+    const int ncol = m * tau;
+    const int nrot = (ncol + d - 1) / d;
+    double *H = malloc(sizeof(double) * d * d);
+    double *M = malloc(sizeof(double) * d * d);
+    double *T = malloc(sizeof(double) * d * d);
+    oracle_hadamard(d, H);
+    for (int r = 0; r < nrot; r++) {
+        /* M = I; then, for D1, D2, D3 in turn, M <- H D M */
+        for (int i = 0; i < d * d; i++) M[i] = 0.0;
+        for (int i = 0; i < d; i++) M[i * d + i] = 1.0;
+        for (int round = 0; round < 3; round++) {
+            const uint64_t s = signs[3 * r + round];
+            for (int i = 0; i < d; i++)          /* T = D M */
+                for (int j = 0; j < d; j++)
+                    T[i * d + j] = ((s >> i) & 1u) ? -M[i * d + j] : M[i * d + j];
+            for (int i = 0; i < d; i++)          /* M = H T */
+                for (int j = 0; j < d; j++) {
+                    double acc = 0.0;
+                    for (int k = 0; k < d; k++) acc += H[i * d + k] * T[k * d + j];
+                    M[i * d + j] = acc;
+                }
+        }
+        for (int l = 0; l < d; l++) {
+            const int c = r * d + l;
+            if (c >= ncol) break;
+            for (int j = 0; j < d; j++) R[(int64_t)j * ncol + c] = M[l * d + j] / d;
+        }
+    }
+    free(H); free(M); free(T);
 }

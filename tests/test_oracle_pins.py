@@ -372,3 +372,99 @@ def test_l2_backward_invariants():
     assert np.allclose(oracle.l2_normalize_backward(x[r:r + 1], gp[None])[0], gp / np.linalg.norm(x[r]), rtol=1e-11)
     assert np.allclose(oracle.l2_normalize_backward(x[r:r + 1], u[None])[0], 0.0, atol=1e-15)
     assert np.all(dx[2] == 0.0)
+
+
+# ---------------------------------------------------------------- fast hash (Sec. 3.2 "Speed-up")
+
+def _signs(seed, nrot):
+    return _rng(seed).integers(0, 2**64, size=(nrot, 3), dtype=np.uint64)
+
+
+def test_hadamard_is_sylvester():
+    """The oracle's Walsh-Hadamard matrix equals scipy's Sylvester construction, and
+    H H^T = d I."""
+    sl = pytest.importorskip("scipy.linalg")
+    for d in (1, 2, 4, 8, 16, 32, 64):
+        H = oracle.hadamard(d)
+        np.testing.assert_array_equal(H, sl.hadamard(d))
+        np.testing.assert_array_equal(H @ H.T, d * np.eye(d))
+
+
+def test_fast_hyperplanes_hand_worked_d2():
+    """d = 2, D1 = diag(1, -1), D2 = D3 = I, worked by hand:
+         H D1 = [[1, -1], [1, 1]],  H H D1 = [[2, 0], [0, -2]],  H H H D1 = [[2, -2], [2, 2]],
+       so M = [[1, -1], [1, 1]] and R (column l = row l of M) = [[1, 1], [-1, 1]].
+       Hashing e_0 gives projections (1, 1) -> code 3; e_1 gives (-1, 1) -> code 2."""
+    signs = np.array([[0b10, 0, 0]], np.uint64)
+    R = oracle.fast_hyperplanes(signs, 2, 1, 2)
+    np.testing.assert_array_equal(R, [[1.0, 1.0], [-1.0, 1.0]])
+    codes = oracle.fast_hash_codes(np.eye(2)[None], signs, 1, 2)
+    np.testing.assert_array_equal(codes[0, 0], [3, 2])
+
+
+def test_fast_hyperplanes_without_signs_are_hadamard_rows():
+    """With no negations M = H^3 / d = H (H^2 = d I), so hashing the basis vector e_j
+    reads row l = c mod d of H at column j: bit = [(-1)^popcount(l & j) > 0]."""
+    d, m, tau = 64, 20, 7                       # 140 columns: three rotations, the last partial
+    nrot = (m * tau + d - 1) // d
+    codes = oracle.fast_hash_codes(np.eye(d)[None], np.zeros((nrot, 3), np.uint64), m, tau)
+    for j in range(d):
+        for h in range(m):
+            want = sum(1 << b for b in range(tau) if bin(((h * tau + b) % d) & j).count("1") % 2 == 0)
+            assert codes[0, h, j] == want
+
+
+def test_fast_hyperplanes_rotations_are_orthogonal():
+    """Each rotation (1/d) H D3 H D2 H D1 has orthogonal rows of length sqrt(d); the
+    columns of R it supplies are those rows, the last rotation only its first ones."""
+    d, m, tau = 64, 30, 9                       # 270 columns: 4 full rotations + 14 rows
+    R = oracle.fast_hyperplanes(_signs(21, 5), d, m, tau)
+    for r in range(5):
+        blk = R[:, r * d:(r + 1) * d]
+        np.testing.assert_allclose(blk.T @ blk, d * np.eye(blk.shape[1]), atol=1e-12)
+    # distinct rotations are not aligned with each other
+    assert np.abs(R[:, :d].T @ R[:, d:2 * d]).max() > 1.0
+
+
+def test_fast_hash_sign_flip_invariances():
+    """D1 acts on the input: negating coordinate j in D1 is the same as negating x_j.
+    Negating every coordinate of any one D_i negates every projection, so every code
+    is complemented (all margins here are nonzero)."""
+    d, m, tau = 64, 16, 8
+    x = _unit(_rng(22).standard_normal((1, 40, d)))
+    s = _signs(23, 2)
+    base, margin = oracle.fast_hash_codes(x, s, m, tau, with_margin=True)
+    assert margin.min() > 0
+    for j in (0, 5, 63):
+        s1 = s.copy()
+        s1[0, 0] ^= np.uint64(1) << np.uint64(j)
+        s1[1, 0] ^= np.uint64(1) << np.uint64(j)
+        xj = x.copy()
+        xj[..., j] = -xj[..., j]
+        np.testing.assert_array_equal(oracle.fast_hash_codes(x, s1, m, tau), oracle.fast_hash_codes(xj, s, m, tau))
+        assert (oracle.fast_hash_codes(x, s1, m, tau) != base).any()
+    for i in range(3):
+        sf = s.copy()
+        sf[:, i] = ~sf[:, i]
+        np.testing.assert_array_equal(oracle.fast_hash_codes(x, sf, m, tau), (~base) & ((1 << tau) - 1))
+
+
+@pytest.mark.parametrize("theta", [math.pi / 6, math.pi / 3, math.pi / 2, 2 * math.pi / 3])
+def test_fast_hash_collision_law(theta):
+    """The pseudo-random rotation stands in for a random rotation (Sec. 3.2 "Speed-up",
+    after Andoni et al. 2015), so its bits follow the hyperplane law 1 - theta/pi and a
+    4-bit code (1 - theta/pi)^4.  The pair is sparse (x = e_0, y in span(e_0, e_1)),
+    where fewer than three D/H rounds visibly fail (one round gives collision 1 or 1/2
+    per bit; two give a 4-bit code rate of ~0.26 at theta = pi/2 instead of 0.0625)."""
+    d, tau, nrot = 64, 4, 1500
+    x = np.zeros((1, 2, d))
+    x[0, 0, 0] = 1.0
+    x[0, 1, 0], x[0, 1, 1] = math.cos(theta), math.sin(theta)
+    R = oracle.fast_hyperplanes(_signs(24, nrot), d, nrot * d // tau, tau)
+    z = x[0] @ R                                  # projections of both rows on every column
+    bit_hits = (z[0] > 0) == (z[1] > 0)
+    codes = oracle.hash_codes(x, R, nrot * d // tau, tau)[0]
+    code_hits = codes[:, 0] == codes[:, 1]
+    p = 1 - theta / math.pi
+    assert abs(bit_hits.mean() - p) <= 0.03
+    assert abs(code_hits.mean() - p ** tau) <= 0.015
