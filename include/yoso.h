@@ -92,6 +92,30 @@ yoso_status yoso_hash(const void *x, yoso_dtype dtype, int64_t bh, int64_t n, in
                       const float *R, int32_t m, int32_t tau, uint16_t *codes, void *stream);
 
 /*
+ * Hyperplanes of the fast hash (Sec. 3.2, "Speed-up": the approximate random
+ * projection of Andoni et al. 2015).  Rotation r = 0 .. ceil(m*tau/64) - 1 is the
+ * pseudo-random rotation
+ *
+ *   M_r = (1/64) H D3 H D2 H D1,   H the 64 x 64 Walsh-Hadamard matrix (Sylvester
+ *                                  order), D_i = diag(+-1) from signs[r][i-1],
+ *
+ * and column c = 64 r + l of R (c < m*tau) is row l of M_r:  R[j][c] = M_r[l][j].
+ * yoso_hash(x, ..., R, m, tau, codes) with this R is the fast hash: bit t of hash
+ * h is [ (M_r x)_l > 0 ] with h*tau + t = 64 r + l.  Expand once, then hash Q and
+ * K with the same R.
+ *
+ * signs  [ceil(m*tau/64)][3] uint64 (device): bit l of signs[r][i] set means
+ *        D_{i+1} of rotation r negates coordinate l.  The caller draws them
+ *        (uniform random bits); they are the hash function.
+ * R      [64][m*tau] fp32 (device), every entry written.  Each row of M_r has
+ *        length 8 (= sqrt(64), the mean length of a Gaussian column); entries are
+ *        multiples of 1/64 and come out exact.
+ * d must be 64; m, tau as for yoso_hash.  One small kernel on `stream`.
+ */
+yoso_status yoso_fast_hyperplanes(const uint64_t *signs, int32_t d, int32_t m, int32_t tau, float *R,
+                                  void *stream);
+
+/*
  * Forward (Sec. 3.2 overview: per hash, a table of 2^tau buckets holding the sum
  * of V over the keys hashed to each bucket; each query reads the bucket of its
  * own code; Sec. 3.1: the m samples are averaged).
@@ -202,7 +226,7 @@ const char *yoso_last_error(void);
  * first launch and live until the next yoso_timing_enable call; 0 disables and
  * frees them).  yoso_timing_reset() forgets the launches recorded so far.
  * yoso_timing_query() waits for the recorded events of `kernel` ("hash_kernel",
- * "table_kernel", "sort_kernel", "split_kernel", "pass_kernel", "reduce_kernel",
+ * "fast_hyperplanes_kernel", "table_kernel", "sort_kernel", "split_kernel", "pass_kernel", "reduce_kernel",
  * "zero_kernel", "l2norm_kernel", "l2norm_bwd_kernel", "expect_fwd_kernel",
  * "expect_bwd_kv_kernel", "expect_bwd_q_kernel")
  * and returns the summed duration and the launch count.

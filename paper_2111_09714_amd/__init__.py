@@ -6,6 +6,7 @@ if the library is missing or a call fails, an exception is raised.
 
 Function names follow the C ABI:
     yoso_hash(x, R, m, tau, codes)                     codes[bh, n, m] (int16/uint16 storage)
+    yoso_fast_hyperplanes(signs, m, tau, R)            R of the fast hash's pseudo-random rotations
     yoso_forward(qcodes, kcodes, v, m, tau, y, ws)     y = (1/m) sum_h B_h v
     yoso_backward(qcodes, kcodes, q, k, v, dy, m, tau, dq, dk, dv, ws)
     yoso_workspace_size(op, dtype, bh, n_q, n_k, d, m, tau) -> bytes
@@ -20,9 +21,11 @@ from typing import Optional
 
 __all__ = [
     "YosoError", "F32", "BF16", "OP_HASH", "OP_FORWARD", "OP_BACKWARD",
-    "lib", "lib_path", "yoso_workspace_size", "yoso_hash", "yoso_forward", "yoso_backward",
+    "lib", "lib_path", "yoso_workspace_size", "yoso_hash", "yoso_fast_hyperplanes", "yoso_forward",
+    "yoso_backward", "yoso_l2_normalize", "yoso_l2_normalize_backward", "yoso_expectation_forward",
+    "yoso_expectation_backward",
     "yoso_timing_enable", "yoso_timing_reset", "yoso_timing_query",
-    "workspace", "hash_qk", "forward", "backward",
+    "workspace", "hash_qk", "fast_hash_qk", "forward", "backward",
 ]
 
 F32, BF16 = 0, 1
@@ -54,6 +57,7 @@ def lib() -> ctypes.CDLL:
         L = ctypes.CDLL(_LIB_PATH)
         P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
         L.yoso_hash.argtypes = [P, I32, I64, I64, I32, P, I32, I32, P, P]
+        L.yoso_fast_hyperplanes.argtypes = [P, I32, I32, I32, P, P]
         L.yoso_forward.argtypes = [P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, SZ, P]
         L.yoso_backward.argtypes = [P, P, P, P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, P, P, SZ, P]
         L.yoso_workspace_size.argtypes = [I32, I32, I64, I64, I64, I32, I32, I32, ctypes.POINTER(SZ)]
@@ -134,6 +138,19 @@ def yoso_hash(x, R, m: int, tau: int, codes, stream=None) -> None:
     _expect(R, (d, m * tau), "R")
     _expect(codes, (bh, n, m), "codes")
     _check(lib().yoso_hash(_ptr(x), _dtype_code(x), bh, n, d, _ptr(R), m, tau, _ptr(codes), _stream(stream)))
+
+
+def yoso_fast_hyperplanes(signs, m: int, tau: int, R, stream=None) -> None:
+    """R[:, 64 r + l] = row l of (1/64) H D3 H D2 H D1 of rotation r (the fast hash's
+    hyperplanes); signs[r, i] (64-bit, int64 or uint64 storage) holds D_{i+1}'s negations."""
+    import torch
+    if signs.dtype not in (torch.int64, torch.uint64):
+        raise TypeError("signs must be an int64 or uint64 tensor (64-bit masks)")
+    if R.dtype != torch.float32:
+        raise TypeError("R must be float32")
+    _expect(signs, ((m * tau + 63) // 64, 3), "signs")
+    _expect(R, (64, m * tau), "R")
+    _check(lib().yoso_fast_hyperplanes(_ptr(signs), 64, m, tau, _ptr(R), _stream(stream)))
 
 
 def yoso_forward(qcodes, kcodes, v, m: int, tau: int, y, ws=None, stream=None) -> None:
@@ -242,6 +259,14 @@ def hash_qk(q, k, R, m: int, tau: int):
     yoso_hash(q, R, m, tau, qc)
     yoso_hash(k, R, m, tau, kc)
     return qc, kc
+
+
+def fast_hash_qk(q, k, signs, m: int, tau: int):
+    """Codes of Q and K under the fast hash of the rotations in ``signs``."""
+    import torch
+    R = torch.empty((64, m * tau), dtype=torch.float32, device=q.device)
+    yoso_fast_hyperplanes(signs, m, tau, R)
+    return hash_qk(q, k, R, m, tau)
 
 
 def forward(qcodes, kcodes, v, m: int, tau: int, n_q: Optional[int] = None):

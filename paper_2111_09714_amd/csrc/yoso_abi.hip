@@ -139,6 +139,17 @@ yoso_status yoso_hash(const void *x, yoso_dtype dtype, int64_t bh, int64_t n, in
                          "yoso_hash");
 }
 
+yoso_status yoso_fast_hyperplanes(const uint64_t *signs, int32_t d, int32_t m, int32_t tau, float *R,
+                                  void *stream) {
+    g_last_error[0] = '\0';
+    if (d != 64) return fail(YOSO_ERR_SHAPE, "d = %d; only d = 64 is supported", d);
+    YOSO_TRY(check_hash(m, tau));
+    YOSO_TRY(check_ptr(signs, 3 * (((int64_t)m * tau + 63) / 64), "signs"));
+    YOSO_TRY(check_ptr(R, (int64_t)d * m * tau, "R"));
+    return device_status(yoso::launch_fast_hyperplanes(signs, m, tau, R, static_cast<hipStream_t>(stream)),
+                         "yoso_fast_hyperplanes");
+}
+
 yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const void *v, yoso_dtype dtype,
                          int64_t bh, int64_t n_q, int64_t n_k, int32_t d, int32_t m, int32_t tau, void *y,
                          void *workspace, size_t workspace_bytes, void *stream) {

@@ -231,3 +231,23 @@ def test_expectation_forward_rejects(L, kw, status):
 ])
 def test_expectation_backward_rejects(L, kw, status):
     assert _ebwd(L, **kw) == status
+
+
+def _fhp(L, signs=FAKE, d=64, m=32, tau=8, R=FAKE):
+    return L.yoso_fast_hyperplanes(signs, d, m, tau, R, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(d=32), 2),
+    (dict(tau=0), 3),
+    (dict(tau=13), 3),
+    (dict(m=0), 3),
+    (dict(m=65), 3),
+    (dict(m=64, tau=9), 3),      # m*tau = 576 > 512
+    (dict(signs=None), 1),
+    (dict(R=None), 1),
+    (dict(signs=FAKE + 8), 5),
+    (dict(R=FAKE + 4), 5),
+])
+def test_fast_hyperplanes_rejects(L, kw, status):
+    assert _fhp(L, **kw) == status

@@ -16,6 +16,9 @@ Input recipe (stated once, used everywhere):
   * V, dY: N(0, 1), same storage dtype as Q.
   * R: N(0, 1) fp32 of shape [d, m*tau], one matrix shared by every head; column
     h*tau+b is hyperplane b of hash h (Sec. 3.2, "we sample a hash function").
+  * signs: uniform random 64-bit masks of shape [ceil(m*tau/64), 3], the +-1
+    diagonals D1, D2, D3 of the fast hash's pseudo-random rotations (Sec. 3.2
+    "Speed-up"), one set shared by every head.
 
 Every array comes from its own numpy PCG64 stream spawned from one seed, so any
 subset of heads can be regenerated identically.
@@ -27,7 +30,7 @@ from typing import Dict, Optional, Sequence
 
 import numpy as np
 
-__all__ = ["Workload", "WORKLOADS", "make_inputs", "bf16_round", "bf16_bits"]
+__all__ = ["Workload", "WORKLOADS", "make_inputs", "fast_hash_signs", "bf16_round", "bf16_bits"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -142,4 +145,15 @@ def make_inputs(
             out[name + "_bits"] = bf16_bits(out[name])
             out[name] = bf16_bits_to_f32(out[name + "_bits"])
     out["R"] = R
+    out["signs"] = fast_hash_signs(w)
     return out
+
+
+def fast_hash_signs(w: Workload) -> np.ndarray:
+    """The D1, D2, D3 masks of the fast hash for workload ``w`` (uint64 [ceil(m*tau/64), 3]).
+
+    Drawn from the seed's child stream number bh + 1, after the bh + 1 streams of
+    the other arrays, so adding them left every other array unchanged."""
+    seq = np.random.SeedSequence(w.seed).spawn(w.bh + 2)[w.bh + 1]
+    nrot = (w.m * w.tau + 63) // 64
+    return np.random.Generator(np.random.PCG64(seq)).integers(0, 2**64, size=(nrot, 3), dtype=np.uint64)
