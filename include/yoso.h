@@ -85,7 +85,8 @@ typedef enum { YOSO_OP_HASH = 0, YOSO_OP_FORWARD = 1, YOSO_OP_BACKWARD = 2 } yos
  * codes  [bh][n][m]  uint16 output, low tau bits used (consumers read only the
  *                    low tau bits of the codes they are given).
  * The sign test is strict (a zero projection gives bit 0).  Bits whose
- * projection lies within about 1e-6 of zero may differ from an exact-arithmetic
+ * projection lies within about 2^-20 |x[b][i]| |R[:, c]| of zero (~1e-5 for a
+ * unit row and Gaussian hyperplanes) may differ from an exact-arithmetic
  * evaluation; everywhere else the code is exact.
  */
 yoso_status yoso_hash(const void *x, yoso_dtype dtype, int64_t bh, int64_t n, int32_t d,
