@@ -117,6 +117,25 @@ yoso_status yoso_fast_hyperplanes(const uint64_t *signs, int32_t d, int32_t m, i
                                   void *stream);
 
 /*
+ * The fast hash itself (Sec. 3.2, "Speed-up"; Andoni et al. 2015): the rotations
+ * of yoso_fast_hyperplanes applied to each row by fast Walsh-Hadamard transforms,
+ * O(m tau log2 d) additions per row instead of a dense projection.
+ *
+ *   codes[b][i][h] = sum_{t<tau} [ (H D3 H D2 H D1 x[b][i])_l > 0 ] << t,
+ *                    rotation r and coordinate l given by h*tau + t = 64 r + l.
+ *
+ * x      [bh][n][d]  rows to hash (fp32 or bf16 per dtype), d = 64.
+ * signs  [ceil(m*tau/64)][3] uint64 (device), as for yoso_fast_hyperplanes.
+ * codes  [bh][n][m]  uint16 output, the same layout and sign convention as
+ *                    yoso_hash (strict test; bit for bit equal to yoso_hash with
+ *                    the R of yoso_fast_hyperplanes except for projections within
+ *                    about 1e-6 |x| of zero).
+ * Arithmetic is fp32 (each butterfly an exact +-1 fused multiply-add).
+ */
+yoso_status yoso_fast_hash(const void *x, yoso_dtype dtype, int64_t bh, int64_t n, int32_t d,
+                           const uint64_t *signs, int32_t m, int32_t tau, uint16_t *codes, void *stream);
+
+/*
  * Forward (Sec. 3.2 overview: per hash, a table of 2^tau buckets holding the sum
  * of V over the keys hashed to each bucket; each query reads the bucket of its
  * own code; Sec. 3.1: the m samples are averaged).
@@ -227,7 +246,7 @@ const char *yoso_last_error(void);
  * first launch and live until the next yoso_timing_enable call; 0 disables and
  * frees them).  yoso_timing_reset() forgets the launches recorded so far.
  * yoso_timing_query() waits for the recorded events of `kernel` ("hash_kernel",
- * "fast_hyperplanes_kernel", "table_kernel", "sort_kernel", "split_kernel", "pass_kernel", "reduce_kernel",
+ * "fast_hash_kernel", "fast_hyperplanes_kernel", "table_kernel", "sort_kernel", "split_kernel", "pass_kernel", "reduce_kernel",
  * "zero_kernel", "l2norm_kernel", "l2norm_bwd_kernel", "expect_fwd_kernel",
  * "expect_bwd_kv_kernel", "expect_bwd_q_kernel")
  * and returns the summed duration and the launch count.

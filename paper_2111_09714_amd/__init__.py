@@ -7,6 +7,7 @@ if the library is missing or a call fails, an exception is raised.
 Function names follow the C ABI:
     yoso_hash(x, R, m, tau, codes)                     codes[bh, n, m] (int16/uint16 storage)
     yoso_fast_hyperplanes(signs, m, tau, R)            R of the fast hash's pseudo-random rotations
+    yoso_fast_hash(x, signs, m, tau, codes)            the fast hash (Walsh-Hadamard rotations per row)
     yoso_forward(qcodes, kcodes, v, m, tau, y, ws)     y = (1/m) sum_h B_h v
     yoso_backward(qcodes, kcodes, q, k, v, dy, m, tau, dq, dk, dv, ws)
     yoso_workspace_size(op, dtype, bh, n_q, n_k, d, m, tau) -> bytes
@@ -21,7 +22,7 @@ from typing import Optional
 
 __all__ = [
     "YosoError", "F32", "BF16", "OP_HASH", "OP_FORWARD", "OP_BACKWARD",
-    "lib", "lib_path", "yoso_workspace_size", "yoso_hash", "yoso_fast_hyperplanes", "yoso_forward",
+    "lib", "lib_path", "yoso_workspace_size", "yoso_hash", "yoso_fast_hyperplanes", "yoso_fast_hash", "yoso_forward",
     "yoso_backward", "yoso_l2_normalize", "yoso_l2_normalize_backward", "yoso_expectation_forward",
     "yoso_expectation_backward",
     "yoso_timing_enable", "yoso_timing_reset", "yoso_timing_query",
@@ -58,6 +59,7 @@ def lib() -> ctypes.CDLL:
         P, I64, I32, SZ = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
         L.yoso_hash.argtypes = [P, I32, I64, I64, I32, P, I32, I32, P, P]
         L.yoso_fast_hyperplanes.argtypes = [P, I32, I32, I32, P, P]
+        L.yoso_fast_hash.argtypes = [P, I32, I64, I64, I32, P, I32, I32, P, P]
         L.yoso_forward.argtypes = [P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, SZ, P]
         L.yoso_backward.argtypes = [P, P, P, P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, P, P, SZ, P]
         L.yoso_workspace_size.argtypes = [I32, I32, I64, I64, I64, I32, I32, I32, ctypes.POINTER(SZ)]
@@ -151,6 +153,19 @@ def yoso_fast_hyperplanes(signs, m: int, tau: int, R, stream=None) -> None:
     _expect(signs, ((m * tau + 63) // 64, 3), "signs")
     _expect(R, (64, m * tau), "R")
     _check(lib().yoso_fast_hyperplanes(_ptr(signs), 64, m, tau, _ptr(R), _stream(stream)))
+
+
+def yoso_fast_hash(x, signs, m: int, tau: int, codes, stream=None) -> None:
+    """codes[b, i, h]: the signs of the rows of x under the rotations H D3 H D2 H D1 of ``signs``."""
+    import torch
+    _codes_ok(codes)
+    if signs.dtype not in (torch.int64, torch.uint64):
+        raise TypeError("signs must be an int64 or uint64 tensor (64-bit masks)")
+    bh, n, d = x.shape
+    _expect(signs, ((m * tau + 63) // 64, 3), "signs")
+    _expect(codes, (bh, n, m), "codes")
+    _check(lib().yoso_fast_hash(_ptr(x), _dtype_code(x), bh, n, d, _ptr(signs), m, tau, _ptr(codes),
+                                _stream(stream)))
 
 
 def yoso_forward(qcodes, kcodes, v, m: int, tau: int, y, ws=None, stream=None) -> None:
@@ -262,11 +277,13 @@ def hash_qk(q, k, R, m: int, tau: int):
 
 
 def fast_hash_qk(q, k, signs, m: int, tau: int):
-    """Codes of Q and K under the fast hash of the rotations in ``signs``."""
+    """Codes of Q and K under the fast hash of the rotations in ``signs`` (fresh int16 tensors)."""
     import torch
-    R = torch.empty((64, m * tau), dtype=torch.float32, device=q.device)
-    yoso_fast_hyperplanes(signs, m, tau, R)
-    return hash_qk(q, k, R, m, tau)
+    qc = torch.empty((q.shape[0], q.shape[1], m), dtype=torch.int16, device=q.device)
+    kc = torch.empty((k.shape[0], k.shape[1], m), dtype=torch.int16, device=k.device)
+    yoso_fast_hash(q, signs, m, tau, qc)
+    yoso_fast_hash(k, signs, m, tau, kc)
+    return qc, kc
 
 
 def forward(qcodes, kcodes, v, m: int, tau: int, n_q: Optional[int] = None):

@@ -15,7 +15,8 @@ CSRC = os.path.join(PKG, "csrc")
 ROOT = os.path.dirname(PKG)
 BUILD_DIR = os.path.join(ROOT, "_build", "libyoso")
 LIB_PATH = os.path.join(PKG, "libyoso.so")
-SOURCES = ["hash.hip", "tables.hip", "pairs.hip", "norm.hip", "expect.hip", "timing.hip", "yoso_abi.hip"]
+SOURCES = ["hash.hip", "fasthash.hip", "tables.hip", "pairs.hip", "norm.hip", "expect.hip", "timing.hip",
+           "yoso_abi.hip"]
 
 
 def hipcc() -> str:

@@ -218,50 +218,6 @@ __global__ __launch_bounds__(64 * WAVES) void hash_kernel(const void *__restrict
     }
 }
 
-// Hyperplanes of the fast hash (Sec. 3.2 "Speed-up": the approximate random
-// projection of Andoni et al. 2015, a pseudo-random rotation H D3 H D2 H D1 with H
-// the 64 x 64 Walsh-Hadamard matrix and D_i random +-1 diagonals).  On gfx950 the
-// rotation is not applied row by row: at d = 64 its 3 * 64 * 6 butterfly additions
-// per 64 projections cost more VALU time than the dense product costs on MFMA.  So
-// each rotation is expanded once into the 64 rows it projects onto, and the hash
-// kernel above evaluates them like any hyperplane matrix R.
-//
-// Thread j of workgroup r pushes e_j through the three rounds (negate the
-// coordinates that D_i flips, then the in-place Walsh-Hadamard butterflies in
-// natural order), which yields column j of H D3 H D2 H D1, i.e. entry j of each of
-// the rotation's 64 rows; scaled by 1/64 they are row j of R's columns 64r .. 64r+63.
-// Every intermediate is an integer of magnitude at most 4096, so the fp32 result
-// is exact (each entry a multiple of 1/64 of magnitude at most 8).
-__global__ __launch_bounds__(64) void fast_hyperplanes_kernel(const uint64_t *__restrict__ signs, int ncol,
-                                                              float *__restrict__ R) {
-    const int r = blockIdx.x;
-    const int j = threadIdx.x;
-    float v[64];
-#pragma unroll
-    for (int l = 0; l < 64; l++) v[l] = l == j ? 1.f : 0.f;
-#pragma unroll
-    for (int round = 0; round < 3; round++) {
-        const uint64_t s = signs[3 * r + round];
-#pragma unroll
-        for (int l = 0; l < 64; l++) v[l] = ((s >> l) & 1u) ? -v[l] : v[l];
-#pragma unroll
-        for (int h = 1; h < 64; h <<= 1) {
-#pragma unroll
-            for (int l = 0; l < 64; l++) {
-                if (l & h) continue;
-                const float a = v[l], b = v[l + h];
-                v[l] = a + b;
-                v[l + h] = a - b;
-            }
-        }
-    }
-    float *dst = R + (int64_t)j * ncol + r * 64;
-    const int valid = ncol - r * 64;  // columns of this rotation that R holds (the last one may be cut)
-#pragma unroll
-    for (int l = 0; l < 64; l++)
-        if (l < valid) dst[l] = v[l] * (1.f / 64.f);
-}
-
 }  // namespace
 
 // Launch shape of the hash kernel: 8-wave workgroups, two per CU, while two fit
@@ -318,14 +274,6 @@ hipError_t launch_hash(const void *x, bool bf16, int64_t bh, int64_t n, const fl
             hipLaunchKernelGGL((hash_kernel<false, 16>), dim3((unsigned)grid), dim3(1024), lds, stream, x, rows, R,
                                m, tau, codes, tiles);
     }
-    return hipGetLastError();
-}
-
-hipError_t launch_fast_hyperplanes(const uint64_t *signs, int m, int tau, float *R, hipStream_t stream) {
-    const int ncol = m * tau;
-    const int nrot = (ncol + 63) / 64;
-    KernelTimer timer("fast_hyperplanes_kernel", stream);
-    hipLaunchKernelGGL(fast_hyperplanes_kernel, dim3(nrot), dim3(64), 0, stream, signs, ncol, R);
     return hipGetLastError();
 }
 

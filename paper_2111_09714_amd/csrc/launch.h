@@ -33,6 +33,8 @@ hipError_t launch_hash(const void *x, bool bf16, int64_t bh, int64_t n, const fl
                        uint16_t *codes, hipStream_t stream);
 
 hipError_t launch_fast_hyperplanes(const uint64_t *signs, int m, int tau, float *R, hipStream_t stream);
+hipError_t launch_fast_hash(const void *x, bool bf16, int64_t bh, int64_t n, const uint64_t *signs, int m, int tau,
+                            uint16_t *codes, hipStream_t stream);
 
 hipError_t launch_table(const uint16_t *src_codes, const void *values, const uint16_t *dst_codes, void *out,
                         bool bf16, int64_t bh, int64_t n_src, int64_t n_dst, int m, int tau, void *workspace,

@@ -150,6 +150,20 @@ yoso_status yoso_fast_hyperplanes(const uint64_t *signs, int32_t d, int32_t m, i
                          "yoso_fast_hyperplanes");
 }
 
+yoso_status yoso_fast_hash(const void *x, yoso_dtype dtype, int64_t bh, int64_t n, int32_t d,
+                           const uint64_t *signs, int32_t m, int32_t tau, uint16_t *codes, void *stream) {
+    g_last_error[0] = '\0';
+    YOSO_TRY(check_dtype(dtype));
+    YOSO_TRY(check_shape(bh, n, 0, d, m));
+    YOSO_TRY(check_hash(m, tau));
+    YOSO_TRY(check_ptr(x, bh * n * d, "x"));
+    YOSO_TRY(check_ptr(signs, 3 * (((int64_t)m * tau + 63) / 64), "signs"));
+    YOSO_TRY(check_ptr(codes, bh * n * m, "codes"));
+    return device_status(yoso::launch_fast_hash(x, dtype == YOSO_BF16, bh, n, signs, m, tau, codes,
+                                                static_cast<hipStream_t>(stream)),
+                         "yoso_fast_hash");
+}
+
 yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const void *v, yoso_dtype dtype,
                          int64_t bh, int64_t n_q, int64_t n_k, int32_t d, int32_t m, int32_t tau, void *y,
                          void *workspace, size_t workspace_bytes, void *stream) {

@@ -251,3 +251,29 @@ def _fhp(L, signs=FAKE, d=64, m=32, tau=8, R=FAKE):
 ])
 def test_fast_hyperplanes_rejects(L, kw, status):
     assert _fhp(L, **kw) == status
+
+
+def _fh(L, x=FAKE, dtype=0, bh=2, n=128, d=64, signs=FAKE, m=32, tau=8, codes=FAKE):
+    return L.yoso_fast_hash(x, dtype, bh, n, d, signs, m, tau, codes, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=2), 4),
+    (dict(d=32), 2),
+    (dict(bh=-1), 2),
+    (dict(n=70000), 2),
+    (dict(tau=13), 3),
+    (dict(m=65), 3),
+    (dict(x=None), 1),
+    (dict(signs=None), 1),
+    (dict(codes=None), 1),
+    (dict(signs=FAKE + 8), 5),
+    (dict(codes=FAKE + 2), 5),
+])
+def test_fast_hash_rejects(L, kw, status):
+    assert _fh(L, **kw) == status
+
+
+def test_fast_hash_empty_is_a_no_op(L):
+    # zero rows: x and codes may be NULL (signs, like R for yoso_hash, is still required)
+    assert L.yoso_fast_hash(None, 0, 0, 128, 64, FAKE, 32, 8, None, None) == 0

@@ -85,7 +85,9 @@ def check_codes(x, signs, m, tau, got):
 
 @pytest.mark.parametrize("bh,n,m,tau,dtype", [(2, 300, 32, 8, "f32"), (1, 1000, 30, 9, "f32"),
                                               (3, 129, 16, 6, "bf16"), (1, 1, 1, 1, "f32"),
-                                              (2, 65, 64, 8, "f32")])
+                                              (2, 65, 64, 8, "f32"), (1, 77, 7, 5, "f32"),
+                                              (2, 300, 32, 9, "bf16"), (1, 200, 20, 2, "f32"),
+                                              (1, 257, 33, 4, "bf16"), (1, 130, 64, 1, "f32")])
 def test_fast_hash_codes(bh, n, m, tau, dtype):
     g = np.random.default_rng(7 * n + m + tau)
     q = g.standard_normal((bh, n, 64))
@@ -135,3 +137,32 @@ def test_attention_on_fast_codes():
         e = np.linalg.norm(host(a) - b) / np.linalg.norm(b)
         log(f"[attention on fast codes] {name} rel err {e:.2e}")
         assert e <= 1e-4, (name, e)
+
+
+def test_fast_hash_matches_dense_hash_of_expanded_rotations():
+    """Both GPU routes to the fast hash agree: the per-row Walsh-Hadamard kernel and
+    the dense hash kernel on the expanded rotations (except near-zero projections)."""
+    w = WORKLOADS["lra_n4096"]
+    inp = make_inputs(w, heads=[3, 17])
+    q = to_dev(inp["q"], "f32")
+    sd = signs_dev(inp["signs"])
+    R = torch.empty((64, w.m * w.tau), device="cuda")
+    Y.yoso_fast_hyperplanes(sd, w.m, w.tau, R)
+    dense = torch.empty((2, w.n, w.m), dtype=torch.int16, device="cuda")
+    fast = torch.empty_like(dense)
+    Y.yoso_hash(q, R, w.m, w.tau, dense)
+    Y.yoso_fast_hash(q, sd, w.m, w.tau, fast)
+    torch.cuda.synchronize()
+    _, margin = oracle.fast_hash_codes(inp["q"], inp["signs"], w.m, w.tau, with_margin=True)
+    differ = codes_np(dense) != codes_np(fast)
+    log(f"[fast vs dense route] differing codes {int(differ.sum())}, all near zero: {bool((margin[differ] <= MARGIN).all())}")
+    assert (margin[differ] <= MARGIN).all()
+
+
+def test_fast_hash_empty():
+    s = torch.zeros((4, 3), dtype=torch.int64, device="cuda")
+    for bh, n in ((0, 5), (2, 0)):
+        x = torch.randn(bh, n, 64, device="cuda")
+        c = torch.empty((bh, n, 32), dtype=torch.int16, device="cuda")
+        Y.yoso_fast_hash(x, s, 32, 8, c)
+    torch.cuda.synchronize()
