@@ -12,7 +12,9 @@ synchronisation.  One JSON line is printed on stdout.
 
 Per-kernel durations come from HIP events that the library records around each
 of its launches on the launch stream (yoso_timing_enable); the roofline object
-describes the kernel with the largest total time.  The CPU baseline is the fp64
+describes the kernel with the largest total time.  For the dQ, dK pair kernel that
+is a matrix-unit roofline (3d multiply-adds per colliding pair, fp32 peak), with
+its HBM figures alongside.  The CPU baseline is the fp64
 oracle, timed on this machine's host cores on a stated sample of heads.
 """
 from __future__ import annotations
@@ -50,6 +52,20 @@ def kernel_algorithmic(w, kernel: str):
     if per_head is None:
         return None
     return per_head * w.bh
+
+
+def colliding_pairs(qc, kc, tau: int) -> int:
+    """Number of (query, key) pairs that share a bucket, summed over heads and hashes:
+    sum over (head, hash, bucket) of count_q * count_k, from the codes on the host."""
+    import numpy as np
+    B = 1 << tau
+    q = qc.cpu().numpy().astype(np.int64) & (B - 1)  # [bh, n_q, m]
+    k = kc.cpu().numpy().astype(np.int64) & (B - 1)  # [bh, n_k, m]
+    bh, _, m = q.shape
+    unit = (np.arange(bh)[:, None, None] * m + np.arange(m)[None, None, :]) * B
+    hq = np.bincount((unit + q).ravel(), minlength=bh * m * B)
+    hk = np.bincount((unit + k).ravel(), minlength=bh * m * B)
+    return int((hq * hk).sum())
 
 
 COPY_BYTES = 256 << 20
@@ -201,6 +217,20 @@ def main() -> int:
         roofline = {"kernel": dominant, "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                     "algorithmic_bytes_per_launch": alg, "avg_launch_us": round(kernels[dominant]["avg_us"], 2)}
+    if dominant == "pass_kernel":
+        # dQ, dK are dense per-bucket contractions, bound by the matrix units: per
+        # colliding (query, key) pair 3d multiply-adds (dy.v once, then its share of
+        # dQ and of dK), in fp32; the pairs are counted exactly from this step's codes
+        pairs = colliding_pairs(qc, kc, w.tau)
+        flops = 6 * w.d * pairs
+        tf = flops / avg_s / 1e12
+        hbm = roofline
+        roofline = {"kernel": dominant, "bound": "mfma", "achieved": round(tf, 2), "peak": FP32_PEAK_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(tf / FP32_PEAK_TFLOPS, 4), "traffic": None,
+                    "algorithmic_flops_per_launch": flops, "colliding_pairs_per_launch": pairs,
+                    "avg_launch_us": round(kernels[dominant]["avg_us"], 2),
+                    "hbm": {"achieved": hbm["achieved"], "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": hbm["frac"],
+                            "algorithmic_bytes_per_launch": alg}}
 
     if roofline is not None:
         roofline["traffic"] = measured_traffic(dominant, w.name)
