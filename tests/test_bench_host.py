@@ -1,0 +1,37 @@
+"""Host-side pieces of bench.py: the colliding-pair count behind the dQ/dK roofline
+and the refusal of more than one GPU (no device needed)."""
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+torch = pytest.importorskip("torch")
+import bench  # noqa: E402
+
+
+@pytest.mark.parametrize("bh,nq,nk,m,tau", [(3, 50, 57, 4, 3), (1, 1, 1, 1, 1), (2, 200, 130, 7, 8)])
+def test_colliding_pairs_matches_brute_force(bh, nq, nk, m, tau):
+    g = np.random.default_rng(bh + nq + m)
+    # high bits above tau are set at random: only the low tau bits are a code
+    q = g.integers(0, 2**15, (bh, nq, m)).astype(np.int16)
+    k = g.integers(0, 2**15, (bh, nk, m)).astype(np.int16)
+    mask = (1 << tau) - 1
+    brute = sum(int(((q[b, :, h, None] & mask) == (k[b, None, :, h] & mask)).sum()) for b in range(bh) for h in range(m))
+    assert bench.colliding_pairs(torch.from_numpy(q), torch.from_numpy(k), tau) == brute
+
+
+def test_identical_codes_give_all_pairs_per_bucket():
+    # every row in bucket 0: n_q * n_k pairs per (head, hash)
+    q = torch.zeros((2, 30, 5), dtype=torch.int16)
+    k = torch.zeros((2, 20, 5), dtype=torch.int16)
+    assert bench.colliding_pairs(q, k, 8) == 2 * 5 * 30 * 20
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode == 2 and "one GPU" in r.stderr
