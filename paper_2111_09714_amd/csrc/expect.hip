@@ -129,8 +129,11 @@ __global__ __launch_bounds__(kExpThreads, 2) void expect_kernel(ExpArgs a) {
     const float half_tau = 0.5f * static_cast<float>(a.tau);
     const int pr = 4 * g + (c >> 2), a4 = c & 3;
 
-    // tile loading: thread t handles streamed row t/4, dims 16 (t%4) + [0, 16)
-    const int lrow = tid >> 2, lq = tid & 3;
+    // tile loading: lane l of wave w stages streamed row 16w + (l & 15), dims
+    // 16 (l >> 4) + [0, 16): the 16 lanes of a quarter-wave write 16 rows at one
+    // chunk, which the swizzle puts on distinct banks (with 4 rows x 4 chunks per
+    // quarter-wave, rows 0-3 would land on one set of 4 chunks)
+    const int lrow = 16 * wave + (lane & 15), lq = lane >> 4;
     auto stage = [&](unsigned char *dst, const void *src, int c0, bool unit) {
         const int row = c0 + lrow;
         float x[16];
@@ -142,8 +145,8 @@ __global__ __launch_bounds__(kExpThreads, 2) void expect_kernel(ExpArgs a) {
             float ss = 0.f;
 #pragma unroll
             for (int i = 0; i < 16; i++) ss += x[i] * x[i];
-            ss += dpp_mov<0xB1>(ss);  // the row's four threads are one aligned quad
-            ss += dpp_mov<0x4E>(ss);
+            ss += __shfl_xor(ss, 16);  // the row's four threads are lanes l, l^16, l^32, l^48
+            ss += __shfl_xor(ss, 32);
             scale = ss > 0.f ? kUnitScale / sqrtf(ss) : 0.f;
         }
         if (row >= a.n_c) scale = 0.f;  // rows past the end are zero (and weighted 0)

@@ -102,10 +102,28 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
     for (int c = tid; c < kSortWaves * B; c += kSortThreads) hist[c] = 0;
     for (int c = tid; c < pw * B; c += kSortThreads) masks[c] = 0ull;
     __syncthreads();
-    for (int64_t i = r0 + lane; i < r1; i += 64) {
-        const int c = codes[i * m] & (B - 1);
-        if (stage) cst[i] = static_cast<uint16_t>(c);
-        atomicAdd(&hist[wave * B + c], 1);
+    {
+        // sixteen codes per lane in flight before their counts are added (the codes
+        // come with stride m, one 64-byte segment each; one at a time, every load's
+        // latency was paid in turn); rows past r1 read row r1 - 1 and are not counted
+        constexpr int U = 16;
+        for (int64_t i0 = r0 + lane; i0 < r1; i0 += 64 * U) {
+            uint32_t cc[U];
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int64_t i = i0 + 64 * u;
+                cc[u] = codes[(i < r1 ? i : r1 - 1) * m];
+            }
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int64_t i = i0 + 64 * u;
+                if (i < r1) {
+                    const int c = static_cast<int>(cc[u]) & (B - 1);
+                    if (stage) cst[i] = static_cast<uint16_t>(c);
+                    atomicAdd(&hist[wave * B + c], 1);
+                }
+            }
+        }
     }
     __syncthreads();
 
