@@ -118,6 +118,22 @@ def test_fast_hash_full_size():
             assert bad == 0
 
 
+def test_fast_hash_full_size_bf16():
+    """The 32768-token bf16 workload (tau = 9: the general, straddling extraction),
+    two of its 24 heads, Q and K, all rows checked."""
+    w = WORKLOADS["bf16_n32768"]
+    inp = make_inputs(w, heads=[0, w.bh - 1])
+    sd = signs_dev(inp["signs"])
+    for name in ("q", "k"):
+        xd = torch.from_numpy(inp[name + "_bits"].view(np.int16)).cuda().view(torch.bfloat16).contiguous()
+        c = torch.empty((2, w.n, w.m), dtype=torch.int16, device="cuda")
+        Y.yoso_fast_hash(xd, sd, w.m, w.tau, c)
+        torch.cuda.synchronize()
+        bad, unsure = check_codes(inp[name], inp["signs"], w.m, w.tau, codes_np(c))
+        log(f"[fast hash bf16_n32768 {name}] mismatches {bad}, unchecked {unsure:.2e}")
+        assert bad == 0
+
+
 def test_attention_on_fast_codes():
     """Hash with the fast hash, then forward and backward; the oracle recomputes the
     attention and its gradients from the same codes (after checking them)."""
