@@ -8,7 +8,10 @@ A step is one pass of the whole hot path over one batch of synthetic input:
 for every (batch, head) of the workload (default: 16 x 2 heads, n = 4096, d = 64,
 m = 32 hashes of tau = 8 bits, fp32).  Inputs are resident in HBM before the
 timed region; W warm-up steps are followed by K timed steps bracketed by device
-synchronisation.  One JSON line is printed on stdout.
+synchronisation.  The timed steps replay the step captured once into a HIP graph
+(the same kernels on the same inputs, without host launch gaps; `execution`
+says which mode ran, and `eager_ms_per_step` gives the eager time as well).
+One JSON line is printed on stdout.
 
 Per-kernel durations come from HIP events that the library records around each
 of its launches on the launch stream (yoso_timing_enable); the roofline object
@@ -179,35 +182,64 @@ def main() -> int:
     ws_b = Y.workspace(Y.OP_BACKWARD, q, w.m, w.tau)
     stream = torch.cuda.current_stream()
 
-    def step():
-        Y.yoso_hash(q, R, w.m, w.tau, qc, stream)
-        Y.yoso_hash(k, R, w.m, w.tau, kc, stream)
-        Y.yoso_forward(qc, kc, v, w.m, w.tau, y, ws_f, stream)
-        Y.yoso_backward(qc, kc, q, k, v, dy, w.m, w.tau, dq, dk, dv, ws_b, stream)
+    def step(s):
+        Y.yoso_hash(q, R, w.m, w.tau, qc, s)
+        Y.yoso_hash(k, R, w.m, w.tau, kc, s)
+        Y.yoso_forward(qc, kc, v, w.m, w.tau, y, ws_f, s)
+        Y.yoso_backward(qc, kc, q, k, v, dy, w.m, w.tau, dq, dk, dv, ws_b, s)
 
+    # per-kernel durations: eager steps with the library's HIP-event timer on
     Y.yoso_timing_enable(4 * (args.steps + args.warmup) + 8)
     for _ in range(args.warmup):
-        step()
+        step(stream)
     torch.cuda.synchronize()
     Y.yoso_timing_reset()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     start.record(stream)
     for _ in range(args.steps):
-        step()
+        step(stream)
     stop.record(stream)
     torch.cuda.synchronize()
-    ms_total = start.elapsed_time(stop)
-    ms_per_step = ms_total / args.steps
-
+    eager_ms_per_step = start.elapsed_time(stop) / args.steps
     kernels = {}
     for name in ("hash_kernel", "table_kernel", "sort_kernel", "split_kernel", "pass_kernel", "reduce_kernel",
                  "zero_kernel"):
         tot, n = Y.yoso_timing_query(name)
         if n:
             kernels[name] = {"launches_per_step": n / args.steps, "avg_us": 1000.0 * tot / n,
-                             "share_of_step": tot / ms_total}
+                             "share_of_step": tot / (eager_ms_per_step * args.steps)}
     Y.yoso_timing_enable(0)
+
+    # The timed run: the step captured once into a HIP graph (stream capture; the
+    # library enqueues kernels only) and replayed: the same kernels on the same
+    # inputs, without the host's launch gaps.  Eager steps if capture fails.
+    execution = "hip_graph"
+    try:
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            step(side)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            step(torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        run = graph.replay
+    except Exception as exc:  # report and time eagerly
+        execution = f"eager (graph capture failed: {type(exc).__name__})"
+        run = lambda: step(stream)  # noqa: E731
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    start.record(stream)
+    for _ in range(args.steps):
+        run()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms_total = start.elapsed_time(stop)
+    ms_per_step = ms_total / args.steps
+
     dominant = max(kernels, key=lambda kname: kernels[kname]["avg_us"] * kernels[kname]["launches_per_step"])
     alg = kernel_algorithmic(w, dominant)
     avg_s = kernels[dominant]["avg_us"] * 1e-6
@@ -357,6 +389,8 @@ def main() -> int:
         "data": "synthetic",
         "config": {"workload": w.name, "batch": w.batch, "heads": w.heads, "seq_len": w.n, "head_dim": w.d,
                    "tau": w.tau, "hashes": w.m, "inputs": w.dist},
+        "execution": execution,
+        "eager_ms_per_step": round(eager_ms_per_step, 5),
         "hbm_roofline_frac": round(hbm_frac, 4),
         "algorithmic_bytes_per_step": alg_step_bytes,
         "roofline": roofline,
