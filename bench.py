@@ -365,9 +365,24 @@ def main() -> int:
             torch.mul(src, 1.0, out=dst)
         torch.cuda.synchronize()
 
+    # measured HBM copy bandwidth (1 GiB device-to-device copy, bytes read + written,
+    # median of five), the practical ceiling next to the 8 TB/s vendor figure
+    csrc = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    cdst = torch.empty_like(csrc)
+    copy_ms = []
+    for _ in range(6):
+        start.record(stream)
+        cdst.copy_(csrc)
+        stop.record(stream)
+        torch.cuda.synchronize()
+        copy_ms.append(start.elapsed_time(stop))
+    copy_gbs = 2 * csrc.numel() * 4 / (sorted(copy_ms[1:])[2] * 1e-3) / 1e9
+    del csrc, cdst
+
     tokens_per_s = w.tokens / (ms_per_step * 1e-3)
     alg_step_bytes = 11 * w.n * w.d * w.elem_bytes * w.bh
     hbm_frac = alg_step_bytes / (ms_per_step * 1e-3) / (HBM_PEAK_GBS * 1e9)
+    copy_frac = alg_step_bytes / (ms_per_step * 1e-3) / (copy_gbs * 1e9)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -392,6 +407,8 @@ def main() -> int:
         "execution": execution,
         "eager_ms_per_step": round(eager_ms_per_step, 5),
         "hbm_roofline_frac": round(hbm_frac, 4),
+        "hbm_copy_GBs": round(copy_gbs, 1),
+        "hbm_roofline_frac_of_copy": round(copy_frac, 4),
         "algorithmic_bytes_per_step": alg_step_bytes,
         "roofline": roofline,
         "kernels": {kn: {kk: round(vv, 3) for kk, vv in kv.items()} for kn, kv in kernels.items()},
