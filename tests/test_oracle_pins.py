@@ -101,12 +101,12 @@ def _angle_pair(theta, d, seed):
 
 
 @pytest.mark.parametrize("d", [3, 64])
-@pytest.mark.parametrize("tau", [1, 8])
+@pytest.mark.parametrize("tau", [1, 8, 9])
 @pytest.mark.parametrize("theta", [0.05, math.pi / 4, math.pi / 2, 2 * math.pi / 3, math.pi - 0.05])
 def test_collision_frequency_matches_closed_form(d, tau, theta):
     """Per-code collision probability of tau concatenated hyperplane hashes is
     (1 - theta/pi)^tau (eq. yoso-expectation; tau = 1 is Charikar's 1 - theta/pi)."""
-    S = 100_000 if tau == 8 else 20_000
+    S = 100_000 if tau > 1 else 20_000
     x = _angle_pair(theta, d, seed=int(theta * 1000) + d + tau)
     R = _rng(10 + d + tau).standard_normal((d, S * tau))
     codes = oracle.hash_codes(x[None], R, S, tau)[0]
@@ -170,6 +170,39 @@ def test_forward_keys_equal_queries_collide_with_themselves():
     e[:, np.arange(17), np.arange(17)] = 1.0   # v_j = e_j reads column j of C
     y = oracle.forward(c, c, e, m, tau) * m
     np.testing.assert_allclose(np.diagonal(y, axis1=1, axis2=2), m, rtol=0, atol=1e-12)
+
+
+def test_antipodal_keys_never_collide():
+    """K = -Q negates every projection, so (all margins being nonzero) every code of
+    a key is the complement of its query's code: a row never collides with its own
+    antipode, and a query whose only key is its antipode gathers exactly zero."""
+    q, _, v, _, R = _rand_problem(30, bh=1, nq=40, nk=40, d=8, m=6, tau=5)
+    qc, margin = oracle.hash_codes(q, R, 6, 5, with_margin=True)
+    assert margin.min() > 0
+    kc = oracle.hash_codes(-q, R, 6, 5)
+    np.testing.assert_array_equal(kc, (~qc) & 31)
+    # (other pairs may still collide; a row and its antipode never do)
+    np.testing.assert_array_equal(np.diagonal(_brute_collisions(qc, kc)[0], axis1=1, axis2=2), 0.0)
+    # with a single query and its antipode as the only key, nothing is ever gathered
+    y = oracle.forward(qc[:, :, :1], kc[:, :, :1], v[:, :1], 6, 5)
+    assert np.all(y == 0.0)
+
+
+def test_forward_table_sums_are_the_value_sums():
+    """One query per bucket (codes 0 .. 2^tau - 1) with m = 1: each query reads one
+    bucket's table row, so the queries' outputs add up to the sum of all values
+    (every key lands in exactly one bucket: sum_c H[c] = sum_j V_j)."""
+    g = _rng(31)
+    tau, nk, d = 4, 57, 5
+    v = g.standard_normal((2, nk, d))
+    kc = g.integers(0, 2 ** tau, size=(2, 1, nk)).astype(np.uint16)
+    qc = np.tile(np.arange(2 ** tau, dtype=np.uint16), (2, 1, 1))
+    y = oracle.forward(qc, kc, v, 1, tau)
+    np.testing.assert_allclose(y.sum(axis=1), v.sum(axis=1), rtol=1e-12, atol=1e-12)
+    # and each bucket's row is the sum of exactly its keys
+    for b in range(2):
+        for c in range(2 ** tau):
+            np.testing.assert_allclose(y[b, c], v[b][kc[b, 0] == c].sum(axis=0), rtol=1e-12, atol=1e-12)
 
 
 def test_forward_empty_keys_give_zero():
