@@ -33,8 +33,9 @@
  *     below 65504 in magnitude.
  *   - Precision.  Y and dV are accumulated as exact fixed-point integers: each
  *     value of a 2-16 wide feature slice is rounded to a multiple of 2^-k, where
- *     2^k is the largest power of two keeping n_src * max|slice value| * 2^k
- *     below 2^30; everything after that rounding is exact.  dQ and dK use fp32
+ *     2^k is the largest power of two keeping 2^k (1 + 2^-10) times the slice's
+ *     largest per-dim sum of |value| over the n_src source rows below 2^30;
+ *     everything after that rounding is exact.  dQ and dK use fp32
  *     accumulation of products formed from fp16 (hi, lo) pairs (about 22
  *     significant bits); the contribution of each hash to a row is kept in block
  *     floating point (16-bit mantissas, one power-of-two exponent per row), exact

@@ -15,13 +15,15 @@
 // Tables hold fixed-point integers, not floats: gfx950 executes LDS fp32
 // atomic adds some 40x slower than integer ones, while a 64-bit integer add
 // carries two values at once.  Each value v of the slice is quantised to
-// q = rint(v 2^k) with one power-of-two scale per workgroup, chosen from the
-// slice's largest |v| so that any bucket sum of up to n_src values stays below
-// 2^30 in magnitude.  Two adjacent dims (q_lo, q_hi) are packed as the 64-bit
-// integer q_hi 2^32 + q_lo; sums of packed words never corrupt each other's
-// field because |sum q_lo| < 2^31.  Integer sums are exact and independent of
-// the order of the atomics, so the tables (and the outputs) are deterministic.
-// The only rounding is the quantisation, |error| <= 2^-k / 2 per value.
+// q = rint(v 2^k) with one power-of-two scale per workgroup, chosen so that
+// 2^k times the largest per-dim sum of |v| over the source rows (a bound on every
+// bucket sum, and never above n_src max|v|) stays below 2^30; a bucket sum of
+// rounded values is then below 2^30 + n_src/2 in magnitude.  Two adjacent dims
+// (q_lo, q_hi) are packed as the 64-bit integer q_hi 2^32 + q_lo; sums of packed
+// words never corrupt each other's field because |sum q_lo| < 2^31.  Integer
+// sums are exact and independent of the order of the atomics, so the tables (and
+// the outputs) are deterministic.  The only rounding is the quantisation,
+// |error| <= 2^-k / 2 per value.
 //
 // LDS layout: word (c*G + h)*P + p holds dims (2p, 2p+1) of bucket c of hash
 // h (P = DS/2 words per row).
@@ -94,7 +96,6 @@ struct TableArgs {
     float *acc;                 // fp32 running sums when the hashes take several LDS passes
     int64_t bh, n_src, n_dst;
     int m, tau, G;              // G = hashes per LDS pass
-    int e_n;                    // ceil(log2(n_src)): bucket populations are < 2^e_n + 1
 };
 
 // (lo, hi) of a packed word whose fields are signed and |field sums| < 2^31:
@@ -111,7 +112,7 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
     constexpr int P = DS / 2;   // packed words per table row
     constexpr int S = D / DS;   // slices per head
     extern __shared__ __align__(16) unsigned long long tab[];  // [2^tau][G][P]
-    __shared__ float wave_red[kTableWaves];
+    __shared__ float wave_red[kTableWaves * DS];
     __shared__ int scale_exp;
 
     const int64_t blocks = a.bh * S;
@@ -124,11 +125,14 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
     const int cmask = (1 << a.tau) - 1;
     const int64_t vbase = b * a.n_src * D + slice * DS;
 
-    // ---- scale: largest |v| of this slice -> exponent k
+    // ---- scale: for each dim of this slice, the sum of |v| over all source rows
+    // bounds every bucket sum of that dim; the largest of these sums -> exponent k.
     // (eight rows per thread in flight at once: the pass is latency-bound; rows past
-    // the end re-read the last row, which cannot change the maximum)
+    // the end re-read the last row and add nothing)
     {
-        float mx = 0.f;
+        float sa[DS];
+#pragma unroll
+        for (int d = 0; d < DS; d++) sa[d] = 0.f;
         constexpr int U = 8;
         const int64_t last = a.n_src - 1;
         for (int64_t j0 = tid; j0 < a.n_src; j0 += U * kTableThreads) {
@@ -139,21 +143,35 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
                 load_slice<BF16, DS>(a.values, vbase + (j < last ? j : last) * D, v[u]);
             }
 #pragma unroll
-            for (int u = 0; u < U; u++)
+            for (int u = 0; u < U; u++) {
+                const bool in = j0 + u * kTableThreads < a.n_src;
 #pragma unroll
-                for (int d = 0; d < DS; d++) mx = fmaxf(mx, fabsf(v[u][d]));
+                for (int d = 0; d < DS; d++) sa[d] += in ? fabsf(v[u][d]) : 0.f;
+            }
         }
-        mx = wave_max(mx);
-        if (lane == 0) wave_red[wave] = mx;
+#pragma unroll
+        for (int d = 0; d < DS; d++) sa[d] = group_sum(sa[d], 64);
+        if (lane == 0) {
+#pragma unroll
+            for (int d = 0; d < DS; d++) wave_red[wave * DS + d] = sa[d];
+        }
         __syncthreads();
         if (tid == 0) {
             float t = 0.f;
-            for (int w = 0; w < kTableWaves; w++) t = fmaxf(t, wave_red[w]);
+            for (int d = 0; d < DS; d++) {
+                float s = 0.f;
+                for (int w = 0; w < kTableWaves; w++) s += wave_red[w * DS + d];
+                t = fmaxf(t, s);
+            }
             int k = 0;
             if (t > 0.f) {
+                // the fp32 sums are low by at most ~140 ulp-units relative (128 terms
+                // per lane, 6 butterfly levels, 8 waves); the margin 1 + 2^-10 covers
+                // it, so 2^k * (exact sum) < 2^30 and every bucket sum of rounded
+                // values stays below 2^30 + n_src/2 < 2^31
                 int ev;
-                frexpf(t, &ev);  // t < 2^ev
-                k = 30 - a.e_n - ev;
+                frexpf(t * (1.0f + 0x1p-10f), &ev);  // t (1 + 2^-10) < 2^ev
+                k = 30 - ev;
             }
             scale_exp = k;
         }
@@ -559,12 +577,6 @@ hipError_t launch_table_ds(int ds, const TableArgs &a, size_t lds, hipStream_t s
     return hipGetLastError();
 }
 
-int ceil_log2(int64_t n) {
-    int e = 0;
-    while ((int64_t{1} << e) < n) e++;
-    return e;
-}
-
 }  // namespace
 
 TablePlan plan_table(int m, int tau) {
@@ -611,7 +623,6 @@ hipError_t launch_table(const uint16_t *src_codes, const void *values, const uin
     a.m = m;
     a.tau = tau;
     a.G = p.G;
-    a.e_n = ceil_log2(n_src);
     // + one private dummy word per lane (targets of lanes without a valid key)
     // + per-wave staging of a chunk's packed words (64 keys x DS/2 words)
     const size_t lds = p.lds + 64 * sizeof(unsigned long long) +

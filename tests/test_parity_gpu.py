@@ -107,6 +107,18 @@ SMALL = [
 
 @pytest.mark.parametrize("bh,nq,nk,m,tau,dtype", SMALL)
 def test_small_shapes(bh, nq, nk, m, tau, dtype):
+    run_case(bh, nq, nk, m, tau, dtype)
+
+
+@pytest.mark.parametrize("bh,nq,nk,m,tau,dtype", [(1, 65536, 65536, 3, 10, "f32"), (1, 65535, 65536, 2, 12, "bf16")])
+def test_maximum_length(bh, nq, nk, m, tau, dtype):
+    """Sequences at the library's limit of 65536 rows (the most that the 16-bit row
+    field of a sorted entry addresses): the bucket sort takes its global-memory path,
+    and in the second case the last row tile is ragged.  Every row is checked."""
+    run_case(bh, nq, nk, m, tau, dtype)
+
+
+def run_case(bh, nq, nk, m, tau, dtype):
     name = f"bh{bh}_nq{nq}_nk{nk}_m{m}_tau{tau}_{dtype}"
     log(f"[{name}] start")
     w = workloads.Workload(name, 1, bh, nq, 64, tau, m, dtype, "gauss", 1234 + nq + 7 * nk + m + tau)
