@@ -366,59 +366,65 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uin
     for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(btl[dt], sh, outT[dt], 0, 0, 0);
 }
 
-template <int CTRL>
-__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
-    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(x), CTRL, 0xF, 0xF, false));
-}
-
 // Write the partial rows of a finished tile: lane (g, c) holds out[row c][16dt +
-// 4g + (0..3)] / oscale.  The tile goes through LDS so that each quarter-wave then
-// stores one whole partial row.  A partial row is stored in block floating point:
-// 64 int16 mantissas and one exponent e with max|value| < 2^e, value = mantissa *
+// 4g + (0..3)] / oscale.  A partial row is stored in block floating point: 64
+// int16 mantissas and one exponent e with max|value| < 2^e, value = mantissa *
 // 2^e / 32767 (rounding error at most 2^e / 65534, i.e. about 2^-15 of the row's
-// largest value).  The stores are non-temporal: the partials are read once, by the
-// reduction, and should not evict the operands from L2.  Exponents go to the block's
-// LDS copy of its exponent row when it fits (written out whole at the end: single-
-// byte stores scattered over the row would each cost a partial-line write), else
-// straight to memory.
+// largest value).  The row maximum is taken where the MFMA leaves the values (16
+// per lane, the rest of the row in the lanes 16, 32 and 48 away: two permlane
+// swaps), and the row's scale reaches the lanes that store it through a 64-byte
+// slot of the tile.  The values go through the tile so that each quarter-wave
+// then stores one whole partial row.  The stores are non-temporal: the partials
+// are read once, by the reduction, and should not evict the operands from L2.
+// Exponents go to the block's LDS copy of its exponent row when it fits (written
+// out whole at the end: single-byte stores scattered over the row would each cost
+// a partial-line write), else straight to memory.
 __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, int8_t *pexp, int8_t *ex_lds,
-                                           bool ex_in_lds, int m, const uint4 &re4, int nvalid, int q, int cl,
-                                           int g, int c, const floatx4 outT[4], float oscale) {
+                                           bool ex_in_lds, int m, const uint4 &re4, uint32_t rent_c, int nvalid,
+                                           int q, int cl, int g, int c, const floatx4 outT[4], float oscale) {
+    // max |value| of row c over this lane's 16 values, then over the row's 4 lanes
+    float mx4[4];
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++)
+        mx4[dt] = fmaxf(fmaxf(fabsf(outT[dt][0]), fabsf(outT[dt][1])), fmaxf(fabsf(outT[dt][2]), fabsf(outT[dt][3])));
+    float mx = fmaxf(fmaxf(mx4[0], mx4[1]), fmaxf(mx4[2], mx4[3]));
+    {
+        const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+        mx = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    }
+    {
+        const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+        mx = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    }
+    // e with max|value| < 2^e, from the biased exponent field of the scaled row
+    // maximum (0 gives a tiny e whose mantissas are all 0), clamped so that 2^-e
+    // stays a normal float
+    const float mxs = mx * oscale;
+    const int e = min(max(static_cast<int>((__float_as_uint(mxs) >> 23) & 0xFFu) - 126, -100), 100);
+    // value * 2^-e lies in (-1, 1); the snorm conversion rounds it to a multiple
+    // of 1/32767 (mantissa = round(value * 2^-e * 32767))
+    const float scale = __uint_as_float(static_cast<uint32_t>(127 - e) << 23) * oscale;
+    constexpr uint32_t kScaleSlot = 16 * 256;  // past the 16 x 256 B of the out tile
+    if (g == 0) {
+        lds_st(tile, kScaleSlot + 4 * c, scale);
+        if (c < nvalid) {
+            const uint32_t row = rent_c & 0xFFFFu;
+            if (ex_in_lds) ex_lds[row] = static_cast<int8_t>(e);
+            else pexp[row] = static_cast<int8_t>(e);
+        }
+    }
 #pragma unroll
     for (int dt = 0; dt < 4; dt++) lds_st(tile, swz(c, 4 * dt + g, 256), outT[dt]);
     const uint32_t e4[4] = {re4.x, re4.y, re4.z, re4.w};
-    // rows 4q + i: all four reads first, then the four exponent reductions side by side
-    // (max over the 16 lanes of a row, on |x| bit patterns, whose integer order is
-    // their order)
+    // rows 4q + i: their chunks cl and their scales
     floatx4 o[4];
 #pragma unroll
     for (int i = 0; i < 4; i++) o[i] = lds_ld<floatx4>(tile, swz(4 * q + i, cl, 256));
-    uint32_t mb[4];
-#pragma unroll
-    for (int i = 0; i < 4; i++) {
-        const uint32_t a0 = max(__float_as_uint(o[i].x) & 0x7FFFFFFFu, __float_as_uint(o[i].y) & 0x7FFFFFFFu);
-        const uint32_t a1 = max(__float_as_uint(o[i].z) & 0x7FFFFFFFu, __float_as_uint(o[i].w) & 0x7FFFFFFFu);
-        mb[i] = max(a0, a1);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; i++) mb[i] = max(mb[i], dpp_u32<0xB1>(mb[i]));
-#pragma unroll
-    for (int i = 0; i < 4; i++) mb[i] = max(mb[i], dpp_u32<0x4E>(mb[i]));
-#pragma unroll
-    for (int i = 0; i < 4; i++) mb[i] = max(mb[i], dpp_u32<0x141>(mb[i]));
-#pragma unroll
-    for (int i = 0; i < 4; i++) mb[i] = max(mb[i], dpp_u32<0x140>(mb[i]));
+    const floatx4 sc4 = lds_ld<floatx4>(tile, kScaleSlot + 16 * q);
 #pragma unroll
     for (int i = 0; i < 4; i++) {
         const int r = 4 * q + i;
-        // e with max|value| < 2^e, from the biased exponent field of the scaled row
-        // maximum (0 gives a tiny e whose mantissas are all 0), clamped so that 2^-e
-        // stays a normal float
-        const float mx = __uint_as_float(mb[i]) * oscale;
-        const int e = min(max(static_cast<int>((__float_as_uint(mx) >> 23) & 0xFFu) - 126, -100), 100);
-        // value * 2^-e lies in (-1, 1); the snorm conversion rounds it to a multiple
-        // of 1/32767 (mantissa = round(value * 2^-e * 32767))
-        const float sc = __uint_as_float(static_cast<uint32_t>(127 - e) << 23) * oscale;
+        const float sc = sc4[i];
         typedef unsigned int uint2v __attribute__((ext_vector_type(2)));
         uint2v w;
         w.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pknorm_i16(o[i].x * sc, o[i].y * sc));
@@ -426,10 +432,6 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, i
         if (r < nvalid) {
             const uint32_t row = e4[i] & 0xFFFFu;
             __builtin_nontemporal_store(w, reinterpret_cast<uint2v *>(part + (row * static_cast<uint32_t>(m)) * D) + cl);
-            if (cl == 0) {
-                if (ex_in_lds) ex_lds[row] = static_cast<int8_t>(e);
-                else pexp[row] = static_cast<int8_t>(e);
-            }
         }
     }
 }
@@ -541,7 +543,7 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
         auto zero_tiles = [&](int ta, int tb) {
             const floatx4 z[4] = {};
             for (int t = ta; t < tb; t++)
-                store_tile(tile, part, pexp, ex_lds, ex_in_lds, a.m, row_entries4(t), row_count(t), q, cl, g, c, z, 0.f);
+                store_tile(tile, part, pexp, ex_lds, ex_in_lds, a.m, row_entries4(t), row_entry(t), row_count(t), q, cl, g, c, z, 0.f);
         };
         // sub-tile j of the run: its tile (searched forward from t) and first partner
         auto tile_of = [&](int j, int t) {
@@ -612,7 +614,7 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
                 if (has1) load_sub(S, nxt.pe, apar, bpar, cl);
                 compute_sub(tile, cur.pe, rh, rl, static_cast<int>(row_entry(cur.t) >> 16), g, c, outT);
                 if (newtile) {
-                    store_tile(tile, part, pexp, ex_lds, ex_in_lds, a.m, row_entries4(cur.t), row_count(cur.t), q, cl, g, c, outT, oscale);
+                    store_tile(tile, part, pexp, ex_lds, ex_in_lds, a.m, row_entries4(cur.t), row_entry(cur.t), row_count(cur.t), q, cl, g, c, outT, oscale);
 #pragma unroll
                     for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
                     zero_tiles(cur.t + 1, has1 ? nxt.t : thi);
