@@ -366,19 +366,29 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uin
     for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(btl[dt], sh, outT[dt], 0, 0, 0);
 }
 
+// Byte offset of 8-byte chunk ch (int16 dims 4ch .. 4ch+3) of the mantissa row in
+// slot s of the tile (16 slots of 128 bytes).  Row r sits in slot r ^ ((r >> 2) & 1),
+// so the two rows that a half-wave reads in the row-major pass have opposite slot
+// parity (opposite halves of the 64 banks); within a slot the 16-byte unit of a
+// chunk is XORed with s >> 1, so the eight same-parity rows that a half-wave writes
+// from the MFMA layout (one unit each) hit distinct banks.
+__device__ __forceinline__ int mant_slot(int r) { return r ^ ((r >> 2) & 1); }
+__device__ __forceinline__ uint32_t mant_off(int s, int ch) {
+    return static_cast<uint32_t>(s * 128 + (((ch >> 1) ^ (s >> 1)) << 4) + ((ch & 1) << 3));
+}
+
 // Write the partial rows of a finished tile: lane (g, c) holds out[row c][16dt +
 // 4g + (0..3)] / oscale.  A partial row is stored in block floating point: 64
 // int16 mantissas and one exponent e with max|value| < 2^e, value = mantissa *
 // 2^e / 32767 (rounding error at most 2^e / 65534, i.e. about 2^-15 of the row's
-// largest value).  The row maximum is taken where the MFMA leaves the values (16
-// per lane, the rest of the row in the lanes 16, 32 and 48 away: two permlane
-// swaps), and the row's scale reaches the lanes that store it through a 64-byte
-// slot of the tile.  The values go through the tile so that each quarter-wave
-// then stores one whole partial row.  The stores are non-temporal: the partials
-// are read once, by the reduction, and should not evict the operands from L2.
-// Exponents go to the block's LDS copy of its exponent row when it fits (written
-// out whole at the end: single-byte stores scattered over the row would each cost
-// a partial-line write), else straight to memory.
+// largest value).  The row maximum and the mantissas are computed where the MFMA
+// leaves the values (16 per lane, the rest of the row in the lanes 16, 32 and 48
+// away: two permlane swaps); the mantissas then go through the tile so that each
+// quarter-wave stores one whole partial row.  The stores are non-temporal: the
+// partials are read once, by the reduction, and should not evict the operands from
+// L2.  Exponents go to the block's LDS copy of its exponent row when it fits
+// (written out whole at the end: single-byte stores scattered over the row would
+// each cost a partial-line write), else straight to memory.
 __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, int8_t *pexp, int8_t *ex_lds,
                                            bool ex_in_lds, int m, const uint4 &re4, uint32_t rent_c, int nvalid,
                                            int q, int cl, int g, int c, const floatx4 outT[4], float oscale) {
@@ -403,35 +413,31 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, i
     const int e = min(max(static_cast<int>((__float_as_uint(mxs) >> 23) & 0xFFu) - 126, -100), 100);
     // value * 2^-e lies in (-1, 1); the snorm conversion rounds it to a multiple
     // of 1/32767 (mantissa = round(value * 2^-e * 32767))
-    const float scale = __uint_as_float(static_cast<uint32_t>(127 - e) << 23) * oscale;
-    constexpr uint32_t kScaleSlot = 16 * 256;  // past the 16 x 256 B of the out tile
-    if (g == 0) {
-        lds_st(tile, kScaleSlot + 4 * c, scale);
-        if (c < nvalid) {
-            const uint32_t row = rent_c & 0xFFFFu;
-            if (ex_in_lds) ex_lds[row] = static_cast<int8_t>(e);
-            else pexp[row] = static_cast<int8_t>(e);
-        }
+    const float sc = __uint_as_float(static_cast<uint32_t>(127 - e) << 23) * oscale;
+    if (g == 0 && c < nvalid) {
+        const uint32_t row = rent_c & 0xFFFFu;
+        if (ex_in_lds) ex_lds[row] = static_cast<int8_t>(e);
+        else pexp[row] = static_cast<int8_t>(e);
     }
+    typedef unsigned int uint2v __attribute__((ext_vector_type(2)));
+    const int sw = mant_slot(c);
 #pragma unroll
-    for (int dt = 0; dt < 4; dt++) lds_st(tile, swz(c, 4 * dt + g, 256), outT[dt]);
+    for (int dt = 0; dt < 4; dt++) {
+        uint2v w;
+        w.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pknorm_i16(outT[dt][0] * sc, outT[dt][1] * sc));
+        w.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pknorm_i16(outT[dt][2] * sc, outT[dt][3] * sc));
+        lds_st(tile, mant_off(sw, 4 * dt + g), w);
+    }
     const uint32_t e4[4] = {re4.x, re4.y, re4.z, re4.w};
-    // rows 4q + i: their chunks cl and their scales
-    floatx4 o[4];
+    // rows 4q + i: this lane's chunk cl of each, then the four stores
+    uint2v w[4];
 #pragma unroll
-    for (int i = 0; i < 4; i++) o[i] = lds_ld<floatx4>(tile, swz(4 * q + i, cl, 256));
-    const floatx4 sc4 = lds_ld<floatx4>(tile, kScaleSlot + 16 * q);
+    for (int i = 0; i < 4; i++) w[i] = lds_ld<uint2v>(tile, mant_off(mant_slot(4 * q + i), cl));
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-        const int r = 4 * q + i;
-        const float sc = sc4[i];
-        typedef unsigned int uint2v __attribute__((ext_vector_type(2)));
-        uint2v w;
-        w.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pknorm_i16(o[i].x * sc, o[i].y * sc));
-        w.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pknorm_i16(o[i].z * sc, o[i].w * sc));
-        if (r < nvalid) {
+        if (4 * q + i < nvalid) {
             const uint32_t row = e4[i] & 0xFFFFu;
-            __builtin_nontemporal_store(w, reinterpret_cast<uint2v *>(part + (row * static_cast<uint32_t>(m)) * D) + cl);
+            __builtin_nontemporal_store(w[i], reinterpret_cast<uint2v *>(part + (row * static_cast<uint32_t>(m)) * D) + cl);
         }
     }
 }
