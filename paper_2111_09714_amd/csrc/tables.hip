@@ -31,9 +31,10 @@
 //            row (code_h, h).  The 32 lanes of a half-wave cover distinct
 //            (h, p) in a row block whose stride is a multiple of the 64 LDS
 //            banks, so they never conflict.
-//   gather:  8 lanes per query, each reading the whole P-word rows of G/8
-//            hashes in a rotated order (the 16 lanes of a 16-byte access pass
-//            hit distinct bank groups), then a DPP butterfly sums the 8 lanes.
+//   gather:  4 lanes per query (8 for 64 hashes), each reading the whole P-word
+//            rows of G/4 hashes in a rotated order (the 16 lanes of a 16-byte
+//            access pass hit distinct bank groups), then a DPP butterfly sums
+//            the lanes of the query.
 #include <type_traits>
 
 #include "common.h"
@@ -200,7 +201,9 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
         sp[ii] = combo % P;
         sh[ii] = combo / P;
     }
-    const int L = GP < 8 ? GP : 8;         // gather lanes per query
+    // gather lanes per query: 4 (8 for 64 hashes, so that a lane sums at most 8
+    // hashes; fewer when there are fewer hashes)
+    const int L = GP <= 4 ? GP : (GP / 8 > 4 ? GP / 8 : 4);
     const int HL = GP / L;                 // hashes per gather lane (<= 8)
     const int QPI = 64 / L;                // queries per gather instruction
     const int gq = lane / L, gr = lane % L;
@@ -427,7 +430,7 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
             };
             const int64_t step = static_cast<int64_t>(kTableWaves) * QPI;
             // codes of the next kGD query groups are in flight while one is summed
-            constexpr int kGD = KM < 2 ? 8 : 2;
+            constexpr int kGD = KM < 2 ? 4 : 2;
             uint32_t cR[kGD][8];
             // (issued in ring order, which the first groups' waits assume)
 #pragma unroll
