@@ -210,3 +210,48 @@ def test_repeatable_and_side_stream():
     # rows summed in hash order), so a repeat is bitwise identical
     for key in ("y", "dq", "dk", "dv"):
         np.testing.assert_array_equal(b[key], a[key], err_msg=key)
+
+
+def one_bucket_inputs(n):
+    """Every row of Q and K is the same unit vector u, so every hash puts every key
+    in one bucket; V and dY are constant rows of dyadic values, so every sum is exact."""
+    u = torch.zeros(64, device="cuda")
+    u[0] = 1.0
+    x = u.expand(1, n, 64).contiguous()
+    v = torch.cat([torch.full((1, n, 32), 1.0), torch.full((1, n, 32), -0.75)], dim=-1).cuda()
+    dy = torch.cat([torch.full((1, n, 32), 0.5), torch.full((1, n, 32), 0.25)], dim=-1).cuda()
+    return u, x, v, dy
+
+
+def test_all_keys_in_one_bucket_forward_at_the_length_limit():
+    """The worst case of the tables' fixed-point bound: all 65536 keys in one bucket,
+    all values of a dim of one sign.  Y is exact (every query reads the sum of V)."""
+    n, m, tau = 65536, 2, 8
+    _, x, v, _ = one_bucket_inputs(n)
+    R = torch.randn(64, m * tau, device="cuda", generator=torch.Generator("cuda").manual_seed(5))
+    qc, kc = Y.hash_qk(x, x, R, m, tau)
+    y = Y.forward(qc, kc, v, m, tau)
+    torch.cuda.synchronize()
+    assert bool((qc == qc[0, 0]).all()) and bool((kc == qc[0, 0]).all())
+    expect = v[0].sum(dim=0)                      # [65536]*32 + [-49152]*32, exact
+    log(f"[one bucket, n={n}] Y row 0 {y[0, 0, :2].tolist()} ... expected {expect[:2].tolist()}")
+    assert torch.equal(y[0], expect.expand(n, 64))
+
+
+def test_all_keys_in_one_bucket_backward_closed_form():
+    """Every pair collides in every hash: dV_j = sum_i dY_i, dQ_i = (tau/2)(dY_i . sum V) u
+    and dK_j = (tau/2)(V_j . sum dY) u (eq. pseudo-gradient-q with B = 1)."""
+    n, m, tau = 4096, 2, 8
+    u, x, v, dy = one_bucket_inputs(n)
+    R = torch.randn(64, m * tau, device="cuda", generator=torch.Generator("cuda").manual_seed(6))
+    qc, kc = Y.hash_qk(x, x, R, m, tau)
+    dq, dk, dv = Y.backward(qc, kc, x, x, v, dy, m, tau)
+    torch.cuda.synchronize()
+    sv, sdy = v[0].double().sum(0), dy[0].double().sum(0)
+    dq_ref = (tau / 2) * (dy[0].double() @ sv)[:, None] * u.double()[None, :]
+    dk_ref = (tau / 2) * (v[0].double() @ sdy)[:, None] * u.double()[None, :]
+    assert torch.equal(dv[0].double(), sdy.expand(n, 64))
+    for name, got, ref in (("dq", dq[0], dq_ref), ("dk", dk[0], dk_ref)):
+        e = (torch.linalg.norm(got.double() - ref) / torch.linalg.norm(ref)).item()
+        log(f"[one bucket, n={n}] {name} rel err {e:.2e}")
+        assert e <= TOL["f32"], (name, e)
