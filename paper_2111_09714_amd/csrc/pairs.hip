@@ -134,15 +134,18 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
     int32_t local = 0;
     for (int c = c0; c < c0 + per && c < B; c++)
         for (int w = 0; w < kSortWaves; w++) local += hist[w * B + c];
-    scan[tid] = local;
-    __syncthreads();
-    for (int s = 1; s < kSortThreads; s <<= 1) {
-        const int32_t v = (tid >= s) ? scan[tid - s] : 0;
-        __syncthreads();
-        scan[tid] += v;
-        __syncthreads();
+    // (inclusive scan: within each wave by shuffles, then the totals of the waves
+    // before it)
+    int32_t incl = local;
+#pragma unroll
+    for (int s = 1; s < 64; s <<= 1) {
+        const int32_t v = __shfl_up(incl, s);
+        if (lane >= s) incl += v;
     }
-    int32_t run = scan[tid] - local;
+    if (lane == 63) scan[wave] = incl;
+    __syncthreads();
+    for (int w = 0; w < wave; w++) incl += scan[w];
+    int32_t run = incl - local;
     for (int c = c0; c < c0 + per && c < B; c++) {
         off[c] = run;
         for (int w = 0; w < kSortWaves; w++) {
@@ -448,7 +451,7 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
     __shared__ __align__(16) unsigned char tiles_lds[kPassWaves * kTileBytes];
     __shared__ int32_t plan_beg[kPlanTiles];      // first partner of each row tile's bucket range
     __shared__ int32_t plan_x[kPlanTiles + 1];    // exclusive prefix of the tiles' sub-tile counts
-    __shared__ int32_t scan_tmp[kPassThreads];
+    __shared__ int32_t scan_tmp[kPassWaves];     // the waves' count totals
     __shared__ __align__(16) uint32_t row_ent[kPlanTiles * 16];  // the run's sorted row entries
     __shared__ __align__(16) int8_t ex_lds[kExpLds];               // the block's exponent row
 
@@ -507,22 +510,25 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
                 }
                 local += cnt[j];
             }
-            scan_tmp[tid] = local;
-            __syncthreads();
-            for (int s = 1; s < kPassThreads; s <<= 1) {
-                const int v = tid >= s ? scan_tmp[tid - s] : 0;
-                __syncthreads();
-                scan_tmp[tid] += v;
-                __syncthreads();
+            // inclusive scan of the counts: within each wave by shuffles, then the
+            // totals of the waves before it (one barrier)
+            int incl = local;
+#pragma unroll
+            for (int s = 1; s < 64; s <<= 1) {
+                const int v = __shfl_up(incl, s);
+                if (lane >= s) incl += v;
             }
-            int run = scan_tmp[tid] - local;
+            if (lane == 63) scan_tmp[wave] = incl;
+            __syncthreads();
+            for (int w = 0; w < wave; w++) incl += scan_tmp[w];
+            int run = incl - local;
 #pragma unroll
             for (int j = 0; j < PER; j++) {
                 const int i = tid * PER + j;
                 if (i < nt) plan_x[i] = run;
                 run += cnt[j];
             }
-            if (tid == kPassThreads - 1) plan_x[nt] = scan_tmp[tid];
+            if (tid == kPassThreads - 1) plan_x[nt] = incl;
             // the run's row entries (16-byte copies; entries past n_r are sentinels)
             for (int i = tid; i < nt * 4; i += kPassThreads)
                 reinterpret_cast<uint4 *>(row_ent)[i] = ld<uint4>(rent, static_cast<uint32_t>(T0 * 16 + 4 * i) * 4);
