@@ -45,11 +45,21 @@ namespace yoso {
 
 namespace {
 
+// Sort workgroups: four waves when the column is staged in LDS; eight when it is
+// not (long sequences: more rows per workgroup to place, 89 -> 72 us at n = 32768)
+// and tau <= 10 (the larger tables and masks of tau 11-12 do not fit twice).
 constexpr int kSortThreads = 256;
-constexpr int kSortWaves = kSortThreads / 64;
+constexpr int kSortThreadsWide = 512;
 
 // Waves of a sort workgroup that place rows: each needs a 64-bit lane mask per bucket.
-__host__ __device__ constexpr int sort_placing_waves(int tau) { return tau <= 10 ? kSortWaves : 1; }
+__host__ __device__ constexpr int sort_placing_waves(int tau, int waves) { return tau <= 10 ? waves : 1; }
+
+// Dynamic LDS of a sort workgroup of `nt` threads before staging: per-wave counts,
+// scan scratch, placing waves' masks.
+inline size_t sort_base_lds(int nt, int tau) {
+    return (static_cast<size_t>(nt / 64) * (size_t{1} << tau) + nt) * 4 +
+           static_cast<size_t>(sort_placing_waves(tau, nt / 64)) * (size_t{1} << tau) * 8;
+}
 constexpr size_t kSortStageLds = 120 * 1024;  // LDS bound of a sort workgroup that stages its column
 constexpr int kPassThreads = 256;
 constexpr int kPassWaves = kPassThreads / 64;
@@ -66,22 +76,24 @@ constexpr uint32_t kSentinel = 0xFFFF0000u;  // code 0xFFFF (no real code), row 
 
 // ---------------------------------------------------------------- counting sort
 // codes are [bh][n][m]; unit = b*m + h reads column h with stride m.
-__global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__restrict__ qcodes,
+template <int NT>
+__global__ __launch_bounds__(NT) void sort_kernel(const uint16_t *__restrict__ qcodes,
                                                             const uint16_t *__restrict__ kcodes, int m,
                                                             int64_t n_q, int64_t n_k, int tau, bool stage,
                                                             int32_t *__restrict__ qoff, int32_t *__restrict__ koff,
                                                             uint32_t *__restrict__ qent,
                                                             uint32_t *__restrict__ kent) {
-    // [kSortWaves][buckets] per-wave counts, then per-wave cursors; + [kSortThreads]
+    // [NW][buckets] per-wave counts, then per-wave cursors; + [NT]
     // scan scratch; + [placing waves][buckets] 64-bit lane masks; when `stage`, the
     // column's codes (read from memory once, with stride m) and the sorted entries,
     // which are then written out whole (single scattered 4-byte stores would each
     // cost a partial-line write)
+    constexpr int NW = NT / 64;
     extern __shared__ int32_t hist[];
     const int B = 1 << tau;
-    int32_t *scan = hist + kSortWaves * B;
-    const int pw = sort_placing_waves(tau);
-    unsigned long long *masks = reinterpret_cast<unsigned long long *>(scan + kSortThreads);
+    int32_t *scan = hist + NW * B;
+    const int pw = sort_placing_waves(tau, NW);
+    unsigned long long *masks = reinterpret_cast<unsigned long long *>(scan + NT);
     uint32_t *est = reinterpret_cast<uint32_t *>(masks + pw * B);
     const int64_t unit = blockIdx.x >> 1;
     const bool kside = blockIdx.x & 1;
@@ -99,8 +111,8 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
     const int64_t seg = (n + pw - 1) / pw;
     const int64_t r0 = wave < pw ? min(n, wave * seg) : n, r1 = wave < pw ? min(n, r0 + seg) : n;
 
-    for (int c = tid; c < kSortWaves * B; c += kSortThreads) hist[c] = 0;
-    for (int c = tid; c < pw * B; c += kSortThreads) masks[c] = 0ull;
+    for (int c = tid; c < NW * B; c += NT) hist[c] = 0;
+    for (int c = tid; c < pw * B; c += NT) masks[c] = 0ull;
     __syncthreads();
     {
         // sixteen codes per lane in flight before their counts are added (the codes
@@ -129,11 +141,11 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
 
     // bucket offsets (exclusive scan of the totals; thread t owns buckets
     // [t*per, (t+1)*per)), and each wave's first position in each bucket
-    const int per = (B + kSortThreads - 1) / kSortThreads;
+    const int per = (B + NT - 1) / NT;
     const int c0 = tid * per;
     int32_t local = 0;
     for (int c = c0; c < c0 + per && c < B; c++)
-        for (int w = 0; w < kSortWaves; w++) local += hist[w * B + c];
+        for (int w = 0; w < NW; w++) local += hist[w * B + c];
     // (inclusive scan: within each wave by shuffles, then the totals of the waves
     // before it)
     int32_t incl = local;
@@ -148,7 +160,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
     int32_t run = incl - local;
     for (int c = c0; c < c0 + per && c < B; c++) {
         off[c] = run;
-        for (int w = 0; w < kSortWaves; w++) {
+        for (int w = 0; w < NW; w++) {
             const int32_t k = hist[w * B + c];
             hist[w * B + c] = run;  // becomes wave w's cursor in bucket c
             run += k;
@@ -192,7 +204,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
         // the entries, then the sentinels, 16 bytes per thread (ent_stride is a
         // multiple of 4 and the unit's entry array starts 16-byte aligned)
         const int64_t n4 = n >> 2;
-        for (int64_t e = tid; e < ent_stride(n) / 4; e += kSortThreads) {
+        for (int64_t e = tid; e < ent_stride(n) / 4; e += NT) {
             uint4 w;
             if (e < n4) {
                 w = reinterpret_cast<const uint4 *>(est)[e];
@@ -206,7 +218,7 @@ __global__ __launch_bounds__(kSortThreads) void sort_kernel(const uint16_t *__re
             reinterpret_cast<uint4 *>(ent)[e] = w;
         }
     } else {
-        for (int64_t i = n + tid; i < ent_stride(n); i += kSortThreads) ent[i] = kSentinel;
+        for (int64_t i = n + tid; i < ent_stride(n); i += NT) ent[i] = kSentinel;
     }
 }
 
@@ -837,17 +849,23 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
     }
 
     {
-        size_t sort_lds = (static_cast<size_t>(kSortWaves) * (1 << tau) + kSortThreads) * 4 +
-                          static_cast<size_t>(sort_placing_waves(tau)) * (1 << tau) * 8;
+        size_t sort_lds = sort_base_lds(kSortThreads, tau);
         // stage the column's codes and entries in LDS when they fit (6 bytes per row)
         const int64_t n_max = n_q > n_k ? n_q : n_k;
         const bool stage = sort_lds + static_cast<size_t>(n_max) * 6 <= kSortStageLds;
         if (stage) sort_lds += static_cast<size_t>(n_max) * 6;
+        const bool wide = !stage && tau <= 10;
         KernelTimer timer("sort_kernel", stream);
-        hipLaunchKernelGGL(sort_kernel, dim3(static_cast<unsigned>(2 * units)), dim3(kSortThreads), sort_lds, stream,
-                           qcodes, kcodes, m, n_q, n_k, tau, stage, reinterpret_cast<int32_t *>(ws + L.qoff),
-                           reinterpret_cast<int32_t *>(ws + L.koff), reinterpret_cast<uint32_t *>(ws + L.qent),
-                           reinterpret_cast<uint32_t *>(ws + L.kent));
+        const dim3 grid(static_cast<unsigned>(2 * units));
+        int32_t *qo = reinterpret_cast<int32_t *>(ws + L.qoff), *ko = reinterpret_cast<int32_t *>(ws + L.koff);
+        uint32_t *qe = reinterpret_cast<uint32_t *>(ws + L.qent), *ke = reinterpret_cast<uint32_t *>(ws + L.kent);
+        if (wide)
+            hipLaunchKernelGGL(sort_kernel<kSortThreadsWide>, grid, dim3(kSortThreadsWide),
+                               sort_base_lds(kSortThreadsWide, tau), stream, qcodes, kcodes, m, n_q, n_k, tau, false,
+                               qo, ko, qe, ke);
+        else
+            hipLaunchKernelGGL(sort_kernel<kSortThreads>, grid, dim3(kSortThreads), sort_lds, stream, qcodes, kcodes,
+                               m, n_q, n_k, tau, stage, qo, ko, qe, ke);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
