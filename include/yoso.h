@@ -59,10 +59,10 @@ typedef enum {
     YOSO_OK = 0,
     YOSO_ERR_NULL = 1,      /* a required pointer is NULL (and its tensor is not empty) */
     YOSO_ERR_SHAPE = 2,     /* bh < 0, n out of [0, 65536], d != 64, or bh*n too large */
-    YOSO_ERR_HASH = 3,      /* tau, m or m*tau out of range */
+    YOSO_ERR_TAU = 3,       /* tau, m or m*tau out of range */
     YOSO_ERR_DTYPE = 4,     /* unknown yoso_dtype */
     YOSO_ERR_ALIGN = 5,     /* a device pointer is not 16-byte aligned */
-    YOSO_ERR_WORKSPACE = 6, /* workspace NULL or smaller than yoso_workspace_size() */
+    YOSO_ERR_WORKSPACE = 6, /* workspace NULL or smaller than yoso_workspace_bytes() */
     YOSO_ERR_DEVICE = 7,    /* a HIP call failed; see yoso_last_error() */
     YOSO_ERR_OP = 8         /* unknown yoso_op */
 } yoso_status;
@@ -146,7 +146,7 @@ yoso_status yoso_fast_hash(const void *x, yoso_dtype dtype, int64_t bh, int64_t 
  * qcodes [bh][n_q][m], kcodes [bh][n_k][m]  from yoso_hash with the same R.
  * v      [bh][n_k][d],  y [bh][n_q][d]  (dtype).  Queries whose buckets are empty
  * get 0 (no renormalisation).
- * workspace: yoso_workspace_size(YOSO_OP_FORWARD, ...) bytes (0 for every shape
+ * workspace: yoso_workspace_bytes(YOSO_OP_FORWARD, ...) bytes (0 for every shape
  * whose tables fit in one LDS pass; then workspace may be NULL).
  */
 yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const void *v,
@@ -163,7 +163,7 @@ yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const v
  * lower-bound surrogate (tau/2) p of the collision-probability derivative.
  *
  * q, dy, dq [bh][n_q][d];  k, v, dk, dv [bh][n_k][d]  (dtype).
- * workspace: yoso_workspace_size(YOSO_OP_BACKWARD, ...) bytes of scratch: the
+ * workspace: yoso_workspace_bytes(YOSO_OP_BACKWARD, ...) bytes of scratch: the
  * per-hash bucket orders, fp16 (hi, lo) copies of q, k, v, dy, and one
  * block-floating-point partial row per (row, hash) for dq and dk: about
  * (2*m*d + 5*m + 8*d) * (n_q + n_k) * bh bytes.
@@ -228,13 +228,14 @@ yoso_status yoso_expectation_backward(const void *q, const void *k, const void *
                                       yoso_dtype dtype, int64_t bh, int64_t n_q, int64_t n_k, int32_t d,
                                       int32_t tau, void *dq, void *dk, void *dv, void *stream);
 
-/* Bytes of device workspace that `op` needs for these arguments (written to
- * *bytes).  Validates the arguments exactly as the call itself does. */
-yoso_status yoso_workspace_size(yoso_op op, yoso_dtype dtype, int64_t bh, int64_t n_q,
-                                int64_t n_k, int32_t d, int32_t m, int32_t tau, size_t *bytes);
+/* Bytes of device workspace that `op` (a yoso_op) needs for these arguments.
+ * The arguments are validated exactly as the call itself validates them; on an
+ * invalid argument the result is SIZE_MAX and yoso_last_error() says why. */
+size_t yoso_workspace_bytes(int op, int64_t bh, int64_t n_q, int64_t n_k, int32_t d, int32_t m,
+                            int32_t tau, yoso_dtype dtype);
 
 /* Static description of a status code. */
-const char *yoso_status_string(yoso_status status);
+const char *yoso_status_str(yoso_status status);
 
 /* Detail of the last failing call on this thread ("" if none). */
 const char *yoso_last_error(void);

@@ -10,9 +10,10 @@ Function names follow the C ABI:
     yoso_fast_hash(x, signs, m, tau, codes)            the fast hash (Walsh-Hadamard rotations per row)
     yoso_forward(qcodes, kcodes, v, m, tau, y, ws)     y = (1/m) sum_h B_h v
     yoso_backward(qcodes, kcodes, q, k, v, dy, m, tau, dq, dk, dv, ws)
-    yoso_workspace_size(op, dtype, bh, n_q, n_k, d, m, tau) -> bytes
-Tensors are torch tensors on the GPU, contiguous, [bh, n, 64], float32 or
-bfloat16.  Work is enqueued on the current torch stream unless `stream` is given.
+    yoso_workspace_bytes(op, bh, n_q, n_k, d, m, tau, dtype) -> bytes
+Tensors are torch tensors on one GPU, contiguous, [bh, n, 64], all float32 or all
+bfloat16 (R is float32, codes 16-bit).  Work is enqueued on the current torch
+stream unless `stream` is given.
 """
 from __future__ import annotations
 
@@ -22,7 +23,7 @@ from typing import Optional
 
 __all__ = [
     "YosoError", "F32", "BF16", "OP_HASH", "OP_FORWARD", "OP_BACKWARD",
-    "lib", "lib_path", "yoso_workspace_size", "yoso_hash", "yoso_fast_hyperplanes", "yoso_fast_hash", "yoso_forward",
+    "lib", "lib_path", "yoso_workspace_bytes", "yoso_status_str", "yoso_hash", "yoso_fast_hyperplanes", "yoso_fast_hash", "yoso_forward",
     "yoso_backward", "yoso_l2_normalize", "yoso_l2_normalize_backward", "yoso_expectation_forward",
     "yoso_expectation_backward",
     "yoso_timing_enable", "yoso_timing_reset", "yoso_timing_query",
@@ -31,7 +32,7 @@ __all__ = [
 
 F32, BF16 = 0, 1
 OP_HASH, OP_FORWARD, OP_BACKWARD = 0, 1, 2
-STATUS = {0: "YOSO_OK", 1: "YOSO_ERR_NULL", 2: "YOSO_ERR_SHAPE", 3: "YOSO_ERR_HASH", 4: "YOSO_ERR_DTYPE",
+STATUS = {0: "YOSO_OK", 1: "YOSO_ERR_NULL", 2: "YOSO_ERR_SHAPE", 3: "YOSO_ERR_TAU", 4: "YOSO_ERR_DTYPE",
           5: "YOSO_ERR_ALIGN", 6: "YOSO_ERR_WORKSPACE", 7: "YOSO_ERR_DEVICE", 8: "YOSO_ERR_OP"}
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -62,15 +63,16 @@ def lib() -> ctypes.CDLL:
         L.yoso_fast_hash.argtypes = [P, I32, I64, I64, I32, P, I32, I32, P, P]
         L.yoso_forward.argtypes = [P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, SZ, P]
         L.yoso_backward.argtypes = [P, P, P, P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, P, P, SZ, P]
-        L.yoso_workspace_size.argtypes = [I32, I32, I64, I64, I64, I32, I32, I32, ctypes.POINTER(SZ)]
+        L.yoso_workspace_bytes.argtypes = [I32, I64, I64, I64, I32, I32, I32, I32]
+        L.yoso_workspace_bytes.restype = SZ
         L.yoso_l2_normalize.argtypes = [P, I32, I64, I32, P, P]
         L.yoso_expectation_forward.argtypes = [P, P, P, I32, I64, I64, I64, I32, I32, P, P]
         L.yoso_expectation_backward.argtypes = [P, P, P, P, I32, I64, I64, I64, I32, I32, P, P, P, P]
         L.yoso_l2_normalize_backward.argtypes = [P, P, I32, I64, I32, P, P]
-        for fn in ("yoso_hash", "yoso_forward", "yoso_backward", "yoso_workspace_size"):
+        for fn in ("yoso_hash", "yoso_forward", "yoso_backward"):
             getattr(L, fn).restype = ctypes.c_int
-        L.yoso_status_string.argtypes = [ctypes.c_int]
-        L.yoso_status_string.restype = ctypes.c_char_p
+        L.yoso_status_str.argtypes = [ctypes.c_int]
+        L.yoso_status_str.restype = ctypes.c_char_p
         L.yoso_last_error.argtypes = []
         L.yoso_last_error.restype = ctypes.c_char_p
         L.yoso_timing_enable.argtypes = [I32]
@@ -121,21 +123,54 @@ def _codes_ok(c) -> None:
         raise TypeError("codes must be int16 or uint16 tensors (16-bit storage)")
 
 
+def _same(ref, named) -> None:
+    """Every tensor in `named` ((tensor, name) pairs) must have the storage type of
+    `ref` and live on its device: the kernels read and write every buffer with the
+    element size of the one dtype code passed to the C ABI."""
+    for t, name in named:
+        if t is None:
+            continue
+        if t.dtype != ref.dtype:
+            raise TypeError(f"{name} is {t.dtype}, expected {ref.dtype} like the other data tensors")
+        if t.device != ref.device:
+            raise ValueError(f"{name} is on {t.device}, expected {ref.device}")
+
+
+def _on(ref, named) -> None:
+    """Tensors of other types (codes, R, signs, workspace) must share ref's device."""
+    for t, name in named:
+        if t is not None and t.device != ref.device:
+            raise ValueError(f"{name} is on {t.device}, expected {ref.device}")
+
+
+def _f32(t, name: str) -> None:
+    import torch
+    if t.dtype != torch.float32:
+        raise TypeError(f"{name} must be float32")
+
+
 def _expect(t, shape, name: str) -> None:
     """The C ABI cannot see buffer sizes, so shapes are checked here before any launch."""
     if tuple(t.shape) != tuple(shape):
         raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
 
 
-def yoso_workspace_size(op: int, dtype: int, bh: int, n_q: int, n_k: int, d: int, m: int, tau: int) -> int:
-    out = ctypes.c_size_t(0)
-    _check(lib().yoso_workspace_size(op, dtype, bh, n_q, n_k, d, m, tau, ctypes.byref(out)))
-    return out.value
+def yoso_workspace_bytes(op: int, bh: int, n_q: int, n_k: int, d: int, m: int, tau: int, dtype: int) -> int:
+    out = lib().yoso_workspace_bytes(op, bh, n_q, n_k, d, m, tau, dtype)
+    if out == ctypes.c_size_t(-1).value:
+        raise YosoError(-1, lib().yoso_last_error().decode())
+    return out
+
+
+def yoso_status_str(status: int) -> str:
+    return lib().yoso_status_str(status).decode()
 
 
 def yoso_hash(x, R, m: int, tau: int, codes, stream=None) -> None:
     """codes[b, i, h] = sum_t [x[b, i] . R[:, h*tau + t] > 0] << t."""
     _codes_ok(codes)
+    _f32(R, "R")
+    _on(x, ((R, "R"), (codes, "codes")))
     bh, n, d = x.shape
     _expect(R, (d, m * tau), "R")
     _expect(codes, (bh, n, m), "codes")
@@ -148,8 +183,8 @@ def yoso_fast_hyperplanes(signs, m: int, tau: int, R, stream=None) -> None:
     import torch
     if signs.dtype not in (torch.int64, torch.uint64):
         raise TypeError("signs must be an int64 or uint64 tensor (64-bit masks)")
-    if R.dtype != torch.float32:
-        raise TypeError("R must be float32")
+    _f32(R, "R")
+    _on(R, ((signs, "signs"),))
     _expect(signs, ((m * tau + 63) // 64, 3), "signs")
     _expect(R, (64, m * tau), "R")
     _check(lib().yoso_fast_hyperplanes(_ptr(signs), 64, m, tau, _ptr(R), _stream(stream)))
@@ -161,6 +196,7 @@ def yoso_fast_hash(x, signs, m: int, tau: int, codes, stream=None) -> None:
     _codes_ok(codes)
     if signs.dtype not in (torch.int64, torch.uint64):
         raise TypeError("signs must be an int64 or uint64 tensor (64-bit masks)")
+    _on(x, ((signs, "signs"), (codes, "codes")))
     bh, n, d = x.shape
     _expect(signs, ((m * tau + 63) // 64, 3), "signs")
     _expect(codes, (bh, n, m), "codes")
@@ -172,6 +208,8 @@ def yoso_forward(qcodes, kcodes, v, m: int, tau: int, y, ws=None, stream=None) -
     """y = (1/m) sum_h B_h v with B_h(i, j) = [qcodes[:, i, h] == kcodes[:, j, h]]."""
     _codes_ok(qcodes)
     _codes_ok(kcodes)
+    _same(v, ((y, "y"),))
+    _on(v, ((qcodes, "qcodes"), (kcodes, "kcodes"), (ws, "ws")))
     bh, n_k, d = v.shape
     n_q = y.shape[1]
     _expect(y, (bh, n_q, d), "y")
@@ -186,6 +224,8 @@ def yoso_backward(qcodes, kcodes, q, k, v, dy, m: int, tau: int, dq, dk, dv, ws,
     """dv = (1/m) sum_h B_h^T dy;  dq, dk = tau/(2m) sum_h [(dy v^T) .* B_h] k, ...^T q."""
     _codes_ok(qcodes)
     _codes_ok(kcodes)
+    _same(q, ((k, "k"), (v, "v"), (dy, "dy"), (dq, "dq"), (dk, "dk"), (dv, "dv")))
+    _on(q, ((qcodes, "qcodes"), (kcodes, "kcodes"), (ws, "ws")))
     bh, n_q, d = q.shape
     n_k = k.shape[1]
     for t, shape, name in ((k, (bh, n_k, d), "k"), (v, (bh, n_k, d), "v"), (dy, (bh, n_q, d), "dy"),
@@ -202,8 +242,7 @@ def yoso_l2_normalize(x, y, stream=None) -> None:
     """y = x / ||x|| row by row over the last dimension (zero rows stay zero)."""
     d = x.shape[-1]
     _expect(y, x.shape, "y")
-    if y.dtype != x.dtype:
-        raise TypeError("y must have the dtype of x")
+    _same(x, ((y, "y"),))
     rows = x.numel() // d if d else 0
     _check(lib().yoso_l2_normalize(_ptr(x), _dtype_code(x), rows, d, _ptr(y), _stream(stream)))
 
@@ -213,8 +252,7 @@ def yoso_l2_normalize_backward(x, dy, dx, stream=None) -> None:
     d = x.shape[-1]
     _expect(dy, x.shape, "dy")
     _expect(dx, x.shape, "dx")
-    if dy.dtype != x.dtype or dx.dtype != x.dtype:
-        raise TypeError("dy and dx must have the dtype of x")
+    _same(x, ((dy, "dy"), (dx, "dx")))
     rows = x.numel() // d if d else 0
     _check(lib().yoso_l2_normalize_backward(_ptr(x), _ptr(dy), _dtype_code(x), rows, d, _ptr(dx), _stream(stream)))
 
@@ -223,6 +261,7 @@ def yoso_expectation_forward(q, k, v, tau: int, y, stream=None) -> None:
     """YOSO-E: y = P v with P_ij = (1 - arccos(cos(q_i, k_j))/pi)^tau."""
     bh, n_q, d = q.shape
     n_k = k.shape[1]
+    _same(q, ((k, "k"), (v, "v"), (y, "y")))
     for t, shape, name in ((k, (bh, n_k, d), "k"), (v, (bh, n_k, d), "v"), (y, (bh, n_q, d), "y")):
         _expect(t, shape, name)
     _check(lib().yoso_expectation_forward(_ptr(q), _ptr(k), _ptr(v), _dtype_code(q), bh, n_q, n_k, d, tau, _ptr(y),
@@ -233,6 +272,7 @@ def yoso_expectation_backward(q, k, v, dy, tau: int, dq, dk, dv, stream=None) ->
     """YOSO-E backward: dv = P^T dy, dq = (tau/2)[(dy v^T) .* P] k, dk = (tau/2)[(dy v^T) .* P]^T q."""
     bh, n_q, d = q.shape
     n_k = k.shape[1]
+    _same(q, ((k, "k"), (v, "v"), (dy, "dy"), (dq, "dq"), (dk, "dk"), (dv, "dv")))
     for t, shape, name in ((k, (bh, n_k, d), "k"), (v, (bh, n_k, d), "v"), (dy, (bh, n_q, d), "dy"),
                            (dq, (bh, n_q, d), "dq"), (dk, (bh, n_k, d), "dk"), (dv, (bh, n_k, d), "dv")):
         _expect(t, shape, name)
@@ -262,7 +302,7 @@ def workspace(op: int, x, m: int, tau: int, n_k: Optional[int] = None):
     import torch
     bh, n_q, d = x.shape
     n_k = n_q if n_k is None else n_k
-    nbytes = yoso_workspace_size(op, _dtype_code(x), bh, n_q, n_k, d, m, tau)
+    nbytes = yoso_workspace_bytes(op, bh, n_q, n_k, d, m, tau, _dtype_code(x))
     return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=x.device)
 
 

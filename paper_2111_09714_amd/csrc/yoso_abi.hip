@@ -55,9 +55,9 @@ yoso_status check_rows(int64_t rows, int32_t d) {
 }
 
 yoso_status check_hash(int32_t m, int32_t tau) {
-    if (tau < 1 || tau > 12) return fail(YOSO_ERR_HASH, "tau = %d outside [1, 12]", tau);
-    if (m < 1 || m > 64) return fail(YOSO_ERR_HASH, "m = %d outside [1, 64]", m);
-    if (m * tau > 512) return fail(YOSO_ERR_HASH, "m*tau = %d > 512", m * tau);
+    if (tau < 1 || tau > 12) return fail(YOSO_ERR_TAU, "tau = %d outside [1, 12]", tau);
+    if (m < 1 || m > 64) return fail(YOSO_ERR_TAU, "m = %d outside [1, 64]", m);
+    if (m * tau > 512) return fail(YOSO_ERR_TAU, "m*tau = %d > 512", m * tau);
     return YOSO_OK;
 }
 
@@ -95,12 +95,12 @@ yoso_status check_workspace(const void *ws, size_t have, size_t need) {
 
 extern "C" {
 
-const char *yoso_status_string(yoso_status status) {
+const char *yoso_status_str(yoso_status status) {
     switch (status) {
         case YOSO_OK: return "ok";
         case YOSO_ERR_NULL: return "null pointer";
         case YOSO_ERR_SHAPE: return "unsupported shape";
-        case YOSO_ERR_HASH: return "tau or m out of range";
+        case YOSO_ERR_TAU: return "tau or m out of range";
         case YOSO_ERR_DTYPE: return "unknown dtype";
         case YOSO_ERR_ALIGN: return "misaligned pointer";
         case YOSO_ERR_WORKSPACE: return "workspace missing or too small";
@@ -112,17 +112,17 @@ const char *yoso_status_string(yoso_status status) {
 
 const char *yoso_last_error(void) { return g_last_error; }
 
-yoso_status yoso_workspace_size(yoso_op op, yoso_dtype dtype, int64_t bh, int64_t n_q, int64_t n_k, int32_t d,
-                                int32_t m, int32_t tau, size_t *bytes) {
+size_t yoso_workspace_bytes(int op, int64_t bh, int64_t n_q, int64_t n_k, int32_t d, int32_t m, int32_t tau,
+                            yoso_dtype dtype) {
     g_last_error[0] = '\0';
-    if (op != YOSO_OP_HASH && op != YOSO_OP_FORWARD && op != YOSO_OP_BACKWARD)
-        return fail(YOSO_ERR_OP, "unknown op %d", (int)op);
-    YOSO_TRY(check_dtype(dtype));
-    YOSO_TRY(check_shape(bh, n_q, n_k, d, m));
-    YOSO_TRY(check_hash(m, tau));
-    if (bytes == nullptr) return fail(YOSO_ERR_NULL, "bytes is NULL");
-    *bytes = required_workspace(op, dtype == YOSO_BF16, bh, n_q, n_k, m, tau);
-    return YOSO_OK;
+    const size_t bad = static_cast<size_t>(-1);
+    if (op != YOSO_OP_HASH && op != YOSO_OP_FORWARD && op != YOSO_OP_BACKWARD) {
+        fail(YOSO_ERR_OP, "unknown op %d", op);
+        return bad;
+    }
+    if (check_dtype(dtype) != YOSO_OK || check_shape(bh, n_q, n_k, d, m) != YOSO_OK || check_hash(m, tau) != YOSO_OK)
+        return bad;
+    return required_workspace(static_cast<yoso_op>(op), dtype == YOSO_BF16, bh, n_q, n_k, m, tau);
 }
 
 yoso_status yoso_hash(const void *x, yoso_dtype dtype, int64_t bh, int64_t n, int32_t d, const float *R,

@@ -31,16 +31,17 @@ def _declared_symbols():
 
 def test_every_declared_symbol_is_exported(L):
     names = _declared_symbols()
-    assert {"yoso_hash", "yoso_forward", "yoso_backward", "yoso_workspace_size",
-            "yoso_status_string", "yoso_last_error"} <= set(names)
+    assert {"yoso_hash", "yoso_forward", "yoso_backward", "yoso_workspace_bytes",
+            "yoso_status_str", "yoso_last_error"} <= set(names)
     for name in names:
         assert hasattr(L, name), name
 
 
 def test_status_strings(L):
     for s in range(9):
-        assert L.yoso_status_string(s)
-    assert L.yoso_status_string(0) == b"ok"
+        assert L.yoso_status_str(s)
+    assert L.yoso_status_str(0) == b"ok"
+    assert Y.yoso_status_str(3) == "tau or m out of range"
 
 
 def _hash(L, x=FAKE, dtype=0, bh=2, n=128, d=64, R=FAKE, m=32, tau=8, codes=FAKE):
@@ -99,7 +100,7 @@ def test_forward_rejects(L, kw, status):
 
 def test_forward_workspace_checks(L):
     # tau = 12, m = 64 needs several hash groups, and bf16 output needs an fp32 accumulator
-    need = Y.yoso_workspace_size(Y.OP_FORWARD, Y.BF16, 2, 128, 128, 64, 32, 12)
+    need = Y.yoso_workspace_bytes(Y.OP_FORWARD, 2, 128, 128, 64, 32, 12, Y.BF16)
     assert need > 0
     assert _fwd(L, dtype=1, tau=12, ws=None, wsb=0) == 6
     assert _fwd(L, dtype=1, tau=12, ws=FAKE, wsb=need - 1) == 6
@@ -134,8 +135,8 @@ def test_workspace_sizes():
     # Q, K, V, dY (4 bytes per element) and one partial row per (row, hash) for dq and
     # dk in block floating point (64 int16 mantissas + one exponent byte), the same
     # for both storage types
-    f32 = Y.yoso_workspace_size(Y.OP_BACKWARD, Y.F32, 32, 4096, 4096, 64, 32, 8)
-    bf = Y.yoso_workspace_size(Y.OP_BACKWARD, Y.BF16, 32, 4096, 4096, 64, 32, 8)
+    f32 = Y.yoso_workspace_bytes(Y.OP_BACKWARD, 32, 4096, 4096, 64, 32, 8, Y.F32)
+    bf = Y.yoso_workspace_bytes(Y.OP_BACKWARD, 32, 4096, 4096, 64, 32, 8, Y.BF16)
     units = 32 * 32
     index = units * (2 * 257 * 4 + 2 * 4096 * 4)
     split = 4 * 32 * 4096 * 64 * 4
@@ -143,10 +144,51 @@ def test_workspace_sizes():
     assert f32 >= index + split + partials
     assert f32 < 1.05 * (index + split + partials) + (1 << 20)
     assert bf == f32
-    assert Y.yoso_workspace_size(Y.OP_HASH, Y.F32, 32, 4096, 4096, 64, 32, 8) == 0
-    assert Y.yoso_workspace_size(Y.OP_FORWARD, Y.F32, 32, 4096, 4096, 64, 32, 8) == 0
+    assert Y.yoso_workspace_bytes(Y.OP_HASH, 32, 4096, 4096, 64, 32, 8, Y.F32) == 0
+    assert Y.yoso_workspace_bytes(Y.OP_FORWARD, 32, 4096, 4096, 64, 32, 8, Y.F32) == 0
     with pytest.raises(Y.YosoError):
-        Y.yoso_workspace_size(9, Y.F32, 1, 1, 1, 64, 1, 1)
+        Y.yoso_workspace_bytes(9, 1, 1, 1, 64, 1, 1, Y.F32)
+
+
+def test_workspace_bytes_rejects_bad_arguments(L):
+    bad = ctypes.c_size_t(-1).value
+    # op, bh, n_q, n_k, d, m, tau, dtype
+    for args in ((9, 1, 1, 1, 64, 1, 1, 0), (2, 1, 1, 1, 32, 1, 1, 0), (2, 1, 1, 1, 64, 1, 13, 0),
+                 (2, 1, 1, 1, 64, 65, 1, 0), (2, -1, 1, 1, 64, 1, 1, 0), (2, 1, 70000, 1, 64, 1, 1, 0),
+                 (2, 1, 1, 1, 64, 1, 1, 5)):
+        assert L.yoso_workspace_bytes(*args) == bad, args
+        assert L.yoso_last_error()
+
+
+def test_binding_refuses_mixed_dtypes_and_devices():
+    """The C ABI takes one dtype code for all data tensors: a tensor of another type
+    (or R that is not fp32) would be read or written with the wrong element size, so
+    the binding refuses it before any call."""
+    torch = pytest.importorskip("torch")
+    f, b = torch.float32, torch.bfloat16
+    x = torch.zeros(1, 16, 64)
+    codes = torch.zeros(1, 16, 2, dtype=torch.int16)
+    with pytest.raises(TypeError):
+        Y.yoso_hash(x, torch.zeros(64, 16, dtype=b), 2, 8, codes)
+    with pytest.raises(TypeError):
+        Y.yoso_forward(codes, codes, torch.zeros(1, 16, 64, dtype=f), 2, 8, torch.zeros(1, 16, 64, dtype=b))
+    q = torch.zeros(1, 16, 64, dtype=f)
+    for bad in range(6):
+        ts = [torch.zeros(1, 16, 64, dtype=f) for _ in range(6)]
+        ts[bad] = ts[bad].to(b)
+        k, v, dy, dq, dk, dv = ts
+        with pytest.raises(TypeError):
+            Y.yoso_backward(codes, codes, q, k, v, dy, 2, 8, dq, dk, dv, None)
+    with pytest.raises(TypeError):
+        Y.yoso_l2_normalize(q, torch.zeros(1, 16, 64, dtype=b))
+    with pytest.raises(TypeError):
+        Y.yoso_l2_normalize_backward(q, q, torch.zeros(1, 16, 64, dtype=b))
+    with pytest.raises(TypeError):
+        Y.yoso_expectation_forward(q, q, q, 8, torch.zeros(1, 16, 64, dtype=b))
+    with pytest.raises(TypeError):
+        Y.yoso_expectation_backward(q, q.to(b), q, q, 8, q, q, q)
+    with pytest.raises(TypeError):
+        Y.yoso_fast_hyperplanes(torch.zeros(1, 3, dtype=torch.int64), 8, 8, torch.zeros(64, 64, dtype=b))
 
 
 def test_binding_refuses_host_tensors():

@@ -13,6 +13,7 @@ import pytest
 
 import oracle
 import workloads
+from parity import check_all
 from workloads import WORKLOADS, make_inputs
 
 pytestmark = pytest.mark.gpu
@@ -149,10 +150,9 @@ def test_attention_on_fast_codes():
         assert check_codes(x, inp["signs"], w.m, w.tau, c)[0] == 0
     yo = oracle.forward(gq, gk, inp["v"], w.m, w.tau)
     dqo, dko, dvo = oracle.backward(gq, gk, inp["q"], inp["k"], inp["v"], inp["dy"], w.m, w.tau)
-    for name, a, b in (("y", y, yo), ("dq", dq, dqo), ("dk", dk, dko), ("dv", dv, dvo)):
-        e = np.linalg.norm(host(a) - b) / np.linalg.norm(b)
-        log(f"[attention on fast codes] {name} rel err {e:.2e}")
-        assert e <= 1e-4, (name, e)
+    check_all("attention on fast codes",
+              [(name, host(a), b) for name, a, b in (("y", y, yo), ("dq", dq, dqo), ("dk", dk, dko), ("dv", dv, dvo))],
+              1e-4)
 
 
 def test_fast_hash_matches_dense_hash_of_expanded_rotations():

@@ -4,17 +4,18 @@ Bars:
   * hash codes bit-exact wherever the oracle's smallest |projection| of the hash
     exceeds 1e-4; the excluded fraction is reported;
   * forward/backward evaluated on the GPU's own codes (so a legitimate flip of a
-    near-zero bit cannot fail output parity): per head
-    ||gpu - ref||_F / ||ref||_F <= 1e-4 for fp32 storage, <= 2e-2 for bf16.
+    near-zero bit cannot fail output parity): per head ||gpu - ref||_F / ||ref||_F
+    and, element by element, |gpu - ref| / (|ref| + rms(ref row)), both <= 1e-4
+    for fp32 storage and <= 2e-2 for bf16 (tests/parity.py).
 """
 import math
-import sys
 
 import numpy as np
 import pytest
 
 import oracle
 import workloads
+from parity import TOL, check_all, log
 from workloads import WORKLOADS, make_inputs
 
 pytestmark = pytest.mark.gpu
@@ -23,18 +24,12 @@ torch = pytest.importorskip("torch")
 import paper_2111_09714_amd as Y  # noqa: E402
 
 MARGIN = 1e-4
-TOL = {"f32": 1e-4, "bf16": 2e-2}
 
 
 @pytest.fixture(scope="module", autouse=True)
 def _gpu():
     assert torch.cuda.is_available(), "GPU tests need a GPU"
     Y.lib()  # fails loudly if the HIP library is missing
-
-
-def log(msg):
-    print(msg, flush=True)
-    sys.stdout.flush()
 
 
 def to_dev(a, dtype):
@@ -45,16 +40,6 @@ def to_dev(a, dtype):
 def codes_np(t):
     """GPU codes [bh, n, m] as the oracle's [bh, m, n] layout."""
     return np.ascontiguousarray(t.cpu().numpy().view(np.uint16).transpose(0, 2, 1))
-
-
-def rel_err(gpu, ref):
-    """Per head relative Frobenius error; heads whose reference is 0 must be 0."""
-    out = []
-    for g, r in zip(gpu, ref):
-        nr = np.linalg.norm(r)
-        ng = np.linalg.norm(g - r)
-        out.append(ng / nr if nr > 0 else (0.0 if ng <= 1e-6 else np.inf))
-    return max(out) if out else 0.0
 
 
 def run_gpu(inp, m, tau, dtype):
@@ -84,10 +69,8 @@ def check_outputs(name, inp, g, m, tau, dtype, heads=None):
     qc, kc = g["qc"][sl], g["kc"][sl]
     y = oracle.forward(qc, kc, v, m, tau)
     dq, dk, dv = oracle.backward(qc, kc, q, k, v, dy, m, tau)
-    errs = {key: rel_err(g[key][sl], ref) for key, ref in (("y", y), ("dq", dq), ("dk", dk), ("dv", dv))}
-    log(f"[{name}] relative errors " + " ".join(f"{k_}={v_:.2e}" for k_, v_ in errs.items()))
-    for key, e in errs.items():
-        assert e <= TOL[dtype], (key, e)
+    check_all(name, [(key, g[key][sl], ref) for key, ref in (("y", y), ("dq", dq), ("dk", dk), ("dv", dv))],
+              TOL[dtype])
 
 
 SMALL = [
@@ -132,12 +115,13 @@ def run_case(bh, nq, nk, m, tau, dtype):
 @pytest.mark.parametrize("name", list(WORKLOADS))
 def test_workload_full_size(name):
     """Every head runs on the GPU exactly as the bench launches it; the oracle
-    recomputes a sample of heads (heads are independent, so this is exact)."""
+    recomputes the first and the last head (heads are independent, so this is
+    exact)."""
     w = WORKLOADS[name]
     log(f"[{name}] start: bh={w.bh} n={w.n} m={w.m} tau={w.tau} {w.dtype}")
     inp = make_inputs(w)
     g = run_gpu(inp, w.m, w.tau, w.dtype)
-    heads = [0, w.bh - 1] if w.n <= 4096 else [w.bh - 1]
+    heads = [0, w.bh - 1]
     sl = np.array(sorted(set(heads)))
     check_codes(name + "/q", inp["q"][sl], inp["R"], w.m, w.tau, g["qc"][sl])
     check_codes(name + "/k", inp["k"][sl], inp["R"], w.m, w.tau, g["kc"][sl])
@@ -175,14 +159,7 @@ def test_golden_worked_example(golden):
     for t, key in ((y, "y"), (dq, "dq"), (dk, "dk"), (dv, "dv")):
         got = t.cpu().numpy()[0]
         ref = np.array(g[key])
-        if key in ("dq", "dk"):
-            # per-hash partial rows are stored with 16-bit mantissas and one exponent per
-            # row: each is exact to 2^-15 of the row's largest value, so the sum of m of
-            # them to m * 2^-15 of the largest |value|
-            tol = m * 2.0 ** -15 * np.abs(ref).max()
-            np.testing.assert_allclose(got[:, :2], ref, rtol=0, atol=tol)
-        else:
-            np.testing.assert_allclose(got[:, :2], ref, rtol=1e-5, atol=1e-5)
+        np.testing.assert_allclose(got[:, :2], ref, rtol=1e-5, atol=1e-5, err_msg=key)
         assert not got[:, 2:].any()
 
 
@@ -251,7 +228,6 @@ def test_all_keys_in_one_bucket_backward_closed_form():
     dq_ref = (tau / 2) * (dy[0].double() @ sv)[:, None] * u.double()[None, :]
     dk_ref = (tau / 2) * (v[0].double() @ sdy)[:, None] * u.double()[None, :]
     assert torch.equal(dv[0].double(), sdy.expand(n, 64))
-    for name, got, ref in (("dq", dq[0], dq_ref), ("dk", dk[0], dk_ref)):
-        e = (torch.linalg.norm(got.double() - ref) / torch.linalg.norm(ref)).item()
-        log(f"[one bucket, n={n}] {name} rel err {e:.2e}")
-        assert e <= TOL["f32"], (name, e)
+    check_all(f"one bucket, n={n}", [(name, got.double().cpu().numpy()[None], ref.cpu().numpy()[None])
+                                     for name, got, ref in (("dq", dq[0], dq_ref), ("dk", dk[0], dk_ref))],
+              TOL["f32"])
