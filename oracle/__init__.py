@@ -45,14 +45,16 @@ def _load():
         lib.oracle_forward.argtypes = [P, P, P, I64, I64, I64, I32, I32, I32, P]
         lib.oracle_backward.argtypes = [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, P, P, P]
         lib.oracle_backward_d2.argtypes = [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, P, P]
-        lib.oracle_expectation.argtypes = [P, P, P, P, I64, I64, I64, I32, I32, P, P, P, P, P]
+        lib.oracle_expectation.argtypes = [P, P, P, P, I64, I64, I64, I32, I32, ctypes.c_double, P, P, P, P, P, P]
+        lib.oracle_backward_star.argtypes = [P, P, P, P, P, P, I64, I64, I64, I32, I32, I32, ctypes.c_double,
+                                             P, P, P]
         lib.oracle_l2_normalize.argtypes = [P, I64, I32, P]
         lib.oracle_l2_normalize_backward.argtypes = [P, P, I64, I32, P]
         lib.oracle_hadamard.argtypes = [I32, P]
         lib.oracle_fast_hyperplanes.argtypes = [P, I32, I32, I32, P]
         lib.oracle_collision_prob.argtypes = [ctypes.c_double, I32]
         lib.oracle_collision_prob.restype = ctypes.c_double
-        for fn in ("oracle_hash", "oracle_forward", "oracle_backward", "oracle_backward_d2",
+        for fn in ("oracle_hash", "oracle_forward", "oracle_backward", "oracle_backward_d2", "oracle_backward_star",
                    "oracle_expectation", "oracle_l2_normalize", "oracle_l2_normalize_backward",
                    "oracle_hadamard", "oracle_fast_hyperplanes"):
             getattr(lib, fn).restype = None
@@ -124,8 +126,32 @@ def backward_d2(qc, kc, q, k, v, dy, m: int, tau: int):
     return dq, dk
 
 
-def expectation(q, k, v, dy, tau: int, true_grad: bool = False):
-    """E[Y], E[dV], E[dQ], E[dK] over hash functions (and the true dQ if asked)."""
+# Bound of 1 - x^2 in *YOSO's weight 1/(pi sqrt(1 - x^2)) (|x| <= 0.99216, at most
+# 8/pi): the reading this build takes of the divergence that Sec. 3.3 points out.
+STAR_FLOOR = 1.0 / 64.0
+
+
+def backward_star(qc, kc, q, k, v, dy, m: int, tau: int, floor: float = STAR_FLOOR):
+    """(dq, dk, dv) of *YOSO: the sampled estimate of the true gradient of
+    eq. (gradient-q) (pairs whose codes agree on all bits but at most one), and
+    dv of eq. (gradient-v)."""
+    qc, kc = _u16(qc), _u16(kc)
+    q, k, v, dy = _f64(q), _f64(k), _f64(v), _f64(dy)
+    bh, nq, d = q.shape
+    nk = k.shape[1]
+    assert qc.shape == (bh, m, nq) and kc.shape == (bh, m, nk)
+    dq = np.zeros((bh, nq, d))
+    dk = np.zeros((bh, nk, d))
+    dv = np.zeros((bh, nk, d))
+    _load().oracle_backward_star(_ptr(qc), _ptr(kc), _ptr(q), _ptr(k), _ptr(v), _ptr(dy),
+                                 bh, nq, nk, d, m, tau, float(floor), _ptr(dq), _ptr(dk), _ptr(dv))
+    return dq, dk, dv
+
+
+def expectation(q, k, v, dy, tau: int, true_grad: bool = False, floor: float = 0.0):
+    """E[Y], E[dV], E[dQ], E[dK] over hash functions; with ``true_grad`` also the
+    true gradients of eq. (gradient-q) for Q and K, their 1 - cos^2 raised to at
+    least ``floor``."""
     q, k, v, dy = _f64(q), _f64(k), _f64(v), _f64(dy)
     bh, nq, d = q.shape
     nk = k.shape[1]
@@ -134,11 +160,12 @@ def expectation(q, k, v, dy, tau: int, true_grad: bool = False):
     edq = np.zeros((bh, nq, d))
     edk = np.zeros((bh, nk, d))
     tdq = np.zeros((bh, nq, d)) if true_grad else None
-    _load().oracle_expectation(_ptr(q), _ptr(k), _ptr(v), _ptr(dy), bh, nq, nk, d, tau,
+    tdk = np.zeros((bh, nk, d)) if true_grad else None
+    _load().oracle_expectation(_ptr(q), _ptr(k), _ptr(v), _ptr(dy), bh, nq, nk, d, tau, float(floor),
                                _ptr(ey), _ptr(edv), _ptr(edq), _ptr(edk),
-                               _ptr(tdq) if true_grad else None)
+                               _ptr(tdq) if true_grad else None, _ptr(tdk) if true_grad else None)
     out = (ey, edv, edq, edk)
-    return out + (tdq,) if true_grad else out
+    return out + (tdq, tdk) if true_grad else out
 
 
 def l2_normalize(x) -> np.ndarray:

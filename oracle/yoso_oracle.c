@@ -20,6 +20,9 @@
  *               symmetric expression for dK; all averaged over the m hashes.
  *   backward_d2 the same surrogate written as eq. (backward-d2): d runs of the
  *               bucket-table subroutine, used to cross-check the pairwise form.
+ *   backward_star  *YOSO (Sec. 3.3 eq. (gradient-q); Sec. 4): an unbiased
+ *               sampled estimate of the true gradient on the same hashes, from
+ *               the pairs whose codes agree on all bits but at most one.
  *   expectation eq. (yoso-expectation): E[B_ij] = (1 - arccos(q_i.k_j)/pi)^tau,
  *               giving E[Y], E[dV], E[dQ], E[dK], and the true dQ of
  *               eq. (gradient-q) for reference.
@@ -191,6 +194,79 @@ void oracle_backward(const uint16_t *qc, const uint16_t *kc,
     free(table); free(qstart); free(kstart); free(qmem); free(kmem); free(fill);
 }
 
+/* *YOSO: a sampled estimate of the TRUE gradient of eq. (gradient-q) and of its
+ * symmetric counterpart for K, on the same m hashes (Sec. 3.3; the variant the
+ * experiments call *YOSO, Sec. 4).
+ *
+ * eq. (gradient-q) weighs the pair (i, j) by tau (1 - theta_ij/pi)^(tau-1) /
+ * (pi sqrt(1 - x_ij^2)), x_ij = q_i . k_j, theta_ij = arccos x_ij.  The factor
+ * (1 - theta/pi)^(tau-1) is the probability that tau-1 independent hyperplane
+ * bits agree (the collision law of the Fig. 2 caption with one bit fewer).  A
+ * tau-bit code minus its bit t is such a (tau-1)-bit hash, so for every hash h
+ *
+ *   C_h(i, j) = sum_{t < tau} [ codes of q_i and k_j agree on every bit except t ]
+ *
+ * has expectation tau (1 - theta_ij/pi)^(tau-1), and
+ *
+ *   dq_i = (1/m) sum_h sum_j C_h(i, j) (dy_i . v_j) / (pi sqrt(max(1 - x_ij^2, eps))) k_j
+ *   dk_j = (1/m) sum_h sum_i C_h(i, j) (dy_i . v_j) / (pi sqrt(max(1 - x_ij^2, eps))) q_i
+ *
+ * is unbiased for eq. (gradient-q) wherever 1 - x^2 >= eps.  The paper notes
+ * that the true gradient diverges as the alignment x approaches 1; eps = `floor`
+ * bounds the weight (floor = 0: no bound).  x is the dot product of the rows as
+ * given, clamped to [-1, 1] (the method takes unit rows).  dv is eq. (gradient-v)
+ * exactly as in oracle_backward. */
+void oracle_backward_star(const uint16_t *qc, const uint16_t *kc,
+                          const double *q, const double *k, const double *v, const double *dy,
+                          int64_t bh, int64_t nq, int64_t nk, int d, int m, int tau, double floor_,
+                          double *dq, double *dk, double *dv)
+{
+    const int64_t buckets = (int64_t)1 << tau;
+    const unsigned full = (unsigned)buckets - 1u;
+    double *table = malloc(sizeof(double) * buckets * d);
+
+    memset(dq, 0, sizeof(double) * bh * nq * d);
+    memset(dk, 0, sizeof(double) * bh * nk * d);
+    memset(dv, 0, sizeof(double) * bh * nk * d);
+
+    for (int64_t b = 0; b < bh; b++) {
+        const double *qb = q + b * nq * d, *kb = k + b * nk * d;
+        const double *vb = v + b * nk * d, *dyb = dy + b * nq * d;
+        double *dqb = dq + b * nq * d, *dkb = dk + b * nk * d;
+        for (int h = 0; h < m; h++) {
+            const uint16_t *qch = &CODE(qc, b, h, 0, m, nq);
+            const uint16_t *kch = &CODE(kc, b, h, 0, m, nk);
+            table_pass(qch, dyb, nq, kch, nk, d, tau, 1.0 / m, dv + b * nk * d, table);
+            for (int64_t i = 0; i < nq; i++) {
+                for (int64_t j = 0; j < nk; j++) {
+                    /* the dropped-bit hashes under which i and j collide */
+                    int count = 0;
+                    for (int t = 0; t < tau; t++) {
+                        const unsigned keep = full & ~(1u << t);
+                        if (((qch[i] ^ kch[j]) & keep) == 0) count++;
+                    }
+                    if (count == 0) continue;
+                    double s = 0.0, x = 0.0;
+                    for (int l = 0; l < d; l++) {
+                        s += dyb[i * d + l] * vb[j * d + l];
+                        x += qb[i * d + l] * kb[j * d + l];
+                    }
+                    if (x > 1.0) x = 1.0;
+                    if (x < -1.0) x = -1.0;
+                    double r = 1.0 - x * x;
+                    if (r < floor_) r = floor_;
+                    const double w = count / (M_PI * sqrt(r)) / m;
+                    for (int l = 0; l < d; l++) {
+                        dqb[i * d + l] += w * s * kb[j * d + l];
+                        dkb[j * d + l] += w * s * qb[i * d + l];
+                    }
+                }
+            }
+        }
+    }
+    free(table);
+}
+
 /* The same dQ, dK surrogate in the form of eq. (backward-d2):
  *   dq_i = (1/m) sum_h sum_l dy_{i,l} sum_j B_h(i,j) (v_{j,l} (tau/2) k_j)
  * i.e. for every value dimension l one bucket-table run whose table rows are
@@ -252,17 +328,21 @@ double oracle_collision_prob(double x, int tau)
  *   ey  = P v,  edv = P^T dy,
  *   edq = (tau/2) [(dy v^T) .* P] k,  edk = (tau/2) [(dy v^T) .* P]^T q,
  *   tdq (optional) = [(dy v^T) .* tau P^{(tau-1)/tau} ./ (pi sqrt(1 - cos^2))] k,
- *   the true gradient of eq. (gradient-q) for unit rows (diverges as cos -> 1).
+ *   the true gradient of eq. (gradient-q) for unit rows (diverges as cos -> 1),
+ *   and tdk (optional) = [...]^T q, its counterpart for K.  With floor > 0 the
+ *   factor 1 - cos^2 is raised to at least `floor` (the bound *YOSO's estimator
+ *   uses; 0 leaves it unbounded).
  * The cosine is taken of the rows as given, normalised by their norms. */
 void oracle_expectation(const double *q, const double *k, const double *v, const double *dy,
-                        int64_t bh, int64_t nq, int64_t nk, int d, int tau,
-                        double *ey, double *edv, double *edq, double *edk, double *tdq)
+                        int64_t bh, int64_t nq, int64_t nk, int d, int tau, double floor_,
+                        double *ey, double *edv, double *edq, double *edk, double *tdq, double *tdk)
 {
     memset(ey, 0, sizeof(double) * bh * nq * d);
     memset(edv, 0, sizeof(double) * bh * nk * d);
     memset(edq, 0, sizeof(double) * bh * nq * d);
     memset(edk, 0, sizeof(double) * bh * nk * d);
     if (tdq) memset(tdq, 0, sizeof(double) * bh * nq * d);
+    if (tdk) memset(tdk, 0, sizeof(double) * bh * nk * d);
     for (int64_t b = 0; b < bh; b++) {
         const double *qb = q + b * nq * d, *kb = k + b * nk * d;
         const double *vb = v + b * nk * d, *dyb = dy + b * nq * d;
@@ -285,11 +365,14 @@ void oracle_expectation(const double *q, const double *k, const double *v, const
                     edq[(b * nq + i) * d + l] += (tau / 2.0) * g * p * kb[j * d + l];
                     edk[(b * nk + j) * d + l] += (tau / 2.0) * g * p * qb[i * d + l];
                 }
-                if (tdq) {
-                    const double w = tau * pow(1.0 - acos(cosv) / M_PI, tau - 1)
-                                     / (M_PI * sqrt(1.0 - cosv * cosv));
-                    for (int l = 0; l < d; l++)
-                        tdq[(b * nq + i) * d + l] += g * w * kb[j * d + l];
+                if (tdq || tdk) {
+                    double r = 1.0 - cosv * cosv;
+                    if (r < floor_) r = floor_;
+                    const double w = tau * pow(1.0 - acos(cosv) / M_PI, tau - 1) / (M_PI * sqrt(r));
+                    for (int l = 0; l < d; l++) {
+                        if (tdq) tdq[(b * nq + i) * d + l] += g * w * kb[j * d + l];
+                        if (tdk) tdk[(b * nk + j) * d + l] += g * w * qb[i * d + l];
+                    }
                 }
             }
         }

@@ -312,7 +312,7 @@ def test_true_gradient_matches_finite_difference_of_expectation():
     k = _unit(g.standard_normal((1, 6, d)))
     v = g.standard_normal((1, 6, d))
     dy = g.standard_normal((1, 4, d))
-    _, _, _, _, tdq = oracle.expectation(q, k, v, dy, tau, true_grad=True)
+    _, _, _, _, tdq, _ = oracle.expectation(q, k, v, dy, tau, true_grad=True)
     i = 2
     t = g.standard_normal(d)
     t -= (t @ q[0, i]) * q[0, i]
@@ -324,6 +324,113 @@ def test_true_gradient_matches_finite_difference_of_expectation():
     h = 1e-5
     fd = (loss(h) - loss(-h)) / (2 * h)
     assert abs(fd - tdq[0, i] @ t) < 1e-6 * max(1.0, abs(fd))
+
+
+def test_true_gradient_of_keys_matches_finite_difference_of_expectation():
+    """The K counterpart of eq. (gradient-q): the derivative of <dY, P V> in k_j."""
+    g = _rng(16)
+    tau, d = 4, 6
+    q = _unit(g.standard_normal((1, 5, d)))
+    k = _unit(g.standard_normal((1, 3, d)))
+    v = g.standard_normal((1, 3, d))
+    dy = g.standard_normal((1, 5, d))
+    _, _, _, _, _, tdk = oracle.expectation(q, k, v, dy, tau, true_grad=True)
+    j = 1
+    t = g.standard_normal(d)
+    t -= (t @ k[0, j]) * k[0, j]
+    t /= np.linalg.norm(t)
+    def loss(eps):
+        kk = k.copy()
+        kk[0, j] = _unit(k[0, j] + eps * t)
+        return np.sum(dy * oracle.expectation(q, kk, v, dy, tau)[0])
+    h = 1e-5
+    fd = (loss(h) - loss(-h)) / (2 * h)
+    assert abs(fd - tdk[0, j] @ t) < 1e-6 * max(1.0, abs(fd))
+
+
+# ---------------------------------------------------------------- *YOSO (true-gradient estimator)
+
+def test_star_worked_example(golden):
+    g = golden["star_backward"]
+    m, tau = g["m"], g["tau"]
+    qc = np.array(g["qc"], np.uint16)[None]
+    kc = np.array(g["kc"], np.uint16)[None]
+    q, k, v, dy = (np.array(g[s])[None] for s in ("q", "k", "v", "dy"))
+    dq, dk, dv = oracle.backward_star(qc, kc, q, k, v, dy, m, tau)
+    np.testing.assert_allclose(dq[0] * math.pi, g["dq_times_pi"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dk[0] * math.pi, g["dk_times_pi"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dv[0], g["dv"], rtol=0, atol=1e-12)
+    f = g["floored"]
+    qc = np.array(f["qc"], np.uint16)[None]
+    kc = np.array(f["kc"], np.uint16)[None]
+    q, k, v, dy = (np.array(f[s])[None] for s in ("q", "k", "v", "dy"))
+    dq, dk, _ = oracle.backward_star(qc, kc, q, k, v, dy, 1, f["tau"])
+    np.testing.assert_allclose(dq[0] * math.pi, f["dq_times_pi"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dk[0] * math.pi, f["dk_times_pi"], rtol=0, atol=1e-12)
+
+
+def test_star_is_exact_at_tau_one():
+    """With one bit per hash every pair collides after dropping that bit, so the
+    estimator is the true gradient of eq. (gradient-q) at tau = 1 for any draw."""
+    q, k, v, dy, R = _rand_problem(20, nq=13, nk=11, d=6, m=3, tau=1)
+    qc, kc = oracle.hash_codes(q, R, 3, 1), oracle.hash_codes(k, R, 3, 1)
+    dq, dk, _ = oracle.backward_star(qc, kc, q, k, v, dy, 3, 1)
+    _, _, _, _, tdq, tdk = oracle.expectation(q, k, v, dy, 1, true_grad=True, floor=oracle.STAR_FLOOR)
+    np.testing.assert_allclose(dq, tdq, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(dk, tdk, rtol=1e-12, atol=1e-12)
+
+
+def test_star_pairs_two_bits_apart_contribute_nothing():
+    """Codes that differ in two or more bits are never counted; dV stays the
+    sampled eq. (gradient-v), which is zero without equal codes."""
+    q, k, v, dy, _ = _rand_problem(21, bh=1, nq=5, nk=4, d=4)
+    qc = np.zeros((1, 2, 5), np.uint16)
+    kc = np.full((1, 2, 4), 0b0110, np.uint16)
+    dq, dk, dv = oracle.backward_star(qc, kc, q, k, v, dy, 2, 4)
+    assert not dq.any() and not dk.any() and not dv.any()
+    kc[0, 1, 2] = 0b0100  # one bit away from 0 in hash 1 only: key 2 meets every query once
+    dq, dk, _ = oracle.backward_star(qc, kc, q, k, v, dy, 2, 4)
+    assert np.abs(dk[0, [0, 1, 3]]).max() == 0 and np.abs(dk[0, 2]).max() > 0
+    assert np.all(np.abs(dq[0]).max(axis=1) > 0)
+
+
+def test_star_inner_products_agree():
+    """<dQ*, Q> = <dK*, K>: both are (1/m) sum C_h(i,j) w_ij (dY_i.V_j)(Q_i.K_j)."""
+    q, k, v, dy, R = _rand_problem(22, nq=29, nk=31, d=7, m=4, tau=3)
+    qc, kc = oracle.hash_codes(q, R, 4, 3), oracle.hash_codes(k, R, 4, 3)
+    dq, dk, _ = oracle.backward_star(qc, kc, q, k, v, dy, 4, 3)
+    a, b = np.sum(dq * q), np.sum(dk * k)
+    assert abs(a) > 1e-3 and abs(a - b) < 1e-10 * abs(a)
+
+
+def test_star_monte_carlo_mean_converges_to_true_gradient():
+    """*YOSO is unbiased for eq. (gradient-q): over many hash draws its mean tends
+    to tau (1 - theta/pi)^(tau-1) / (pi sqrt(max(1 - x^2, 1/64))) weighting, for Q and
+    K.  One query-key pair is nearly parallel (x = 0.998) so that the bound is active."""
+    g = _rng(23)
+    tau, d = 4, 3
+    q = _unit(g.standard_normal((1, 12, d)))
+    k = _unit(g.standard_normal((1, 10, d)))
+    k[0, 0] = _unit(q[0, 0] + 0.063 * _unit(g.standard_normal(d)))
+    assert 1 - (q[0, 0] @ k[0, 0]) ** 2 < oracle.STAR_FLOOR
+    v = g.standard_normal((1, 10, d))
+    dy = g.standard_normal((1, 12, d))
+    _, _, _, _, tdq, tdk = oracle.expectation(q, k, v, dy, tau, true_grad=True, floor=oracle.STAR_FLOOR)
+    want = np.concatenate([tdq.ravel(), tdk.ravel()])
+    outs = []
+    for _ in range(40):
+        R = g.standard_normal((d, 256 * tau))
+        qc, kc = oracle.hash_codes(q, R, 256, tau), oracle.hash_codes(k, R, 256, tau)
+        dq, dk, _ = oracle.backward_star(qc, kc, q, k, v, dy, 256, tau)
+        outs.append(np.concatenate([dq.ravel(), dk.ravel()]))
+    samples = np.stack(outs)
+    mean = samples.mean(0)
+    se = samples.std(0, ddof=1) / math.sqrt(samples.shape[0])
+    z = np.abs(mean - want) / np.maximum(se, 1e-12)
+    assert np.all(z < 6.0), z.max()
+    # and the surrogate of eq. (pseudo-gradient-q) is a different quantity
+    _, _, edq, _ = oracle.expectation(q, k, v, dy, tau)
+    assert np.linalg.norm(edq - tdq) > 10 * np.linalg.norm(se[:tdq.size])
 
 
 # ---------------------------------------------------------------- l2 normalisation (N-YOSO, Q/K prologue)
