@@ -27,20 +27,26 @@
  *     returned as YOSO_ERR_DEVICE; yoso_last_error() then holds its text.
  *   - Limits: d == 64; 1 <= tau <= 12; 1 <= m <= 64; m*tau <= 512;
  *     0 <= n <= 65536 per tensor; bh >= 0.  Zero-sized tensors are valid.
+ *     tau stops at 12 because the tables live in LDS: one hash's 2^tau buckets
+ *     for two feature dims take 2^tau x 8 bytes, 32 KiB at tau = 12, and the
+ *     bucket sort keeps 2^tau counters and 64-bit lane masks per wave; with at
+ *     most 65536 rows, tau > 12 would leave almost every bucket with 0 or 1 key.
  *   - Inputs must be finite.  The hash stages rows through fp16 pairs after a
  *     2^8 scaling, so |x| must stay below 255 (unit rows always do) and |R| below
- *     65504; V and dY entries and their dot products times tau/(2m) must stay
- *     below 65504 in magnitude.
+ *     65504.  The backward and YOSO-E scale every operand by a power of two
+ *     before it is split into fp16 (hi, lo) pairs (per head and tensor, per row,
+ *     or per 64-row tile), so V, dY, Q, K may have any magnitude between about
+ *     2^-40 and 2^40; values more than about 2^20 below the largest of their
+ *     head (backward) or tile (YOSO-E) keep less than 22 significant bits.
  *   - Precision.  Y and dV are accumulated as exact fixed-point integers: each
- *     value of a 2-16 wide feature slice is rounded to a multiple of 2^-k, where
- *     2^k is the largest power of two keeping 2^k (1 + 2^-10) times the slice's
- *     largest per-dim sum of |value| over the n_src source rows below 2^30;
- *     everything after that rounding is exact.  dQ and dK use fp32
- *     accumulation of products formed from fp16 (hi, lo) pairs (about 22
- *     significant bits); the contribution of each hash to a row is kept in block
- *     floating point (16-bit mantissas, one power-of-two exponent per row), exact
- *     to about 2^-15 of that row's largest value, and the m contributions are
- *     summed in hash order in fp32 (about 3e-5 relative at unit-norm Q, K).
+ *     value of feature dim d is rounded to a multiple of 2^-k_d, where 2^k_d is
+ *     the largest power of two keeping 2^k_d (1 + 2^-10) times that dim's sum of
+ *     |value| over the n_src source rows below 2^30; everything after that
+ *     rounding is exact.  dQ and dK use fp32 accumulation of products formed
+ *     from fp16 (hi, lo) pairs (about 22 significant bits); the contribution of
+ *     each hash to a row is kept in 24-bit fixed point (one power-of-two
+ *     exponent per row, exact to 2^-23 of that row's largest value), and the m
+ *     contributions are summed in hash order in fp32.
  *   - Reproducibility.  Every accumulation order is fixed (integer tables, a
  *     stable bucket order, partial rows summed in hash order), so repeating a
  *     call on the same inputs gives bitwise identical outputs on any stream.
@@ -164,9 +170,9 @@ yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const v
  *
  * q, dy, dq [bh][n_q][d];  k, v, dk, dv [bh][n_k][d]  (dtype).
  * workspace: yoso_workspace_bytes(YOSO_OP_BACKWARD, ...) bytes of scratch: the
- * per-hash bucket orders, fp16 (hi, lo) copies of q, k, v, dy, and one
- * block-floating-point partial row per (row, hash) for dq and dk: about
- * (2*m*d + 5*m + 8*d) * (n_q + n_k) * bh bytes.
+ * per-hash bucket orders, the per-head maxima of |q|, |k|, |v|, |dy|, fp16
+ * (hi, lo) copies of q, k, v, dy, and one 24-bit fixed-point partial row per
+ * (row, hash) for dq and dk: about (3*m*d + 5*m + 8*d) * (n_q + n_k) * bh bytes.
  */
 yoso_status yoso_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q,
                           const void *k, const void *v, const void *dy, yoso_dtype dtype,

@@ -57,10 +57,18 @@ __device__ __forceinline__ float load1(const void *base, int64_t elem_off) {
 // (a power of two, so the scaling is exact).  hi + lo carries about 22
 // significant bits: enough that the three MFMA products hi*hi, hi*lo, lo*hi
 // reproduce an fp32 dot product to ~1e-6 relative.
+// The scaled value passes through an empty asm operand, so that hi and lo are
+// both derived from the one fp32 register s.  Left visible, the product that
+// produced s gets fused into the conversions (v_fma_mixlo_f16 rounds the exact
+// product to fp16 once) for one use of hi while the kept hi is rounded to fp32
+// first; where the two roundings differ (an fp32 result on an fp16 tie), lo
+// compensates the wrong hi and hi + lo is off by one fp16 ulp.
 __device__ __forceinline__ void split8(const float v[8], float scale, half8 &hi, half8 &lo) {
+#pragma clang fp contract(off)
 #pragma unroll
     for (int i = 0; i < 8; i++) {
-        const float s = v[i] * scale;
+        float s = v[i] * scale;
+        asm volatile("" : "+v"(s));
         const _Float16 h = static_cast<_Float16>(s);
         hi[i] = h;
         lo[i] = static_cast<_Float16>(s - static_cast<float>(h));
@@ -68,9 +76,11 @@ __device__ __forceinline__ void split8(const float v[8], float scale, half8 &hi,
 }
 
 __device__ __forceinline__ void split4(const float v[4], float scale, half4 &hi, half4 &lo) {
+#pragma clang fp contract(off)
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-        const float s = v[i] * scale;
+        float s = v[i] * scale;
+        asm volatile("" : "+v"(s));
         const _Float16 h = static_cast<_Float16>(s);
         hi[i] = h;
         lo[i] = static_cast<_Float16>(s - static_cast<float>(h));
@@ -136,6 +146,14 @@ __device__ __forceinline__ float wave_max(float x) {
         x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
     }
     return x;
+}
+
+// Exponent e with amax < 2^e (amax >= 0 finite; 0 for amax == 0), clamped to
+// [-60, 60] so that scales 2^(13 - e) stay normal floats.
+__device__ __forceinline__ int pow2_above(float amax) {
+    int e = 0;
+    if (amax > 0.f) frexpf(amax, &e);  // amax = f 2^e, f in [0.5, 1)
+    return min(max(e, -60), 60);
 }
 
 // Workgroups are dispatched to the 8 XCDs round-robin (id % 8).  Remap so that

@@ -23,8 +23,14 @@
 //             G = V_R dY_C^T
 //   bwd_q   : R = queries, C = keys;    W2 = (tau/2) G .* P   -> dQ (Y_C = K),
 //             G = dY_R V_C^T
-// Scaling for the fp16 pairs: unit rows by 2^8 and the other rows by 2^4, so that
-// lo parts stay normal; the scales are divided out in fp32.
+// Scaling for the fp16 pairs, so that hi and lo stay normal fp16 numbers whatever
+// the data's magnitude (all scales powers of two, divided out in fp32):
+//   cosine rows: normalised, times 2^8;
+//   fixed G rows (V in bwd_kv, dY in bwd_q): each row by 2^(13 - e), max|row| < 2^e;
+//   streamed data rows (G rows, summed rows): each 64-row tile by 2^(13 - e), e from
+//   the tile's largest |value|; the accumulators are rescaled (exactly, by a power
+//   of two) whenever a tile's scale differs from the previous one;
+//   weights: P by 2^15 and (tau/2) G P by 2^-k_tau, both then below 2^15.
 #include "common.h"
 #include "launch.h"
 #include "timing.h"
@@ -36,7 +42,8 @@ namespace {
 constexpr int kExpThreads = 256;
 constexpr int kExpRows = 64;   // fixed rows per workgroup (16 per wave)
 constexpr int kExpTile = 64;   // streamed rows per LDS tile
-constexpr float kUnitScale = 256.0f, kDataScale = 16.0f;
+constexpr float kUnitScale = 256.0f;  // cosine rows: unit length times 2^8
+constexpr float kPScale = 32768.0f;   // P weights: P 2^15 <= 2^15
 
 enum : int { kExpFwd = 0, kExpBwdKV = 1, kExpBwdQ = 2 };
 
@@ -83,6 +90,7 @@ __global__ __launch_bounds__(kExpThreads, 2) void expect_kernel(ExpArgs a) {
     __shared__ __align__(16) unsigned char xc_lds[kExpTile * 256];
     __shared__ __align__(16) unsigned char bc_lds[kG ? kExpTile * 256 : 16];
     __shared__ __align__(16) unsigned char yc_lds[kExpTile * 256];
+    __shared__ float tmax[8];  // the waves' largest |value| of the staged G rows and summed rows
 
     const int64_t tiles_r = (a.n_r + kExpRows - 1) / kExpRows;
     const int64_t blk = xcd_remap(blockIdx.x, a.bh * tiles_r);
@@ -97,6 +105,7 @@ __global__ __launch_bounds__(kExpThreads, 2) void expect_kernel(ExpArgs a) {
     const int rrow = r0 + wave * 16 + c;
     const int rcl = min(rrow, a.n_r - 1);  // rows past the end read the last row, never stored
     half8 xrh[2], xrl[2], arh[2], arl[2];
+    int ea = 0;  // the lane's G row is scaled by 2^(13 - ea)
     {
         float x[2][8];
         const int64_t off = (b * a.n_r + rcl) * D;
@@ -117,8 +126,16 @@ __global__ __launch_bounds__(kExpThreads, 2) void expect_kernel(ExpArgs a) {
             float y[2][8];
             load8<BF16>(a.ar, off + 8 * g, y[0]);
             load8<BF16>(a.ar, off + 32 + 8 * g, y[1]);
+            float mx = 0.f;
 #pragma unroll
-            for (int kb = 0; kb < 2; kb++) split8(y[kb], kDataScale, arh[kb], arl[kb]);
+            for (int kb = 0; kb < 2; kb++)
+#pragma unroll
+                for (int i = 0; i < 8; i++) mx = fmaxf(mx, fabsf(y[kb][i]));
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            ea = pow2_above(mx);
+#pragma unroll
+            for (int kb = 0; kb < 2; kb++) split8(y[kb], ldexpf(1.0f, 13 - ea), arh[kb], arl[kb]);
         }
     }
 
@@ -134,22 +151,22 @@ __global__ __launch_bounds__(kExpThreads, 2) void expect_kernel(ExpArgs a) {
     // chunk, which the swizzle puts on distinct banks (with 4 rows x 4 chunks per
     // quarter-wave, rows 0-3 would land on one set of 4 chunks)
     const int lrow = 16 * wave + (lane & 15), lq = lane >> 4;
-    auto stage = [&](unsigned char *dst, const void *src, int c0, bool unit) {
+    // this lane's 16 values of streamed row c0 + lrow (0 past the end) and their max |.|
+    auto load_row = [&](const void *src, int c0, float x[16]) {
         const int row = c0 + lrow;
-        float x[16];
         const int64_t off = (b * a.n_c + min(row, a.n_c - 1)) * D + 16 * lq;
         load8<BF16>(src, off, x);
         load8<BF16>(src, off + 8, x + 8);
-        float scale = kDataScale;
-        if (unit) {
-            float ss = 0.f;
+        const bool ok = row < a.n_c;
+        float mx = 0.f;
 #pragma unroll
-            for (int i = 0; i < 16; i++) ss += x[i] * x[i];
-            ss += __shfl_xor(ss, 16);  // the row's four threads are lanes l, l^16, l^32, l^48
-            ss += __shfl_xor(ss, 32);
-            scale = ss > 0.f ? kUnitScale / sqrtf(ss) : 0.f;
+        for (int i = 0; i < 16; i++) {
+            x[i] = ok ? x[i] : 0.f;
+            mx = fmaxf(mx, fabsf(x[i]));
         }
-        if (row >= a.n_c) scale = 0.f;  // rows past the end are zero (and weighted 0)
+        return mx;
+    };
+    auto put_row = [&](unsigned char *dst, const float x[16], float scale) {
         half8 h[2], l[2];
         split8(x, scale, h[0], l[0]);
         split8(x + 8, scale, h[1], l[1]);
@@ -158,6 +175,17 @@ __global__ __launch_bounds__(kExpThreads, 2) void expect_kernel(ExpArgs a) {
             *reinterpret_cast<half8 *>(dst + xswz(lrow, 2 * lq + u)) = h[u];
             *reinterpret_cast<half8 *>(dst + xswz(lrow, 8 + 2 * lq + u)) = l[u];
         }
+    };
+    // cosine rows, normalised (the row's four threads are lanes l, l^16, l^32, l^48)
+    auto stage_unit = [&](unsigned char *dst, const void *src, int c0) {
+        float x[16];
+        load_row(src, c0, x);
+        float ss = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; i++) ss += x[i] * x[i];
+        ss += __shfl_xor(ss, 16);
+        ss += __shfl_xor(ss, 32);
+        put_row(dst, x, ss > 0.f ? kUnitScale / sqrtf(ss) : 0.f);
     };
     // A-operand rows of sub-block cb (lane (g, c): row 16cb + c, dims kb*32 + 8g + [0, 8))
     auto read_rows = [&](const unsigned char *t, int cb, half8 h[2], half8 l[2]) {
@@ -196,11 +224,44 @@ __global__ __launch_bounds__(kExpThreads, 2) void expect_kernel(ExpArgs a) {
         for (int dt = 0; dt < 4; dt++) out[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(yl[dt], wh, out[dt], 0, 0, 0);
     };
 
+    // tile exponents of the streamed data rows (G rows bc, summed rows yc) of the
+    // tile whose products the accumulators hold
+    int eb = 0, ey = 0;
+    // (tau/2) G P is scaled by 2^-ktau: |G| < 2^32 after the row and tile scalings
+    // (both sides' norms below 2^16), so the weight stays below 2^15
+    int ktau = 0;
+    while ((1 << ktau) < a.tau) ktau++;  // 2^ktau >= tau, i.e. 2^(ktau-1) >= tau/2
+    const float wg = half_tau * ldexpf(1.0f, -(17 + ktau - 1));
     for (int c0 = 0; c0 < a.n_c; c0 += kExpTile) {
-        __syncthreads();  // the previous tile has been read
-        stage(xc_lds, a.xc, c0, true);
-        if constexpr (kG) stage(bc_lds, a.bc, c0, false);
-        stage(yc_lds, a.yc, c0, false);
+        __syncthreads();  // the previous tile has been read, and its maxima
+        stage_unit(xc_lds, a.xc, c0);
+        float xb[16], xy[16];
+        float mb = 0.f;
+        if constexpr (kG) mb = load_row(a.bc, c0, xb);
+        float my = load_row(a.yc, c0, xy);
+        mb = wave_max(mb);
+        my = wave_max(my);
+        if (lane == 0) {
+            tmax[wave] = mb;
+            tmax[4 + wave] = my;
+        }
+        __syncthreads();
+        const int eb_new = pow2_above(fmaxf(fmaxf(tmax[0], tmax[1]), fmaxf(tmax[2], tmax[3])));
+        const int ey_new = pow2_above(fmaxf(fmaxf(tmax[4], tmax[5]), fmaxf(tmax[6], tmax[7])));
+        if constexpr (kG) put_row(bc_lds, xb, ldexpf(1.0f, 13 - eb_new));
+        put_row(yc_lds, xy, ldexpf(1.0f, 13 - ey_new));
+        // bring the sums so far to this tile's scales (exact power-of-two factors)
+        if (c0 > 0) {
+            const int e1o = MODE == kExpFwd ? ey : eb, e1n = MODE == kExpFwd ? ey_new : eb_new;
+            const float f1 = ldexpf(1.0f, e1o - e1n), f2 = ldexpf(1.0f, eb + ey - eb_new - ey_new);
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) {
+                if constexpr (kP) out1[dt] *= f1;
+                if constexpr (kG) out2[dt] *= f2;
+            }
+        }
+        eb = eb_new;
+        ey = ey_new;
         __syncthreads();
 #pragma unroll 1
         for (int cb = 0; cb < kExpTile / 16; cb++) {
@@ -216,10 +277,10 @@ __global__ __launch_bounds__(kExpThreads, 2) void expect_kernel(ExpArgs a) {
                 p[i] = ok ? collision_p(st[i] * (1.0f / (kUnitScale * kUnitScale)), a.tau) : 0.f;
             }
             if constexpr (kP) {
-                // P, scaled 2^8, against the P-summed rows (V forward, dY in bwd_kv)
+                // P 2^15 against the P-summed rows (V forward, dY in bwd_kv)
                 float w[4];
 #pragma unroll
-                for (int i = 0; i < 4; i++) w[i] = p[i] * kUnitScale;
+                for (int i = 0; i < 4; i++) w[i] = p[i] * kPScale;
                 half4 yh[4], yl[4];
                 read_rows_t(MODE == kExpFwd ? yc_lds : bc_lds, cb, yh, yl);
                 accum(out1, yh, yl, w);
@@ -227,11 +288,12 @@ __global__ __launch_bounds__(kExpThreads, 2) void expect_kernel(ExpArgs a) {
             if constexpr (kG) {
                 half8 bh[2], bl[2];
                 read_rows(bc_lds, cb, bh, bl);
-                // G^T block: lane (g, c) = (b_C row 16cb + 4g + i) . (a_R row c), scaled 2^8
+                // G^T block: lane (g, c) = (b_C row 16cb + 4g + i) . (a_R row c), scaled
+                // 2^(13 - eb) 2^(13 - ea)
                 const floatx4 gt = sdot(bh, bl, arh, arl);
                 float w[4];
 #pragma unroll
-                for (int i = 0; i < 4; i++) w[i] = half_tau * gt[i] * (1.0f / (kDataScale * kDataScale)) * p[i];
+                for (int i = 0; i < 4; i++) w[i] = gt[i] * p[i] * wg;
                 half4 yh[4], yl[4];
                 read_rows_t(yc_lds, cb, yh, yl);
                 accum(out2, yh, yl, w);
@@ -258,8 +320,11 @@ __global__ __launch_bounds__(kExpThreads, 2) void expect_kernel(ExpArgs a) {
                 }
             }
         };
-        if constexpr (kP) put(a.out1, out1, 1.0f / (kUnitScale * kDataScale));
-        if constexpr (kG) put(a.out2, out2, 1.0f / kDataScale);
+        // out1 = P 2^15 x (summed rows 2^(13 - e1)); out2 = (tau/2) G P 2^-ktau' x
+        // (G rows 2^(13 - eb)) (fixed G row 2^(13 - ea)) x (summed rows 2^(13 - ey))
+        const int e1 = MODE == kExpFwd ? ey : eb;
+        if constexpr (kP) put(a.out1, out1, ldexpf(1.0f / kPScale, e1 - 13));
+        if constexpr (kG) put(a.out2, out2, ldexpf(1.0f, (17 + ktau - 1) + eb - 13 + ea - 13 + ey - 13));
     }
 }
 

@@ -20,6 +20,11 @@
 //                  as packed entries (code << 16 | row): a stable counting sort in
 //                  LDS (rows of a bucket in increasing index), so the order in which
 //                  the pair passes accumulate, and hence every result, is reproducible.
+//   absmax_kernel  partial maxima of |Q|, |dY|, |K|, |V| per head, from which every
+//                  consumer derives the same power-of-two scale per (head, tensor).
+//   split_kernel   Q, K, V, dY -> fp16 (hi, lo) rows, each head's tensor scaled by
+//                  2^(13 - e) with max|x| < 2^e, so that hi and lo stay normal fp16
+//                  numbers whatever the data's magnitude.
 //   pass_kernel    one workgroup per (head, hash, side).  Each wave walks 16-row
 //                  tiles of sorted rows; the partners that can collide with a tile
 //                  form one contiguous range of sorted partners, visited 16 at a
@@ -28,15 +33,18 @@
 //                  sub-tile are fetched while the current one computes; B_y is
 //                  transposed through a per-wave LDS tile.  The finished tile is the
 //                  hash's share of out for those rows; it is stored, not added, into a
-//                  partial buffer [bh][n][m][64] (each row of each hash is written
-//                  exactly once, so no atomics are needed).  Partials are fp32, or
-//                  bf16 when the outputs are bf16.
+//                  partial buffer (each row of each hash is written exactly once, so no
+//                  atomics are needed) as a 24-bit fixed-point row: one power-of-two
+//                  exponent per row, 16 high bits and 8 low bits per value.
 //   reduce_kernel  out[b][x] = sum over the m hashes of the partial rows, in hash
 //                  order (deterministic), written as fp32 or bf16.
 // gfx950's global fp32 atomics sustain roughly 1.3 TB/s of payload, so a plain
 // store of every partial plus one coalesced reduction beats accumulating with
-// atomics.  Every fp32 product uses three fp16 MFMAs (hi*hi + hi*lo + lo*hi);
-// the b vectors are scaled by 2^8 before splitting (undone on the way out).
+// atomics.  Every fp32 product uses three fp16 MFMAs (hi*hi + hi*lo + lo*hi).
+// Before S is split for the second product it is scaled per row by 2^-(2 + e_x),
+// ||a_x|| < 2^e_x, which keeps |S| below 2^14 (||a'_y|| < 2^16 after the head
+// scaling) and keeps a small row's S as precise as a large one's; the row's
+// factor is undone when its partial row is stored.
 #include "common.h"
 #include "launch.h"
 #include "timing.h"
@@ -68,6 +76,8 @@ constexpr int kTileBytes = 16 * 512;   // LDS bytes of one wave's operand tile
 constexpr int kPlanTiles = 256;        // row tiles planned per run (multiple of kPassThreads)
 constexpr int kExpLds = 16384;         // rows whose exponents a pass block stages in LDS
 constexpr int kEntPad = 16;            // at least this many sentinel entries after each unit's sorted entries
+constexpr int kMaxParts = 8;           // partial maxima per (head, tensor)
+constexpr int kMantBytes = 16 * 128;   // LDS bytes of a finished tile's 16-bit mantissas (the low bytes follow)
 
 // Entries per unit: n rounded up to a multiple of 4 (16-byte aligned units), then
 // at least kEntPad sentinels.
@@ -222,6 +232,56 @@ __global__ __launch_bounds__(NT) void sort_kernel(const uint16_t *__restrict__ q
     }
 }
 
+// ---------------------------------------------------------------- per-head scales
+// Tensor t of head b: 0 = Q, 1 = dY (n_q rows), 2 = K, 3 = V (n_k rows).
+// Block (b*4 + t)*kMaxParts + p takes the p-th of kMaxParts contiguous row ranges
+// and writes max |x| over it; pmax[(b*4 + t)*kMaxParts + p].
+template <bool BF16>
+__global__ __launch_bounds__(256) void absmax_kernel(const void *__restrict__ q, const void *__restrict__ dy,
+                                                     const void *__restrict__ k, const void *__restrict__ v,
+                                                     int64_t n_q, int64_t n_k, float *__restrict__ pmax) {
+    __shared__ float wred[4];
+    const int64_t blk = blockIdx.x;
+    const int p = static_cast<int>(blk % kMaxParts);
+    const int64_t bt = blk / kMaxParts;
+    const int t = static_cast<int>(bt & 3);
+    const int64_t b = bt >> 2;
+    const void *src = t == 0 ? q : t == 1 ? dy : t == 2 ? k : v;
+    const int64_t n = t < 2 ? n_q : n_k;
+    const int64_t per = (n + kMaxParts - 1) / kMaxParts;
+    const int64_t r0 = min(n, p * per), r1 = min(n, r0 + per);
+    const int64_t base = (b * n + r0) * D, count = (r1 - r0) * D;
+    float mx = 0.f;
+    constexpr int U = 4;  // loads in flight per thread
+    for (int64_t e0 = static_cast<int64_t>(threadIdx.x) * 8; e0 < count; e0 += 256 * 8 * U) {
+        float x[U][8];
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int64_t e = e0 + u * 256 * 8;
+            load8<BF16>(src, base + (e < count ? e : 0), x[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            if (e0 + u * 256 * 8 < count) {
+#pragma unroll
+                for (int i = 0; i < 8; i++) mx = fmaxf(mx, fabsf(x[u][i]));
+            }
+        }
+    }
+    mx = wave_max(mx);
+    if ((threadIdx.x & 63) == 0) wred[threadIdx.x >> 6] = mx;
+    __syncthreads();
+    if (threadIdx.x == 0) pmax[blk] = fmaxf(fmaxf(wred[0], wred[1]), fmaxf(wred[2], wred[3]));
+}
+
+// e with max |x| < 2^e over tensor t of head b (the tensor is scaled by 2^(13 - e)).
+__device__ __forceinline__ int head_exp(const float *pmax, int64_t b, int t) {
+    const float4 *p = reinterpret_cast<const float4 *>(pmax + (b * 4 + t) * kMaxParts);
+    const float4 x = p[0], y = p[1];
+    const float m = fmaxf(fmaxf(fmaxf(x.x, x.y), fmaxf(x.z, x.w)), fmaxf(fmaxf(y.x, y.y), fmaxf(y.z, y.w)));
+    return pow2_above(m);
+}
+
 // ---------------------------------------------------------------- pair passes
 struct Side {
     const uint32_t *ent;  // [units][ent_stride(n)]: (code << 16 | row) in bucket order, then sentinels
@@ -232,9 +292,11 @@ struct Side {
 struct PassArgs {
     Side q, k;
     // Q, K, V, dY split into fp16 (hi, lo) pairs by split_kernel: row r holds 64 hi
-    // halves then 64 lo halves; Q and K are scaled by 2^8 first
+    // halves then 64 lo halves, each head's tensor scaled by its power of two
     const _Float16 *qs, *ks, *vs, *dys;
-    int16_t *pq, *pk;                // partials [bh][n][m][64] int16 mantissas
+    const float *pmax;               // per-head partial maxima (absmax_kernel)
+    int16_t *pq, *pk;                // partials [bh][n][m][64]: high 16 bits of the 24-bit mantissas
+    uint8_t *lq, *lk;                // [bh][n][m][64]: their low 8 bits
     int8_t *eq, *ek;                 // their exponents [bh][m][n] (one block writes one n-byte run)
     int64_t bh;
     int m, tau;
@@ -304,9 +366,11 @@ __device__ __forceinline__ void load_row_tile(uint4 r[4], const uint4 &re4, cons
 }
 
 // Rows through the tile into the MFMA B-operand layout of S^T: lane (g, c) gets
-// row c, dims kb*32 + 8g + [0, 8) (hi and lo).
-__device__ __forceinline__ void stage_rows(const uint4 r[4], unsigned char *tile, int q, int cl, int g, int c,
-                                           half8 rh[2], half8 rl[2]) {
+// row c, dims kb*32 + 8g + [0, 8) (hi and lo).  Returns e_c with ||a_c|| < 2^e_c
+// for the lane's row c (from the fp16 pairs the products use; the row's other
+// three quarters sit in the lanes 16, 32 and 48 away).
+__device__ __forceinline__ int stage_rows(const uint4 r[4], unsigned char *tile, int q, int cl, int g, int c,
+                                          half8 rh[2], half8 rl[2]) {
 #pragma unroll
     for (int i = 0; i < 4; i++) lds_st(tile, swz(4 * q + i, cl, 256), r[i]);
 #pragma unroll
@@ -314,6 +378,27 @@ __device__ __forceinline__ void stage_rows(const uint4 r[4], unsigned char *tile
         rh[kb] = lds_ld<half8>(tile, swz(c, kb * 4 + g, 256));
         rl[kb] = lds_ld<half8>(tile, swz(c, 8 + kb * 4 + g, 256));
     }
+    float ss = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; kb++)
+#pragma unroll
+        for (int i = 0; i < 8; i++) {
+            const float x = static_cast<float>(rh[kb][i]) + static_cast<float>(rl[kb][i]);
+            ss = fmaf(x, x, ss);
+        }
+    {
+        const auto t = __builtin_amdgcn_permlane16_swap(__float_as_uint(ss), __float_as_uint(ss), false, false);
+        ss = __uint_as_float(t[0]) + __uint_as_float(t[1]);
+    }
+    {
+        const auto t = __builtin_amdgcn_permlane32_swap(__float_as_uint(ss), __float_as_uint(ss), false, false);
+        ss = __uint_as_float(t[0]) + __uint_as_float(t[1]);
+    }
+    // ss < 2^e2  ->  ||a|| < 2^ceil(e2 / 2); the sum's rounding (far below one part in
+    // 2^20) is covered by the factor 4 of slack in the 2^14 bound of S
+    int e2 = 0;
+    if (ss > 0.f) frexpf(ss, &e2);
+    return (e2 + 1) >> 1;
 }
 
 __device__ __forceinline__ half4 tr_load(const unsigned char *p) {
@@ -336,7 +421,7 @@ __device__ __forceinline__ void publish_sub(const Sub &s, unsigned char *tile, i
 // code equality.  `pe` as in load_sub: in the MFMA layout it holds the entries of
 // exactly the partners 4g+i whose S^T values this lane computes.
 __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uint4 &pe, const half8 rh[2],
-                                            const half8 rl[2], int rcode, int g, int c, floatx4 outT[4]) {
+                                            const half8 rl[2], int rcode, float sfac, int g, int c, floatx4 outT[4]) {
     // A'_y in the A-operand layout: lane (g, c) = partner c, dims kb*32 + 8g + [0, 8)
     half8 ah[2], al[2];
 #pragma unroll
@@ -370,8 +455,9 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uin
     float sv[4];
 #pragma unroll
     for (int i = 0; i < 4; i++) sv[i] = static_cast<int>(e[i] >> 16) == rcode ? st[i] : 0.f;
+    // the row's factor 2^-(2 + e_c): |S| < 2^14 (see the header), hi and lo stay normal
     half4 sh, sl;
-    split4(sv, 1.0f, sh, sl);
+    split4(sv, sfac, sh, sl);
     // out^T += B_y^T S^T (hi*hi + hi*lo + lo*hi), the four dim blocks interleaved
 #pragma unroll
     for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(bth[dt], sh, outT[dt], 0, 0, 0);
@@ -391,22 +477,32 @@ __device__ __forceinline__ int mant_slot(int r) { return r ^ ((r >> 2) & 1); }
 __device__ __forceinline__ uint32_t mant_off(int s, int ch) {
     return static_cast<uint32_t>(s * 128 + (((ch >> 1) ^ (s >> 1)) << 4) + ((ch & 1) << 3));
 }
+// Byte offset of dword w (low bytes of dims 4w .. 4w+3) of row r's 64 low bytes,
+// after the mantissas: the dword's group of four (w >> 2) is XORed with (r >> 2) & 3.
+// MFMA-layout writes (rows c, dwords 4dt + g) and row-major reads (row 4i + q,
+// dword cl) then both fall on 64 distinct banks.
+__device__ __forceinline__ uint32_t low_off(int r, int w) {
+    return static_cast<uint32_t>(kMantBytes + r * 64 + ((((w >> 2) ^ (r >> 2)) & 3) << 4) + ((w & 3) << 2));
+}
 
 // Write the partial rows of a finished tile: lane (g, c) holds out[row c][16dt +
-// 4g + (0..3)] / oscale.  A partial row is stored in block floating point: 64
-// int16 mantissas and one exponent e with max|value| < 2^e, value = mantissa *
-// 2^e / 32767 (rounding error at most 2^e / 65534, i.e. about 2^-15 of the row's
-// largest value).  The row maximum and the mantissas are computed where the MFMA
-// leaves the values (16 per lane, the rest of the row in the lanes 16, 32 and 48
-// away: two permlane swaps); the mantissas then go through the tile so that each
-// quarter-wave stores one whole partial row.  The stores are non-temporal: the
-// partials are read once, by the reduction, and should not evict the operands from
-// L2.  Exponents go to the block's LDS copy of its exponent row when it fits
+// 4g + (0..3)] / orow, orow being the lane's row factor.  A partial row is stored
+// as 24-bit fixed point: one exponent e with max|value| < 2^e, and per value the
+// integer M = round(value * 2^(23 - e)), |M| < 2^23, kept as its high 16 bits
+// (M >> 8, int16) and its low 8 bits (M & 255); value = M 2^(e - 23) (rounding
+// error at most 2^(e - 24), i.e. below 2^-23 of the row's largest value).  The row
+// maximum and M are computed where the MFMA leaves the values (16 per lane, the
+// rest of the row in the lanes 16, 32 and 48 away: two permlane swaps); both parts
+// then go through the tile so that each quarter-wave stores one whole 128-byte
+// high-part row and one whole 64-byte low-part row.  The stores are non-temporal:
+// the partials are read once, by the reduction, and should not evict the operands
+// from L2.  Exponents go to the block's LDS copy of its exponent row when it fits
 // (written out whole at the end: single-byte stores scattered over the row would
 // each cost a partial-line write), else straight to memory.
-__device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, int8_t *pexp, int8_t *ex_lds,
-                                           bool ex_in_lds, int m, const uint4 &re4, uint32_t rent_c, int nvalid,
-                                           int q, int cl, int g, int c, const floatx4 outT[4], float oscale) {
+__device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, uint8_t *plow, int8_t *pexp,
+                                           int8_t *ex_lds, bool ex_in_lds, int m, const uint32_t *tile_ent,
+                                           int nvalid, int q, int cl, int g, int c, const floatx4 outT[4],
+                                           float orow) {
     // max |value| of row c over this lane's 16 values, then over the row's 4 lanes
     float mx4[4];
 #pragma unroll
@@ -422,15 +518,16 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, i
         mx = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
     }
     // e with max|value| < 2^e, from the biased exponent field of the scaled row
-    // maximum (0 gives a tiny e whose mantissas are all 0), clamped so that 2^-e
-    // stays a normal float
-    const float mxs = mx * oscale;
+    // maximum (0 gives a tiny e whose mantissas are all 0), clamped so that
+    // 2^(23 - e) stays a normal float
+    const float mxs = mx * orow;
     const int e = min(max(static_cast<int>((__float_as_uint(mxs) >> 23) & 0xFFu) - 126, -100), 100);
-    // value * 2^-e lies in (-1, 1); the snorm conversion rounds it to a multiple
-    // of 1/32767 (mantissa = round(value * 2^-e * 32767))
-    const float sc = __uint_as_float(static_cast<uint32_t>(127 - e) << 23) * oscale;
+    // value * 2^(23 - e) lies in (-2^23, 2^23): a power-of-two scaling of the
+    // rounded product value * orow, so the row maximum stays below 2^23 before
+    // rounding (and at most 2^23 after, hence the clamp)
+    const float sc = mx > 0.f ? __uint_as_float(static_cast<uint32_t>(127 + 23 - e) << 23) * orow : 0.f;
     if (g == 0 && c < nvalid) {
-        const uint32_t row = rent_c & 0xFFFFu;
+        const uint32_t row = tile_ent[c] & 0xFFFFu;
         if (ex_in_lds) ex_lds[row] = static_cast<int8_t>(e);
         else pexp[row] = static_cast<int8_t>(e);
     }
@@ -438,21 +535,39 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, i
     const int sw = mant_slot(c);
 #pragma unroll
     for (int dt = 0; dt < 4; dt++) {
+        int mm[4];
+#pragma unroll
+        for (int j = 0; j < 4; j++) mm[j] = min(max(__float2int_rn(outT[dt][j] * sc), -0x7FFFFF), 0x7FFFFF);
         uint2v w;
-        w.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pknorm_i16(outT[dt][0] * sc, outT[dt][1] * sc));
-        w.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pknorm_i16(outT[dt][2] * sc, outT[dt][3] * sc));
+        w.x = (static_cast<uint32_t>(mm[0] >> 8) & 0xFFFFu) | (static_cast<uint32_t>(mm[1] >> 8) << 16);
+        w.y = (static_cast<uint32_t>(mm[2] >> 8) & 0xFFFFu) | (static_cast<uint32_t>(mm[3] >> 8) << 16);
         lds_st(tile, mant_off(sw, 4 * dt + g), w);
+        const uint32_t lo = (static_cast<uint32_t>(mm[0]) & 0xFFu) | ((static_cast<uint32_t>(mm[1]) & 0xFFu) << 8) |
+                            ((static_cast<uint32_t>(mm[2]) & 0xFFu) << 16) | (static_cast<uint32_t>(mm[3]) << 24);
+        lds_st(tile, low_off(c, 4 * dt + g), lo);
     }
-    const uint32_t e4[4] = {re4.x, re4.y, re4.z, re4.w};
-    // rows 4q + i: this lane's chunk cl of each, then the four stores
+    // rows 4q + i: this lane's chunk cl of each high-part row, then the four stores
     uint2v w[4];
+    uint32_t lw[4];
 #pragma unroll
     for (int i = 0; i < 4; i++) w[i] = lds_ld<uint2v>(tile, mant_off(mant_slot(4 * q + i), cl));
+    // rows 4i + q: dword cl of each low-part row
+#pragma unroll
+    for (int i = 0; i < 4; i++) lw[i] = lds_ld<uint32_t>(tile, low_off(4 * i + q, cl));
+    const uint4 e4 = reinterpret_cast<const uint4 *>(tile_ent)[q];
+    const uint32_t re[4] = {e4.x, e4.y, e4.z, e4.w};
 #pragma unroll
     for (int i = 0; i < 4; i++) {
         if (4 * q + i < nvalid) {
-            const uint32_t row = e4[i] & 0xFFFFu;
+            const uint32_t row = re[i] & 0xFFFFu;
             __builtin_nontemporal_store(w[i], reinterpret_cast<uint2v *>(part + (row * static_cast<uint32_t>(m)) * D) + cl);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        if (4 * i + q < nvalid) {
+            const uint32_t row = tile_ent[4 * i + q] & 0xFFFFu;
+            __builtin_nontemporal_store(lw[i], reinterpret_cast<uint32_t *>(plow + (row * static_cast<uint32_t>(m)) * D) + cl);
         }
     }
 }
@@ -485,9 +600,10 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
     const _Float16 *arow = (kside ? a.vs : a.dys) + b * n_r * (2 * D);
     const _Float16 *apar = (kside ? a.dys : a.vs) + b * n_p * (2 * D);
     const _Float16 *bpar = (kside ? a.qs : a.ks) + b * n_p * (2 * D);
-    // partial row (row r, hash h) starts r*m*64 elements past this base, its
+    // partial row (row r, hash h) starts r*m*64 elements past these bases, its
     // exponent r bytes past the other
     int16_t *part = (kside ? a.pk : a.pq) + ((b * n_r) * a.m + h) * D;
+    uint8_t *plow = (kside ? a.lk : a.lq) + ((b * n_r) * a.m + h) * D;
     int8_t *pexp = (kside ? a.ek : a.eq) + (b * a.m + h) * n_r;
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -496,7 +612,13 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
     const int q = lane >> 4, cl = lane & 15; // coalesced layout: quarter q, 16-byte chunk cl
     unsigned char *tile = tiles_lds + wave * kTileBytes;
     const int tiles = (n_r + 15) >> 4;
-    const float oscale = a.scale * (1.0f / 256.0f);
+    // the operands carry the head scales 2^(13 - e) of a (rows), a' (partners) and
+    // b (partners), and S the row factor 2^-(2 + e_c): out = s * outT * 2^(e_a +
+    // e_a' + e_b - 39) * 2^(2 + e_c)
+    // (tensors: 0 Q, 1 dY, 2 K, 3 V; dQ: a = dY, a' = V, b = K; dK: a = V, a' = dY, b = Q)
+    const int esum = head_exp(a.pmax, b, kside ? 3 : 1) + head_exp(a.pmax, b, kside ? 1 : 3) +
+                     head_exp(a.pmax, b, kside ? 0 : 2);
+    const float oscale = ldexpf(a.scale, esum - 39 + 2);
     const bool ex_in_lds = n_r <= kExpLds;
 
     for (int T0 = 0; T0 < tiles; T0 += kPlanTiles) {
@@ -562,12 +684,13 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
 
         auto row_entry = [&](int t) { return row_ent[t * 16 + c]; };
         auto row_entries4 = [&](int t) { return reinterpret_cast<const uint4 *>(row_ent)[t * 4 + q]; };
+        auto tile_ents = [&](int t) { return static_cast<const uint32_t *>(row_ent + t * 16); };
         auto row_count = [&](int t) { return min(16, n_r - (T0 + t) * 16); };
         // tiles with no partner at all still own partial rows: they are zero
         auto zero_tiles = [&](int ta, int tb) {
             const floatx4 z[4] = {};
             for (int t = ta; t < tb; t++)
-                store_tile(tile, part, pexp, ex_lds, ex_in_lds, a.m, row_entries4(t), row_entry(t), row_count(t), q, cl, g, c, z, 0.f);
+                store_tile(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, tile_ents(t), row_count(t), q, cl, g, c, z, 0.f);
         };
         // sub-tile j of the run: its tile (searched forward from t) and first partner
         auto tile_of = [&](int j, int t) {
@@ -614,7 +737,7 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
                 cursor_at(t1);
             }
             half8 rh[2], rl[2];
-            stage_rows(A.rw, tile, q, cl, g, c, rh, rl);
+            int erow = stage_rows(A.rw, tile, q, cl, g, c, rh, rl);  // ||a_c|| < 2^erow
             // one operand buffer: a sub-tile's registers are reloaded with the next
             // sub-tile as soon as they have been written to the tile
             Sub S;
@@ -636,13 +759,15 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
                 fill(nn, t2, y2, has2 && t2 != nxt.t);
                 const bool newtile = !has1 || nxt.t != cur.t;
                 if (has1) load_sub(S, nxt.pe, apar, bpar, cl);
-                compute_sub(tile, cur.pe, rh, rl, static_cast<int>(row_entry(cur.t) >> 16), g, c, outT);
+                compute_sub(tile, cur.pe, rh, rl, static_cast<int>(row_entry(cur.t) >> 16), ldexpf(1.0f, -2 - erow), g,
+                            c, outT);
                 if (newtile) {
-                    store_tile(tile, part, pexp, ex_lds, ex_in_lds, a.m, row_entries4(cur.t), row_entry(cur.t), row_count(cur.t), q, cl, g, c, outT, oscale);
+                    store_tile(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, tile_ents(cur.t), row_count(cur.t), q, cl,
+                               g, c, outT, ldexpf(oscale, erow));
 #pragma unroll
                     for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
                     zero_tiles(cur.t + 1, has1 ? nxt.t : thi);
-                    if (has1) stage_rows(nxt.rw, tile, q, cl, g, c, rh, rl);
+                    if (has1) erow = stage_rows(nxt.rw, tile, q, cl, g, c, rh, rl);
                 }
                 return has1;
             };
@@ -665,20 +790,24 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
     }
 }
 
-// Q, K, V, dY -> fp16 (hi, lo) rows [hi 64 | lo 64] for the pair passes; Q and K
-// (the vectors that multiply S) are scaled by 2^8 so that their lo parts stay
-// normal fp16 numbers.  One thread per 8 values.
+// Q, K, V, dY -> fp16 (hi, lo) rows [hi 64 | lo 64] for the pair passes, each
+// head's tensor scaled by 2^(13 - e) (max |x| < 2^e over that tensor of that head),
+// so that the largest value lands in [2^12, 2^13) and hi, lo stay normal fp16
+// numbers for every value within about 2^-20 of it.  One thread per 8 values.
 template <bool BF16>
 __global__ __launch_bounds__(256) void split_kernel(const void *__restrict__ q, const void *__restrict__ k,
                                                     const void *__restrict__ v, const void *__restrict__ dy,
                                                     _Float16 *__restrict__ qs, _Float16 *__restrict__ ks,
                                                     _Float16 *__restrict__ vs, _Float16 *__restrict__ dys,
-                                                    int64_t rows_q, int64_t rows_k) {
+                                                    const float *__restrict__ pmax, int64_t bh, int64_t n_q,
+                                                    int64_t n_k) {
+    const int64_t rows_q = bh * n_q, rows_k = bh * n_k;
     const int64_t per_q = rows_q * (D / 8), per_k = rows_k * (D / 8);
     const int64_t total = 2 * (per_q + per_k);
     for (int64_t tid = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; tid < total;
          tid += static_cast<int64_t>(gridDim.x) * 256) {
-        // which: 0 = Q, 1 = dY (query side), 2 = K, 3 = V (key side)
+        // which: 0 = Q, 1 = dY (query side), 2 = K, 3 = V (key side), the tensor
+        // numbering of absmax_kernel
         int which;
         int64_t t;
         if (tid < per_q) { which = 0; t = tid; }
@@ -687,8 +816,9 @@ __global__ __launch_bounds__(256) void split_kernel(const void *__restrict__ q, 
         else { which = 3; t = tid - 2 * per_q - per_k; }
         const void *src = which == 0 ? q : which == 1 ? dy : which == 2 ? k : v;
         _Float16 *dst = which == 0 ? qs : which == 1 ? dys : which == 2 ? ks : vs;
-        const float scale = (which == 0 || which == 2) ? 256.0f : 1.0f;
         const int64_t row = t / (D / 8);
+        const int64_t head = row / (which < 2 ? n_q : n_k);
+        const float scale = ldexpf(1.0f, 13 - head_exp(pmax, head, which));
         const int o = static_cast<int>(t - row * (D / 8)) * 8;
         float x[8];
         load8<BF16>(src, row * D + o, x);
@@ -699,11 +829,13 @@ __global__ __launch_bounds__(256) void split_kernel(const void *__restrict__ q, 
     }
 }
 
-// out[r][:] = sum_h part[r][h][:] * 2^e[r][h] / 32767, in hash order; 8 lanes per
-// row, 8 values each.  The hashes go in groups of eight, each group's loads issued
-// before the previous group is added, so that a lane keeps up to 256 bytes in flight.
+// out[r][:] = sum_h M[r][h][:] * 2^(e[r][h] - 23), M = (high part) * 256 + (low byte),
+// in hash order; 8 lanes per row, 8 values each.  The hashes go in groups of
+// eight, each group's loads issued before the previous group is added, so that a
+// lane keeps up to 384 bytes in flight.
 template <bool BF16>
 __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *__restrict__ part,
+                                                                const uint8_t *__restrict__ plow,
                                                                 const int8_t *__restrict__ pexp,
                                                                 void *__restrict__ out, int64_t rows, int64_t n,
                                                                 int m) {
@@ -711,44 +843,52 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *_
     const int q = threadIdx.x & 7;
     if (r >= rows) return;
     typedef unsigned int uint4v __attribute__((ext_vector_type(4)));
+    typedef unsigned int uint2v __attribute__((ext_vector_type(2)));
     const uint4v *src = reinterpret_cast<const uint4v *>(part + r * m * D) + q;
+    const uint2v *srl = reinterpret_cast<const uint2v *>(plow + r * m * D) + q;
     const int64_t b = r / n;
     const int8_t *ex = pexp + b * m * n + (r - b * n);
     float s[8];
 #pragma unroll
     for (int i = 0; i < 8; i++) s[i] = 0.f;
-    auto add = [&](const uint4v &v, int e) {
-        const float sc = ldexpf(1.0f / 32767.0f, e);
+    auto add = [&](const uint4v &v, const uint2v &l, int e) {
+        const float sc = ldexpf(1.0f, e - 23);
         const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+        const uint32_t lb[2] = {l.x, l.y};
 #pragma unroll
-        for (int i = 0; i < 4; i++) {
-            s[2 * i] = fmaf(static_cast<float>(static_cast<int16_t>(w[i] & 0xFFFFu)), sc, s[2 * i]);
-            s[2 * i + 1] = fmaf(static_cast<float>(static_cast<int16_t>(w[i] >> 16)), sc, s[2 * i + 1]);
+        for (int i = 0; i < 8; i++) {
+            const int hi = static_cast<int16_t>((w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+            const int lo = static_cast<int>((lb[i >> 2] >> (8 * (i & 3))) & 0xFFu);
+            s[i] = fmaf(static_cast<float>(hi * 256 + lo), sc, s[i]);  // |M| < 2^23: exact in fp32
         }
     };
     // groups of eight hashes, double-buffered: group g+1 is loaded while g is added
     uint4v v[2][8];
+    uint2v l[2][8];
     int e[2][8];
-    auto load = [&](uint4v w[8], int f[8], int h0) {
+    auto load = [&](uint4v w[8], uint2v lw[8], int f[8], int h0) {
 #pragma unroll
         for (int u = 0; u < 8; u++) w[u] = __builtin_nontemporal_load(src + (h0 + u) * (D / 8));
+#pragma unroll
+        for (int u = 0; u < 8; u++) lw[u] = __builtin_nontemporal_load(srl + (h0 + u) * (D / 8));
 #pragma unroll
         for (int u = 0; u < 8; u++) f[u] = ex[(h0 + u) * n];
     };
     const int ng = m >> 3;
-    if (ng > 0) load(v[0], e[0], 0);
+    if (ng > 0) load(v[0], l[0], e[0], 0);
     for (int g = 0; g < ng; g += 2) {
-        if (g + 1 < ng) load(v[1], e[1], 8 * (g + 1));
+        if (g + 1 < ng) load(v[1], l[1], e[1], 8 * (g + 1));
 #pragma unroll
-        for (int u = 0; u < 8; u++) add(v[0][u], e[0][u]);
+        for (int u = 0; u < 8; u++) add(v[0][u], l[0][u], e[0][u]);
         if (g + 1 < ng) {
-            if (g + 2 < ng) load(v[0], e[0], 8 * (g + 2));
+            if (g + 2 < ng) load(v[0], l[0], e[0], 8 * (g + 2));
 #pragma unroll
-            for (int u = 0; u < 8; u++) add(v[1][u], e[1][u]);
+            for (int u = 0; u < 8; u++) add(v[1][u], l[1][u], e[1][u]);
         }
     }
     int h = 8 * ng;
-    for (; h < m; h++) add(__builtin_nontemporal_load(src + h * (D / 8)), ex[h * n]);
+    for (; h < m; h++)
+        add(__builtin_nontemporal_load(src + h * (D / 8)), __builtin_nontemporal_load(srl + h * (D / 8)), ex[h * n]);
     if constexpr (BF16) {
         uint4 o;
         o.x = static_cast<uint32_t>(f32_to_bf16(s[0])) | (static_cast<uint32_t>(f32_to_bf16(s[1])) << 16);
@@ -777,13 +917,13 @@ unsigned elementwise_grid(int64_t count) {
 size_t align_up(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 template <bool BF16>
-hipError_t launch_reduce(const int16_t *part, const int8_t *pexp, void *out, int64_t rows, int64_t n, int m,
-                         hipStream_t stream) {
+hipError_t launch_reduce(const int16_t *part, const uint8_t *plow, const int8_t *pexp, void *out, int64_t rows,
+                         int64_t n, int m, hipStream_t stream) {
     if (rows == 0) return hipSuccess;
     const int64_t blocks = (rows * 8 + kReduceThreads - 1) / kReduceThreads;
     KernelTimer timer("reduce_kernel", stream);
     hipLaunchKernelGGL(reduce_kernel<BF16>, dim3(static_cast<unsigned>(blocks)), dim3(kReduceThreads), 0, stream,
-                       part, pexp, out, rows, n, m);
+                       part, plow, pexp, out, rows, n, m);
     return hipGetLastError();
 }
 
@@ -821,8 +961,11 @@ BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, 
     L.vs = o; o = align_up(o + static_cast<size_t>(bh) * n_k * D * 4);
     L.pq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m * D * 2);
     L.pk = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m * D * 2);
+    L.lq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m * D);
+    L.lk = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m * D);
     L.eq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m);
     L.ek = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m);
+    L.pmax = o; o = align_up(o + static_cast<size_t>(bh) * 4 * kMaxParts * 4);
     L.table = o; o = align_up(o + table_workspace_bytes(bf16, bh, n_k, m, tau));
     L.total = o;
     return L;
@@ -871,16 +1014,26 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
 
     _Float16 *qs = reinterpret_cast<_Float16 *>(ws + L.qs), *ks = reinterpret_cast<_Float16 *>(ws + L.ks);
     _Float16 *vs = reinterpret_cast<_Float16 *>(ws + L.vs), *dys = reinterpret_cast<_Float16 *>(ws + L.dys);
+    float *pmax = reinterpret_cast<float *>(ws + L.pmax);
+    {
+        KernelTimer timer("absmax_kernel", stream);
+        const dim3 grid(static_cast<unsigned>(bh * 4 * kMaxParts));
+        if (bf16)
+            hipLaunchKernelGGL(absmax_kernel<true>, grid, dim3(256), 0, stream, q, dy, k, v, n_q, n_k, pmax);
+        else
+            hipLaunchKernelGGL(absmax_kernel<false>, grid, dim3(256), 0, stream, q, dy, k, v, n_q, n_k, pmax);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     {
         const int64_t threads = 2 * bh * (n_q + n_k) * (D / 8);
         const int64_t blocks = (threads + 255) / 256 < 65536 ? (threads + 255) / 256 : 65536;
         KernelTimer timer("split_kernel", stream);
         if (bf16)
             hipLaunchKernelGGL(split_kernel<true>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, q, k, v,
-                               dy, qs, ks, vs, dys, bh * n_q, bh * n_k);
+                               dy, qs, ks, vs, dys, pmax, bh, n_q, n_k);
         else
             hipLaunchKernelGGL(split_kernel<false>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, q, k,
-                               v, dy, qs, ks, vs, dys, bh * n_q, bh * n_k);
+                               v, dy, qs, ks, vs, dys, pmax, bh, n_q, n_k);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
@@ -888,8 +1041,11 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
     a.q = Side{reinterpret_cast<const uint32_t *>(ws + L.qent), reinterpret_cast<const int32_t *>(ws + L.qoff), n_q};
     a.k = Side{reinterpret_cast<const uint32_t *>(ws + L.kent), reinterpret_cast<const int32_t *>(ws + L.koff), n_k};
     a.qs = qs; a.ks = ks; a.vs = vs; a.dys = dys;
+    a.pmax = pmax;
     a.pq = reinterpret_cast<int16_t *>(ws + L.pq);
     a.pk = reinterpret_cast<int16_t *>(ws + L.pk);
+    a.lq = reinterpret_cast<uint8_t *>(ws + L.lq);
+    a.lk = reinterpret_cast<uint8_t *>(ws + L.lk);
     a.eq = reinterpret_cast<int8_t *>(ws + L.eq);
     a.ek = reinterpret_cast<int8_t *>(ws + L.ek);
     a.bh = bh; a.m = m; a.tau = tau;
@@ -897,11 +1053,11 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
     e = launch_pass(a, units, stream);
     if (e != hipSuccess) return e;
     if (bf16) {
-        if ((e = launch_reduce<true>(a.pq, a.eq, dq, bh * n_q, n_q, m, stream)) != hipSuccess) return e;
-        return launch_reduce<true>(a.pk, a.ek, dk, bh * n_k, n_k, m, stream);
+        if ((e = launch_reduce<true>(a.pq, a.lq, a.eq, dq, bh * n_q, n_q, m, stream)) != hipSuccess) return e;
+        return launch_reduce<true>(a.pk, a.lk, a.ek, dk, bh * n_k, n_k, m, stream);
     }
-    if ((e = launch_reduce<false>(a.pq, a.eq, dq, bh * n_q, n_q, m, stream)) != hipSuccess) return e;
-    return launch_reduce<false>(a.pk, a.ek, dk, bh * n_k, n_k, m, stream);
+    if ((e = launch_reduce<false>(a.pq, a.lq, a.eq, dq, bh * n_q, n_q, m, stream)) != hipSuccess) return e;
+    return launch_reduce<false>(a.pk, a.lk, a.ek, dk, bh * n_k, n_k, m, stream);
 }
 
 }  // namespace yoso

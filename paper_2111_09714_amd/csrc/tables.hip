@@ -14,11 +14,12 @@
 //
 // Tables hold fixed-point integers, not floats: gfx950 executes LDS fp32
 // atomic adds some 40x slower than integer ones, while a 64-bit integer add
-// carries two values at once.  Each value v of the slice is quantised to
-// q = rint(v 2^k) with one power-of-two scale per workgroup, chosen so that
-// 2^k times the largest per-dim sum of |v| over the source rows (a bound on every
-// bucket sum, and never above n_src max|v|) stays below 2^30; a bucket sum of
-// rounded values is then below 2^30 + n_src/2 in magnitude.  Two adjacent dims
+// carries two values at once.  Each value v of feature dim d is quantised to
+// q = rint(v 2^k_d) with one power-of-two scale per dim of the workgroup's
+// slice, chosen so that 2^k_d times that dim's sum of |v| over the source rows (a
+// bound on every bucket sum of the dim, and never above n_src max|v|) stays below
+// 2^30; a bucket sum of rounded values is then below 2^30 + n_src/2 in magnitude.
+// A dim of small values is thus resolved as finely as a dim of large ones.  Two adjacent dims
 // (q_lo, q_hi) are packed as the 64-bit integer q_hi 2^32 + q_lo; sums of packed
 // words never corrupt each other's field because |sum q_lo| < 2^31.  Integer
 // sums are exact and independent of the order of the atomics, so the tables (and
@@ -114,7 +115,7 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
     constexpr int S = D / DS;   // slices per head
     extern __shared__ __align__(16) unsigned long long tab[];  // [2^tau][G][P]
     __shared__ float wave_red[kTableWaves * DS];
-    __shared__ int scale_exp;
+    __shared__ int scale_exp[DS];
 
     const int64_t blocks = a.bh * S;
     const int64_t logical = xcd_remap(blockIdx.x, blocks);
@@ -157,13 +158,10 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
             for (int d = 0; d < DS; d++) wave_red[wave * DS + d] = sa[d];
         }
         __syncthreads();
-        if (tid == 0) {
+        if (tid < DS) {
+            const int d = tid;
             float t = 0.f;
-            for (int d = 0; d < DS; d++) {
-                float s = 0.f;
-                for (int w = 0; w < kTableWaves; w++) s += wave_red[w * DS + d];
-                t = fmaxf(t, s);
-            }
+            for (int w = 0; w < kTableWaves; w++) t += wave_red[w * DS + d];
             int k = 0;
             if (t > 0.f) {
                 // the fp32 sums are low by at most ~140 ulp-units relative (128 terms
@@ -174,11 +172,14 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
                 frexpf(t * (1.0f + 0x1p-10f), &ev);  // t (1 + 2^-10) < 2^ev
                 k = 30 - ev;
             }
-            scale_exp = k;
+            scale_exp[d] = k;
         }
         __syncthreads();
     }
-    const int k = scale_exp;
+    // per-dim scales as wave-uniform exponents
+    int kd[DS];
+#pragma unroll
+    for (int d = 0; d < DS; d++) kd[d] = __builtin_amdgcn_readfirstlane(scale_exp[d]);
 
     // lane roles
     // hashes rounded up to a power of two: fixed by (DS, KM) for the one- and
@@ -288,8 +289,8 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
                 // fetching the next chunk's values (the last chunk fetches itself again)
 #pragma unroll
                 for (int p = 0; p < P; p++) {
-                    const int lo = kok ? __float2int_rn(ldexpf(vr[2 * p], k)) : 0;
-                    const int hi = kok ? __float2int_rn(ldexpf(vr[2 * p + 1], k)) : 0;
+                    const int lo = kok ? __float2int_rn(ldexpf(vr[2 * p], kd[2 * p])) : 0;
+                    const int hi = kok ? __float2int_rn(ldexpf(vr[2 * p + 1], kd[2 * p + 1])) : 0;
                     wstage[lane * P + p] = (static_cast<unsigned long long>(static_cast<uint32_t>(hi)) << 32) +
                                            static_cast<unsigned long long>(static_cast<long long>(lo));
                 }
@@ -338,8 +339,8 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
                         }
 #pragma unroll
                         for (int p = 0; p < P; p++) {
-                            const int lo = __float2int_rn(ldexpf(v[2 * p], k));
-                            const int hi = __float2int_rn(ldexpf(v[2 * p + 1], k));
+                            const int lo = __float2int_rn(ldexpf(v[2 * p], kd[2 * p]));
+                            const int hi = __float2int_rn(ldexpf(v[2 * p + 1], kd[2 * p + 1]));
                             const unsigned long long w =
                                 (static_cast<unsigned long long>(static_cast<uint32_t>(hi)) << 32) +
                                 static_cast<unsigned long long>(static_cast<long long>(lo));
@@ -369,15 +370,25 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
         }
         __syncthreads();
 
-        // ---- integer sums -> floats scaled by 2^-k / m, in place (a packed word and
-        // its two floats have the same 8 bytes)
+        // ---- integer sums -> floats scaled by 2^-k_d / m, in place (a packed word and
+        // its two floats have the same 8 bytes).  Word e holds dims 2p, 2p+1 with
+        // p = e mod P, and P divides the thread count, so p is fixed per thread.
         {
+            static_assert(kTableThreads % P == 0, "word slot must be fixed per thread");
             const int words = (cmask + 1) * G * P;
+            const int pw = tid % P;
+            int klo = kd[0], khi = kd[1];
+#pragma unroll
+            for (int p = 1; p < P; p++) {
+                klo = pw == p ? kd[2 * p] : klo;
+                khi = pw == p ? kd[2 * p + 1] : khi;
+            }
             float2 *tf = reinterpret_cast<float2 *>(tab);
             for (int e = tid; e < words; e += kTableThreads) {
                 int lo, hi;
                 unpack(tab[e], lo, hi);
-                tf[e] = make_float2(ldexpf(static_cast<float>(lo), -k) * inv_m, ldexpf(static_cast<float>(hi), -k) * inv_m);
+                tf[e] = make_float2(ldexpf(static_cast<float>(lo), -klo) * inv_m,
+                                    ldexpf(static_cast<float>(hi), -khi) * inv_m);
             }
         }
         __syncthreads();
@@ -560,15 +571,20 @@ void launch_table_km(int km, const TableArgs &a, size_t lds, hipStream_t stream)
         hipLaunchKernelGGL((table_kernel<BF16, DS, 2>), grid, block, lds, stream, a);
 }
 
-template <bool BF16>
-hipError_t launch_table_ds(int ds, const TableArgs &a, size_t lds, hipStream_t stream) {
+// Step form of a table launch: 0 -> one key per step, 1 -> two keys per step (both
+// with LDS staging of a chunk's packed words), 2 -> the general form.
+int table_step_form(const TableArgs &a, int ds) {
     int gp = 1;
     while (gp < a.G) gp <<= 1;
     const int cpk = gp * (ds / 2);
     // the one- and two-key forms read codes as aligned 32-bit pairs
     const bool pairs = a.m % 2 == 0 && (reinterpret_cast<uintptr_t>(a.src_codes) & 3) == 0 &&
                        (reinterpret_cast<uintptr_t>(a.dst_codes) & 3) == 0;
-    const int km = (ds > 8 || !pairs) ? 2 : (cpk == 64 ? 0 : (cpk == 32 ? 1 : 2));
+    return (ds > 8 || !pairs) ? 2 : (cpk == 64 ? 0 : (cpk == 32 ? 1 : 2));
+}
+
+template <bool BF16>
+hipError_t launch_table_ds(int ds, int km, const TableArgs &a, size_t lds, hipStream_t stream) {
     KernelTimer timer("table_kernel", stream);
     switch (ds) {
         case 2: launch_table_km<BF16, 2>(km, a, lds, stream); break;
@@ -626,11 +642,16 @@ hipError_t launch_table(const uint16_t *src_codes, const void *values, const uin
     a.m = m;
     a.tau = tau;
     a.G = p.G;
-    // + one private dummy word per lane (targets of lanes without a valid key)
-    // + per-wave staging of a chunk's packed words (64 keys x DS/2 words)
-    const size_t lds = p.lds + 64 * sizeof(unsigned long long) +
-                       static_cast<size_t>(kTableWaves) * 64 * (p.DS / 2) * sizeof(unsigned long long);
-    return bf16 ? launch_table_ds<true>(p.DS, a, lds, stream) : launch_table_ds<false>(p.DS, a, lds, stream);
+    // the one- and two-key step forms also need one private dummy word per lane
+    // (targets of lanes without a valid key) and per-wave staging of a chunk's
+    // packed words (64 keys x DS/2 words); the general form needs neither (with 128
+    // KiB of tables and 16-dim slices they would not fit beside them)
+    const int km = table_step_form(a, p.DS);
+    const size_t lds = p.lds + (km < 2 ? 64 * sizeof(unsigned long long) +
+                                             static_cast<size_t>(kTableWaves) * 64 * (p.DS / 2) *
+                                                 sizeof(unsigned long long)
+                                       : 0);
+    return bf16 ? launch_table_ds<true>(p.DS, km, a, lds, stream) : launch_table_ds<false>(p.DS, km, a, lds, stream);
 }
 
 }  // namespace yoso

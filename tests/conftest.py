@@ -17,3 +17,14 @@ def golden():
     import json
     with open(os.path.join(ROOT, "tests", "golden", "worked_examples.json")) as f:
         return json.load(f)
+
+
+def pytest_terminal_summary(terminalreporter):
+    """Every parity figure of the session (per-head Frobenius ratio and the
+    element-wise |gpu - ref| / (|ref| + rms(ref row))), passing or not."""
+    parity = sys.modules.get("parity")
+    if parity is None or not parity.RECORD:
+        return
+    terminalreporter.section("parity figures (frob / elem vs tolerance)")
+    for tag, name, frob, elem, tol in parity.RECORD:
+        terminalreporter.write_line(f"{tag:48.48s} {name:3s} frob {frob:.2e} elem {elem:.2e} tol {tol:.0e}")

@@ -18,6 +18,10 @@ import numpy as np
 
 TOL = {"f32": 1e-4, "bf16": 2e-2}
 
+# (tag, tensor, frob, elem, tol) of every check in this session; the terminal
+# summary of tests/conftest.py prints them, so a passing run still shows them.
+RECORD = []
+
 
 def log(msg: str) -> None:
     print(msg, flush=True)
@@ -57,6 +61,7 @@ def check_all(tag: str, pairs, tol: float) -> dict:
     then asserts them."""
     errs = {name: errors(g, r) for name, g, r in pairs}
     log(f"[{tag}] " + " ".join(f"{k}: frob {f:.2e} elem {e:.2e}" for k, (f, e) in errs.items()))
+    RECORD.extend((tag, k, f, e, tol) for k, (f, e) in errs.items())
     for name, (f, e) in errs.items():
         assert f <= tol and e <= tol, (tag, name, f, e, tol)
     return errs

@@ -133,14 +133,14 @@ def test_empty_tensors_need_no_pointers(L):
 def test_workspace_sizes():
     # backward workspace: bucket offsets + sorted entries, the fp16 (hi, lo) copies of
     # Q, K, V, dY (4 bytes per element) and one partial row per (row, hash) for dq and
-    # dk in block floating point (64 int16 mantissas + one exponent byte), the same
-    # for both storage types
+    # dk in 24-bit fixed point (64 int16 high parts, 64 low bytes and one exponent
+    # byte), the same for both storage types
     f32 = Y.yoso_workspace_bytes(Y.OP_BACKWARD, 32, 4096, 4096, 64, 32, 8, Y.F32)
     bf = Y.yoso_workspace_bytes(Y.OP_BACKWARD, 32, 4096, 4096, 64, 32, 8, Y.BF16)
     units = 32 * 32
     index = units * (2 * 257 * 4 + 2 * 4096 * 4)
     split = 4 * 32 * 4096 * 64 * 4
-    partials = 2 * 32 * 4096 * 32 * (64 * 2 + 1)
+    partials = 2 * 32 * 4096 * 32 * (64 * 3 + 1)
     assert f32 >= index + split + partials
     assert f32 < 1.05 * (index + split + partials) + (1 << 20)
     assert bf == f32

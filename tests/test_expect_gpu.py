@@ -63,6 +63,32 @@ def test_expectation_small(bh, nq, nk, tau, dtype):
               [("y", y, ey), ("dq", dq, edq), ("dk", dk, edk), ("dv", dv, edv)], TOL[dtype])
 
 
+@pytest.mark.parametrize("what,scale", [("dy", 1e-6), ("dy", 1e3), ("v", 1e-5), ("rows", None)])
+def test_expectation_far_from_unit_scale(what, scale):
+    """Gradients and values far from unit size (training gradients are small): the
+    per-row and per-tile power-of-two scalings before the fp16 (hi, lo) split keep
+    every output at the fp32 bar; "rows" gives every row of dY and V its own scale
+    (10^-4 .. 1 and 10^-3 .. 10)."""
+    g = np.random.default_rng(4000 + len(what))
+    bh, nq, nk, tau = 2, 200, 150, 8
+    q = unit(g.standard_normal((bh, nq, 64)))
+    k = unit(g.standard_normal((bh, nk, 64)))
+    v = g.standard_normal((bh, nk, 64))
+    dy = g.standard_normal((bh, nq, 64))
+    if what == "rows":
+        dy = dy * 10.0 ** g.uniform(-4, 0, size=(bh, nq, 1))
+        v = v * 10.0 ** g.uniform(-3, 1, size=(bh, nk, 1))
+    elif what == "dy":
+        dy = dy * scale
+    else:
+        v = v * scale
+    qd, kd, vd, dyd = (to_dev(a, "f32") for a in (q, k, v, dy))
+    y, dq, dk, dv = run_gpu(qd, kd, vd, dyd, tau)
+    ey, edv, edq, edk = oracle.expectation(host(qd), host(kd), host(vd), host(dyd), tau)
+    check_all(f"yoso-e scaled {what} {scale}", [("y", y, ey), ("dq", dq, edq), ("dk", dk, edk), ("dv", dv, edv)],
+              TOL["f32"])
+
+
 def test_expectation_closed_forms():
     """P = 1 for identical directions, 2^-tau for orthogonal ones, 0 for opposite ones."""
     tau = 5

@@ -128,6 +128,53 @@ def test_workload_full_size(name):
     check_outputs(name, inp, g, w.m, w.tau, w.dtype, heads=sl)
 
 
+@pytest.mark.parametrize("what,scale", [("dy", 1e-6), ("dy", 1e3), ("v", 1e-5), ("rows", None)])
+def test_backward_far_from_unit_scale(what, scale):
+    """Upstream gradients (and values) far from unit size: typical training
+    gradients are small, and the fp16 (hi, lo) split would lose them without the
+    per-head power-of-two scaling; "rows" gives every row of dY and V its own scale
+    (10^-4 .. 1 and 10^-3 .. 10), which the per-row factor on S covers."""
+    bh, n, m, tau = 2, 700, 16, 8
+    name = f"scaled {what} {scale}"
+    log(f"[{name}] start")
+    w = workloads.Workload(name, 1, bh, n, 64, tau, m, "f32", "gauss", 4321)
+    inp = make_inputs(w)
+    if what == "rows":
+        g = np.random.default_rng(99)
+        inp["dy"] = inp["dy"] * 10.0 ** g.uniform(-4, 0, size=(bh, n, 1))
+        inp["v"] = inp["v"] * 10.0 ** g.uniform(-3, 1, size=(bh, n, 1))
+    else:
+        inp[what] = inp[what] * scale
+    # the oracle sees the fp32 values the GPU reads
+    for key in ("dy", "v"):
+        inp[key] = inp[key].astype(np.float32).astype(np.float64)
+    g = run_gpu(inp, m, tau, "f32")
+    y = oracle.forward(g["qc"], g["kc"], inp["v"], m, tau)
+    dq, dk, dv = oracle.backward(g["qc"], g["kc"], inp["q"], inp["k"], inp["v"], inp["dy"], m, tau)
+    check_all(name, [(key, g[key], ref) for key, ref in (("y", y), ("dq", dq), ("dk", dk), ("dv", dv))], TOL["f32"])
+
+
+def test_tables_resolve_every_feature_dim():
+    """Feature dims of very different scales (10^-3 .. 10^3 within every table slice):
+    each dim has its own fixed-point scale, so each column of Y and dV meets the bar
+    on its own, not only the rows dominated by the largest dims."""
+    bh, n, m, tau = 1, 16384, 8, 8
+    w = workloads.Workload("anisotropic", 1, bh, n, 64, tau, m, "f32", "gauss", 777)
+    inp = make_inputs(w)
+    g = np.random.default_rng(5)
+    for key in ("v", "dy"):
+        scales = 10.0 ** g.permutation(np.linspace(-3, 3, 64))
+        inp[key] = (inp[key] * scales).astype(np.float32).astype(np.float64)
+    out = run_gpu(inp, m, tau, "f32")
+    y = oracle.forward(out["qc"], out["kc"], inp["v"], m, tau)
+    _, _, dv = oracle.backward(out["qc"], out["kc"], inp["q"], inp["k"], inp["v"], inp["dy"], m, tau)
+    for key, ref in (("y", y), ("dv", dv)):
+        got = out[key][0]
+        col = np.linalg.norm(got - ref[0], axis=0) / np.linalg.norm(ref[0], axis=0)
+        log(f"[anisotropic] {key}: worst column rel err {col.max():.2e} (dim {int(col.argmax())})")
+        assert col.max() <= TOL["f32"], (key, col.max())
+
+
 def test_empty_and_degenerate():
     # bh = 0, n_q = 0, n_k = 0: valid calls; empty key set gives zero outputs
     m, tau = 4, 3
