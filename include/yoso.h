@@ -181,6 +181,30 @@ yoso_status yoso_backward(const uint16_t *qcodes, const uint16_t *kcodes, const 
                           void *stream);
 
 /*
+ * yoso_backward without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation).  Same arguments, results and errors as yoso_backward;
+ * its scratch is a fixed array inside the library, one per GPU, reserved when the
+ * library is loaded and held until the process ends (its size:
+ * yoso_backward_noalloc_limit(), 64 MiB; one head of 4096 queries and keys at
+ * m = 32, tau = 8 needs about 56 MB).  Shapes whose backward needs more than
+ * that return YOSO_ERR_WORKSPACE before anything is launched.  The call makes
+ * no allocation; the first call on a device looks up that device's copy of the
+ * array (the stream must belong to the current device, else YOSO_ERR_DEVICE).
+ * Every call on one GPU uses the same array: calls that overlap in time on one
+ * GPU (other streams, other threads) race and must be serialised by the caller.
+ * Nothing in the array needs to start at zero (every byte read is first written
+ * by the same call).
+ */
+yoso_status yoso_backward_noalloc(const uint16_t *qcodes, const uint16_t *kcodes, const void *q,
+                                  const void *k, const void *v, const void *dy, yoso_dtype dtype,
+                                  int64_t bh, int64_t n_q, int64_t n_k, int32_t d, int32_t m, int32_t tau,
+                                  void *dq, void *dk, void *dv, void *stream);
+
+/* Bytes of the fixed scratch array of yoso_backward_noalloc (per GPU). */
+size_t yoso_backward_noalloc_limit(void);
+
+/*
  * Row l2 normalisation: the output normalisation of N-YOSO (Sec. 3.1,
  * "Normalizing Attention", eq. normalized-yoso: N-YOSO(Q, K, V) = l2(B(Q, K) V))
  * and the normalisation of Q and K before hashing that the experiments use

@@ -24,7 +24,7 @@ from typing import Optional
 __all__ = [
     "YosoError", "F32", "BF16", "OP_HASH", "OP_FORWARD", "OP_BACKWARD",
     "lib", "lib_path", "yoso_workspace_bytes", "yoso_status_str", "yoso_hash", "yoso_fast_hyperplanes", "yoso_fast_hash", "yoso_forward",
-    "yoso_backward", "yoso_l2_normalize", "yoso_l2_normalize_backward", "yoso_expectation_forward",
+    "yoso_backward", "yoso_backward_noalloc", "yoso_backward_noalloc_limit", "yoso_l2_normalize", "yoso_l2_normalize_backward", "yoso_expectation_forward",
     "yoso_expectation_backward",
     "yoso_timing_enable", "yoso_timing_reset", "yoso_timing_query",
     "workspace", "hash_qk", "fast_hash_qk", "forward", "backward",
@@ -63,6 +63,10 @@ def lib() -> ctypes.CDLL:
         L.yoso_fast_hash.argtypes = [P, I32, I64, I64, I32, P, I32, I32, P, P]
         L.yoso_forward.argtypes = [P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, SZ, P]
         L.yoso_backward.argtypes = [P, P, P, P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, P, P, SZ, P]
+        L.yoso_backward_noalloc.argtypes = [P, P, P, P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, P, P]
+        L.yoso_backward_noalloc.restype = ctypes.c_int
+        L.yoso_backward_noalloc_limit.argtypes = []
+        L.yoso_backward_noalloc_limit.restype = SZ
         L.yoso_workspace_bytes.argtypes = [I32, I64, I64, I64, I32, I32, I32, I32]
         L.yoso_workspace_bytes.restype = SZ
         L.yoso_l2_normalize.argtypes = [P, I32, I64, I32, P, P]
@@ -236,6 +240,29 @@ def yoso_backward(qcodes, kcodes, q, k, v, dy, m: int, tau: int, dq, dk, dv, ws,
     _check(lib().yoso_backward(_ptr(qcodes), _ptr(kcodes), _ptr(q), _ptr(k), _ptr(v), _ptr(dy), _dtype_code(q),
                                bh, n_q, n_k, d, m, tau, _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws), nbytes,
                                _stream(stream)))
+
+
+def yoso_backward_noalloc(qcodes, kcodes, q, k, v, dy, m: int, tau: int, dq, dk, dv, stream=None) -> None:
+    """yoso_backward on the library's fixed per-GPU scratch (no workspace, no
+    allocation); shapes needing more than yoso_backward_noalloc_limit() bytes are
+    refused.  Calls that overlap on one GPU race."""
+    _codes_ok(qcodes)
+    _codes_ok(kcodes)
+    _same(q, ((k, "k"), (v, "v"), (dy, "dy"), (dq, "dq"), (dk, "dk"), (dv, "dv")))
+    _on(q, ((qcodes, "qcodes"), (kcodes, "kcodes")))
+    bh, n_q, d = q.shape
+    n_k = k.shape[1]
+    for t, shape, name in ((k, (bh, n_k, d), "k"), (v, (bh, n_k, d), "v"), (dy, (bh, n_q, d), "dy"),
+                           (dq, (bh, n_q, d), "dq"), (dk, (bh, n_k, d), "dk"), (dv, (bh, n_k, d), "dv"),
+                           (qcodes, (bh, n_q, m), "qcodes"), (kcodes, (bh, n_k, m), "kcodes")):
+        _expect(t, shape, name)
+    _check(lib().yoso_backward_noalloc(_ptr(qcodes), _ptr(kcodes), _ptr(q), _ptr(k), _ptr(v), _ptr(dy),
+                                       _dtype_code(q), bh, n_q, n_k, d, m, tau, _ptr(dq), _ptr(dk), _ptr(dv),
+                                       _stream(stream)))
+
+
+def yoso_backward_noalloc_limit() -> int:
+    return lib().yoso_backward_noalloc_limit()
 
 
 def yoso_l2_normalize(x, y, stream=None) -> None:

@@ -3,8 +3,17 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <mutex>
+
 #include "../../include/yoso.h"
 #include "launch.h"
+
+// Workspace of yoso_backward_noalloc: one copy of this array per GPU the library
+// runs on, held until the process ends.  Host code never uses the name itself
+// (on the host it is only a stand-in for the device symbol): it asks
+// hipGetSymbolAddress for each device's address once and passes that pointer.
+constexpr size_t kNoAllocScratchBytes = size_t{64} << 20;
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
 
 namespace {
 
@@ -82,6 +91,34 @@ yoso_status check_workspace(const void *ws, size_t have, size_t need) {
     if (ws == nullptr) return fail(YOSO_ERR_WORKSPACE, "workspace is NULL but %zu bytes are needed", need);
     if (have < need) return fail(YOSO_ERR_WORKSPACE, "workspace has %zu bytes, %zu needed", have, need);
     if (reinterpret_cast<uintptr_t>(ws) & 15u) return fail(YOSO_ERR_ALIGN, "workspace is not 16-byte aligned");
+    return YOSO_OK;
+}
+
+// The scratch array's address on the device of `stream` (which must be the
+// current device), looked up on the first call on that device.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+yoso_status scratch_for(hipStream_t stream, void **ptr) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return device_status(e, "hipGetDevice");
+    if (stream != nullptr) {
+        int sdev = 0;
+        if ((e = hipStreamGetDevice(stream, &sdev)) != hipSuccess) return device_status(e, "hipStreamGetDevice");
+        if (sdev != dev)
+            return fail(YOSO_ERR_DEVICE, "the stream belongs to device %d but device %d is current", sdev, dev);
+    }
+    if (dev < 0 || dev >= kMaxDevices) return fail(YOSO_ERR_DEVICE, "device %d beyond the %d supported", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void *p = nullptr;
+        if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess)
+            return device_status(e, "hipGetSymbolAddress(scratch)");
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
     return YOSO_OK;
 }
 
@@ -205,6 +242,40 @@ yoso_status yoso_backward(const uint16_t *qcodes, const uint16_t *kcodes, const 
                                                workspace, static_cast<hipStream_t>(stream)),
                          "yoso_backward");
 }
+
+yoso_status yoso_backward_noalloc(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
+                                  const void *v, const void *dy, yoso_dtype dtype, int64_t bh, int64_t n_q,
+                                  int64_t n_k, int32_t d, int32_t m, int32_t tau, void *dq, void *dk, void *dv,
+                                  void *stream) {
+    g_last_error[0] = '\0';
+    YOSO_TRY(check_dtype(dtype));
+    YOSO_TRY(check_shape(bh, n_q, n_k, d, m));
+    YOSO_TRY(check_hash(m, tau));
+    YOSO_TRY(check_ptr(qcodes, bh * m * n_q, "qcodes"));
+    YOSO_TRY(check_ptr(kcodes, bh * m * n_k, "kcodes"));
+    YOSO_TRY(check_ptr(q, bh * n_q * d, "q"));
+    YOSO_TRY(check_ptr(k, bh * n_k * d, "k"));
+    YOSO_TRY(check_ptr(v, bh * n_k * d, "v"));
+    YOSO_TRY(check_ptr(dy, bh * n_q * d, "dy"));
+    YOSO_TRY(check_ptr(dq, bh * n_q * d, "dq"));
+    YOSO_TRY(check_ptr(dk, bh * n_k * d, "dk"));
+    YOSO_TRY(check_ptr(dv, bh * n_k * d, "dv"));
+    const bool bf16 = dtype == YOSO_BF16;
+    const size_t need = required_workspace(YOSO_OP_BACKWARD, bf16, bh, n_q, n_k, m, tau);
+    if (need > kNoAllocScratchBytes)
+        return fail(YOSO_ERR_WORKSPACE,
+                    "these shapes need %zu bytes of scratch; yoso_backward_noalloc has %zu (use yoso_backward with a "
+                    "workspace)",
+                    need, kNoAllocScratchBytes);
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    void *ws = nullptr;
+    if (need > 0) YOSO_TRY(scratch_for(s, &ws));
+    return device_status(yoso::launch_backward(qcodes, kcodes, q, k, v, dy, bf16, bh, n_q, n_k, m, tau, dq, dk, dv,
+                                               ws, s),
+                         "yoso_backward_noalloc");
+}
+
+size_t yoso_backward_noalloc_limit(void) { return kNoAllocScratchBytes; }
 
 yoso_status yoso_l2_normalize(const void *x, yoso_dtype dtype, int64_t rows, int32_t d, void *y, void *stream) {
     g_last_error[0] = '\0';

@@ -122,6 +122,19 @@ def test_backward_rejects(L, kw, status):
     assert _bwd(L, **kw) == status
 
 
+def test_noalloc_refuses_shapes_beyond_its_scratch(L):
+    """yoso_backward_noalloc checks the workspace its shapes need against its fixed
+    64 MiB scratch before any HIP call."""
+    assert L.yoso_backward_noalloc_limit() == 64 << 20
+    p = [FAKE] * 6
+    # 32 heads of 4096 rows at m = 32 need about 0.9 GB
+    st = L.yoso_backward_noalloc(*p, 0, 32, 4096, 4096, 64, 32, 8, FAKE, FAKE, FAKE, None)
+    assert st == 6 and b"scratch" in L.yoso_last_error()
+    assert L.yoso_backward_noalloc(*p, 0, 1, 128, 128, 32, 32, 8, FAKE, FAKE, FAKE, None) == 2  # d
+    assert L.yoso_backward_noalloc(*p, 0, 1, 128, 128, 64, 32, 13, FAKE, FAKE, FAKE, None) == 3  # tau
+    assert L.yoso_backward_noalloc(FAKE, None, *p[2:], 0, 1, 128, 128, 64, 32, 8, FAKE, FAKE, FAKE, None) == 1
+
+
 def test_empty_tensors_need_no_pointers(L):
     # zero-sized tensors are valid and their pointers may be NULL; with every size 0
     # nothing is launched, so these calls return OK even without a GPU.
