@@ -78,7 +78,12 @@ typedef enum {
  * once at the end. */
 typedef enum { YOSO_F32 = 0, YOSO_BF16 = 1 } yoso_dtype;
 
-typedef enum { YOSO_OP_HASH = 0, YOSO_OP_FORWARD = 1, YOSO_OP_BACKWARD = 2 } yoso_op;
+typedef enum {
+    YOSO_OP_HASH = 0,
+    YOSO_OP_FORWARD = 1,
+    YOSO_OP_BACKWARD = 2,
+    YOSO_OP_BACKWARD_STAR = 3
+} yoso_op;
 
 /*
  * Sign-random-projection hash (Sec. 3.2 overview; Fig. 2 caption: tau
@@ -179,6 +184,37 @@ yoso_status yoso_backward(const uint16_t *qcodes, const uint16_t *kcodes, const 
                           int64_t bh, int64_t n_q, int64_t n_k, int32_t d, int32_t m, int32_t tau,
                           void *dq, void *dk, void *dv, void *workspace, size_t workspace_bytes,
                           void *stream);
+
+/*
+ * *YOSO (Sec. 3.3, eq. gradient-q; the *YOSO rows of Sec. 4): a sampled estimate
+ * of the TRUE gradient of the expected attention for Q and K, on the same codes.
+ * eq. gradient-q weighs the pair (i, j) by tau (1 - theta/pi)^(tau-1) /
+ * (pi sqrt(1 - x^2)), x = q_i . k_j; (1 - theta/pi)^(tau-1) is the collision
+ * probability of tau-1 hyperplane bits, so per hash
+ *
+ *   C_h(i, j) = #{ t < tau : codes of q_i, k_j agree on every bit except t }
+ *             = tau [codes equal] + [codes differ in exactly one bit]
+ *
+ * has expectation tau (1 - theta/pi)^(tau-1), and
+ *
+ *   dq = (1/m) sum_h [(dy v^T) .* C_h ./ (pi sqrt(max(1 - (q k^T)^2, 1/64)))] k
+ *   dk = (1/m) sum_h [(dy v^T) .* C_h ./ (pi sqrt(max(1 - (q k^T)^2, 1/64)))]^T q
+ *   dv = (1/m) sum_h B_h^T dy                    (eq. gradient-v, as yoso_backward)
+ *
+ * is unbiased for eq. gradient-q wherever 1 - x^2 >= 1/64.  The true gradient
+ * diverges as the alignment x approaches 1; the bound 1/64 caps the weight at
+ * 8/pi (|x| > 0.99216).  x is the dot product of the rows as given, taken as
+ * unit length (Remark 1).  Arguments, layouts and errors as for yoso_backward;
+ * workspace: yoso_workspace_bytes(YOSO_OP_BACKWARD_STAR, ...) bytes, about
+ * (3*m*tau*d + 7*m*tau + 8*d) * (n_q + n_k) * bh (the pairs of m*tau derived
+ * (tau-1)-bit hashes, one 24-bit partial row per row and derived hash); m*tau is
+ * also the limit on bh that yoso_backward puts on m.  Its pair pass does about
+ * tau + 1 times the work of yoso_backward's (pairs one bit apart count too).
+ */
+yoso_status yoso_backward_star(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
+                               const void *v, const void *dy, yoso_dtype dtype, int64_t bh, int64_t n_q,
+                               int64_t n_k, int32_t d, int32_t m, int32_t tau, void *dq, void *dk,
+                               void *dv, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * yoso_backward without a workspace argument, for callers that cannot allocate

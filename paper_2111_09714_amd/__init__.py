@@ -22,16 +22,16 @@ import os
 from typing import Optional
 
 __all__ = [
-    "YosoError", "F32", "BF16", "OP_HASH", "OP_FORWARD", "OP_BACKWARD",
+    "YosoError", "F32", "BF16", "OP_HASH", "OP_FORWARD", "OP_BACKWARD", "OP_BACKWARD_STAR",
     "lib", "lib_path", "yoso_workspace_bytes", "yoso_status_str", "yoso_hash", "yoso_fast_hyperplanes", "yoso_fast_hash", "yoso_forward",
-    "yoso_backward", "yoso_backward_noalloc", "yoso_backward_noalloc_limit", "yoso_l2_normalize", "yoso_l2_normalize_backward", "yoso_expectation_forward",
+    "yoso_backward", "yoso_backward_star", "backward_star", "yoso_backward_noalloc", "yoso_backward_noalloc_limit", "yoso_l2_normalize", "yoso_l2_normalize_backward", "yoso_expectation_forward",
     "yoso_expectation_backward",
     "yoso_timing_enable", "yoso_timing_reset", "yoso_timing_query",
     "workspace", "hash_qk", "fast_hash_qk", "forward", "backward",
 ]
 
 F32, BF16 = 0, 1
-OP_HASH, OP_FORWARD, OP_BACKWARD = 0, 1, 2
+OP_HASH, OP_FORWARD, OP_BACKWARD, OP_BACKWARD_STAR = 0, 1, 2, 3
 STATUS = {0: "YOSO_OK", 1: "YOSO_ERR_NULL", 2: "YOSO_ERR_SHAPE", 3: "YOSO_ERR_TAU", 4: "YOSO_ERR_DTYPE",
           5: "YOSO_ERR_ALIGN", 6: "YOSO_ERR_WORKSPACE", 7: "YOSO_ERR_DEVICE", 8: "YOSO_ERR_OP"}
 
@@ -63,6 +63,8 @@ def lib() -> ctypes.CDLL:
         L.yoso_fast_hash.argtypes = [P, I32, I64, I64, I32, P, I32, I32, P, P]
         L.yoso_forward.argtypes = [P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, SZ, P]
         L.yoso_backward.argtypes = [P, P, P, P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, P, P, SZ, P]
+        L.yoso_backward_star.argtypes = [P, P, P, P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, P, P, SZ, P]
+        L.yoso_backward_star.restype = ctypes.c_int
         L.yoso_backward_noalloc.argtypes = [P, P, P, P, P, P, I32, I64, I64, I64, I32, I32, I32, P, P, P, P]
         L.yoso_backward_noalloc.restype = ctypes.c_int
         L.yoso_backward_noalloc_limit.argtypes = []
@@ -242,6 +244,26 @@ def yoso_backward(qcodes, kcodes, q, k, v, dy, m: int, tau: int, dq, dk, dv, ws,
                                _stream(stream)))
 
 
+def yoso_backward_star(qcodes, kcodes, q, k, v, dy, m: int, tau: int, dq, dk, dv, ws, stream=None) -> None:
+    """*YOSO: dq, dk estimate the true gradient of eq. (gradient-q) (pairs whose codes
+    agree on all bits but at most one, weighted 1/(pi sqrt(max(1 - (q.k)^2, 1/64))));
+    dv as yoso_backward."""
+    _codes_ok(qcodes)
+    _codes_ok(kcodes)
+    _same(q, ((k, "k"), (v, "v"), (dy, "dy"), (dq, "dq"), (dk, "dk"), (dv, "dv")))
+    _on(q, ((qcodes, "qcodes"), (kcodes, "kcodes"), (ws, "ws")))
+    bh, n_q, d = q.shape
+    n_k = k.shape[1]
+    for t, shape, name in ((k, (bh, n_k, d), "k"), (v, (bh, n_k, d), "v"), (dy, (bh, n_q, d), "dy"),
+                           (dq, (bh, n_q, d), "dq"), (dk, (bh, n_k, d), "dk"), (dv, (bh, n_k, d), "dv"),
+                           (qcodes, (bh, n_q, m), "qcodes"), (kcodes, (bh, n_k, m), "kcodes")):
+        _expect(t, shape, name)
+    nbytes = ws.numel() * ws.element_size() if ws is not None else 0
+    _check(lib().yoso_backward_star(_ptr(qcodes), _ptr(kcodes), _ptr(q), _ptr(k), _ptr(v), _ptr(dy),
+                                    _dtype_code(q), bh, n_q, n_k, d, m, tau, _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws),
+                                    nbytes, _stream(stream)))
+
+
 def yoso_backward_noalloc(qcodes, kcodes, q, k, v, dy, m: int, tau: int, dq, dk, dv, stream=None) -> None:
     """yoso_backward on the library's fixed per-GPU scratch (no workspace, no
     allocation); shapes needing more than yoso_backward_noalloc_limit() bytes are
@@ -367,4 +389,12 @@ def backward(qcodes, kcodes, q, k, v, dy, m: int, tau: int):
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     ws = workspace(OP_BACKWARD, q, m, tau, n_k=k.shape[1])
     yoso_backward(qcodes, kcodes, q, k, v, dy, m, tau, dq, dk, dv, ws)
+    return dq, dk, dv
+
+
+def backward_star(qcodes, kcodes, q, k, v, dy, m: int, tau: int):
+    import torch
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = workspace(OP_BACKWARD_STAR, q, m, tau, n_k=k.shape[1])
+    yoso_backward_star(qcodes, kcodes, q, k, v, dy, m, tau, dq, dk, dv, ws)
     return dq, dk, dv

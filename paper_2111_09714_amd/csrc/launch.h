@@ -29,6 +29,14 @@ struct BackwardLayout {
 };
 BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m, int tau);
 
+// *YOSO: the pair layout for m*tau derived hashes of tau-1 bits, then the derived
+// codes of both sides and the dV table's scratch.
+struct StarLayout {
+    BackwardLayout pairs;
+    size_t qcodes, kcodes, table, total;
+};
+StarLayout backward_star_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m, int tau);
+
 hipError_t launch_hash(const void *x, bool bf16, int64_t bh, int64_t n, const float *R, int m, int tau,
                        uint16_t *codes, hipStream_t stream);
 
@@ -53,5 +61,8 @@ hipError_t launch_expect_backward(const void *q, const void *k, const void *v, c
 hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
                            const void *v, const void *dy, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m,
                            int tau, void *dq, void *dk, void *dv, void *workspace, hipStream_t stream);
+hipError_t launch_backward_star(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
+                                const void *v, const void *dy, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m,
+                                int tau, void *dq, void *dk, void *dv, void *workspace, hipStream_t stream);
 
 }  // namespace yoso

@@ -401,6 +401,21 @@ __device__ __forceinline__ int stage_rows(const uint4 r[4], unsigned char *tile,
     return (e2 + 1) >> 1;
 }
 
+// The rows' own b vectors (the q of a query row, the k of a key row; used by
+// *YOSO for q.k) through the second half of the tile into the same B-operand
+// layout: lane (g, c) gets row c, dims kb*32 + 8g + [0, 8).
+__device__ __forceinline__ void stage_rows_b(const uint4 r[4], unsigned char *tile, int q, int cl, int g, int c,
+                                             half8 bh[2], half8 bl[2]) {
+    unsigned char *t = tile + 16 * 256;
+#pragma unroll
+    for (int i = 0; i < 4; i++) lds_st(t, swz(4 * q + i, cl, 256), r[i]);
+#pragma unroll
+    for (int kb = 0; kb < 2; kb++) {
+        bh[kb] = lds_ld<half8>(t, swz(c, kb * 4 + g, 256));
+        bl[kb] = lds_ld<half8>(t, swz(c, 8 + kb * 4 + g, 256));
+    }
+}
+
 __device__ __forceinline__ half4 tr_load(const unsigned char *p) {
     typedef short short4v __attribute__((ext_vector_type(4)));
     typedef __attribute__((address_space(3))) short4v lds_short4;
@@ -420,8 +435,13 @@ __device__ __forceinline__ void publish_sub(const Sub &s, unsigned char *tile, i
 // out^T += B_y^T S^T for the sub-tile in the tile: S^T = A'_y A_x^T masked by
 // code equality.  `pe` as in load_sub: in the MFMA layout it holds the entries of
 // exactly the partners 4g+i whose S^T values this lane computes.
+// *YOSO's weight bound: 1 - x^2 is raised to at least 1/64 (|x| <= 0.99216).
+constexpr float kStarFloor = 1.0f / 64.0f;
+
+template <bool STAR>
 __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uint4 &pe, const half8 rh[2],
-                                            const half8 rl[2], int rcode, float sfac, int g, int c, floatx4 outT[4]) {
+                                            const half8 rl[2], const half8 rbh[2], const half8 rbl[2], float xscale,
+                                            int rcode, float sfac, int g, int c, floatx4 outT[4]) {
     // A'_y in the A-operand layout: lane (g, c) = partner c, dims kb*32 + 8g + [0, 8)
     half8 ah[2], al[2];
 #pragma unroll
@@ -455,6 +475,29 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uin
     float sv[4];
 #pragma unroll
     for (int i = 0; i < 4; i++) sv[i] = static_cast<int>(e[i] >> 16) == rcode ? st[i] : 0.f;
+    if constexpr (STAR) {
+        // x = q.k of each pair (the partner's b from the tile in the A-operand
+        // layout, the row's own b in the B layout), then the weight
+        // 1 / (pi sqrt(max(1 - x^2, 1/64))) of eq. (gradient-q)
+        half8 xh[2], xl[2];
+#pragma unroll
+        for (int kb = 0; kb < 2; kb++) {
+            xh[kb] = lds_ld<half8>(tile, swz(c, 16 + kb * 4 + g, 512));
+            xl[kb] = lds_ld<half8>(tile, swz(c, 24 + kb * 4 + g, 512));
+        }
+        floatx4 x0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xh[0], rbh[0], z, 0, 0, 0);
+        floatx4 x1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xh[1], rbh[1], z, 0, 0, 0);
+        x0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xh[0], rbl[0], x0, 0, 0, 0);
+        x1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xh[1], rbl[1], x1, 0, 0, 0);
+        x0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xl[0], rbh[0], x0, 0, 0, 0);
+        x1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xl[1], rbh[1], x1, 0, 0, 0);
+        const floatx4 xt = x0 + x1;
+#pragma unroll
+        for (int i = 0; i < 4; i++) {
+            const float x = xt[i] * xscale;
+            sv[i] *= rsqrtf(fmaxf(fmaf(-x, x, 1.0f), kStarFloor)) * 0.31830988618379067f;
+        }
+    }
     // the row's factor 2^-(2 + e_c): |S| < 2^14 (see the header), hi and lo stay normal
     half4 sh, sl;
     split4(sv, sfac, sh, sl);
@@ -574,7 +617,10 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
 
 __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlane(x); }
 
-__global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
+// STAR: *YOSO's estimator on derived codes (see launch_backward_star); its extra
+// operands run at one workgroup per CU.
+template <bool STAR>
+__global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassArgs a) {
     __shared__ __align__(16) unsigned char tiles_lds[kPassWaves * kTileBytes];
     __shared__ int32_t plan_beg[kPlanTiles];      // first partner of each row tile's bucket range
     __shared__ int32_t plan_x[kPlanTiles + 1];    // exclusive prefix of the tiles' sub-tile counts
@@ -600,6 +646,9 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
     const _Float16 *arow = (kside ? a.vs : a.dys) + b * n_r * (2 * D);
     const _Float16 *apar = (kside ? a.dys : a.vs) + b * n_p * (2 * D);
     const _Float16 *bpar = (kside ? a.qs : a.ks) + b * n_p * (2 * D);
+    const _Float16 *brow = (kside ? a.ks : a.qs) + b * n_r * (2 * D);  // *YOSO only
+    // *YOSO: x = (q 2^(13 - e_Q)) . (k 2^(13 - e_K)) * xscale
+    const float xscale = STAR ? ldexpf(1.0f, head_exp(a.pmax, b, 0) + head_exp(a.pmax, b, 2) - 26) : 0.f;
     // partial row (row r, hash h) starts r*m*64 elements past these bases, its
     // exponent r bytes past the other
     int16_t *part = (kside ? a.pk : a.pq) + ((b * n_r) * a.m + h) * D;
@@ -712,11 +761,15 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
                 int t;        // its tile (wave-uniform)
                 uint4 pe;     // entries of its partners 4q .. 4q+3
                 uint4 rw[4];  // its tile's rows, loaded when the tile starts here
+                uint4 rb[4];  // (*YOSO) the same rows' own b vectors
             };
             auto fill = [&](Slot &sl, int t, int y, bool new_tile) {
                 sl.t = t;
                 sl.pe = pent4(y);
-                if (new_tile) load_row_tile(sl.rw, row_entries4(t), arow, cl);
+                if (new_tile) {
+                    load_row_tile(sl.rw, row_entries4(t), arow, cl);
+                    if constexpr (STAR) load_row_tile(sl.rb, row_entries4(t), brow, cl);
+                }
             };
             Slot A, B, C;
             // the prefetch cursor: tile pt holds sub-tiles [plan_x[pt], pxe); sub-tile j
@@ -736,8 +789,9 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
                 fill(B, t1, y1, t1 != t0);
                 cursor_at(t1);
             }
-            half8 rh[2], rl[2];
+            half8 rh[2], rl[2], rbh[2], rbl[2];
             int erow = stage_rows(A.rw, tile, q, cl, g, c, rh, rl);  // ||a_c|| < 2^erow
+            if constexpr (STAR) stage_rows_b(A.rb, tile, q, cl, g, c, rbh, rbl);
             // one operand buffer: a sub-tile's registers are reloaded with the next
             // sub-tile as soon as they have been written to the tile
             Sub S;
@@ -759,15 +813,18 @@ __global__ __launch_bounds__(kPassThreads, 2) void pass_kernel(PassArgs a) {
                 fill(nn, t2, y2, has2 && t2 != nxt.t);
                 const bool newtile = !has1 || nxt.t != cur.t;
                 if (has1) load_sub(S, nxt.pe, apar, bpar, cl);
-                compute_sub(tile, cur.pe, rh, rl, static_cast<int>(row_entry(cur.t) >> 16), ldexpf(1.0f, -2 - erow), g,
-                            c, outT);
+                compute_sub<STAR>(tile, cur.pe, rh, rl, rbh, rbl, xscale, static_cast<int>(row_entry(cur.t) >> 16),
+                                  ldexpf(1.0f, -2 - erow), g, c, outT);
                 if (newtile) {
                     store_tile(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, tile_ents(cur.t), row_count(cur.t), q, cl,
                                g, c, outT, ldexpf(oscale, erow));
 #pragma unroll
                     for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
                     zero_tiles(cur.t + 1, has1 ? nxt.t : thi);
-                    if (has1) erow = stage_rows(nxt.rw, tile, q, cl, g, c, rh, rl);
+                    if (has1) {
+                        erow = stage_rows(nxt.rw, tile, q, cl, g, c, rh, rl);
+                        if constexpr (STAR) stage_rows_b(nxt.rb, tile, q, cl, g, c, rbh, rbl);
+                    }
                 }
                 return has1;
             };
@@ -938,10 +995,35 @@ hipError_t zero_output(void *out, int64_t bytes, hipStream_t stream) {
     return hipGetLastError();
 }
 
-hipError_t launch_pass(const PassArgs &a, int64_t units, hipStream_t stream) {
-    KernelTimer timer("pass_kernel", stream);
-    hipLaunchKernelGGL(pass_kernel, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0, stream, a);
+hipError_t launch_pass(const PassArgs &a, int64_t units, bool star, hipStream_t stream) {
+    if (star) {
+        KernelTimer timer("pass_star_kernel", stream);
+        hipLaunchKernelGGL(pass_kernel<true>, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0, stream,
+                           a);
+    } else {
+        KernelTimer timer("pass_kernel", stream);
+        hipLaunchKernelGGL(pass_kernel<false>, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0, stream,
+                           a);
+    }
     return hipGetLastError();
+}
+
+// *YOSO's derived codes: for every (row, hash h, bit t < tau) the code of hash h
+// with bit t removed, a (tau-1)-bit code: out[r][h*tau + t] = (c >> (t+1)) << t |
+// (c & (2^t - 1)).  Two rows collide under it exactly when their codes agree on
+// every bit but t, so the pair passes over these m*tau hashes count, per pair and
+// hash, the bits whose removal makes the codes agree.
+__global__ void drop_bit_kernel(const uint16_t *__restrict__ codes, uint16_t *__restrict__ out, int64_t rows, int m,
+                                int tau) {
+    const int64_t total = rows * m * tau;
+    for (int64_t e = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; e < total;
+         e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t r = e / (m * tau);
+        const int ht = static_cast<int>(e - r * m * tau);
+        const int h = ht / tau, t = ht - h * tau;
+        const uint32_t c = codes[r * m + h] & ((1u << tau) - 1u);
+        out[e] = static_cast<uint16_t>(((c >> (t + 1)) << t) | (c & ((1u << t) - 1u)));
+    }
 }
 
 }  // namespace
@@ -971,17 +1053,16 @@ BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, 
     return L;
 }
 
-hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
-                           const void *v, const void *dy, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m,
-                           int tau, void *dq, void *dk, void *dv, void *workspace, hipStream_t stream) {
+namespace {
+
+// dQ and dK from codes with m hashes of tau bits: bucket sort, per-head maxima,
+// the fp16 split, the pair passes (weights of *YOSO when `star`) and the hash sums.
+// `L` is backward_layout(bf16, bh, n_q, n_k, m, tau) within `ws`.
+hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k, const void *v,
+                        const void *dy, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m, int tau, float scale,
+                        bool star, void *dq, void *dk, const BackwardLayout &L, unsigned char *ws,
+                        hipStream_t stream) {
     hipError_t e;
-    const BackwardLayout L = backward_layout(bf16, bh, n_q, n_k, m, tau);
-    unsigned char *ws = static_cast<unsigned char *>(workspace);
-
-    // dV: the forward's table machinery with the roles of queries and keys swapped.
-    e = launch_table(qcodes, dy, kcodes, dv, bf16, bh, n_q, n_k, m, tau, ws + L.table, stream);
-    if (e != hipSuccess) return e;
-
     const int64_t units = bh * m;
     if (units == 0) return hipSuccess;
     const int64_t ebytes = bf16 ? 2 : 4;
@@ -1049,8 +1130,8 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
     a.eq = reinterpret_cast<int8_t *>(ws + L.eq);
     a.ek = reinterpret_cast<int8_t *>(ws + L.ek);
     a.bh = bh; a.m = m; a.tau = tau;
-    a.scale = static_cast<float>(tau) / (2.0f * static_cast<float>(m));
-    e = launch_pass(a, units, stream);
+    a.scale = scale;
+    e = launch_pass(a, units, star, stream);
     if (e != hipSuccess) return e;
     if (bf16) {
         if ((e = launch_reduce<true>(a.pq, a.lq, a.eq, dq, bh * n_q, n_q, m, stream)) != hipSuccess) return e;
@@ -1058,6 +1139,55 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
     }
     if ((e = launch_reduce<false>(a.pq, a.lq, a.eq, dq, bh * n_q, n_q, m, stream)) != hipSuccess) return e;
     return launch_reduce<false>(a.pk, a.lk, a.ek, dk, bh * n_k, n_k, m, stream);
+}
+
+}  // namespace
+
+hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
+                           const void *v, const void *dy, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m,
+                           int tau, void *dq, void *dk, void *dv, void *workspace, hipStream_t stream) {
+    const BackwardLayout L = backward_layout(bf16, bh, n_q, n_k, m, tau);
+    unsigned char *ws = static_cast<unsigned char *>(workspace);
+    // dV: the forward's table machinery with the roles of queries and keys swapped.
+    hipError_t e = launch_table(qcodes, dy, kcodes, dv, bf16, bh, n_q, n_k, m, tau, ws + L.table, stream);
+    if (e != hipSuccess) return e;
+    return launch_pairs(qcodes, kcodes, q, k, v, dy, bf16, bh, n_q, n_k, m, tau,
+                        static_cast<float>(tau) / (2.0f * static_cast<float>(m)), false, dq, dk, L, ws, stream);
+}
+
+StarLayout backward_star_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m, int tau) {
+    StarLayout S;
+    S.pairs = backward_layout(bf16, bh, n_q, n_k, m * tau, tau - 1);
+    size_t o = align_up(S.pairs.total);
+    S.qcodes = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m * tau * 2);
+    S.kcodes = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m * tau * 2);
+    S.table = o; o = align_up(o + table_workspace_bytes(bf16, bh, n_k, m, tau));
+    S.total = o;
+    return S;
+}
+
+hipError_t launch_backward_star(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
+                                const void *v, const void *dy, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m,
+                                int tau, void *dq, void *dk, void *dv, void *workspace, hipStream_t stream) {
+    const StarLayout S = backward_star_layout(bf16, bh, n_q, n_k, m, tau);
+    unsigned char *ws = static_cast<unsigned char *>(workspace);
+    // dV: eq. (gradient-v), as in launch_backward
+    hipError_t e = launch_table(qcodes, dy, kcodes, dv, bf16, bh, n_q, n_k, m, tau, ws + S.table, stream);
+    if (e != hipSuccess) return e;
+    uint16_t *qd = reinterpret_cast<uint16_t *>(ws + S.qcodes), *kd = reinterpret_cast<uint16_t *>(ws + S.kcodes);
+    for (int side = 0; side < 2; side++) {
+        const int64_t rows = bh * (side ? n_k : n_q);
+        if (rows == 0) continue;
+        const int64_t total = rows * m * tau;
+        KernelTimer timer("drop_bit_kernel", stream);
+        hipLaunchKernelGGL(drop_bit_kernel, dim3(elementwise_grid(total)), dim3(256), 0, stream, side ? kcodes : qcodes,
+                           side ? kd : qd, rows, m, tau);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    // the pairs of the m*tau derived (tau-1)-bit hashes, each weighted by
+    // 1/(pi sqrt(max(1 - x^2, 1/64))) and averaged over the m original hashes
+    return launch_pairs(qd, kd, q, k, v, dy, bf16, bh, n_q, n_k, m * tau, tau - 1, 1.0f / static_cast<float>(m), true,
+                        dq, dk, S.pairs, ws, stream);
 }
 
 }  // namespace yoso

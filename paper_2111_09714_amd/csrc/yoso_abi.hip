@@ -82,6 +82,7 @@ size_t required_workspace(yoso_op op, bool bf16, int64_t bh, int64_t n_q, int64_
         case YOSO_OP_HASH: return 0;
         case YOSO_OP_FORWARD: return yoso::table_workspace_bytes(bf16, bh, n_q, m, tau);
         case YOSO_OP_BACKWARD: return yoso::backward_layout(bf16, bh, n_q, n_k, m, tau).total;
+        case YOSO_OP_BACKWARD_STAR: return yoso::backward_star_layout(bf16, bh, n_q, n_k, m, tau).total;
     }
     return 0;
 }
@@ -153,7 +154,7 @@ size_t yoso_workspace_bytes(int op, int64_t bh, int64_t n_q, int64_t n_k, int32_
                             yoso_dtype dtype) {
     g_last_error[0] = '\0';
     const size_t bad = static_cast<size_t>(-1);
-    if (op != YOSO_OP_HASH && op != YOSO_OP_FORWARD && op != YOSO_OP_BACKWARD) {
+    if (op != YOSO_OP_HASH && op != YOSO_OP_FORWARD && op != YOSO_OP_BACKWARD && op != YOSO_OP_BACKWARD_STAR) {
         fail(YOSO_ERR_OP, "unknown op %d", op);
         return bad;
     }
@@ -241,6 +242,31 @@ yoso_status yoso_backward(const uint16_t *qcodes, const uint16_t *kcodes, const 
     return device_status(yoso::launch_backward(qcodes, kcodes, q, k, v, dy, bf16, bh, n_q, n_k, m, tau, dq, dk, dv,
                                                workspace, static_cast<hipStream_t>(stream)),
                          "yoso_backward");
+}
+
+yoso_status yoso_backward_star(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
+                               const void *v, const void *dy, yoso_dtype dtype, int64_t bh, int64_t n_q, int64_t n_k,
+                               int32_t d, int32_t m, int32_t tau, void *dq, void *dk, void *dv, void *workspace,
+                               size_t workspace_bytes, void *stream) {
+    g_last_error[0] = '\0';
+    YOSO_TRY(check_dtype(dtype));
+    YOSO_TRY(check_shape(bh, n_q, n_k, d, m * tau));
+    YOSO_TRY(check_hash(m, tau));
+    YOSO_TRY(check_ptr(qcodes, bh * m * n_q, "qcodes"));
+    YOSO_TRY(check_ptr(kcodes, bh * m * n_k, "kcodes"));
+    YOSO_TRY(check_ptr(q, bh * n_q * d, "q"));
+    YOSO_TRY(check_ptr(k, bh * n_k * d, "k"));
+    YOSO_TRY(check_ptr(v, bh * n_k * d, "v"));
+    YOSO_TRY(check_ptr(dy, bh * n_q * d, "dy"));
+    YOSO_TRY(check_ptr(dq, bh * n_q * d, "dq"));
+    YOSO_TRY(check_ptr(dk, bh * n_k * d, "dk"));
+    YOSO_TRY(check_ptr(dv, bh * n_k * d, "dv"));
+    const bool bf16 = dtype == YOSO_BF16;
+    YOSO_TRY(check_workspace(workspace, workspace_bytes,
+                             required_workspace(YOSO_OP_BACKWARD_STAR, bf16, bh, n_q, n_k, m, tau)));
+    return device_status(yoso::launch_backward_star(qcodes, kcodes, q, k, v, dy, bf16, bh, n_q, n_k, m, tau, dq, dk,
+                                                    dv, workspace, static_cast<hipStream_t>(stream)),
+                         "yoso_backward_star");
 }
 
 yoso_status yoso_backward_noalloc(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,

@@ -135,6 +135,41 @@ def test_noalloc_refuses_shapes_beyond_its_scratch(L):
     assert L.yoso_backward_noalloc(FAKE, None, *p[2:], 0, 1, 128, 128, 64, 32, 8, FAKE, FAKE, FAKE, None) == 1
 
 
+def _star(L, dtype=0, bh=2, nq=128, nk=128, d=64, m=32, tau=8, ws=FAKE, wsb=1 << 40, **ptrs):
+    p = dict(qc=FAKE, kc=FAKE, q=FAKE, k=FAKE, v=FAKE, dy=FAKE, dq=FAKE, dk=FAKE, dv=FAKE)
+    p.update(ptrs)
+    return L.yoso_backward_star(p["qc"], p["kc"], p["q"], p["k"], p["v"], p["dy"], dtype, bh, nq, nk, d, m, tau,
+                                p["dq"], p["dk"], p["dv"], ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=3), 4),
+    (dict(d=16), 2),
+    (dict(tau=13), 3),
+    (dict(m=64, tau=9), 3),
+    (dict(dk=None), 1),
+    (dict(q=FAKE + 2), 5),
+    (dict(ws=None), 6),
+    (dict(wsb=1024), 6),
+])
+def test_backward_star_rejects(L, kw, status):
+    assert _star(L, **kw) == status
+
+
+def test_backward_star_workspace():
+    """*YOSO runs the pair passes over m*tau derived hashes of tau-1 bits: its
+    workspace is the backward layout of those, plus the derived codes."""
+    bh, nq, nk, m, tau = 2, 512, 300, 32, 8
+    star = Y.yoso_workspace_bytes(Y.OP_BACKWARD_STAR, bh, nq, nk, 64, m, tau, Y.F32)
+    mh = m * tau                                           # derived hashes
+    partials = bh * (nq + nk) * mh * (64 * 3 + 1)          # 24-bit rows + exponents
+    index = bh * mh * (2 * (2 ** (tau - 1) + 1) * 4 + (nq + 16 + nk + 16) * 4)
+    split = 4 * bh * (nq + nk) // 2 * 64 * 4
+    codes = bh * (nq + nk) * mh * 2
+    need = partials + index + split + codes
+    assert need <= star < 1.02 * need + (1 << 16)
+
+
 def test_empty_tensors_need_no_pointers(L):
     # zero-sized tensors are valid and their pointers may be NULL; with every size 0
     # nothing is launched, so these calls return OK even without a GPU.
