@@ -19,6 +19,11 @@ describes the kernel with the largest total time.  For the dQ, dK pair kernel th
 is a matrix-unit roofline (3d multiply-adds per colliding pair, fp32 peak), with
 its HBM figures alongside.  The CPU baseline is the fp64
 oracle, timed on this machine's host cores on a stated sample of heads.
+
+The `configs` object repeats the step measurement (graph replay, fewer steps for
+the long sequences) for each of the five workloads, with the dominant kernel's
+roofline and a bounded oracle sample; `yoso_star` times the *YOSO backward on
+the bench workload.
 """
 from __future__ import annotations
 
@@ -111,8 +116,9 @@ def measured_traffic(kernel: str, workload: str):
         return None
 
 
-def cpu_baseline(w, inp, heads):
-    """Time the oracle (hash + forward + backward) on `heads`, one head per thread."""
+def cpu_baseline(w, inp, heads, min_wall: float = 10.0):
+    """Time the oracle (hash + forward + backward) on `heads`, one head per thread,
+    repeating the sample until `min_wall` seconds have been spent (at most 30 s)."""
     import oracle
     oracle._load()
     threads = min(len(os.sched_getaffinity(0)), len(heads))
@@ -123,7 +129,7 @@ def cpu_baseline(w, inp, heads):
     # repeat the sample until about 10 s of wall time have been spent (at most 30 s)
     reps, wall = 0, 0.0
     with concurrent.futures.ThreadPoolExecutor(max_workers=threads) as ex:
-        while reps == 0 or (wall < 10.0 and wall * (reps + 1) / reps < 30.0):
+        while reps == 0 or (wall < min_wall and wall * (reps + 1) / reps < 30.0):
             t0 = time.perf_counter()
             list(ex.map(one, heads))
             wall += time.perf_counter() - t0
@@ -139,75 +145,53 @@ def cpu_baseline(w, inp, heads):
     }
 
 
-def main() -> int:
-    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="lra_n4096")
-    ap.add_argument("--cpu-heads", type=int, default=-1, help="heads in the oracle sample (-1: all)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--copy-calibration", action="store_true",
-                    help="after the timed steps, run a plain 256 MiB device copy (read + write) three times, "
-                         "so that a counter run sees a kernel of known traffic")
-    args = ap.parse_args()
+STEP_KERNELS = ("hash_kernel", "table_kernel", "sort_kernel", "absmax_kernel", "split_kernel", "pass_kernel",
+                "reduce_kernel", "zero_kernel")
 
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): "
-              "the (batch, head) units of YOSO attention are independent, so N GPUs would each run "
-              "this same kernel sequence on BH/N heads with no communication.", file=sys.stderr)
-        return 2
 
-    import numpy as np
-    import torch
-
-    import paper_2111_09714_amd as Y
-    from workloads import WORKLOADS, make_inputs
-
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        return 1
-    w = WORKLOADS[args.workload]
-    inp = make_inputs(w)
+def make_step(Y, torch, w, inp, dev):
+    """Device tensors of workload `w` and the step (hash Q, hash K, forward, backward)."""
     tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
-    dev = torch.device("cuda:0")
-    q, k, v, dy = (torch.from_numpy(inp[s]).to(dev).to(tdt).contiguous() for s in ("q", "k", "v", "dy"))
-    R = torch.from_numpy(inp["R"]).to(dev)
-    qc = torch.empty((w.bh, w.n, w.m), dtype=torch.int16, device=dev)
-    kc = torch.empty_like(qc)
-    y = torch.empty_like(q)
-    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
-    ws_f = Y.workspace(Y.OP_FORWARD, q, w.m, w.tau)
-    ws_b = Y.workspace(Y.OP_BACKWARD, q, w.m, w.tau)
-    stream = torch.cuda.current_stream()
+    t = {s: torch.from_numpy(inp[s]).to(dev).to(tdt).contiguous() for s in ("q", "k", "v", "dy")}
+    t["R"] = torch.from_numpy(inp["R"]).to(dev)
+    t["qc"] = torch.empty((w.bh, w.n, w.m), dtype=torch.int16, device=dev)
+    t["kc"] = torch.empty_like(t["qc"])
+    t["y"] = torch.empty_like(t["q"])
+    t["dq"], t["dk"], t["dv"] = torch.empty_like(t["q"]), torch.empty_like(t["k"]), torch.empty_like(t["v"])
+    t["ws_f"] = Y.workspace(Y.OP_FORWARD, t["q"], w.m, w.tau)
+    t["ws_b"] = Y.workspace(Y.OP_BACKWARD, t["q"], w.m, w.tau)
 
     def step(s):
-        Y.yoso_hash(q, R, w.m, w.tau, qc, s)
-        Y.yoso_hash(k, R, w.m, w.tau, kc, s)
-        Y.yoso_forward(qc, kc, v, w.m, w.tau, y, ws_f, s)
-        Y.yoso_backward(qc, kc, q, k, v, dy, w.m, w.tau, dq, dk, dv, ws_b, s)
+        Y.yoso_hash(t["q"], t["R"], w.m, w.tau, t["qc"], s)
+        Y.yoso_hash(t["k"], t["R"], w.m, w.tau, t["kc"], s)
+        Y.yoso_forward(t["qc"], t["kc"], t["v"], w.m, w.tau, t["y"], t["ws_f"], s)
+        Y.yoso_backward(t["qc"], t["kc"], t["q"], t["k"], t["v"], t["dy"], w.m, w.tau, t["dq"], t["dk"], t["dv"],
+                        t["ws_b"], s)
+    return t, step
 
+
+def time_step(Y, torch, step, steps, warmup):
+    """(eager ms per step, per-kernel timings, graph-replay ms per step, execution mode)."""
+    stream = torch.cuda.current_stream()
     # per-kernel durations: eager steps with the library's HIP-event timer on
-    Y.yoso_timing_enable(4 * (args.steps + args.warmup) + 8)
-    for _ in range(args.warmup):
+    Y.yoso_timing_enable(4 * (steps + warmup) + 8)
+    for _ in range(warmup):
         step(stream)
     torch.cuda.synchronize()
     Y.yoso_timing_reset()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record(stream)
-    for _ in range(args.steps):
+    for _ in range(steps):
         step(stream)
     stop.record(stream)
     torch.cuda.synchronize()
-    eager_ms_per_step = start.elapsed_time(stop) / args.steps
+    eager_ms_per_step = start.elapsed_time(stop) / steps
     kernels = {}
-    for name in ("hash_kernel", "table_kernel", "sort_kernel", "split_kernel", "pass_kernel", "reduce_kernel",
-                 "zero_kernel"):
+    for name in STEP_KERNELS:
         tot, n = Y.yoso_timing_query(name)
         if n:
-            kernels[name] = {"launches_per_step": n / args.steps, "avg_us": 1000.0 * tot / n,
-                             "share_of_step": tot / (eager_ms_per_step * args.steps)}
+            kernels[name] = {"launches_per_step": n / steps, "avg_us": 1000.0 * tot / n,
+                             "share_of_step": tot / (eager_ms_per_step * steps)}
     Y.yoso_timing_enable(0)
 
     # The timed run: the step captured once into a HIP graph (stream capture; the
@@ -229,17 +213,21 @@ def main() -> int:
     except Exception as exc:  # report and time eagerly
         execution = f"eager (graph capture failed: {type(exc).__name__})"
         run = lambda: step(stream)  # noqa: E731
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         run()
     torch.cuda.synchronize()
     start.record(stream)
-    for _ in range(args.steps):
+    for _ in range(steps):
         run()
     stop.record(stream)
     torch.cuda.synchronize()
-    ms_total = start.elapsed_time(stop)
-    ms_per_step = ms_total / args.steps
+    return eager_ms_per_step, kernels, start.elapsed_time(stop) / steps, execution
 
+
+def dominant_roofline(w, kernels, qc, kc):
+    """Roofline of the kernel with the largest time per step: HBM for the streaming
+    kernels, the fp32 matrix peak for the pair kernel (3d multiply-adds per colliding
+    pair, counted exactly from the codes) with its HBM figures alongside."""
     dominant = max(kernels, key=lambda kname: kernels[kname]["avg_us"] * kernels[kname]["launches_per_step"])
     alg = kernel_algorithmic(w, dominant)
     avg_s = kernels[dominant]["avg_us"] * 1e-6
@@ -263,9 +251,139 @@ def main() -> int:
                     "avg_launch_us": round(kernels[dominant]["avg_us"], 2),
                     "hbm": {"achieved": hbm["achieved"], "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": hbm["frac"],
                             "algorithmic_bytes_per_launch": alg}}
-
     if roofline is not None:
         roofline["traffic"] = measured_traffic(dominant, w.name)
+    return roofline
+
+
+# Steps and warm-up steps per workload in the `configs` object (the long
+# sequences take tens of milliseconds per step).
+CONFIG_STEPS = {"single_head_n512": (20, 5), "bert_base_n512": (10, 3), "lra_n4096": (10, 3),
+                "skewed_n16384": (4, 1), "bf16_n32768": (4, 1)}
+
+
+def measure_configs(Y, torch, dev, cpu: bool):
+    """The step on every workload: graph-replayed time, tokens/s, HBM fraction, the
+    dominant kernel's roofline, the kernel table, and the oracle on a sample of heads."""
+    from workloads import WORKLOADS, make_inputs
+    out = {}
+    for name, (steps, warmup) in CONFIG_STEPS.items():
+        w = WORKLOADS[name]
+        inp = make_inputs(w)
+        t, step = make_step(Y, torch, w, inp, dev)
+        _, kernels, ms, execution = time_step(Y, torch, step, steps, warmup)
+        alg = 11 * w.n * w.d * w.elem_bytes * w.bh
+        entry = {"config": {"batch": w.batch, "heads": w.heads, "seq_len": w.n, "tau": w.tau, "hashes": w.m,
+                            "dtype": w.dtype, "inputs": w.dist},
+                 "steps": steps, "ms_per_step": round(ms, 4), "execution": execution,
+                 "tokens_per_s": round(w.tokens / (ms * 1e-3), 1),
+                 "hbm_roofline_frac": round(alg / (ms * 1e-3) / (HBM_PEAK_GBS * 1e9), 4),
+                 "roofline": dominant_roofline(w, kernels, t["qc"], t["kc"]),
+                 "kernels": {kn: {"launches_per_step": round(kv["launches_per_step"], 2),
+                                  "avg_us": round(kv["avg_us"], 2)} for kn, kv in kernels.items()}}
+        del t, step
+        torch.cuda.empty_cache()
+        if cpu:
+            # one oracle pass over as many heads as there are cores (at most the head
+            # count; long sequences: 4 heads), scaled to all heads
+            cores = len(os.sched_getaffinity(0))
+            nh = min(w.bh, cores, 4 if w.n > 4096 else cores)
+            entry["cpu_baseline"] = cpu_baseline(w, inp, list(range(nh)), min_wall=0.0)
+        out[name] = entry
+        del inp
+    return out
+
+
+def star_timing(Y, torch, w, t, stream):
+    """*YOSO's backward (yoso_backward_star) on the bench workload, outside the timed
+    step: its pair kernel runs over the m*tau derived hashes (pairs whose codes agree
+    on all bits but at most one); 8d flops per derived pair (s = dy.v and x = q.k,
+    then the dQ and the dK share)."""
+    import numpy as np
+    ws = Y.workspace(Y.OP_BACKWARD_STAR, t["q"], w.m, w.tau)
+    dq, dk, dv = torch.empty_like(t["q"]), torch.empty_like(t["k"]), torch.empty_like(t["v"])
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def call():
+        Y.yoso_backward_star(t["qc"], t["kc"], t["q"], t["k"], t["v"], t["dy"], w.m, w.tau, dq, dk, dv, ws, stream)
+
+    call()
+    torch.cuda.synchronize()
+    Y.yoso_timing_enable(64)
+    start.record(stream)
+    for _ in range(3):
+        call()
+    stop.record(stream)
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / 3
+    tot, n = Y.yoso_timing_query("pass_star_kernel")
+    Y.yoso_timing_enable(0)
+    # pairs of the derived hashes (code minus bit t), counted from the codes
+    B = 1 << (w.tau - 1)
+    qc = t["qc"].cpu().numpy().astype(np.int64) & ((1 << w.tau) - 1)
+    kc = t["kc"].cpu().numpy().astype(np.int64) & ((1 << w.tau) - 1)
+    bh, _, m = qc.shape
+    unit = (np.arange(bh)[:, None, None] * m + np.arange(m)[None, None, :]) * B
+    pairs = 0
+    for bit in range(w.tau):
+        low = (1 << bit) - 1
+        qd = ((qc >> (bit + 1)) << bit) | (qc & low)
+        kd = ((kc >> (bit + 1)) << bit) | (kc & low)
+        hq = np.bincount((unit + qd).ravel(), minlength=bh * m * B)
+        hk = np.bincount((unit + kd).ravel(), minlength=bh * m * B)
+        pairs += int((hq * hk).sum())
+    del ws, dq, dk, dv
+    out = {"ms_per_backward": round(ms, 3), "derived_pairs": pairs}
+    if n:
+        avg_s = tot / n * 1e-3
+        tf = 8 * w.d * pairs / avg_s / 1e12
+        out["pass_star_kernel"] = {"avg_us": round(avg_s * 1e6, 1), "bound": "mfma", "achieved": round(tf, 2),
+                                   "peak": FP32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                   "frac": round(tf / FP32_PEAK_TFLOPS, 4),
+                                   "algorithmic_flops_per_launch": 8 * w.d * pairs}
+    return out
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="lra_n4096")
+    ap.add_argument("--cpu-heads", type=int, default=-1, help="heads in the oracle sample (-1: all)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true", help="skip the per-workload `configs` object")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed steps, run a plain 256 MiB device copy (read + write) three times, "
+                         "so that a counter run sees a kernel of known traffic")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): "
+              "the (batch, head) units of YOSO attention are independent, so N GPUs would each run "
+              "this same kernel sequence on BH/N heads with no communication.", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2111_09714_amd as Y
+    from workloads import WORKLOADS, make_inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    w = WORKLOADS[args.workload]
+    inp = make_inputs(w)
+    dev = torch.device("cuda:0")
+    t, step = make_step(Y, torch, w, inp, dev)
+    q, k, v, dy, qc, kc = (t[s] for s in ("q", "k", "v", "dy", "qc", "kc"))
+    stream = torch.cuda.current_stream()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    eager_ms_per_step, kernels, ms_per_step, execution = time_step(Y, torch, step, args.steps, args.warmup)
+    roofline = dominant_roofline(w, kernels, qc, kc)
+    star = star_timing(Y, torch, w, t, stream)
 
     # the l2 row normalisation (N-YOSO output / Q, K prologue) on this workload's Q
     # rows, outside the timed step: HBM-bound, algorithmic bytes = rows read + written
@@ -416,7 +534,12 @@ def main() -> int:
         "l2_normalize": l2,
         "yoso_e": expect,
         "fast_hash": fast,
+        "yoso_star": star,
     }
+    if not args.no_configs:
+        del t, step, q, k, v, dy, qc, kc
+        torch.cuda.empty_cache()
+        out["configs"] = measure_configs(Y, torch, dev, cpu=not args.no_cpu_baseline)
     print(json.dumps(out), flush=True)
     return 0
 
