@@ -146,7 +146,7 @@ def cpu_baseline(w, inp, heads, min_wall: float = 10.0):
 
 
 STEP_KERNELS = ("hash_kernel", "table_kernel", "sort_kernel", "absmax_kernel", "split_kernel", "pass_kernel",
-                "reduce_kernel", "zero_kernel")
+                "reduce_kernel", "dense_kernel", "zero_kernel")
 
 
 def make_step(Y, torch, w, inp, dev):
@@ -251,6 +251,15 @@ def dominant_roofline(w, kernels, qc, kc):
                     "avg_launch_us": round(kernels[dominant]["avg_us"], 2),
                     "hbm": {"achieved": hbm["achieved"], "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": hbm["frac"],
                             "algorithmic_bytes_per_launch": alg}}
+    if dominant == "dense_kernel":
+        # short sequences: dQ, dK and dV as dense blocks over every (query, key) pair,
+        # 5 d multiply-adds per pair (dy.v once for each of the two sides, then its
+        # shares of dQ, dK and the count-weighted dV), in fp32
+        flops = 10 * w.d * w.n * w.n * w.bh
+        tf = flops / avg_s / 1e12
+        roofline = {"kernel": dominant, "bound": "mfma", "achieved": round(tf, 2), "peak": FP32_PEAK_TFLOPS,
+                    "unit": "TFLOP/s", "frac": round(tf / FP32_PEAK_TFLOPS, 4), "traffic": None,
+                    "algorithmic_flops_per_launch": flops, "avg_launch_us": round(kernels[dominant]["avg_us"], 2)}
     if roofline is not None:
         roofline["traffic"] = measured_traffic(dominant, w.name)
     return roofline

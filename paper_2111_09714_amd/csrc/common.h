@@ -87,6 +87,18 @@ __device__ __forceinline__ void split4(const float v[4], float scale, half4 &hi,
     }
 }
 
+// split4 for a power-of-two `scale`: v * scale is exact, so rounding the product to
+// fp16 once or through fp32 gives the same hi, and the operand barrier is not needed.
+__device__ __forceinline__ void split4_pow2(const float v[4], float scale, half4 &hi, half4 &lo) {
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        const float s = v[i] * scale;
+        const _Float16 h = static_cast<_Float16>(s);
+        hi[i] = h;
+        lo[i] = static_cast<_Float16>(s - static_cast<float>(h));
+    }
+}
+
 // Three-product fp16 emulation of an fp32 MFMA step: acc += a*b.
 __device__ __forceinline__ floatx4 mfma3_16x16x32(const half8 &ah, const half8 &al, const half8 &bh,
                                                   const half8 &bl, floatx4 acc) {

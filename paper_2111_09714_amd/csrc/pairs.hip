@@ -500,7 +500,10 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uin
     }
     // the row's factor 2^-(2 + e_c): |S| < 2^14 (see the header), hi and lo stay normal
     half4 sh, sl;
-    split4(sv, sfac, sh, sl);
+    if constexpr (STAR)
+        split4(sv, sfac, sh, sl);  // sv carries the weight, a product of its own
+    else
+        split4_pow2(sv, sfac, sh, sl);
     // out^T += B_y^T S^T (hi*hi + hi*lo + lo*hi), the four dim blocks interleaved
 #pragma unroll
     for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(bth[dt], sh, outT[dt], 0, 0, 0);
@@ -966,6 +969,308 @@ __global__ void zero_kernel(uint32_t *__restrict__ p, int64_t count) {
         p[e] = 0u;
 }
 
+// ---------------------------------------------------------------- dense form (short sequences)
+// eq. (pseudo-gradient-q) with the hashes summed first: C = sum_h B_h (C_ij is the
+// number of hashes under which q_i and k_j collide), then
+//   dQ = tau/(2m) [(dY V^T) .* C] K,     dK = tau/(2m) [(dY V^T) .* C]^T Q,
+// every (query, key) pair of a head visited once in dense 16 x 16 MFMA blocks.
+// With a few rows per bucket (short sequences) the pair tiles above are nearly
+// empty; this form does n_q n_k (2d + d) multiply-adds per side with full tiles,
+// needs no fp16 copies, no partial rows and no reduction.
+//
+// One workgroup (4 waves) per (head, 64 fixed rows, side), both sides in one
+// launch.  dQ: fixed = queries (a = dY), streamed = keys (g = V, y = K); dK: fixed =
+// keys (a = V), streamed = queries (g = dY, y = Q), and there also dV = (1/m) C^T dY
+// from the same staged dY rows (eq. gradient-v with the hashes summed first).
+//   1. C[fixed row][streamed row] as bytes in LDS from the streamed side's bucket
+//      lists (sort_kernel): for each fixed row and hash, +1 at every streamed row
+//      of the fixed row's bucket (counts <= m <= 64 fit a byte).
+//   2. the fixed rows' a in the MFMA B layout, each row scaled by 2^(13 - e_a).
+//   3. streamed tiles of 64 rows: g and y rows staged in LDS, each tile scaled by
+//      2^(13 - e) from its largest |value|; per 16 x 16 block G^T = g a^T (three
+//      fp16 products), W = G .* C tau/(2m) 2^-(16 + k), out^T += y^T W.  The
+//      accumulators are rescaled exactly when a tile's scales change.
+constexpr int kDenseRows = 64;     // fixed rows per workgroup (16 per wave)
+constexpr int kDenseTile = 64;     // streamed rows per LDS tile
+constexpr int kDenseMaxN = 1024;   // streamed rows whose counts fit in LDS
+
+// u32 words per fixed row of the count matrix: a multiple of 64 plus 4, so that
+// the 16 rows x 4 words a block reads (rows c, words 4g / 4 + ...) hit distinct banks
+__host__ __device__ constexpr int dense_stride(int64_t n_s) {
+    return static_cast<int>(((n_s + 3) / 4 + 63) / 64 * 64 + 4);
+}
+
+struct DenseSide {
+    const uint16_t *fcodes;  // fixed side's codes [bh][n_f][m]
+    const uint32_t *sent;    // streamed side's sorted entries [bh*m][ent_stride(n_s)]
+    const int32_t *soff;     // streamed side's bucket offsets [bh*m][2^tau + 1]
+    const void *fa;          // fixed side's a rows [bh][n_f][64]
+    const void *sg, *sy;     // streamed side's g rows and y rows [bh][n_s][64]
+    void *out;               // [bh][n_f][64]: dQ or dK
+    void *out2;              // [bh][n_f][64]: dV (key side), else nullptr
+    int64_t n_f, n_s;
+};
+
+struct DenseArgs {
+    DenseSide side[2];       // 0: dQ (queries fixed), 1: dK and dV (keys fixed)
+    int64_t bh;
+    int m, tau;
+};
+
+template <bool BF16>
+__device__ __forceinline__ void dense_store(void *dst, int64_t off, const floatx4 &o, float sc) {
+    if constexpr (BF16) {
+        uint2 w2;
+        w2.x = static_cast<uint32_t>(f32_to_bf16(o[0] * sc)) | (static_cast<uint32_t>(f32_to_bf16(o[1] * sc)) << 16);
+        w2.y = static_cast<uint32_t>(f32_to_bf16(o[2] * sc)) | (static_cast<uint32_t>(f32_to_bf16(o[3] * sc)) << 16);
+        *reinterpret_cast<uint2 *>(static_cast<uint16_t *>(dst) + off) = w2;
+    } else {
+        *reinterpret_cast<float4 *>(static_cast<float *>(dst) + off) =
+            make_float4(o[0] * sc, o[1] * sc, o[2] * sc, o[3] * sc);
+    }
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
+    extern __shared__ __align__(16) uint32_t cnt[];  // [kDenseRows][dense_stride(n_s)]
+    __shared__ __align__(16) unsigned char g_lds[kDenseTile * 256];
+    __shared__ __align__(16) unsigned char y_lds[kDenseTile * 256];
+    __shared__ float tmax[8];
+
+    // blocks of side 0, then side 1 (both sides' tile counts)
+    const int64_t t0 = (args.side[0].n_f + kDenseRows - 1) / kDenseRows;
+    const int64_t t1 = (args.side[1].n_f + kDenseRows - 1) / kDenseRows;
+    const int64_t blk = xcd_remap(blockIdx.x, args.bh * (t0 + t1));
+    const bool kside = blk >= args.bh * t0;
+    const DenseSide a = args.side[kside ? 1 : 0];
+    const int64_t tiles_f = kside ? t1 : t0;
+    const int64_t lblk = kside ? blk - args.bh * t0 : blk;
+    const int64_t b = lblk / tiles_f;
+    const int r0 = static_cast<int>(lblk - b * tiles_f) * kDenseRows;
+    const int m = args.m, tau = args.tau;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, c = lane & 15;
+    const int stride = dense_stride(a.n_s);
+    const int nf = static_cast<int>(a.n_f), ns = static_cast<int>(a.n_s);
+
+    // ---- 1. collision counts.  Items (fixed row, hash) in groups of eight per
+    // thread: their codes, then their bucket ranges, then the entries, each stage's
+    // loads all in flight before the next stage uses them.
+    for (int e = tid; e < kDenseRows * stride; e += 256) cnt[e] = 0u;
+    __syncthreads();
+    {
+        const int B = 1 << tau;
+        const int64_t es = ent_stride(a.n_s);
+        const int items = kDenseRows * m;
+        constexpr int U = 8;
+        for (int i0 = tid; i0 < items; i0 += 256 * U) {
+            int beg[U], len[U], r[U];
+            int64_t unit[U];
+            int code[U];
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int item = min(i0 + 256 * u, items - 1);
+                r[u] = item / m;
+                const int h = item - r[u] * m;
+                unit[u] = b * m + h;
+                code[u] = a.fcodes[(b * a.n_f + min(r0 + r[u], nf - 1)) * m + h] & (B - 1);
+            }
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int32_t *off = a.soff + unit[u] * (B + 1) + code[u];
+                beg[u] = off[0];
+                len[u] = off[1];
+            }
+            int most = 0;
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const bool ok = i0 + 256 * u < items && r0 + r[u] < nf;
+                len[u] = ok ? len[u] - beg[u] : 0;
+                most = max(most, len[u]);
+            }
+            for (int p = 0; p < most; p++) {
+                uint32_t j[U];
+#pragma unroll
+                for (int u = 0; u < U; u++) j[u] = a.sent[unit[u] * es + beg[u] + min(p, max(len[u] - 1, 0))];
+#pragma unroll
+                for (int u = 0; u < U; u++) {
+                    if (p < len[u]) {
+                        const uint32_t jj = j[u] & 0xFFFFu;
+                        atomicAdd(&cnt[r[u] * stride + (jj >> 2)], 1u << (8 * (jj & 3)));
+                    }
+                }
+            }
+        }
+    }
+
+    // ---- 2. the fixed rows' a: lane (g, c) holds row r0 + 16 wave + c, dims kb*32 + 8g + [0, 8)
+    const int frow = r0 + wave * 16 + c;
+    half8 arh[2], arl[2];
+    int ea = 0;
+    {
+        float y[2][8];
+        const int64_t off = (b * a.n_f + min(frow, nf - 1)) * D;
+        load8<BF16>(a.fa, off + 8 * g, y[0]);
+        load8<BF16>(a.fa, off + 32 + 8 * g, y[1]);
+        float mx = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 2; kb++)
+#pragma unroll
+            for (int i = 0; i < 8; i++) mx = fmaxf(mx, fabsf(y[kb][i]));
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        ea = pow2_above(mx);
+#pragma unroll
+        for (int kb = 0; kb < 2; kb++) split8(y[kb], ldexpf(1.0f, 13 - ea), arh[kb], arl[kb]);
+    }
+
+    // ---- 3. streamed tiles.  Staging: lane l of wave w stages row 16w + (l & 15),
+    // dims 16 (l >> 4) + [0, 16) (a quarter-wave writes 16 rows at one chunk).
+    const int lrow = 16 * wave + (lane & 15), lq = lane >> 4;
+    auto load_row = [&](const void *src, int c0, float x[16]) {
+        const int row = c0 + lrow;
+        const int64_t off = (b * a.n_s + min(row, ns - 1)) * D + 16 * lq;
+        load8<BF16>(src, off, x);
+        load8<BF16>(src, off + 8, x + 8);
+        const bool ok = row < ns;
+        float mx = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; i++) {
+            x[i] = ok ? x[i] : 0.f;
+            mx = fmaxf(mx, fabsf(x[i]));
+        }
+        return mx;
+    };
+    auto put_row = [&](unsigned char *dst, const float x[16], float scale) {
+        half8 h[2], l[2];
+        split8(x, scale, h[0], l[0]);
+        split8(x + 8, scale, h[1], l[1]);
+#pragma unroll
+        for (int u = 0; u < 2; u++) {
+            *reinterpret_cast<half8 *>(dst + swz(lrow, 2 * lq + u, 256)) = h[u];
+            *reinterpret_cast<half8 *>(dst + swz(lrow, 8 + 2 * lq + u, 256)) = l[u];
+        }
+    };
+    const int pr = 4 * g + (c >> 2), a4 = c & 3;
+    const floatx4 z4 = {0.f, 0.f, 0.f, 0.f};
+    floatx4 out[4], out2[4];
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++) out[dt] = out2[dt] = z4;
+    // tau/(2m) G C is scaled by 2^-(16 + k), 2^k >= tau: |G| < 2^32 after the row and
+    // tile scalings and C <= m, so the weight stays below 2^15; dV's weight C/m is
+    // scaled by 2^15 (at most 2^15)
+    int k2 = 0;
+    while ((1 << k2) < tau) k2++;
+    const float wgd = static_cast<float>(tau) / (2.0f * static_cast<float>(m)) * ldexpf(1.0f, -(16 + k2));
+    const float wvd = 32768.0f / static_cast<float>(m);
+    const bool with_dv = a.out2 != nullptr;
+    const uint32_t *crow = cnt + (16 * wave + c) * stride;  // the lane's fixed row of counts
+    int eg = 0, ey = 0;
+    for (int c0 = 0; c0 < ns; c0 += kDenseTile) {
+        __syncthreads();  // counts complete (first tile); the previous tile has been read
+        float xg[16], xy[16];
+        float mg = load_row(a.sg, c0, xg);
+        float my = load_row(a.sy, c0, xy);
+        mg = wave_max(mg);
+        my = wave_max(my);
+        if (lane == 0) {
+            tmax[wave] = mg;
+            tmax[4 + wave] = my;
+        }
+        __syncthreads();
+        const int eg_new = pow2_above(fmaxf(fmaxf(tmax[0], tmax[1]), fmaxf(tmax[2], tmax[3])));
+        const int ey_new = pow2_above(fmaxf(fmaxf(tmax[4], tmax[5]), fmaxf(tmax[6], tmax[7])));
+        put_row(g_lds, xg, ldexpf(1.0f, 13 - eg_new));
+        put_row(y_lds, xy, ldexpf(1.0f, 13 - ey_new));
+        if (c0 > 0) {
+            const float f = ldexpf(1.0f, eg + ey - eg_new - ey_new), f2 = ldexpf(1.0f, eg - eg_new);
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) {
+                out[dt] *= f;
+                out2[dt] *= f2;
+            }
+        }
+        eg = eg_new;
+        ey = ey_new;
+        __syncthreads();
+#pragma unroll 1
+        for (int cb = 0; cb < kDenseTile / 16; cb++) {
+            if (c0 + 16 * cb >= ns) break;
+            // G^T block: lane (g, c) = (g row c0 + 16cb + 4g + i) . (a row c)
+            half8 bh[2], bl[2];
+#pragma unroll
+            for (int kb = 0; kb < 2; kb++) {
+                bh[kb] = lds_ld<half8>(g_lds, swz(16 * cb + c, kb * 4 + g, 256));
+                bl[kb] = lds_ld<half8>(g_lds, swz(16 * cb + c, 8 + kb * 4 + g, 256));
+            }
+            floatx4 s0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(bh[0], arh[0], z4, 0, 0, 0);
+            floatx4 s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(bh[1], arh[1], z4, 0, 0, 0);
+            s0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(bh[0], arl[0], s0, 0, 0, 0);
+            s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(bh[1], arl[1], s1, 0, 0, 0);
+            s0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(bl[0], arh[0], s0, 0, 0, 0);
+            s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(bl[1], arh[1], s1, 0, 0, 0);
+            const floatx4 gt = s0 + s1;
+            // counts of streamed rows c0 + 16cb + 4g .. +3 against the lane's fixed row
+            const uint32_t cw = crow[(c0 + 16 * cb + 4 * g) >> 2];
+            float w[4];
+#pragma unroll
+            for (int i = 0; i < 4; i++) w[i] = gt[i] * static_cast<float>((cw >> (8 * i)) & 0xFFu) * wgd;
+            half4 wh, wl;
+            split4(w, 1.0f, wh, wl);
+            // y^T of the block as the A operand (lane (g, c): dim 16dt + c, rows 4g .. 4g+3)
+            half4 yh[4], yl[4];
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) {
+                yh[dt] = tr_load(y_lds + swz(16 * cb + pr, 2 * dt + (a4 >> 1), 256) + 8 * (a4 & 1));
+                yl[dt] = tr_load(y_lds + swz(16 * cb + pr, 8 + 2 * dt + (a4 >> 1), 256) + 8 * (a4 & 1));
+            }
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) out[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(yh[dt], wh, out[dt], 0, 0, 0);
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) out[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(yh[dt], wl, out[dt], 0, 0, 0);
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) out[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(yl[dt], wh, out[dt], 0, 0, 0);
+            if (with_dv) {
+                // dV^T += dY^T (C / m) 2^15: the staged g rows are dY on this side
+                float wv[4];
+#pragma unroll
+                for (int i = 0; i < 4; i++) wv[i] = static_cast<float>((cw >> (8 * i)) & 0xFFu) * wvd;
+                half4 vh, vl;
+                split4(wv, 1.0f, vh, vl);
+                half4 gh[4], gl[4];
+#pragma unroll
+                for (int dt = 0; dt < 4; dt++) {
+                    gh[dt] = tr_load(g_lds + swz(16 * cb + pr, 2 * dt + (a4 >> 1), 256) + 8 * (a4 & 1));
+                    gl[dt] = tr_load(g_lds + swz(16 * cb + pr, 8 + 2 * dt + (a4 >> 1), 256) + 8 * (a4 & 1));
+                }
+#pragma unroll
+                for (int dt = 0; dt < 4; dt++)
+                    out2[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(gh[dt], vh, out2[dt], 0, 0, 0);
+#pragma unroll
+                for (int dt = 0; dt < 4; dt++)
+                    out2[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(gh[dt], vl, out2[dt], 0, 0, 0);
+#pragma unroll
+                for (int dt = 0; dt < 4; dt++)
+                    out2[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(gl[dt], vh, out2[dt], 0, 0, 0);
+            }
+        }
+    }
+
+    // ---- 4. out = acc 2^(16 + k) (a row 2^(13 - e_a)) (g tile 2^(13 - e_g)) (y tile 2^(13 - e_y));
+    // dV = acc2 2^-15 (g tile 2^(13 - e_g)); lane (g, c) holds out[fixed row c][16dt + 4g + i]
+    if (frow < nf) {
+        const float sc = ldexpf(1.0f, 16 + k2 + ea - 13 + eg - 13 + ey - 13);
+        const float sc2 = ldexpf(1.0f / 32768.0f, eg - 13);
+#pragma unroll
+        for (int dt = 0; dt < 4; dt++) {
+            const int64_t off = (b * a.n_f + frow) * D + 16 * dt + 4 * g;
+            dense_store<BF16>(a.out, off, out[dt], sc);
+            if (with_dv) dense_store<BF16>(a.out2, off, out2[dt], sc2);
+        }
+    }
+}
+
 unsigned elementwise_grid(int64_t count) {
     const int64_t blocks = (count + 255) / 256;
     return static_cast<unsigned>(blocks < 8192 ? (blocks > 0 ? blocks : 1) : 8192);
@@ -1055,12 +1360,17 @@ BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, 
 
 namespace {
 
+// The dense form serves short sequences (both sides at most kDenseMaxN rows);
+// *YOSO always takes the pair passes.
+bool dense_form(int64_t n_q, int64_t n_k, bool star) { return !star && n_q <= kDenseMaxN && n_k <= kDenseMaxN; }
+
 // dQ and dK from codes with m hashes of tau bits: bucket sort, per-head maxima,
-// the fp16 split, the pair passes (weights of *YOSO when `star`) and the hash sums.
-// `L` is backward_layout(bf16, bh, n_q, n_k, m, tau) within `ws`.
+// the fp16 split, the pair passes (weights of *YOSO when `star`) and the hash sums;
+// for short sequences the dense form instead, which also writes dV.  `L` is
+// backward_layout(bf16, bh, n_q, n_k, m, tau) within `ws`.
 hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k, const void *v,
                         const void *dy, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m, int tau, float scale,
-                        bool star, void *dq, void *dk, const BackwardLayout &L, unsigned char *ws,
+                        bool star, void *dq, void *dk, void *dv, const BackwardLayout &L, unsigned char *ws,
                         hipStream_t stream) {
     hipError_t e;
     const int64_t units = bh * m;
@@ -1092,6 +1402,33 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
                                m, n_q, n_k, tau, stage, qo, ko, qe, ke);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
+
+    if (dense_form(n_q, n_k, star)) {
+        // short sequences: dQ, dK (and dV) from dense blocks masked by the collision counts
+        DenseArgs d;
+        for (int side = 0; side < 2; side++) {
+            DenseSide &ds = d.side[side];
+            ds.fcodes = side ? kcodes : qcodes;
+            ds.sent = reinterpret_cast<const uint32_t *>(ws + (side ? L.qent : L.kent));
+            ds.soff = reinterpret_cast<const int32_t *>(ws + (side ? L.qoff : L.koff));
+            ds.fa = side ? v : dy;
+            ds.sg = side ? dy : v;
+            ds.sy = side ? q : k;
+            ds.out = side ? dk : dq;
+            ds.out2 = side ? dv : nullptr;
+            ds.n_f = side ? n_k : n_q;
+            ds.n_s = side ? n_q : n_k;
+        }
+        d.bh = bh; d.m = m; d.tau = tau;
+        const int64_t blocks = bh * ((n_q + kDenseRows - 1) / kDenseRows + (n_k + kDenseRows - 1) / kDenseRows);
+        const size_t lds = static_cast<size_t>(kDenseRows) * dense_stride(n_q > n_k ? n_q : n_k) * 4;
+        KernelTimer timer("dense_kernel", stream);
+        if (bf16)
+            hipLaunchKernelGGL(dense_kernel<true>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, stream, d);
+        else
+            hipLaunchKernelGGL(dense_kernel<false>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, stream, d);
+        return hipGetLastError();
+    }
 
     _Float16 *qs = reinterpret_cast<_Float16 *>(ws + L.qs), *ks = reinterpret_cast<_Float16 *>(ws + L.ks);
     _Float16 *vs = reinterpret_cast<_Float16 *>(ws + L.vs), *dys = reinterpret_cast<_Float16 *>(ws + L.dys);
@@ -1148,11 +1485,15 @@ hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const
                            int tau, void *dq, void *dk, void *dv, void *workspace, hipStream_t stream) {
     const BackwardLayout L = backward_layout(bf16, bh, n_q, n_k, m, tau);
     unsigned char *ws = static_cast<unsigned char *>(workspace);
-    // dV: the forward's table machinery with the roles of queries and keys swapped.
-    hipError_t e = launch_table(qcodes, dy, kcodes, dv, bf16, bh, n_q, n_k, m, tau, ws + L.table, stream);
-    if (e != hipSuccess) return e;
+    // dV: the forward's table machinery with the roles of queries and keys swapped
+    // (the dense form of short sequences computes it with dQ, dK)
+    const bool dense = dense_form(n_q, n_k, false) && bh > 0 && n_q > 0 && n_k > 0;
+    if (!dense) {
+        const hipError_t e = launch_table(qcodes, dy, kcodes, dv, bf16, bh, n_q, n_k, m, tau, ws + L.table, stream);
+        if (e != hipSuccess) return e;
+    }
     return launch_pairs(qcodes, kcodes, q, k, v, dy, bf16, bh, n_q, n_k, m, tau,
-                        static_cast<float>(tau) / (2.0f * static_cast<float>(m)), false, dq, dk, L, ws, stream);
+                        static_cast<float>(tau) / (2.0f * static_cast<float>(m)), false, dq, dk, dv, L, ws, stream);
 }
 
 StarLayout backward_star_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m, int tau) {
@@ -1187,7 +1528,7 @@ hipError_t launch_backward_star(const uint16_t *qcodes, const uint16_t *kcodes, 
     // the pairs of the m*tau derived (tau-1)-bit hashes, each weighted by
     // 1/(pi sqrt(max(1 - x^2, 1/64))) and averaged over the m original hashes
     return launch_pairs(qd, kd, q, k, v, dy, bf16, bh, n_q, n_k, m * tau, tau - 1, 1.0f / static_cast<float>(m), true,
-                        dq, dk, S.pairs, ws, stream);
+                        dq, dk, nullptr, S.pairs, ws, stream);
 }
 
 }  // namespace yoso
