@@ -362,6 +362,9 @@ def main() -> int:
     ap.add_argument("--cpu-heads", type=int, default=-1, help="heads in the oracle sample (-1: all)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-configs", action="store_true", help="skip the per-workload `configs` object")
+    ap.add_argument("--parts", default="star,l2,yoso_e,fast_hash",
+                    help="measurements besides the step (comma list of star, l2, yoso_e, fast_hash; '' for none), "
+                         "e.g. to profile the step's kernels alone")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, run a plain 256 MiB device copy (read + write) three times, "
                          "so that a counter run sees a kernel of known traffic")
@@ -392,19 +395,21 @@ def main() -> int:
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     eager_ms_per_step, kernels, ms_per_step, execution = time_step(Y, torch, step, args.steps, args.warmup)
     roofline = dominant_roofline(w, kernels, qc, kc)
-    star = star_timing(Y, torch, w, t, stream)
+    parts = {p.strip() for p in args.parts.split(",") if p.strip()}
+    star = star_timing(Y, torch, w, t, stream) if "star" in parts else None
 
     # the l2 row normalisation (N-YOSO output / Q, K prologue) on this workload's Q
     # rows, outside the timed step: HBM-bound, algorithmic bytes = rows read + written
     l2 = {}
     qn, dqn = torch.empty_like(q), torch.empty_like(q)
+    l2_reps = 10 if "l2" in parts else 0
     Y.yoso_timing_enable(64)
-    for _ in range(3):
+    for _ in range(3 if l2_reps else 0):
         Y.yoso_l2_normalize(q, qn, stream)
         Y.yoso_l2_normalize_backward(q, dy, dqn, stream)
     torch.cuda.synchronize()
     Y.yoso_timing_reset()
-    for _ in range(10):
+    for _ in range(l2_reps):
         Y.yoso_l2_normalize(q, qn, stream)
         Y.yoso_l2_normalize_backward(q, dy, dqn, stream)
     torch.cuda.synchronize()
@@ -427,12 +432,14 @@ def main() -> int:
     expect = {}
     ye = torch.empty_like(q)
     dqe, dke, dve = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    e_reps = 3 if "yoso_e" in parts else 0
     Y.yoso_timing_enable(64)
-    Y.yoso_expectation_forward(q, k, v, w.tau, ye, stream)
-    Y.yoso_expectation_backward(q, k, v, dy, w.tau, dqe, dke, dve, stream)
+    if e_reps:
+        Y.yoso_expectation_forward(q, k, v, w.tau, ye, stream)
+        Y.yoso_expectation_backward(q, k, v, dy, w.tau, dqe, dke, dve, stream)
     torch.cuda.synchronize()
     Y.yoso_timing_reset()
-    for _ in range(3):
+    for _ in range(e_reps):
         Y.yoso_expectation_forward(q, k, v, w.tau, ye, stream)
         Y.yoso_expectation_backward(q, k, v, dy, w.tau, dqe, dke, dve, stream)
     torch.cuda.synchronize()
@@ -461,7 +468,7 @@ def main() -> int:
     signs = torch.from_numpy(inp["signs"].view(np.int64)).to(dev)
     Rf = torch.empty((w.d, w.m * w.tau), dtype=torch.float32, device=dev)
     Y.yoso_timing_enable(64)
-    for it in range(11):
+    for it in range(11 if "fast_hash" in parts else 0):
         if it == 1:
             torch.cuda.synchronize()
             Y.yoso_timing_reset()
