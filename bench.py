@@ -146,6 +146,7 @@ def cpu_baseline(w, inp, heads, min_wall: float = 10.0):
 
 
 STEP_KERNELS = ("hash_kernel", "table_kernel", "sort_kernel", "absmax_kernel", "split_kernel", "pass_kernel",
+                "bucket_kernel",
                 "reduce_kernel", "dense_kernel", "zero_kernel")
 
 

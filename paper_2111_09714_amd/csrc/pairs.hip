@@ -83,6 +83,26 @@ constexpr int kMantBytes = 16 * 128;   // LDS bytes of a finished tile's 16-bit 
 // at least kEntPad sentinels.
 __host__ __device__ constexpr int64_t ent_stride(int64_t n) { return ((n + 3) & ~int64_t{3}) + kEntPad; }
 constexpr uint32_t kSentinel = 0xFFFF0000u;  // code 0xFFFF (no real code), row 0
+// A pass block's copy of a row entry whose bucket takes the table form gets this
+// code: no partner matches it and its partial row is not stored.
+constexpr uint32_t kSkipCode = 0xFFFEu;
+
+// ---- the table form of a large bucket
+// For bucket c of one hash, with b_q queries and b_k keys, the pairs cost 4 d b_q b_k
+// multiply-adds (S and the output, both sides).  The same sums follow from one d x d
+// matrix per side: M_c = sum_y a'_y b_y^T over the partners, then out_x = s a_x^T M_c
+// for every row, 2 d^2 (b_q + b_k) multiply-adds (the table subroutine of Sec. 3.3
+// restricted to one bucket).  The table form wins when b_q b_k > (d / 2)(b_q + b_k)
+// counted in multiply-adds; its dense 64 x 64 products run the matrix cores far
+// better than the masked 16 x 16 pair tiles, so the bucket switches over at a
+// threshold below d / 2.  kTableT >= 16 keeps every table bucket above 16 rows on
+// both sides, so within a 16-row tile its rows are a prefix and/or a suffix.
+constexpr int kTableT = 16;
+static_assert(kTableT >= 16, "table buckets must span more than one row tile");
+
+__device__ __forceinline__ bool table_bucket(int32_t bq, int32_t bk, int t) {
+    return t > 0 && static_cast<int64_t>(bq) * bk > static_cast<int64_t>(t) * (bq + bk);
+}
 
 // ---------------------------------------------------------------- counting sort
 // codes are [bh][n][m]; unit = b*m + h reads column h with stride m.
@@ -301,6 +321,7 @@ struct PassArgs {
     int64_t bh;
     int m, tau;
     float scale;                     // tau / (2m)
+    int tab_t;                       // table form for buckets with b_q b_k > tab_t (b_q + b_k); 0: none
 };
 
 // Load a T at `byte_off` bytes past `base` (a wave-uniform pointer): keeps the
@@ -544,7 +565,9 @@ __device__ __forceinline__ uint32_t low_off(int r, int w) {
 // the partials are read once, by the reduction, and should not evict the operands
 // from L2.  Exponents go to the block's LDS copy of its exponent row when it fits
 // (written out whole at the end: single-byte stores scattered over the row would
-// each cost a partial-line write), else straight to memory.
+// each cost a partial-line write), else straight to memory.  Rows past nvalid and
+// rows whose entry carries kSkipCode (their bucket takes the table form) are not
+// stored.
 __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, uint8_t *plow, int8_t *pexp,
                                            int8_t *ex_lds, bool ex_in_lds, int m, const uint32_t *tile_ent,
                                            int nvalid, int q, int cl, int g, int c, const floatx4 outT[4],
@@ -572,7 +595,7 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
     // rounded product value * orow, so the row maximum stays below 2^23 before
     // rounding (and at most 2^23 after, hence the clamp)
     const float sc = mx > 0.f ? __uint_as_float(static_cast<uint32_t>(127 + 23 - e) << 23) * orow : 0.f;
-    if (g == 0 && c < nvalid) {
+    if (g == 0 && c < nvalid && (tile_ent[c] >> 16) != kSkipCode) {
         const uint32_t row = tile_ent[c] & 0xFFFFu;
         if (ex_in_lds) ex_lds[row] = static_cast<int8_t>(e);
         else pexp[row] = static_cast<int8_t>(e);
@@ -604,15 +627,16 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
     const uint32_t re[4] = {e4.x, e4.y, e4.z, e4.w};
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-        if (4 * q + i < nvalid) {
+        if (4 * q + i < nvalid && (re[i] >> 16) != kSkipCode) {
             const uint32_t row = re[i] & 0xFFFFu;
             __builtin_nontemporal_store(w[i], reinterpret_cast<uint2v *>(part + (row * static_cast<uint32_t>(m)) * D) + cl);
         }
     }
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-        if (4 * i + q < nvalid) {
-            const uint32_t row = tile_ent[4 * i + q] & 0xFFFFu;
+        const uint32_t le = tile_ent[4 * i + q];
+        if (4 * i + q < nvalid && (le >> 16) != kSkipCode) {
+            const uint32_t row = le & 0xFFFFu;
             __builtin_nontemporal_store(lw[i], reinterpret_cast<uint32_t *>(plow + (row * static_cast<uint32_t>(m)) * D) + cl);
         }
     }
@@ -630,6 +654,7 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
     __shared__ int32_t scan_tmp[kPassWaves];     // the waves' count totals
     __shared__ __align__(16) uint32_t row_ent[kPlanTiles * 16];  // the run's sorted row entries
     __shared__ __align__(16) int8_t ex_lds[kExpLds];               // the block's exponent row
+    __shared__ uint8_t tab_lds[STAR ? 1 : 4096];  // 1 where the bucket takes the table form
 
     const int64_t units = a.bh * a.m;
     const int64_t id = xcd_remap(blockIdx.x, 2 * units);
@@ -673,6 +698,20 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
     const float oscale = ldexpf(a.scale, esum - 39 + 2);
     const bool ex_in_lds = n_r <= kExpLds;
 
+    // buckets in the table form (bucket_kernel writes their rows' partials): the
+    // plan leaves their rows out of every tile's partner range and the run's copy
+    // of their entries carries kSkipCode
+    const int nb = 1 << a.tau;
+    const bool tab = !STAR && a.tab_t > 0;
+    const int32_t *roff = (kside ? a.k.off : a.q.off) + unit * (nb + 1);
+    if (tab) {
+        const int32_t *qo = a.q.off + unit * (nb + 1), *ko = a.k.off + unit * (nb + 1);
+        for (int cb = tid; cb < nb; cb += kPassThreads)
+            tab_lds[cb] = table_bucket(qo[cb + 1] - qo[cb], ko[cb + 1] - ko[cb], a.tab_t) ? 1 : 0;
+        __syncthreads();
+    }
+    auto is_tab = [&](uint32_t code) { return tab && code < static_cast<uint32_t>(nb) && tab_lds[code]; };
+
     for (int T0 = 0; T0 < tiles; T0 += kPlanTiles) {
         const int nt = min(kPlanTiles, tiles - T0);
         // ---- plan: the bucket range of every row tile and its number of 16-partner sub-tiles
@@ -686,13 +725,26 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
                 cnt[j] = 0;
                 if (i < nt) {
                     const int r0 = (T0 + i) * 16;
-                    const int nrow = min(16, n_r - r0);
-                    const int cf = static_cast<int>(rent[r0] >> 16), cl2 = static_cast<int>(rent[r0 + nrow - 1] >> 16);
-                    // start at a multiple of 4 (aligned entry loads); the extra
-                    // partners belong to earlier buckets and are masked by their codes
-                    const int pb = poff[cf] & ~3, pe = poff[cl2 + 1];
-                    plan_beg[i] = pb;
-                    cnt[j] = (pe - pb + 15) >> 4;
+                    int lo = r0, hi = r0 + min(16, n_r - r0);  // the tile's rows that take pairs
+                    uint32_t cf = rent[lo] >> 16, cl2 = rent[hi - 1] >> 16;
+                    if (tab) {
+                        // a table bucket holds more than 16 rows: within the tile it is
+                        // a prefix or a suffix
+                        if (is_tab(cf)) lo = roff[cf + 1];
+                        if (is_tab(cl2)) hi = roff[cl2];
+                        if (lo < hi) {
+                            cf = rent[lo] >> 16;
+                            cl2 = rent[hi - 1] >> 16;
+                        }
+                    }
+                    plan_beg[i] = 0;
+                    if (lo < hi) {
+                        // start at a multiple of 4 (aligned entry loads); the extra
+                        // partners belong to earlier buckets and are masked by their codes
+                        const int pb = poff[cf] & ~3, pe = poff[cl2 + 1];
+                        plan_beg[i] = pb;
+                        cnt[j] = (pe - pb + 15) >> 4;
+                    }
                 }
                 local += cnt[j];
             }
@@ -716,8 +768,14 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
             }
             if (tid == kPassThreads - 1) plan_x[nt] = incl;
             // the run's row entries (16-byte copies; entries past n_r are sentinels)
-            for (int i = tid; i < nt * 4; i += kPassThreads)
-                reinterpret_cast<uint4 *>(row_ent)[i] = ld<uint4>(rent, static_cast<uint32_t>(T0 * 16 + 4 * i) * 4);
+            for (int i = tid; i < nt * 4; i += kPassThreads) {
+                uint4 e4 = ld<uint4>(rent, static_cast<uint32_t>(T0 * 16 + 4 * i) * 4);
+                if (tab) {
+                    auto mark = [&](uint32_t e) { return is_tab(e >> 16) ? (kSkipCode << 16) | (e & 0xFFFFu) : e; };
+                    e4.x = mark(e4.x); e4.y = mark(e4.y); e4.z = mark(e4.z); e4.w = mark(e4.w);
+                }
+                reinterpret_cast<uint4 *>(row_ent)[i] = e4;
+            }
             __syncthreads();
         }
         // ---- this wave's tiles: a contiguous run holding about a quarter of the sub-tiles
@@ -847,6 +905,253 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
         for (int e = tid; e < n16; e += kPassThreads)
             reinterpret_cast<uint4 *>(pexp)[e] = reinterpret_cast<const uint4 *>(ex_lds)[e];
         for (int e = (n16 << 4) + tid; e < n_r; e += kPassThreads) pexp[e] = ex_lds[e];
+    }
+}
+
+// ---------------------------------------------------------------- table form
+// bucket_kernel: one workgroup per (head, hash, side), launched after pass_kernel,
+// for the buckets that take the table form (table_bucket).  Each wave takes whole
+// buckets, one after another, from a counter shared by the workgroup:
+//   build  M = sum_y a'_y b_y^T (64 x 64) over the bucket's partners, 32 at a time:
+//          the group is staged in the wave's LDS tile and all sixteen 16x16 blocks
+//          of M accumulate on 16x16x32 MFMAs (three fp16 products each).  The
+//          contraction runs over the staged rows, so both operands are read
+//          transposed (ds_read_b64_tr_b16).  Entries are fetched two groups ahead
+//          and partner rows one group ahead.
+//   scale  one power of two brings max |M| below 2^14; M^T is split into fp16
+//          (hi, lo), passed through the tile and kept in registers.
+//   apply  the bucket's rows, 16 at a time: out^T = M^T A_x^T, stored as the rows'
+//          partials like a pass tile; entries two tiles ahead, rows one tile ahead.
+// The result for a row is the pass kernel's sum over the same partners, added in
+// another order.  No barrier follows the bucket list: the waves share nothing else.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kBuildRows = 32;                 // partners per build step
+constexpr int kStageBytes = kBuildRows * 512;  // a wave's tile: staged rows [a' hi | a' lo | b hi | b lo]
+
+__global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
+    __shared__ __align__(16) unsigned char stage_lds[kPassWaves * kStageBytes];
+    __shared__ __align__(16) uint32_t tent_lds[kPassWaves * 16];  // each wave's tile entries
+    __shared__ int16_t list[4096];                                 // the unit's table buckets
+    __shared__ int list_n, list_next;
+
+    const int64_t units = a.bh * a.m;
+    const int64_t id = xcd_remap(blockIdx.x, 2 * units);
+    const int64_t unit = id >> 1;
+    const bool kside = id & 1;
+    const int64_t b = unit / a.m;
+    const int h = static_cast<int>(unit - b * a.m);
+    // roles as in pass_kernel: dQ rows = queries (a = dY), partners = keys (a' = V, b = K);
+    // dK rows = keys (a = V), partners = queries (a' = dY, b = Q)
+    const int n_r = static_cast<int>(kside ? a.k.n : a.q.n);
+    const int n_p = static_cast<int>(kside ? a.q.n : a.k.n);
+    const int nb = 1 << a.tau;
+    const uint32_t *rent = (kside ? a.k.ent : a.q.ent) + unit * ent_stride(n_r);
+    const uint32_t *pent = (kside ? a.q.ent : a.k.ent) + unit * ent_stride(n_p);
+    const int32_t *qo = a.q.off + unit * (nb + 1), *ko = a.k.off + unit * (nb + 1);
+    const int32_t *roff = kside ? ko : qo, *poff = kside ? qo : ko;
+    const _Float16 *arow = (kside ? a.vs : a.dys) + b * n_r * (2 * D);
+    const _Float16 *apar = (kside ? a.dys : a.vs) + b * n_p * (2 * D);
+    const _Float16 *bpar = (kside ? a.qs : a.ks) + b * n_p * (2 * D);
+    int16_t *part = (kside ? a.pk : a.pq) + ((b * n_r) * a.m + h) * D;
+    uint8_t *plow = (kside ? a.lk : a.lq) + ((b * n_r) * a.m + h) * D;
+    int8_t *pexp = (kside ? a.ek : a.eq) + (b * a.m + h) * n_r;
+    // the operands carry the head scales 2^(13 - e) of a, a' and b
+    const int esum = head_exp(a.pmax, b, kside ? 3 : 1) + head_exp(a.pmax, b, kside ? 1 : 3) +
+                     head_exp(a.pmax, b, kside ? 0 : 2);
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = uni(tid >> 6);
+    const int g = lane >> 4, c = lane & 15;   // MFMA layout
+    const int q = lane >> 4, cl = lane & 15;  // coalesced layout
+    unsigned char *st = stage_lds + wave * kStageBytes;
+    uint32_t *tent = tent_lds + wave * 16;
+
+    if (tid == 0) {
+        list_n = 0;
+        list_next = 0;
+    }
+    __syncthreads();
+    for (int cb = tid; cb < nb; cb += kPassThreads)
+        if (table_bucket(qo[cb + 1] - qo[cb], ko[cb + 1] - ko[cb], a.tab_t))
+            list[atomicAdd(&list_n, 1)] = static_cast<int16_t>(cb);
+    __syncthreads();
+    const int nl = uni(list_n);
+
+    // Transposed reads of the staged partners for a 16x16x32 operand: lane (g, c)
+    // needs partners 8g .. 8g+7 at one dim.  Source lane (g, 4 i4 + a4) addresses
+    // partner 8g + i4 (first read) or 8g + 4 + i4 (second), dims 4 a4 .. 4 a4 + 3 of
+    // the 16-dim block that starts at 16-byte chunk `chunk` of the staged row;
+    // partner p sits in half p >> 4 of the tile, row p & 15.
+    const int i4 = c >> 2, a4 = c & 3;
+    const unsigned char *sp = st + (g >> 1) * (16 * 512);
+    const int ra = 8 * (g & 1) + i4;
+    auto trpair = [&](int chunk) {
+        const uint32_t o = 8 * (a4 & 1);
+        const half4 x = tr_load(sp + swz(ra, chunk + (a4 >> 1), 512) + o);
+        const half4 y = tr_load(sp + swz(ra + 4, chunk + (a4 >> 1), 512) + o);
+        return __builtin_shufflevector(x, y, 0, 1, 2, 3, 4, 5, 6, 7);
+    };
+
+    for (;;) {
+        int li = 0;
+        if (lane == 0) li = atomicAdd(&list_next, 1);
+        li = uni(li);
+        if (li >= nl) break;
+        const int cb = uni(list[li]);
+        const int p0 = uni(poff[cb]), p1 = uni(poff[cb + 1]);
+        const int r0 = uni(roff[cb]), r1 = uni(roff[cb + 1]);
+
+        // ---- build.  Staged row 16 (j >> 2) + 4q + (j & 3) of a group holds partner
+        // y0 + that; slots past the bucket's end load row 0 and are staged as zeros
+        // (bit j of the mask), so no loaded value is waited for before it is staged
+        auto group_ents = [&](int y0, uint32_t e[8]) {
+#pragma unroll
+            for (int j = 0; j < 8; j++) {
+                const int y = y0 + 16 * (j >> 2) + 4 * q + (j & 3);
+                e[j] = y < p1 ? (pent[y] & 0xFFFFu) : 0xFFFFFFFFu;
+            }
+        };
+        u32x4 av[8], bv[8];
+        unsigned okr = 0;
+        auto group_rows = [&](const uint32_t e[8]) {
+            okr = 0;
+#pragma unroll
+            for (int j = 0; j < 8; j++) {
+                const bool ok = e[j] != 0xFFFFFFFFu;
+                okr |= ok ? 1u << j : 0u;
+                const uint32_t off = (ok ? e[j] : 0u) * (4 * D) + 16 * cl;
+                av[j] = ld<u32x4>(apar, off);
+                bv[j] = ld<u32x4>(bpar, off);
+            }
+        };
+        floatx4 acc[4][4];
+#pragma unroll
+        for (int fi = 0; fi < 4; fi++)
+#pragma unroll
+            for (int ei = 0; ei < 4; ei++) acc[fi][ei] = floatx4{0.f, 0.f, 0.f, 0.f};
+        const int ngrp = (p1 - p0 + kBuildRows - 1) / kBuildRows;
+        uint32_t en[8];
+        group_ents(p0, en);
+        group_rows(en);
+        if (ngrp > 1) group_ents(p0 + kBuildRows, en);
+        for (int gi = 0; gi < ngrp; gi++) {
+#pragma unroll
+            for (int j = 0; j < 8; j++) {
+                unsigned char *half_tile = st + (j >> 2) * (16 * 512);
+                const u32x4 keep = u32x4(0u - ((okr >> j) & 1u));  // all ones or all zeros
+                lds_st(half_tile, swz(4 * q + (j & 3), cl, 512), av[j] & keep);
+                lds_st(half_tile, swz(4 * q + (j & 3), 16 + cl, 512), bv[j] & keep);
+            }
+            if (gi + 1 < ngrp) group_rows(en);
+            if (gi + 2 < ngrp) group_ents(p0 + (gi + 2) * kBuildRows, en);
+            // A = A'^T (rows f, from the a' part), B = B_y (columns e, from the b part)
+            half8 bh[4], bl[4];
+#pragma unroll
+            for (int ei = 0; ei < 4; ei++) {
+                bh[ei] = trpair(16 + 2 * ei);
+                bl[ei] = trpair(24 + 2 * ei);
+            }
+#pragma unroll
+            for (int fi = 0; fi < 4; fi++) {
+                const half8 ah = trpair(2 * fi), al = trpair(8 + 2 * fi);
+#pragma unroll
+                for (int ei = 0; ei < 4; ei++)
+                    acc[fi][ei] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bh[ei], acc[fi][ei], 0, 0, 0);
+#pragma unroll
+                for (int ei = 0; ei < 4; ei++)
+                    acc[fi][ei] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl[ei], acc[fi][ei], 0, 0, 0);
+#pragma unroll
+                for (int ei = 0; ei < 4; ei++)
+                    acc[fi][ei] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bh[ei], acc[fi][ei], 0, 0, 0);
+            }
+        }
+
+        // ---- scale: lane (g, c) of block (fi, ei) holds M[16 fi + 4g + i][16 ei + c]
+        float mx = 0.f;
+#pragma unroll
+        for (int fi = 0; fi < 4; fi++)
+#pragma unroll
+            for (int ei = 0; ei < 4; ei++)
+#pragma unroll
+                for (int i = 0; i < 4; i++) mx = fmaxf(mx, fabsf(acc[fi][ei][i]));
+        // max |M| < 2^em: M 2^(14 - em) is below 2^14, a normal fp16 pair
+        const int em = pow2_above(wave_max(mx));
+        const float msc = ldexpf(1.0f, 14 - em);
+        // M^T through the tile: row e = 16 ei + c (group ei of 16 rows, 256 bytes each),
+        // dims f = 16 fi + 4g + (0..3): 8 bytes of chunk 2 fi + (g >> 1) (hi) and of
+        // chunk 8 + that (lo).  (The tile's last transposed reads come first: one
+        // wave's LDS accesses execute in order.)
+#pragma unroll
+        for (int fi = 0; fi < 4; fi++)
+#pragma unroll
+            for (int ei = 0; ei < 4; ei++) {
+                const float v[4] = {acc[fi][ei][0], acc[fi][ei][1], acc[fi][ei][2], acc[fi][ei][3]};
+                half4 hi, lo;
+                split4_pow2(v, msc, hi, lo);
+                unsigned char *grp = st + ei * (16 * 256);
+                lds_st(grp, swz(c, 2 * fi + (g >> 1), 256) + 8 * (g & 1), hi);
+                lds_st(grp, swz(c, 8 + 2 * fi + (g >> 1), 256) + 8 * (g & 1), lo);
+            }
+        // M^T as the A operand: lane (g, c) = row e = 16 dt + c, dims 32 kb + 8g + [0, 8)
+        half8 mth[4][2], mtl[4][2];
+#pragma unroll
+        for (int dt = 0; dt < 4; dt++)
+#pragma unroll
+            for (int kb = 0; kb < 2; kb++) {
+                mth[dt][kb] = lds_ld<half8>(st + dt * (16 * 256), swz(c, 4 * kb + g, 256));
+                mtl[dt][kb] = lds_ld<half8>(st + dt * (16 * 256), swz(c, 8 + 4 * kb + g, 256));
+            }
+        // out = s * outT * 2^(e_a + e_a' + e_b - 39) * 2^(em - 14)
+        const float orow = ldexpf(a.scale, esum - 39 + em - 14);
+
+        // ---- apply.  Lane (q, cl) loads chunk cl of rows 4q .. 4q+3 of a tile; slots
+        // past the bucket's end repeat its first row and are not stored
+        const int ntile = (r1 - r0 + 15) >> 4;
+        auto tile_ents = [&](int t, uint32_t e[4]) {
+            const int pos = r0 + 16 * t;
+#pragma unroll
+            for (int i = 0; i < 4; i++) e[i] = rent[pos + 4 * q + i < r1 ? pos + 4 * q + i : pos];
+        };
+        auto tile_rows = [&](const uint32_t e[4], uint4 r[4]) {
+#pragma unroll
+            for (int i = 0; i < 4; i++) r[i] = ld<uint4>(arow, (e[i] & 0xFFFFu) * (4 * D) + 16 * cl);
+        };
+        uint32_t ec[4], en4[4];
+        uint4 rc[4];
+        tile_ents(0, ec);
+        tile_rows(ec, rc);
+        if (ntile > 1) tile_ents(1, en4);
+        for (int t = 0; t < ntile; t++) {
+            const int nvalid = min(16, r1 - (r0 + 16 * t));
+            half8 rh[2], rl[2];
+            stage_rows(rc, st, q, cl, g, c, rh, rl);
+            if (cl == 0) reinterpret_cast<uint4 *>(tent)[q] = make_uint4(ec[0], ec[1], ec[2], ec[3]);
+            if (t + 1 < ntile) {
+#pragma unroll
+                for (int i = 0; i < 4; i++) ec[i] = en4[i];
+                tile_rows(ec, rc);
+                if (t + 2 < ntile) tile_ents(t + 2, en4);
+            }
+            floatx4 outT[4];
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kb = 0; kb < 2; kb++)
+#pragma unroll
+                for (int dt = 0; dt < 4; dt++)
+                    outT[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(mth[dt][kb], rh[kb], outT[dt], 0, 0, 0);
+#pragma unroll
+            for (int kb = 0; kb < 2; kb++)
+#pragma unroll
+                for (int dt = 0; dt < 4; dt++)
+                    outT[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(mth[dt][kb], rl[kb], outT[dt], 0, 0, 0);
+#pragma unroll
+            for (int kb = 0; kb < 2; kb++)
+#pragma unroll
+                for (int dt = 0; dt < 4; dt++)
+                    outT[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(mtl[dt][kb], rh[kb], outT[dt], 0, 0, 0);
+            store_tile(st, part, plow, pexp, nullptr, false, a.m, tent, nvalid, q, cl, g, c, outT, orow);
+        }
     }
 }
 
@@ -1306,9 +1611,17 @@ hipError_t launch_pass(const PassArgs &a, int64_t units, bool star, hipStream_t 
         hipLaunchKernelGGL(pass_kernel<true>, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0, stream,
                            a);
     } else {
-        KernelTimer timer("pass_kernel", stream);
-        hipLaunchKernelGGL(pass_kernel<false>, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0, stream,
-                           a);
+        {
+            KernelTimer timer("pass_kernel", stream);
+            hipLaunchKernelGGL(pass_kernel<false>, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0,
+                               stream, a);
+        }
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess || a.tab_t == 0) return e;
+        // after the pass: the pass blocks write their whole exponent rows, the table
+        // buckets' entries included, and these writes must land last
+        KernelTimer timer("bucket_kernel", stream);
+        hipLaunchKernelGGL(bucket_kernel, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0, stream, a);
     }
     return hipGetLastError();
 }
@@ -1468,6 +1781,7 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
     a.ek = reinterpret_cast<int8_t *>(ws + L.ek);
     a.bh = bh; a.m = m; a.tau = tau;
     a.scale = scale;
+    a.tab_t = star ? 0 : kTableT;
     e = launch_pass(a, units, star, stream);
     if (e != hipSuccess) return e;
     if (bf16) {

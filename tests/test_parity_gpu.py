@@ -104,15 +104,53 @@ def test_maximum_length(bh, nq, nk, m, tau, dtype):
     run_case(bh, nq, nk, m, tau, dtype)
 
 
-def run_case(bh, nq, nk, m, tau, dtype):
-    name = f"bh{bh}_nq{nq}_nk{nk}_m{m}_tau{tau}_{dtype}"
+def run_case(bh, nq, nk, m, tau, dtype, dist="gauss"):
+    name = f"bh{bh}_nq{nq}_nk{nk}_m{m}_tau{tau}_{dtype}" + ("" if dist == "gauss" else f"_{dist}")
     log(f"[{name}] start")
-    w = workloads.Workload(name, 1, bh, nq, 64, tau, m, dtype, "gauss", 1234 + nq + 7 * nk + m + tau)
+    w = workloads.Workload(name, 1, bh, nq, 64, tau, m, dtype, dist, 1234 + nq + 7 * nk + m + tau)
     inp = make_inputs(w, n=nq, n_k=nk)
     g = run_gpu(inp, m, tau, dtype)
     check_codes(name + "/q", inp["q"], inp["R"], m, tau, g["qc"])
     check_codes(name + "/k", inp["k"], inp["R"], m, tau, g["kc"])
     check_outputs(name, inp, g, m, tau, dtype)
+    return g
+
+
+def large_bucket_share(qc, kc, tau, t=16):
+    """Fraction of the (row, hash) pairs of both sides that sit in buckets with
+    b_q b_k > t (b_q + b_k): the buckets whose dQ, dK rows the backward computes in
+    the bucket-table form (its switch-over threshold is 16)."""
+    nb = 1 << tau
+    rows = big = 0
+    for b in range(qc.shape[0]):
+        for h in range(qc.shape[1]):
+            bq = np.bincount(qc[b, h], minlength=nb).astype(np.int64)
+            bk = np.bincount(kc[b, h], minlength=nb).astype(np.int64)
+            sel = bq * bk > t * (bq + bk)
+            big += int((bq + bk)[sel].sum())
+            rows += int((bq + bk).sum())
+    return big / max(rows, 1)
+
+
+TABLE_FORM = [
+    # (bh, n_q, n_k, m, tau, dtype, dist): buckets of hundreds of rows on both sides
+    (2, 1500, 1100, 4, 4, "f32", "gauss"),     # 16 buckets, every one large
+    (1, 2000, 1300, 6, 6, "f32", "mixture"),   # large and small buckets side by side in one row tile
+    (2, 1100, 3000, 3, 3, "bf16", "mixture"),
+    (1, 1025, 1030, 2, 1, "f32", "gauss"),     # two buckets; ragged last tiles and partner groups
+    (1, 6000, 5999, 2, 12, "f32", "mixture"),  # a few large buckets among thousands of tiny ones
+]
+
+
+@pytest.mark.parametrize("bh,nq,nk,m,tau,dtype,dist", TABLE_FORM)
+def test_bucket_table_form(bh, nq, nk, m, tau, dtype, dist):
+    """Large buckets: their dQ, dK rows come from one 64 x 64 matrix per bucket
+    (the table form) while the other buckets keep the pair passes; every row is
+    checked against the oracle's pairwise sums."""
+    g = run_case(bh, nq, nk, m, tau, dtype, dist)
+    share = large_bucket_share(g["qc"], g["kc"], tau)
+    log(f"[table form {bh}x{nq}x{nk} tau {tau} {dist}] rows in large buckets: {share:.3f}")
+    assert share > 0.05
 
 
 @pytest.mark.parametrize("name", list(WORKLOADS))
@@ -155,6 +193,30 @@ def test_backward_far_from_unit_scale(what, scale):
     y = oracle.forward(g["qc"], g["kc"], inp["v"], m, tau)
     dq, dk, dv = oracle.backward(g["qc"], g["kc"], inp["q"], inp["k"], inp["v"], inp["dy"], m, tau)
     check_all(name, [(key, g[key], ref) for key, ref in (("y", y), ("dq", dq), ("dk", dk), ("dv", dv))], TOL["f32"])
+
+
+@pytest.mark.parametrize("what,scale", [("dy", 1e-6), ("v", 1e3), ("rows", None)])
+def test_bucket_table_form_far_from_unit_scale(what, scale):
+    """The table form's per-bucket power-of-two scaling of M = sum a' b^T: small and
+    large gradients and rows of very different size (10^-4 .. 1 in dY, 10^-3 .. 10
+    in V) in buckets of a few hundred rows."""
+    bh, nq, nk, m, tau = 2, 1200, 1400, 6, 4
+    name = f"table form scaled {what} {scale}"
+    log(f"[{name}] start")
+    w = workloads.Workload(name, 1, bh, nq, 64, tau, m, "f32", "mixture", 8642)
+    inp = make_inputs(w, n=nq, n_k=nk)
+    if what == "rows":
+        g = np.random.default_rng(98)
+        inp["dy"] = inp["dy"] * 10.0 ** g.uniform(-4, 0, size=(bh, nq, 1))
+        inp["v"] = inp["v"] * 10.0 ** g.uniform(-3, 1, size=(bh, nk, 1))
+    else:
+        inp[what] = inp[what] * scale
+    for key in ("dy", "v"):
+        inp[key] = inp[key].astype(np.float32).astype(np.float64)
+    g = run_gpu(inp, m, tau, "f32")
+    assert large_bucket_share(g["qc"], g["kc"], tau) > 0.05
+    dq, dk, _ = oracle.backward(g["qc"], g["kc"], inp["q"], inp["k"], inp["v"], inp["dy"], m, tau)
+    check_all(name, [(key, g[key], ref) for key, ref in (("dq", dq), ("dk", dk))], TOL["f32"])
 
 
 def test_tables_resolve_every_feature_dim():
