@@ -62,9 +62,12 @@ def kernel_algorithmic(w, kernel: str):
     return per_head * w.bh
 
 
-def colliding_pairs(qc, kc, tau: int) -> int:
-    """Number of (query, key) pairs that share a bucket, summed over heads and hashes:
-    sum over (head, hash, bucket) of count_q * count_k, from the codes on the host."""
+def bucket_work(qc, kc, tau: int, t: int):
+    """Work of the backward's two forms, from the codes on the host, summed over
+    heads and hashes: (pairs, pair_form_pairs, table_form_rows).  `pairs` counts the
+    colliding (query, key) pairs, sum of count_q * count_k over (head, hash, bucket);
+    buckets with count_q * count_k > t (count_q + count_k) take the table form and
+    contribute count_q + count_k rows, the others their pairs."""
     import numpy as np
     B = 1 << tau
     q = qc.cpu().numpy().astype(np.int64) & (B - 1)  # [bh, n_q, m]
@@ -73,7 +76,9 @@ def colliding_pairs(qc, kc, tau: int) -> int:
     unit = (np.arange(bh)[:, None, None] * m + np.arange(m)[None, None, :]) * B
     hq = np.bincount((unit + q).ravel(), minlength=bh * m * B)
     hk = np.bincount((unit + k).ravel(), minlength=bh * m * B)
-    return int((hq * hk).sum())
+    prod = hq * hk
+    tab = prod > t * (hq + hk)
+    return int(prod.sum()), int(prod[~tab].sum()), int((hq + hk)[tab].sum())
 
 
 COPY_BYTES = 256 << 20
@@ -238,20 +243,25 @@ def dominant_roofline(w, kernels, qc, kc):
         roofline = {"kernel": dominant, "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                     "algorithmic_bytes_per_launch": alg, "avg_launch_us": round(kernels[dominant]["avg_us"], 2)}
-    if dominant == "pass_kernel":
-        # dQ, dK are dense per-bucket contractions, bound by the matrix units: per
-        # colliding (query, key) pair 3d multiply-adds (dy.v once, then its share of
-        # dQ and of dK), in fp32; the pairs are counted exactly from this step's codes
-        pairs = colliding_pairs(qc, kc, w.tau)
-        flops = 6 * w.d * pairs
+    if dominant in ("pass_kernel", "bucket_kernel"):
+        # dQ, dK are dense per-bucket contractions, bound by the matrix units, in fp32.
+        # Pair form (pass_kernel): per colliding (query, key) pair 3d multiply-adds
+        # (dy.v once, then its share of dQ and of dK).  Table form (bucket_kernel): per
+        # row of a table bucket and side 2 d^2 (its share of M = sum a' b^T, then its
+        # row of a^T M).  Both counted exactly from this step's codes.
+        import paper_2111_09714_amd as Y
+        pairs, pair_form, table_rows = bucket_work(qc, kc, w.tau, Y.yoso_backward_table_threshold())
+        flops = 6 * w.d * pair_form if dominant == "pass_kernel" else 4 * w.d * w.d * table_rows
         tf = flops / avg_s / 1e12
         hbm = roofline
         roofline = {"kernel": dominant, "bound": "mfma", "achieved": round(tf, 2), "peak": FP32_PEAK_TFLOPS,
                     "unit": "TFLOP/s", "frac": round(tf / FP32_PEAK_TFLOPS, 4), "traffic": None,
                     "algorithmic_flops_per_launch": flops, "colliding_pairs_per_launch": pairs,
-                    "avg_launch_us": round(kernels[dominant]["avg_us"], 2),
-                    "hbm": {"achieved": hbm["achieved"], "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": hbm["frac"],
-                            "algorithmic_bytes_per_launch": alg}}
+                    "pair_form_pairs_per_launch": pair_form, "table_form_rows_per_launch": table_rows,
+                    "avg_launch_us": round(kernels[dominant]["avg_us"], 2)}
+        if hbm is not None:
+            roofline["hbm"] = {"achieved": hbm["achieved"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                               "frac": hbm["frac"], "algorithmic_bytes_per_launch": alg}
     if dominant == "dense_kernel":
         # short sequences: dQ, dK and dV as dense blocks over every (query, key) pair,
         # 5 d multiply-adds per pair (dy.v once for each of the two sides, then its

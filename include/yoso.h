@@ -178,6 +178,11 @@ yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const v
  * per-hash bucket orders, the per-head maxima of |q|, |k|, |v|, |dy|, fp16
  * (hi, lo) copies of q, k, v, dy, and one 24-bit fixed-point partial row per
  * (row, hash) for dq and dk: about (3*m*d + 5*m + 8*d) * (n_q + n_k) * bh bytes.
+ * A bucket with b_q queries and b_k keys whose sizes pass
+ * yoso_backward_table_threshold() is summed in the table form of Sec. 3.3
+ * restricted to that bucket (one d x d matrix per side and bucket, applied to the
+ * bucket's rows); the others pair by pair.  Both give the same sums up to the
+ * order of fp32 additions.
  */
 yoso_status yoso_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q,
                           const void *k, const void *v, const void *dy, yoso_dtype dtype,
@@ -239,6 +244,10 @@ yoso_status yoso_backward_noalloc(const uint16_t *qcodes, const uint16_t *kcodes
 
 /* Bytes of the fixed scratch array of yoso_backward_noalloc (per GPU). */
 size_t yoso_backward_noalloc_limit(void);
+
+/* T of yoso_backward's switch-over rule: a bucket takes the table form when
+ * b_q * b_k > T * (b_q + b_k).  Informational (for work accounting by callers). */
+int32_t yoso_backward_table_threshold(void);
 
 /*
  * Row l2 normalisation: the output normalisation of N-YOSO (Sec. 3.1,

@@ -24,7 +24,7 @@ from typing import Optional
 __all__ = [
     "YosoError", "F32", "BF16", "OP_HASH", "OP_FORWARD", "OP_BACKWARD", "OP_BACKWARD_STAR",
     "lib", "lib_path", "yoso_workspace_bytes", "yoso_status_str", "yoso_hash", "yoso_fast_hyperplanes", "yoso_fast_hash", "yoso_forward",
-    "yoso_backward", "yoso_backward_star", "backward_star", "yoso_backward_noalloc", "yoso_backward_noalloc_limit", "yoso_l2_normalize", "yoso_l2_normalize_backward", "yoso_expectation_forward",
+    "yoso_backward", "yoso_backward_star", "backward_star", "yoso_backward_noalloc", "yoso_backward_noalloc_limit", "yoso_backward_table_threshold", "yoso_l2_normalize", "yoso_l2_normalize_backward", "yoso_expectation_forward",
     "yoso_expectation_backward",
     "yoso_timing_enable", "yoso_timing_reset", "yoso_timing_query",
     "workspace", "hash_qk", "fast_hash_qk", "forward", "backward",
@@ -69,6 +69,8 @@ def lib() -> ctypes.CDLL:
         L.yoso_backward_noalloc.restype = ctypes.c_int
         L.yoso_backward_noalloc_limit.argtypes = []
         L.yoso_backward_noalloc_limit.restype = SZ
+        L.yoso_backward_table_threshold.argtypes = []
+        L.yoso_backward_table_threshold.restype = ctypes.c_int32
         L.yoso_workspace_bytes.argtypes = [I32, I64, I64, I64, I32, I32, I32, I32]
         L.yoso_workspace_bytes.restype = SZ
         L.yoso_l2_normalize.argtypes = [P, I32, I64, I32, P, P]
@@ -285,6 +287,11 @@ def yoso_backward_noalloc(qcodes, kcodes, q, k, v, dy, m: int, tau: int, dq, dk,
 
 def yoso_backward_noalloc_limit() -> int:
     return lib().yoso_backward_noalloc_limit()
+
+
+def yoso_backward_table_threshold() -> int:
+    """T of the backward's rule: a bucket takes the table form when b_q b_k > T (b_q + b_k)."""
+    return lib().yoso_backward_table_threshold()
 
 
 def yoso_l2_normalize(x, y, stream=None) -> None:

@@ -58,6 +58,9 @@ hipError_t launch_expect_backward(const void *q, const void *k, const void *v, c
                                   void *dv, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int tau,
                                   hipStream_t stream);
 
+// T of the backward's rule: a bucket takes the table form when b_q b_k > T (b_q + b_k).
+int backward_table_threshold();
+
 hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
                            const void *v, const void *dy, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m,
                            int tau, void *dq, void *dk, void *dv, void *workspace, hipStream_t stream);

@@ -97,7 +97,7 @@ constexpr uint32_t kSkipCode = 0xFFFEu;
 // better than the masked 16 x 16 pair tiles, so the bucket switches over at a
 // threshold below d / 2.  kTableT >= 16 keeps every table bucket above 16 rows on
 // both sides, so within a 16-row tile its rows are a prefix and/or a suffix.
-constexpr int kTableT = 16;
+constexpr int kTableT = 32;
 static_assert(kTableT >= 16, "table buckets must span more than one row tile");
 
 __device__ __forceinline__ bool table_bucket(int32_t bq, int32_t bk, int t) {
@@ -1002,24 +1002,26 @@ __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
         const int r0 = uni(roff[cb]), r1 = uni(roff[cb + 1]);
 
         // ---- build.  Staged row 16 (j >> 2) + 4q + (j & 3) of a group holds partner
-        // y0 + that; slots past the bucket's end load row 0 and are staged as zeros
-        // (bit j of the mask), so no loaded value is waited for before it is staged
+        // y0 + that.  Slots past the bucket's end load the bucket's first partner and
+        // are staged as zeros (bit j of the masks, computed from the position alone):
+        // no load is conditional and no loaded value is used before it is needed, so
+        // nothing waits for the loads in flight
+        unsigned okn = 0, okr = 0;
         auto group_ents = [&](int y0, uint32_t e[8]) {
+            okn = 0;
 #pragma unroll
             for (int j = 0; j < 8; j++) {
                 const int y = y0 + 16 * (j >> 2) + 4 * q + (j & 3);
-                e[j] = y < p1 ? (pent[y] & 0xFFFFu) : 0xFFFFFFFFu;
+                okn |= y < p1 ? 1u << j : 0u;
+                e[j] = pent[y < p1 ? y : p0];
             }
         };
         u32x4 av[8], bv[8];
-        unsigned okr = 0;
         auto group_rows = [&](const uint32_t e[8]) {
-            okr = 0;
+            okr = okn;
 #pragma unroll
             for (int j = 0; j < 8; j++) {
-                const bool ok = e[j] != 0xFFFFFFFFu;
-                okr |= ok ? 1u << j : 0u;
-                const uint32_t off = (ok ? e[j] : 0u) * (4 * D) + 16 * cl;
+                const uint32_t off = (e[j] & 0xFFFFu) * (4 * D) + 16 * cl;
                 av[j] = ld<u32x4>(apar, off);
                 bv[j] = ld<u32x4>(bpar, off);
             }
@@ -1105,10 +1107,18 @@ __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
         const float orow = ldexpf(a.scale, esum - 39 + em - 14);
 
         // ---- apply.  Lane (q, cl) loads chunk cl of rows 4q .. 4q+3 of a tile; slots
-        // past the bucket's end repeat its first row and are not stored
+        // past the bucket's end repeat its first row and are not stored.  A tile's
+        // entries are fetched two tiles ahead and its rows one tile ahead, every load
+        // unconditional (past the last tile: the last tile again) and the per-tile
+        // state rotating through three slots with the loop unrolled three times, so
+        // no register that a load is still filling is ever copied
         const int ntile = (r1 - r0 + 15) >> 4;
+        struct ASlot {
+            uint32_t e[4];
+            uint4 r[4];
+        };
         auto tile_ents = [&](int t, uint32_t e[4]) {
-            const int pos = r0 + 16 * t;
+            const int pos = r0 + 16 * min(t, ntile - 1);
 #pragma unroll
             for (int i = 0; i < 4; i++) e[i] = rent[pos + 4 * q + i < r1 ? pos + 4 * q + i : pos];
         };
@@ -1116,22 +1126,17 @@ __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
 #pragma unroll
             for (int i = 0; i < 4; i++) r[i] = ld<uint4>(arow, (e[i] & 0xFFFFu) * (4 * D) + 16 * cl);
         };
-        uint32_t ec[4], en4[4];
-        uint4 rc[4];
-        tile_ents(0, ec);
-        tile_rows(ec, rc);
-        if (ntile > 1) tile_ents(1, en4);
-        for (int t = 0; t < ntile; t++) {
+        ASlot A, B, C;
+        tile_ents(0, A.e);
+        tile_rows(A.e, A.r);
+        tile_ents(1, B.e);
+        auto astep = [&](int t, ASlot &cur, ASlot &nxt, ASlot &nn) -> bool {
+            tile_rows(nxt.e, nxt.r);
+            tile_ents(t + 2, nn.e);
             const int nvalid = min(16, r1 - (r0 + 16 * t));
             half8 rh[2], rl[2];
-            stage_rows(rc, st, q, cl, g, c, rh, rl);
-            if (cl == 0) reinterpret_cast<uint4 *>(tent)[q] = make_uint4(ec[0], ec[1], ec[2], ec[3]);
-            if (t + 1 < ntile) {
-#pragma unroll
-                for (int i = 0; i < 4; i++) ec[i] = en4[i];
-                tile_rows(ec, rc);
-                if (t + 2 < ntile) tile_ents(t + 2, en4);
-            }
+            stage_rows(cur.r, st, q, cl, g, c, rh, rl);
+            if (cl == 0) reinterpret_cast<uint4 *>(tent)[q] = make_uint4(cur.e[0], cur.e[1], cur.e[2], cur.e[3]);
             floatx4 outT[4];
 #pragma unroll
             for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -1151,6 +1156,12 @@ __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
                 for (int dt = 0; dt < 4; dt++)
                     outT[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(mtl[dt][kb], rh[kb], outT[dt], 0, 0, 0);
             store_tile(st, part, plow, pexp, nullptr, false, a.m, tent, nvalid, q, cl, g, c, outT, orow);
+            return t + 1 < ntile;
+        };
+        for (int t = 0;; t += 3) {
+            if (!astep(t, A, B, C)) break;
+            if (!astep(t + 1, B, C, A)) break;
+            if (!astep(t + 2, C, A, B)) break;
         }
     }
 }
@@ -1793,6 +1804,8 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
 }
 
 }  // namespace
+
+int backward_table_threshold() { return kTableT; }
 
 hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
                            const void *v, const void *dy, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m,

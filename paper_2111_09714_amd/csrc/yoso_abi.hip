@@ -303,6 +303,8 @@ yoso_status yoso_backward_noalloc(const uint16_t *qcodes, const uint16_t *kcodes
 
 size_t yoso_backward_noalloc_limit(void) { return kNoAllocScratchBytes; }
 
+int32_t yoso_backward_table_threshold(void) { return yoso::backward_table_threshold(); }
+
 yoso_status yoso_l2_normalize(const void *x, yoso_dtype dtype, int64_t rows, int32_t d, void *y, void *stream) {
     g_last_error[0] = '\0';
     YOSO_TRY(check_dtype(dtype));

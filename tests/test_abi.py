@@ -126,6 +126,7 @@ def test_noalloc_refuses_shapes_beyond_its_scratch(L):
     """yoso_backward_noalloc checks the workspace its shapes need against its fixed
     64 MiB scratch before any HIP call."""
     assert L.yoso_backward_noalloc_limit() == 64 << 20
+    assert L.yoso_backward_table_threshold() >= 16  # table buckets span more than one 16-row tile
     p = [FAKE] * 6
     # 32 heads of 4096 rows at m = 32 need about 0.9 GB
     st = L.yoso_backward_noalloc(*p, 0, 32, 4096, 4096, 64, 32, 8, FAKE, FAKE, FAKE, None)

@@ -1,4 +1,4 @@
-"""Host-side pieces of bench.py: the colliding-pair count behind the dQ/dK roofline
+"""Host-side pieces of bench.py: the pair and table-row counts behind the dQ/dK roofline
 and the refusal of more than one GPU (no device needed)."""
 import os
 import subprocess
@@ -13,22 +13,37 @@ torch = pytest.importorskip("torch")
 import bench  # noqa: E402
 
 
-@pytest.mark.parametrize("bh,nq,nk,m,tau", [(3, 50, 57, 4, 3), (1, 1, 1, 1, 1), (2, 200, 130, 7, 8)])
-def test_colliding_pairs_matches_brute_force(bh, nq, nk, m, tau):
+@pytest.mark.parametrize("bh,nq,nk,m,tau,t", [(3, 50, 57, 4, 3, 2), (1, 1, 1, 1, 1, 0), (2, 200, 130, 7, 8, 1),
+                                              (2, 300, 310, 3, 2, 32)])
+def test_bucket_work_matches_brute_force(bh, nq, nk, m, tau, t):
     g = np.random.default_rng(bh + nq + m)
     # high bits above tau are set at random: only the low tau bits are a code
     q = g.integers(0, 2**15, (bh, nq, m)).astype(np.int16)
     k = g.integers(0, 2**15, (bh, nk, m)).astype(np.int16)
     mask = (1 << tau) - 1
+    pairs = pair_form = table_rows = 0
+    for b in range(bh):
+        for h in range(m):
+            for c in range(1 << tau):
+                bq = int(((q[b, :, h] & mask) == c).sum())
+                bk = int(((k[b, :, h] & mask) == c).sum())
+                pairs += bq * bk
+                if bq * bk > t * (bq + bk):
+                    table_rows += bq + bk
+                else:
+                    pair_form += bq * bk
     brute = sum(int(((q[b, :, h, None] & mask) == (k[b, None, :, h] & mask)).sum()) for b in range(bh) for h in range(m))
-    assert bench.colliding_pairs(torch.from_numpy(q), torch.from_numpy(k), tau) == brute
+    assert pairs == brute
+    assert bench.bucket_work(torch.from_numpy(q), torch.from_numpy(k), tau, t) == (pairs, pair_form, table_rows)
 
 
 def test_identical_codes_give_all_pairs_per_bucket():
-    # every row in bucket 0: n_q * n_k pairs per (head, hash)
+    # every row in bucket 0: n_q * n_k pairs per (head, hash), in the table form when
+    # 600 > t * 50
     q = torch.zeros((2, 30, 5), dtype=torch.int16)
     k = torch.zeros((2, 20, 5), dtype=torch.int16)
-    assert bench.colliding_pairs(q, k, 8) == 2 * 5 * 30 * 20
+    assert bench.bucket_work(q, k, 8, 32) == (2 * 5 * 30 * 20, 2 * 5 * 30 * 20, 0)
+    assert bench.bucket_work(q, k, 8, 11) == (2 * 5 * 30 * 20, 0, 2 * 5 * 50)
 
 
 def test_more_than_one_gpu_is_refused():

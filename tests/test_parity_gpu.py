@@ -116,10 +116,12 @@ def run_case(bh, nq, nk, m, tau, dtype, dist="gauss"):
     return g
 
 
-def large_bucket_share(qc, kc, tau, t=16):
+def large_bucket_share(qc, kc, tau, t=None):
     """Fraction of the (row, hash) pairs of both sides that sit in buckets with
-    b_q b_k > t (b_q + b_k): the buckets whose dQ, dK rows the backward computes in
-    the bucket-table form (its switch-over threshold is 16)."""
+    b_q b_k > t (b_q + b_k): with the library's own threshold (the default), the
+    buckets whose dQ, dK rows the backward computes in the bucket-table form."""
+    if t is None:
+        t = Y.yoso_backward_table_threshold()
     nb = 1 << tau
     rows = big = 0
     for b in range(qc.shape[0]):
@@ -138,7 +140,7 @@ TABLE_FORM = [
     (1, 2000, 1300, 6, 6, "f32", "mixture"),   # large and small buckets side by side in one row tile
     (2, 1100, 3000, 3, 3, "bf16", "mixture"),
     (1, 1025, 1030, 2, 1, "f32", "gauss"),     # two buckets; ragged last tiles and partner groups
-    (1, 6000, 5999, 2, 12, "f32", "mixture"),  # a few large buckets among thousands of tiny ones
+    (1, 16000, 15999, 2, 12, "f32", "mixture"),  # a few large buckets among thousands of tiny ones
 ]
 
 
