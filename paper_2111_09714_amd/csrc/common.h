@@ -99,6 +99,13 @@ __device__ __forceinline__ void split4_pow2(const float v[4], float scale, half4
     }
 }
 
+// Load a T at `byte_off` bytes past `base` (a wave-uniform pointer): keeps the
+// per-lane part of the address in one 32-bit register.
+template <typename T>
+__device__ __forceinline__ T ld(const void *base, uint32_t byte_off) {
+    return *reinterpret_cast<const T *>(static_cast<const char *>(base) + byte_off);
+}
+
 // Three-product fp16 emulation of an fp32 MFMA step: acc += a*b.
 __device__ __forceinline__ floatx4 mfma3_16x16x32(const half8 &ah, const half8 &al, const half8 &bh,
                                                   const half8 &bl, floatx4 acc) {

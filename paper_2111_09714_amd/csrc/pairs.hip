@@ -324,13 +324,6 @@ struct PassArgs {
     int tab_t;                       // table form for buckets with b_q b_k > tab_t (b_q + b_k); 0: none
 };
 
-// Load a T at `byte_off` bytes past `base` (a wave-uniform pointer): keeps the
-// per-lane part of the address in one 32-bit register.
-template <typename T>
-__device__ __forceinline__ T ld(const void *base, uint32_t byte_off) {
-    return *reinterpret_cast<const T *>(static_cast<const char *>(base) + byte_off);
-}
-
 // ---- the wave's LDS tile
 // Operands reach the MFMA layouts through one 8 KiB LDS tile per wave.  Global
 // loads are coalesced: the 16 lanes of a quarter-wave read 256 contiguous bytes
@@ -572,12 +565,14 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
                                            int8_t *ex_lds, bool ex_in_lds, int m, const uint32_t *tile_ent,
                                            int nvalid, int q, int cl, int g, int c, const floatx4 outT[4],
                                            float orow) {
-    // max |value| of row c over this lane's 16 values, then over the row's 4 lanes
-    float mx4[4];
+    // max |value| of row c over this lane's 16 values (a chain of 3-input maxima),
+    // then over the row's 4 lanes
+    float mx = 0.f;
 #pragma unroll
-    for (int dt = 0; dt < 4; dt++)
-        mx4[dt] = fmaxf(fmaxf(fabsf(outT[dt][0]), fabsf(outT[dt][1])), fmaxf(fabsf(outT[dt][2]), fabsf(outT[dt][3])));
-    float mx = fmaxf(fmaxf(mx4[0], mx4[1]), fmaxf(mx4[2], mx4[3]));
+    for (int dt = 0; dt < 4; dt++) {
+        mx = fmaxf(fmaxf(mx, fabsf(outT[dt][0])), fabsf(outT[dt][1]));
+        mx = fmaxf(fmaxf(mx, fabsf(outT[dt][2])), fabsf(outT[dt][3]));
+    }
     {
         const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
         mx = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
@@ -607,13 +602,17 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
         int mm[4];
 #pragma unroll
         for (int j = 0; j < 4; j++) mm[j] = min(max(__float2int_rn(outT[dt][j] * sc), -0x7FFFFF), 0x7FFFFF);
+        // byte permutes: the high parts are bytes 1-2 of each M, the low part byte 0
+        // (v_perm_b32 picks any bytes of a register pair: {first operand : second})
+        const uint32_t u[4] = {static_cast<uint32_t>(mm[0]), static_cast<uint32_t>(mm[1]),
+                               static_cast<uint32_t>(mm[2]), static_cast<uint32_t>(mm[3])};
         uint2v w;
-        w.x = (static_cast<uint32_t>(mm[0] >> 8) & 0xFFFFu) | (static_cast<uint32_t>(mm[1] >> 8) << 16);
-        w.y = (static_cast<uint32_t>(mm[2] >> 8) & 0xFFFFu) | (static_cast<uint32_t>(mm[3] >> 8) << 16);
+        w.x = __builtin_amdgcn_perm(u[1], u[0], 0x06050201u);
+        w.y = __builtin_amdgcn_perm(u[3], u[2], 0x06050201u);
         lds_st(tile, mant_off(sw, 4 * dt + g), w);
-        const uint32_t lo = (static_cast<uint32_t>(mm[0]) & 0xFFu) | ((static_cast<uint32_t>(mm[1]) & 0xFFu) << 8) |
-                            ((static_cast<uint32_t>(mm[2]) & 0xFFu) << 16) | (static_cast<uint32_t>(mm[3]) << 24);
-        lds_st(tile, low_off(c, 4 * dt + g), lo);
+        const uint32_t lo01 = __builtin_amdgcn_perm(u[1], u[0], 0x0C0C0400u);  // [b0 of M0, b0 of M1, 0, 0]
+        const uint32_t lo23 = __builtin_amdgcn_perm(u[3], u[2], 0x0C0C0400u);
+        lds_st(tile, low_off(c, 4 * dt + g), __builtin_amdgcn_perm(lo23, lo01, 0x05040100u));
     }
     // rows 4q + i: this lane's chunk cl of each high-part row, then the four stores
     uint2v w[4];
@@ -625,20 +624,24 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
     for (int i = 0; i < 4; i++) lw[i] = lds_ld<uint32_t>(tile, low_off(4 * i + q, cl));
     const uint4 e4 = reinterpret_cast<const uint4 *>(tile_ent)[q];
     const uint32_t re[4] = {e4.x, e4.y, e4.z, e4.w};
+    // (row, hash) record index row * m by a full-rate 24-bit multiply (row < 2^16,
+    // m < 2^10), kept opaque so that it is not folded back into a 32-bit multiply
+    // by m * 64
+    auto rec = [&](uint32_t row) {
+        uint32_t r = __umul24(row, static_cast<uint32_t>(m));
+        asm("" : "+v"(r));
+        return static_cast<uint64_t>(r);
+    };
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-        if (4 * q + i < nvalid && (re[i] >> 16) != kSkipCode) {
-            const uint32_t row = re[i] & 0xFFFFu;
-            __builtin_nontemporal_store(w[i], reinterpret_cast<uint2v *>(part + (row * static_cast<uint32_t>(m)) * D) + cl);
-        }
+        if (4 * q + i < nvalid && (re[i] >> 16) != kSkipCode)
+            __builtin_nontemporal_store(w[i], reinterpret_cast<uint2v *>(part + rec(re[i] & 0xFFFFu) * D) + cl);
     }
 #pragma unroll
     for (int i = 0; i < 4; i++) {
         const uint32_t le = tile_ent[4 * i + q];
-        if (4 * i + q < nvalid && (le >> 16) != kSkipCode) {
-            const uint32_t row = le & 0xFFFFu;
-            __builtin_nontemporal_store(lw[i], reinterpret_cast<uint32_t *>(plow + (row * static_cast<uint32_t>(m)) * D) + cl);
-        }
+        if (4 * i + q < nvalid && (le >> 16) != kSkipCode)
+            __builtin_nontemporal_store(lw[i], reinterpret_cast<uint32_t *>(plow + rec(le & 0xFFFFu) * D) + cl);
     }
 }
 

@@ -247,23 +247,32 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
             const uint32_t *cbase = reinterpret_cast<const uint32_t *>(a.src_codes + src_row0 * a.m);
             const int nsrc = static_cast<int>(a.n_src);
             const int tab_words = (cmask + 1) * G * P;
-            // the lane's word index is code * cmul + loff; a lane whose hash does not exist
-            // adds into a private dummy slot.  Keys past the end add zero words into real
-            // slots (their values are zeroed, their codes read from a clamped row), so a
-            // step has no branch
-            const int cmul = hok ? G * P : 0;
-            const int loff = hok ? hh * P + pp : tab_words + lane;
+            // the lane's word is code * G * P + hh * P + pp: per step one bit-field extract
+            // (the code) and one 24-bit multiply-add give its LDS byte address.  A lane
+            // whose hash does not exist extracts a 0-bit code and adds into a private
+            // dummy slot.  Keys past the end add zero words into real slots (their values
+            // are zeroed, their codes read from a clamped row), so a step has no branch
+            const uint32_t rowb = static_cast<uint32_t>(G * P) * 8u;
+            const uint32_t loffb = static_cast<uint32_t>(hok ? hh * P + pp : tab_words + lane) * 8u;
+            const uint32_t cwid = hok ? static_cast<uint32_t>(a.tau) : 0u;
+            unsigned char *tabb = reinterpret_cast<unsigned char *>(tab);
             // codes are fetched kAhead steps ahead of their use, from a clamped (always
             // valid) row, into a ring of full registers (a 16-bit ring gets packed, and
-            // packing at the chunk loop's back edge waits for every load in flight)
+            // packing at the chunk loop's back edge waits for every load in flight).  With
+            // one key per step the row is the same for the whole wave: a uniform row
+            // pointer and a per-lane constant offset, no per-lane address arithmetic
             constexpr int kAhead = 32;
             static_assert(SPC % kAhead == 0, "prefetch distance must divide the chunk");
             const uint32_t last = static_cast<uint32_t>(nsrc - 1), mm = static_cast<uint32_t>(a.m);
             const uint32_t hcol = static_cast<uint32_t>(h0) + (hok ? static_cast<uint32_t>(hh) : 0u);
             const uint32_t csh = (hcol & 1u) * 16u;
+            const uint32_t hpair = hcol >> 1;  // the lane's 32-bit pair within a row (m even)
             auto code_at = [&](int tc, int st) -> uint32_t {
-                const uint32_t row = static_cast<uint32_t>((wave + kTableWaves * tc) * 64 + st * KPI_C + slot);
-                return cbase[(min(row, last) * mm + hcol) >> 1];
+                const uint32_t row = static_cast<uint32_t>((wave + kTableWaves * tc) * 64 + st * KPI_C);
+                if constexpr (KPI_C == 1)
+                    return ld<uint32_t>(cbase + min(row, last) * (mm >> 1), hpair * 4u);
+                else
+                    return ld<uint32_t>(cbase, (__umul24(min(row + static_cast<uint32_t>(slot), last), mm >> 1) + hpair) * 4u);
             };
             // values of a chunk, lane = key, from a clamped row; rows past the end are
             // zeroed when the chunk is quantised (a select right after the load would
@@ -311,8 +320,9 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
 #pragma unroll
                     for (int u = 0; u < 8; u++) {
                         const int st = 8 * g + u;
-                        const int idx = static_cast<int>((cr[st % kAhead] >> csh) & cmask) * cmul + loff;
-                        atomicAdd(&tab[idx], wd[g & 1][u]);
+                        const uint32_t code = __builtin_amdgcn_ubfe(cr[st % kAhead], csh, cwid);
+                        atomicAdd(reinterpret_cast<unsigned long long *>(tabb + __umul24(code, rowb) + loffb),
+                                  wd[g & 1][u]);
                         cr[st % kAhead] = st + kAhead < SPC ? code_at(tc, st + kAhead) : code_at(tc + 1, st + kAhead - SPC);
                     }
                     // keep the scheduler from hoisting the unrolled chunk (register pressure)
@@ -418,27 +428,35 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
                 csh[t] = KM < 2 ? (hcol[t] & 1u) * 16u : 0u;
             }
             const uint16_t *qhead = a.dst_codes + dst_row0 * a.m;
+            // the byte offset of the 32-bit pair holding hash t's code within a row (m even)
+            uint32_t hbyte[8];
+#pragma unroll
+            for (int t = 0; t < 8; t++) hbyte[t] = (hcol[t] >> 1) * 4u;
             auto fetch = [&](uint32_t cc[8], int64_t i0) {
                 const int64_t i = i0 + gq;
                 const uint32_t icl = i < a.n_dst ? static_cast<uint32_t>(i) : qlast;
+                const uint32_t qbyte = __umul24(icl, 2u * mm);  // the query's row of codes
 #pragma unroll
                 for (int t = 0; t < 8; t++) {
                     if (t < HL) {
                         if constexpr (KM < 2)
-                            cc[t] = reinterpret_cast<const uint32_t *>(qhead)[(icl * mm + hcol[t]) >> 1];
+                            cc[t] = ld<uint32_t>(qhead, qbyte + hbyte[t]);
                         else
                             cc[t] = qhead[icl * mm + hcol[t]];
                     }
                 }
             };
-            // bit t: query i0+gq exists and its lane's hash t exists
-            auto valid = [&](int64_t i0) {
-                const bool qok = i0 + gq < a.n_dst;
-                uint32_t mask = 0;
+            // weight of hash t's row: 1 where the lane's hash t exists.  A query past the
+            // end reads clamped, valid rows and is never stored, so it needs no weight
+            float wt[8];
 #pragma unroll
-                for (int t = 0; t < 8; t++) mask |= (qok && t < HL && hh[t] < gcount) ? (1u << t) : 0u;
-                return mask;
-            };
+            for (int t = 0; t < 8; t++) wt[t] = (t < HL && hh[t] < gcount) ? 1.f : 0.f;
+            // byte offset of hash t's row within a bucket's block of G rows, and of one bucket
+            uint32_t hrow[8];
+#pragma unroll
+            for (int t = 0; t < 8; t++) hrow[t] = static_cast<uint32_t>(min(hh[t], gcount - 1)) * (DS * 4u);
+            const uint32_t bucket_bytes = static_cast<uint32_t>(G) * (DS * 4u);
+            const unsigned char *tabc = reinterpret_cast<const unsigned char *>(tab);
             const int64_t step = static_cast<int64_t>(kTableWaves) * QPI;
             // codes of the next kGD query groups are in flight while one is summed
             constexpr int kGD = KM < 2 ? 4 : 2;
@@ -456,21 +474,18 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
                     if (i0 >= a.n_dst) break;
                     const int64_t i = i0 + gq;
                     const bool qok = i < a.n_dst;
-                    // every lane reads a row (invalid ones read a clamped row and weight
-                    // it by 0): no divergent branch between the reads, and all of a
-                    // group's reads are issued before the first is used
-                    const uint32_t vmask = valid(i0);
+                    // every lane reads a row (a lane whose hash does not exist reads a
+                    // clamped row and weights it by 0): no divergent branch between the
+                    // reads, and all of a group's reads are issued before the first is used
                     float xs[8][DS];
 #pragma unroll
                     for (int t = 0; t < 8; t++) {
                         if (t < HL) {
-                            const int hcl = min(hh[t], gcount - 1);
                             // (a 24-bit multiply: a 32-bit one becomes v_mad_u64_u32, whose unused
                             // high addend half can be allocated to a load in flight, which then
                             // has to be waited for)
-                            const uint32_t rw = __umul24((cR[u][t] >> csh[t]) & static_cast<uint32_t>(cmask),
-                                                         static_cast<uint32_t>(G)) + static_cast<uint32_t>(hcl);
-                            const float *row = reinterpret_cast<const float *>(tab) + rw * DS;
+                            const uint32_t code = __builtin_amdgcn_ubfe(cR[u][t], csh[t], static_cast<uint32_t>(a.tau));
+                            const float *row = reinterpret_cast<const float *>(tabc + __umul24(code, bucket_bytes) + hrow[t]);
                             if constexpr (DS == 2) {
                                 const float2 x = *reinterpret_cast<const float2 *>(row);
                                 xs[t][0] = x.x;
@@ -494,9 +509,8 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
 #pragma unroll
                     for (int t = 0; t < 8; t++) {
                         if (t < HL) {
-                            const float w = ((vmask >> t) & 1u) ? 1.f : 0.f;
 #pragma unroll
-                            for (int d = 0; d < DS; d++) acc[d] = fmaf(xs[t][d], w, acc[d]);
+                            for (int d = 0; d < DS; d++) acc[d] = fmaf(xs[t][d], wt[t], acc[d]);
                         }
                     }
                     // every lane of the query's group holds the sums; lane c4 % L
