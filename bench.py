@@ -94,9 +94,12 @@ def source_digest(files) -> str:
 
 
 # Kernel -> the sources its code comes from (the traffic figure is void once they change).
+_PAIRS = ["paper_2111_09714_amd/csrc/pairs.hip", "paper_2111_09714_amd/csrc/common.h"]
 KERNEL_SOURCES = {
-    "pass_kernel": ["paper_2111_09714_amd/csrc/pairs.hip", "paper_2111_09714_amd/csrc/common.h"],
+    "hash_kernel": ["paper_2111_09714_amd/csrc/hash.hip", "paper_2111_09714_amd/csrc/common.h"],
     "table_kernel": ["paper_2111_09714_amd/csrc/tables.hip", "paper_2111_09714_amd/csrc/common.h"],
+    **{k: _PAIRS for k in ("sort_kernel", "absmax_kernel", "split_kernel", "pass_kernel", "bucket_kernel",
+                           "reduce_kernel", "dense_kernel")},
 }
 
 
@@ -374,7 +377,7 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-configs", action="store_true", help="skip the per-workload `configs` object")
     ap.add_argument("--parts", default="star,l2,yoso_e,fast_hash",
-                    help="measurements besides the step (comma list of star, l2, yoso_e, fast_hash; '' for none), "
+                    help="measurements besides the step (comma list of star, l2, yoso_e, fast_hash; 'none' for none), "
                          "e.g. to profile the step's kernels alone")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, run a plain 256 MiB device copy (read + write) three times, "
