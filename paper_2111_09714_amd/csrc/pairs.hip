@@ -927,10 +927,15 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
 //          partials like a pass tile; entries two tiles ahead, rows one tile ahead.
 // The result for a row is the pass kernel's sum over the same partners, added in
 // another order.  No barrier follows the bucket list: the waves share nothing else.
+// HI1 (bf16 inputs): a bf16 value scaled by a power of two is an fp16 number
+// whenever it lies in fp16's normal range (every value above 2^-27 of its head's
+// largest), so its lo part is zero: only the hi parts are read (half the operand
+// bytes), M takes one product and the apply two.
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kBuildRows = 32;                 // partners per build step
 constexpr int kStageBytes = kBuildRows * 512;  // a wave's tile: staged rows [a' hi | a' lo | b hi | b lo]
 
+template <bool HI1>
 __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
     __shared__ __align__(16) unsigned char stage_lds[kPassWaves * kStageBytes];
     __shared__ __align__(16) uint32_t tent_lds[kPassWaves * 16];  // each wave's tile entries
@@ -1004,27 +1009,31 @@ __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
         const int p0 = uni(poff[cb]), p1 = uni(poff[cb + 1]);
         const int r0 = uni(roff[cb]), r1 = uni(roff[cb + 1]);
 
-        // ---- build.  Staged row 16 (j >> 2) + 4q + (j & 3) of a group holds partner
-        // y0 + that.  Slots past the bucket's end load the bucket's first partner and
-        // are staged as zeros (bit j of the masks, computed from the position alone):
-        // no load is conditional and no loaded value is used before it is needed, so
-        // nothing waits for the loads in flight
+        // ---- build.  Slot j of lane (q, cl) holds 16-byte chunk lch of staged row
+        // slot_row(j), which is partner y0 + that: all 16 chunks of rows 16 (j >> 2) +
+        // 4q + (j & 3), or (HI1) the 8 hi chunks of rows 8j + 2q + (cl >> 3).  Slots past
+        // the bucket's end load the bucket's first partner and are staged as zeros (bit j
+        // of the masks, computed from the position alone): no load is conditional and no
+        // loaded value is used before it is needed, so nothing waits for the loads in flight
+        constexpr int NJ = HI1 ? 4 : 8;
+        const int lch = HI1 ? (cl & 7) : cl;
+        auto slot_row = [&](int j) { return HI1 ? 8 * j + 2 * q + (cl >> 3) : 16 * (j >> 2) + 4 * q + (j & 3); };
         unsigned okn = 0, okr = 0;
-        auto group_ents = [&](int y0, uint32_t e[8]) {
+        auto group_ents = [&](int y0, uint32_t e[NJ]) {
             okn = 0;
 #pragma unroll
-            for (int j = 0; j < 8; j++) {
-                const int y = y0 + 16 * (j >> 2) + 4 * q + (j & 3);
+            for (int j = 0; j < NJ; j++) {
+                const int y = y0 + slot_row(j);
                 okn |= y < p1 ? 1u << j : 0u;
                 e[j] = pent[y < p1 ? y : p0];
             }
         };
-        u32x4 av[8], bv[8];
-        auto group_rows = [&](const uint32_t e[8]) {
+        u32x4 av[NJ], bv[NJ];
+        auto group_rows = [&](const uint32_t e[NJ]) {
             okr = okn;
 #pragma unroll
-            for (int j = 0; j < 8; j++) {
-                const uint32_t off = (e[j] & 0xFFFFu) * (4 * D) + 16 * cl;
+            for (int j = 0; j < NJ; j++) {
+                const uint32_t off = (e[j] & 0xFFFFu) * (4 * D) + 16 * lch;
                 av[j] = ld<u32x4>(apar, off);
                 bv[j] = ld<u32x4>(bpar, off);
             }
@@ -1035,17 +1044,18 @@ __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
 #pragma unroll
             for (int ei = 0; ei < 4; ei++) acc[fi][ei] = floatx4{0.f, 0.f, 0.f, 0.f};
         const int ngrp = (p1 - p0 + kBuildRows - 1) / kBuildRows;
-        uint32_t en[8];
+        uint32_t en[NJ];
         group_ents(p0, en);
         group_rows(en);
         if (ngrp > 1) group_ents(p0 + kBuildRows, en);
         for (int gi = 0; gi < ngrp; gi++) {
 #pragma unroll
-            for (int j = 0; j < 8; j++) {
-                unsigned char *half_tile = st + (j >> 2) * (16 * 512);
+            for (int j = 0; j < NJ; j++) {
+                const int rr = slot_row(j);
+                unsigned char *half_tile = st + (rr >> 4) * (16 * 512);
                 const u32x4 keep = u32x4(0u - ((okr >> j) & 1u));  // all ones or all zeros
-                lds_st(half_tile, swz(4 * q + (j & 3), cl, 512), av[j] & keep);
-                lds_st(half_tile, swz(4 * q + (j & 3), 16 + cl, 512), bv[j] & keep);
+                lds_st(half_tile, swz(rr & 15, lch, 512), av[j] & keep);
+                lds_st(half_tile, swz(rr & 15, 16 + lch, 512), bv[j] & keep);
             }
             if (gi + 1 < ngrp) group_rows(en);
             if (gi + 2 < ngrp) group_ents(p0 + (gi + 2) * kBuildRows, en);
@@ -1054,20 +1064,23 @@ __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
 #pragma unroll
             for (int ei = 0; ei < 4; ei++) {
                 bh[ei] = trpair(16 + 2 * ei);
-                bl[ei] = trpair(24 + 2 * ei);
+                if constexpr (!HI1) bl[ei] = trpair(24 + 2 * ei);
             }
 #pragma unroll
             for (int fi = 0; fi < 4; fi++) {
-                const half8 ah = trpair(2 * fi), al = trpair(8 + 2 * fi);
+                const half8 ah = trpair(2 * fi);
 #pragma unroll
                 for (int ei = 0; ei < 4; ei++)
                     acc[fi][ei] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bh[ei], acc[fi][ei], 0, 0, 0);
+                if constexpr (!HI1) {
+                    const half8 al = trpair(8 + 2 * fi);
 #pragma unroll
-                for (int ei = 0; ei < 4; ei++)
-                    acc[fi][ei] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl[ei], acc[fi][ei], 0, 0, 0);
+                    for (int ei = 0; ei < 4; ei++)
+                        acc[fi][ei] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah, bl[ei], acc[fi][ei], 0, 0, 0);
 #pragma unroll
-                for (int ei = 0; ei < 4; ei++)
-                    acc[fi][ei] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bh[ei], acc[fi][ei], 0, 0, 0);
+                    for (int ei = 0; ei < 4; ei++)
+                        acc[fi][ei] = __builtin_amdgcn_mfma_f32_16x16x32_f16(al, bh[ei], acc[fi][ei], 0, 0, 0);
+                }
             }
         }
 
@@ -1116,18 +1129,22 @@ __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
         // state rotating through three slots with the loop unrolled three times, so
         // no register that a load is still filling is ever copied
         const int ntile = (r1 - r0 + 15) >> 4;
+        // slot i of lane (q, cl): all 16 chunks of row 4q + i, or (HI1) hi chunk cl & 7
+        // of row 8i + 2q + (cl >> 3)
+        constexpr int NI = HI1 ? 2 : 4;
+        auto tile_row = [&](int i) { return HI1 ? 8 * i + 2 * q + (cl >> 3) : 4 * q + i; };
         struct ASlot {
-            uint32_t e[4];
-            uint4 r[4];
+            uint32_t e[NI];
+            uint4 r[NI];
         };
-        auto tile_ents = [&](int t, uint32_t e[4]) {
+        auto tile_ents = [&](int t, uint32_t e[NI]) {
             const int pos = r0 + 16 * min(t, ntile - 1);
 #pragma unroll
-            for (int i = 0; i < 4; i++) e[i] = rent[pos + 4 * q + i < r1 ? pos + 4 * q + i : pos];
+            for (int i = 0; i < NI; i++) e[i] = rent[pos + tile_row(i) < r1 ? pos + tile_row(i) : pos];
         };
-        auto tile_rows = [&](const uint32_t e[4], uint4 r[4]) {
+        auto tile_rows = [&](const uint32_t e[NI], uint4 r[NI]) {
 #pragma unroll
-            for (int i = 0; i < 4; i++) r[i] = ld<uint4>(arow, (e[i] & 0xFFFFu) * (4 * D) + 16 * cl);
+            for (int i = 0; i < NI; i++) r[i] = ld<uint4>(arow, (e[i] & 0xFFFFu) * (4 * D) + 16 * (HI1 ? (cl & 7) : cl));
         };
         ASlot A, B, C;
         tile_ents(0, A.e);
@@ -1138,8 +1155,20 @@ __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
             tile_ents(t + 2, nn.e);
             const int nvalid = min(16, r1 - (r0 + 16 * t));
             half8 rh[2], rl[2];
-            stage_rows(cur.r, st, q, cl, g, c, rh, rl);
-            if (cl == 0) reinterpret_cast<uint4 *>(tent)[q] = make_uint4(cur.e[0], cur.e[1], cur.e[2], cur.e[3]);
+            if constexpr (HI1) {
+                // the rows' hi chunks into the tile, then the B-operand layout of the hi part
+#pragma unroll
+                for (int i = 0; i < NI; i++) lds_st(st, swz(tile_row(i), cl & 7, 256), cur.r[i]);
+#pragma unroll
+                for (int kb = 0; kb < 2; kb++) rh[kb] = lds_ld<half8>(st, swz(c, kb * 4 + g, 256));
+                if ((cl & 7) == 0) {
+#pragma unroll
+                    for (int i = 0; i < NI; i++) tent[tile_row(i)] = cur.e[i];
+                }
+            } else {
+                stage_rows(cur.r, st, q, cl, g, c, rh, rl);
+                if (cl == 0) reinterpret_cast<uint4 *>(tent)[q] = make_uint4(cur.e[0], cur.e[1], cur.e[2], cur.e[3]);
+            }
             floatx4 outT[4];
 #pragma unroll
             for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -1148,11 +1177,13 @@ __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
 #pragma unroll
                 for (int dt = 0; dt < 4; dt++)
                     outT[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(mth[dt][kb], rh[kb], outT[dt], 0, 0, 0);
+            if constexpr (!HI1) {
 #pragma unroll
-            for (int kb = 0; kb < 2; kb++)
+                for (int kb = 0; kb < 2; kb++)
 #pragma unroll
-                for (int dt = 0; dt < 4; dt++)
-                    outT[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(mth[dt][kb], rl[kb], outT[dt], 0, 0, 0);
+                    for (int dt = 0; dt < 4; dt++)
+                        outT[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(mth[dt][kb], rl[kb], outT[dt], 0, 0, 0);
+            }
 #pragma unroll
             for (int kb = 0; kb < 2; kb++)
 #pragma unroll
@@ -1619,7 +1650,9 @@ hipError_t zero_output(void *out, int64_t bytes, hipStream_t stream) {
     return hipGetLastError();
 }
 
-hipError_t launch_pass(const PassArgs &a, int64_t units, bool star, hipStream_t stream) {
+// hi1: the inputs are bf16, so the fp16 lo parts of their scaled copies are zero (see
+// bucket_kernel) and the table form reads hi parts only.
+hipError_t launch_pass(const PassArgs &a, int64_t units, bool star, bool hi1, hipStream_t stream) {
     if (star) {
         KernelTimer timer("pass_star_kernel", stream);
         hipLaunchKernelGGL(pass_kernel<true>, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0, stream,
@@ -1635,7 +1668,12 @@ hipError_t launch_pass(const PassArgs &a, int64_t units, bool star, hipStream_t 
         // after the pass: the pass blocks write their whole exponent rows, the table
         // buckets' entries included, and these writes must land last
         KernelTimer timer("bucket_kernel", stream);
-        hipLaunchKernelGGL(bucket_kernel, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0, stream, a);
+        if (hi1)
+            hipLaunchKernelGGL(bucket_kernel<true>, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0,
+                               stream, a);
+        else
+            hipLaunchKernelGGL(bucket_kernel<false>, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0,
+                               stream, a);
     }
     return hipGetLastError();
 }
@@ -1796,7 +1834,7 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
     a.bh = bh; a.m = m; a.tau = tau;
     a.scale = scale;
     a.tab_t = star ? 0 : kTableT;
-    e = launch_pass(a, units, star, stream);
+    e = launch_pass(a, units, star, bf16, stream);
     if (e != hipSuccess) return e;
     if (bf16) {
         if ((e = launch_reduce<true>(a.pq, a.lq, a.eq, dq, bh * n_q, n_q, m, stream)) != hipSuccess) return e;
