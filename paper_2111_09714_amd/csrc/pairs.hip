@@ -350,8 +350,25 @@ __device__ __forceinline__ void lds_st(unsigned char *base, uint32_t off, const 
     *reinterpret_cast<T *>(base + off) = v;
 }
 
-// One 16-partner sub-tile as loaded: lane l holds 16-byte chunk (l & 15) of
-// partner 4(l >> 4) + i of a' (a[i]) and of b (b[i]).
+// HI1 (bf16 inputs): a bf16 value scaled by a power of two is an fp16 number
+// wherever it lies in fp16's normal range (every value above 2^-27 of its head's
+// largest), so the lo halves of the fp16 (hi, lo) copies are zero.  Only the hi
+// halves are then loaded, staged and multiplied: slot i of lane (q, cl) holds hi
+// chunk cl & 7 of partner (or row) 4q + 2i + (cl >> 3), two slots per lane; in the
+// general form slot i holds chunk cl of partner (or row) 4q + i, four slots.
+template <bool HI1>
+__device__ __forceinline__ int slot_row(int q, int cl, int i) { return HI1 ? 4 * q + 2 * i + (cl >> 3) : 4 * q + i; }
+template <bool HI1>
+__device__ __forceinline__ int slot_chunk(int cl) { return HI1 ? (cl & 7) : cl; }
+// the entry of slot i from the lane's entries of partners (rows) 4q .. 4q+3
+template <bool HI1>
+__device__ __forceinline__ uint32_t slot_entry(const uint4 &e4, int cl, int i) {
+    const uint32_t e[4] = {e4.x, e4.y, e4.z, e4.w};
+    if constexpr (HI1) return (cl >> 3) ? e[2 * i + 1] : e[2 * i];
+    return e[i];
+}
+
+// One 16-partner sub-tile as loaded: slot i of a' (a[i]) and of b (b[i]).
 struct Sub {
     uint4 a[4], b[4];
 };
@@ -360,37 +377,42 @@ struct Sub {
 // aligned 16-byte load.  Entries past the unit's end are sentinels (row 0, an
 // impossible code), so every load is in bounds and a partner outside the tile's
 // buckets is masked by its code.
+template <bool HI1>
 __device__ __forceinline__ void load_sub(Sub &s, const uint4 &pe, const _Float16 *apar, const _Float16 *bpar,
                                          int cl) {
-    const uint32_t e[4] = {pe.x, pe.y, pe.z, pe.w};
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-        const uint32_t off = (e[i] & 0xFFFFu) * (4 * D) + 16 * cl;
+    for (int i = 0; i < (HI1 ? 2 : 4); i++) {
+        const uint32_t off = (slot_entry<HI1>(pe, cl, i) & 0xFFFFu) * (4 * D) + 16 * slot_chunk<HI1>(cl);
         s.a[i] = ld<uint4>(apar, off);
         s.b[i] = ld<uint4>(bpar, off);
     }
 }
 
-// The 16 rows of a tile as loaded: lane l holds chunk (l & 15) of row 4(l >> 4) + i;
-// `re4` holds the entries of rows 4q .. 4q+3.
+// The 16 rows of a tile as loaded (slots as above); `re4` holds the entries of rows
+// 4q .. 4q+3.
+template <bool HI1>
 __device__ __forceinline__ void load_row_tile(uint4 r[4], const uint4 &re4, const _Float16 *arow, int cl) {
-    const uint32_t e[4] = {re4.x, re4.y, re4.z, re4.w};
 #pragma unroll
-    for (int i = 0; i < 4; i++) r[i] = ld<uint4>(arow, (e[i] & 0xFFFFu) * (4 * D) + 16 * cl);
+    for (int i = 0; i < (HI1 ? 2 : 4); i++)
+        r[i] = ld<uint4>(arow, (slot_entry<HI1>(re4, cl, i) & 0xFFFFu) * (4 * D) + 16 * slot_chunk<HI1>(cl));
 }
 
 // Rows through the tile into the MFMA B-operand layout of S^T: lane (g, c) gets
-// row c, dims kb*32 + 8g + [0, 8) (hi and lo).  Returns e_c with ||a_c|| < 2^e_c
-// for the lane's row c (from the fp16 pairs the products use; the row's other
-// three quarters sit in the lanes 16, 32 and 48 away).
+// row c, dims kb*32 + 8g + [0, 8) (hi and lo; HI1: hi, and lo is zero).  Returns
+// e_c with ||a_c|| < 2^e_c for the lane's row c (from the fp16 pairs the products
+// use; the row's other three quarters sit in the lanes 16, 32 and 48 away).
+template <bool HI1>
 __device__ __forceinline__ int stage_rows(const uint4 r[4], unsigned char *tile, int q, int cl, int g, int c,
                                           half8 rh[2], half8 rl[2]) {
 #pragma unroll
-    for (int i = 0; i < 4; i++) lds_st(tile, swz(4 * q + i, cl, 256), r[i]);
+    for (int i = 0; i < (HI1 ? 2 : 4); i++) lds_st(tile, swz(slot_row<HI1>(q, cl, i), slot_chunk<HI1>(cl), 256), r[i]);
 #pragma unroll
     for (int kb = 0; kb < 2; kb++) {
         rh[kb] = lds_ld<half8>(tile, swz(c, kb * 4 + g, 256));
-        rl[kb] = lds_ld<half8>(tile, swz(c, 8 + kb * 4 + g, 256));
+        if constexpr (HI1)
+            rl[kb] = half8{};
+        else
+            rl[kb] = lds_ld<half8>(tile, swz(c, 8 + kb * 4 + g, 256));
     }
     float ss = 0.f;
 #pragma unroll
@@ -418,15 +440,19 @@ __device__ __forceinline__ int stage_rows(const uint4 r[4], unsigned char *tile,
 // The rows' own b vectors (the q of a query row, the k of a key row; used by
 // *YOSO for q.k) through the second half of the tile into the same B-operand
 // layout: lane (g, c) gets row c, dims kb*32 + 8g + [0, 8).
+template <bool HI1>
 __device__ __forceinline__ void stage_rows_b(const uint4 r[4], unsigned char *tile, int q, int cl, int g, int c,
                                              half8 bh[2], half8 bl[2]) {
     unsigned char *t = tile + 16 * 256;
 #pragma unroll
-    for (int i = 0; i < 4; i++) lds_st(t, swz(4 * q + i, cl, 256), r[i]);
+    for (int i = 0; i < (HI1 ? 2 : 4); i++) lds_st(t, swz(slot_row<HI1>(q, cl, i), slot_chunk<HI1>(cl), 256), r[i]);
 #pragma unroll
     for (int kb = 0; kb < 2; kb++) {
         bh[kb] = lds_ld<half8>(t, swz(c, kb * 4 + g, 256));
-        bl[kb] = lds_ld<half8>(t, swz(c, 8 + kb * 4 + g, 256));
+        if constexpr (HI1)
+            bl[kb] = half8{};
+        else
+            bl[kb] = lds_ld<half8>(t, swz(c, 8 + kb * 4 + g, 256));
     }
 }
 
@@ -438,11 +464,12 @@ __device__ __forceinline__ half4 tr_load(const unsigned char *p) {
 
 // Sub-tile into the tile (LDS executes one wave's accesses in order, so the reads
 // of compute_sub see these writes; the tile is private to the wave).
+template <bool HI1>
 __device__ __forceinline__ void publish_sub(const Sub &s, unsigned char *tile, int q, int cl) {
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-        lds_st(tile, swz(4 * q + i, cl, 512), s.a[i]);
-        lds_st(tile, swz(4 * q + i, 16 + cl, 512), s.b[i]);
+    for (int i = 0; i < (HI1 ? 2 : 4); i++) {
+        lds_st(tile, swz(slot_row<HI1>(q, cl, i), slot_chunk<HI1>(cl), 512), s.a[i]);
+        lds_st(tile, swz(slot_row<HI1>(q, cl, i), 16 + slot_chunk<HI1>(cl), 512), s.b[i]);
     }
 }
 
@@ -452,7 +479,9 @@ __device__ __forceinline__ void publish_sub(const Sub &s, unsigned char *tile, i
 // *YOSO's weight bound: 1 - x^2 is raised to at least 1/64 (|x| <= 0.99216).
 constexpr float kStarFloor = 1.0f / 64.0f;
 
-template <bool STAR>
+// HI1: the lo halves are zero; only the products with a hi operand on both sides of
+// a' . a and b . S remain (S itself is a general fp32 value and keeps its pair).
+template <bool STAR, bool HI1>
 __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uint4 &pe, const half8 rh[2],
                                             const half8 rl[2], const half8 rbh[2], const half8 rbl[2], float xscale,
                                             int rcode, float sfac, int g, int c, floatx4 outT[4]) {
@@ -461,7 +490,7 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uin
 #pragma unroll
     for (int kb = 0; kb < 2; kb++) {
         ah[kb] = lds_ld<half8>(tile, swz(c, kb * 4 + g, 512));
-        al[kb] = lds_ld<half8>(tile, swz(c, 8 + kb * 4 + g, 512));
+        if constexpr (!HI1) al[kb] = lds_ld<half8>(tile, swz(c, 8 + kb * 4 + g, 512));
     }
     // B_y^T as the A operand of a 16x16x16 MFMA: lane (g, c) needs partners 4g+i of
     // dim 16dt+c.  ds_read_b64_tr_b16 gives destination lane 4a+b of a 16-lane
@@ -473,17 +502,19 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uin
 #pragma unroll
     for (int dt = 0; dt < 4; dt++) {
         bth[dt] = tr_load(tile + swz(pr, 16 + 2 * dt + (a4 >> 1), 512) + 8 * (a4 & 1));
-        btl[dt] = tr_load(tile + swz(pr, 24 + 2 * dt + (a4 >> 1), 512) + 8 * (a4 & 1));
+        if constexpr (!HI1) btl[dt] = tr_load(tile + swz(pr, 24 + 2 * dt + (a4 >> 1), 512) + 8 * (a4 & 1));
     }
     // S^T[partner 4g+i][row c]: two independent accumulation chains (one per 32
     // dims) interleaved, so consecutive MFMAs do not wait on each other
     const floatx4 z = {0.f, 0.f, 0.f, 0.f};
     floatx4 s0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[0], rh[0], z, 0, 0, 0);
     floatx4 s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[1], rh[1], z, 0, 0, 0);
-    s0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[0], rl[0], s0, 0, 0, 0);
-    s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[1], rl[1], s1, 0, 0, 0);
-    s0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[0], rh[0], s0, 0, 0, 0);
-    s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[1], rh[1], s1, 0, 0, 0);
+    if constexpr (!HI1) {
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[0], rl[0], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[1], rl[1], s1, 0, 0, 0);
+        s0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[0], rh[0], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(al[1], rh[1], s1, 0, 0, 0);
+    }
     const floatx4 st = s0 + s1;
     const uint32_t e[4] = {pe.x, pe.y, pe.z, pe.w};
     float sv[4];
@@ -497,14 +528,16 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uin
 #pragma unroll
         for (int kb = 0; kb < 2; kb++) {
             xh[kb] = lds_ld<half8>(tile, swz(c, 16 + kb * 4 + g, 512));
-            xl[kb] = lds_ld<half8>(tile, swz(c, 24 + kb * 4 + g, 512));
+            if constexpr (!HI1) xl[kb] = lds_ld<half8>(tile, swz(c, 24 + kb * 4 + g, 512));
         }
         floatx4 x0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xh[0], rbh[0], z, 0, 0, 0);
         floatx4 x1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xh[1], rbh[1], z, 0, 0, 0);
-        x0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xh[0], rbl[0], x0, 0, 0, 0);
-        x1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xh[1], rbl[1], x1, 0, 0, 0);
-        x0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xl[0], rbh[0], x0, 0, 0, 0);
-        x1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xl[1], rbh[1], x1, 0, 0, 0);
+        if constexpr (!HI1) {
+            x0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xh[0], rbl[0], x0, 0, 0, 0);
+            x1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xh[1], rbl[1], x1, 0, 0, 0);
+            x0 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xl[0], rbh[0], x0, 0, 0, 0);
+            x1 = __builtin_amdgcn_mfma_f32_16x16x32_f16(xl[1], rbh[1], x1, 0, 0, 0);
+        }
         const floatx4 xt = x0 + x1;
 #pragma unroll
         for (int i = 0; i < 4; i++) {
@@ -523,8 +556,10 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uin
     for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(bth[dt], sh, outT[dt], 0, 0, 0);
 #pragma unroll
     for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(bth[dt], sl, outT[dt], 0, 0, 0);
+    if constexpr (!HI1) {
 #pragma unroll
-    for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(btl[dt], sh, outT[dt], 0, 0, 0);
+        for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(btl[dt], sh, outT[dt], 0, 0, 0);
+    }
 }
 
 // Byte offset of 8-byte chunk ch (int16 dims 4ch .. 4ch+3) of the mantissa row in
@@ -649,7 +684,7 @@ __device__ __forceinline__ int uni(int x) { return __builtin_amdgcn_readfirstlan
 
 // STAR: *YOSO's estimator on derived codes (see launch_backward_star); its extra
 // operands run at one workgroup per CU.
-template <bool STAR>
+template <bool STAR, bool HI1>
 __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassArgs a) {
     __shared__ __align__(16) unsigned char tiles_lds[kPassWaves * kTileBytes];
     __shared__ int32_t plan_beg[kPlanTiles];      // first partner of each row tile's bucket range
@@ -831,8 +866,8 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
                 sl.t = t;
                 sl.pe = pent4(y);
                 if (new_tile) {
-                    load_row_tile(sl.rw, row_entries4(t), arow, cl);
-                    if constexpr (STAR) load_row_tile(sl.rb, row_entries4(t), brow, cl);
+                    load_row_tile<HI1>(sl.rw, row_entries4(t), arow, cl);
+                    if constexpr (STAR) load_row_tile<HI1>(sl.rb, row_entries4(t), brow, cl);
                 }
             };
             Slot A, B, C;
@@ -854,12 +889,12 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
                 cursor_at(t1);
             }
             half8 rh[2], rl[2], rbh[2], rbl[2];
-            int erow = stage_rows(A.rw, tile, q, cl, g, c, rh, rl);  // ||a_c|| < 2^erow
-            if constexpr (STAR) stage_rows_b(A.rb, tile, q, cl, g, c, rbh, rbl);
+            int erow = stage_rows<HI1>(A.rw, tile, q, cl, g, c, rh, rl);  // ||a_c|| < 2^erow
+            if constexpr (STAR) stage_rows_b<HI1>(A.rb, tile, q, cl, g, c, rbh, rbl);
             // one operand buffer: a sub-tile's registers are reloaded with the next
             // sub-tile as soon as they have been written to the tile
             Sub S;
-            load_sub(S, A.pe, apar, bpar, cl);
+            load_sub<HI1>(S, A.pe, apar, bpar, cl);
             floatx4 outT[4];
 #pragma unroll
             for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -873,11 +908,11 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
                     t2 = pt;
                     y2 = pbase + 16 * (j + 2);
                 }
-                publish_sub(S, tile, q, cl);
+                publish_sub<HI1>(S, tile, q, cl);
                 fill(nn, t2, y2, has2 && t2 != nxt.t);
                 const bool newtile = !has1 || nxt.t != cur.t;
-                if (has1) load_sub(S, nxt.pe, apar, bpar, cl);
-                compute_sub<STAR>(tile, cur.pe, rh, rl, rbh, rbl, xscale, static_cast<int>(row_entry(cur.t) >> 16),
+                if (has1) load_sub<HI1>(S, nxt.pe, apar, bpar, cl);
+                compute_sub<STAR, HI1>(tile, cur.pe, rh, rl, rbh, rbl, xscale, static_cast<int>(row_entry(cur.t) >> 16),
                                   ldexpf(1.0f, -2 - erow), g, c, outT);
                 if (newtile) {
                     store_tile(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, tile_ents(cur.t), row_count(cur.t), q, cl,
@@ -886,8 +921,8 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
                     for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
                     zero_tiles(cur.t + 1, has1 ? nxt.t : thi);
                     if (has1) {
-                        erow = stage_rows(nxt.rw, tile, q, cl, g, c, rh, rl);
-                        if constexpr (STAR) stage_rows_b(nxt.rb, tile, q, cl, g, c, rbh, rbl);
+                        erow = stage_rows<HI1>(nxt.rw, tile, q, cl, g, c, rh, rl);
+                        if constexpr (STAR) stage_rows_b<HI1>(nxt.rb, tile, q, cl, g, c, rbh, rbl);
                     }
                 }
                 return has1;
@@ -1166,7 +1201,7 @@ __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
                     for (int i = 0; i < NI; i++) tent[tile_row(i)] = cur.e[i];
                 }
             } else {
-                stage_rows(cur.r, st, q, cl, g, c, rh, rl);
+                stage_rows<false>(cur.r, st, q, cl, g, c, rh, rl);
                 if (cl == 0) reinterpret_cast<uint4 *>(tent)[q] = make_uint4(cur.e[0], cur.e[1], cur.e[2], cur.e[3]);
             }
             floatx4 outT[4];
@@ -1235,7 +1270,9 @@ __global__ __launch_bounds__(256) void split_kernel(const void *__restrict__ q, 
         half8 hi, lo;
         split8(x, scale, hi, lo);
         *reinterpret_cast<half8 *>(dst + row * (2 * D) + o) = hi;
-        *reinterpret_cast<half8 *>(dst + row * (2 * D) + D + o) = lo;
+        // bf16 inputs: the lo halves are zero (wherever the scaled value is a normal
+        // fp16 number) and the pair passes read hi halves only
+        if constexpr (!BF16) *reinterpret_cast<half8 *>(dst + row * (2 * D) + D + o) = lo;
     }
 }
 
@@ -1651,17 +1688,22 @@ hipError_t zero_output(void *out, int64_t bytes, hipStream_t stream) {
 }
 
 // hi1: the inputs are bf16, so the fp16 lo parts of their scaled copies are zero (see
-// bucket_kernel) and the table form reads hi parts only.
+// load_sub) and both forms read hi parts only.
 hipError_t launch_pass(const PassArgs &a, int64_t units, bool star, bool hi1, hipStream_t stream) {
+    const dim3 grid(static_cast<unsigned>(2 * units)), block(kPassThreads);
     if (star) {
         KernelTimer timer("pass_star_kernel", stream);
-        hipLaunchKernelGGL(pass_kernel<true>, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0, stream,
-                           a);
+        if (hi1)
+            hipLaunchKernelGGL((pass_kernel<true, true>), grid, block, 0, stream, a);
+        else
+            hipLaunchKernelGGL((pass_kernel<true, false>), grid, block, 0, stream, a);
     } else {
         {
             KernelTimer timer("pass_kernel", stream);
-            hipLaunchKernelGGL(pass_kernel<false>, dim3(static_cast<unsigned>(2 * units)), dim3(kPassThreads), 0,
-                               stream, a);
+            if (hi1)
+                hipLaunchKernelGGL((pass_kernel<false, true>), grid, block, 0, stream, a);
+            else
+                hipLaunchKernelGGL((pass_kernel<false, false>), grid, block, 0, stream, a);
         }
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess || a.tab_t == 0) return e;
