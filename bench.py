@@ -98,7 +98,7 @@ _PAIRS = ["paper_2111_09714_amd/csrc/pairs.hip", "paper_2111_09714_amd/csrc/comm
 KERNEL_SOURCES = {
     "hash_kernel": ["paper_2111_09714_amd/csrc/hash.hip", "paper_2111_09714_amd/csrc/common.h"],
     "table_kernel": ["paper_2111_09714_amd/csrc/tables.hip", "paper_2111_09714_amd/csrc/common.h"],
-    **{k: _PAIRS for k in ("sort_kernel", "absmax_kernel", "split_kernel", "pass_kernel", "bucket_kernel",
+    **{k: _PAIRS for k in ("codes_t_kernel", "sort_kernel", "absmax_kernel", "split_kernel", "pass_kernel", "bucket_kernel",
                            "reduce_kernel", "dense_kernel")},
 }
 
@@ -153,7 +153,8 @@ def cpu_baseline(w, inp, heads, min_wall: float = 10.0):
     }
 
 
-STEP_KERNELS = ("hash_kernel", "table_kernel", "sort_kernel", "absmax_kernel", "split_kernel", "pass_kernel",
+STEP_KERNELS = ("hash_kernel", "table_kernel", "codes_t_kernel", "sort_kernel", "absmax_kernel", "split_kernel",
+                "pass_kernel",
                 "bucket_kernel",
                 "reduce_kernel", "dense_kernel", "zero_kernel")
 

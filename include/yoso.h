@@ -177,7 +177,8 @@ yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const v
  * workspace: yoso_workspace_bytes(YOSO_OP_BACKWARD, ...) bytes of scratch: the
  * per-hash bucket orders, the per-head maxima of |q|, |k|, |v|, |dy|, fp16
  * (hi, lo) copies of q, k, v, dy, and one 24-bit fixed-point partial row per
- * (row, hash) for dq and dk: about (3*m*d + 5*m + 8*d) * (n_q + n_k) * bh bytes.
+ * (row, hash) for dq and dk, the codes transposed to [bh][m][n] for the bucket
+ * sort: about (3*m*d + 7*m + 8*d) * (n_q + n_k) * bh bytes.
  * A bucket with b_q queries and b_k keys whose sizes pass
  * yoso_backward_table_threshold() is summed in the table form of Sec. 3.3
  * restricted to that bucket (one d x d matrix per side and bucket, applied to the
@@ -211,7 +212,7 @@ yoso_status yoso_backward(const uint16_t *qcodes, const uint16_t *kcodes, const 
  * 8/pi (|x| > 0.99216).  x is the dot product of the rows as given, taken as
  * unit length (Remark 1).  Arguments, layouts and errors as for yoso_backward;
  * workspace: yoso_workspace_bytes(YOSO_OP_BACKWARD_STAR, ...) bytes, about
- * (3*m*tau*d + 7*m*tau + 8*d) * (n_q + n_k) * bh (the pairs of m*tau derived
+ * (3*m*tau*d + 9*m*tau + 8*d) * (n_q + n_k) * bh (the pairs of m*tau derived
  * (tau-1)-bit hashes, one 24-bit partial row per row and derived hash); m*tau is
  * also the limit on bh that yoso_backward puts on m.  Its pair pass does about
  * tau + 1 times the work of yoso_backward's (pairs one bit apart count too).

@@ -68,7 +68,8 @@ inline size_t sort_base_lds(int nt, int tau) {
     return (static_cast<size_t>(nt / 64) * (size_t{1} << tau) + nt) * 4 +
            static_cast<size_t>(sort_placing_waves(tau, nt / 64)) * (size_t{1} << tau) * 8;
 }
-constexpr size_t kSortStageLds = 120 * 1024;  // LDS bound of a sort workgroup that stages its column
+constexpr size_t kSortStageLds = 120 * 1024;  // LDS bound of a sort workgroup that stages codes and entries
+constexpr size_t kSortEntLds = 160 * 1024;    // LDS bound of a sort workgroup that stages its entries only
 constexpr int kPassThreads = 256;
 constexpr int kPassWaves = kPassThreads / 64;
 constexpr int kReduceThreads = 256;
@@ -105,19 +106,80 @@ __device__ __forceinline__ bool table_bucket(int32_t bq, int32_t bk, int t) {
 }
 
 // ---------------------------------------------------------------- counting sort
-// codes are [bh][n][m]; unit = b*m + h reads column h with stride m.
+// Codes transposed to [bh][m][n] (codes_t_kernel): one block's column is contiguous.
+// (Read from the [bh][n][m] layout, every 2-byte code of a column was a 64-byte
+// segment of its own, and each of a head's m hash blocks fetched the whole array.)
+// VEC (m a multiple of 8): the tile's rows are read 8 codes (16 bytes) at a time;
+// its columns are written 8 codes at a time where the 8 rows are all there.
+template <bool VEC>
+__global__ __launch_bounds__(256) void codes_t_kernel(const uint16_t *__restrict__ in, uint16_t *__restrict__ out,
+                                                      int64_t bh, int64_t n, int m) {
+    // item (b, row tile of 64, column tile of 64), grid-stride; the tile is padded so
+    // that the transposed reads of a row of it hit distinct banks
+    __shared__ uint16_t tile[64][66];
+    const int64_t ntr = (n + 63) / 64;
+    const int ntc = (m + 63) / 64;
+    for (int64_t blk = blockIdx.x; blk < bh * ntr * ntc; blk += gridDim.x) {
+        const int tc = static_cast<int>(blk % ntc);
+        const int64_t tr = (blk / ntc) % ntr;
+        const int64_t b = blk / (static_cast<int64_t>(ntc) * ntr);
+        const int64_t r0 = tr * 64;
+        const int c0 = tc * 64;
+        if constexpr (VEC) {
+            // 64 rows x 8 groups of 8 codes: one 16-byte load per thread and pass
+            for (int e = threadIdx.x; e < 64 * 8; e += 256) {
+                const int r = e >> 3, c8 = (e & 7) * 8;
+                if (r0 + r < n && c0 + c8 < m) {
+                    const uint4 w = *reinterpret_cast<const uint4 *>(in + (b * n + r0 + r) * m + c0 + c8);
+                    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+                    for (int i = 0; i < 4; i++) {
+                        tile[c8 + 2 * i][r] = static_cast<uint16_t>(ws[i]);
+                        tile[c8 + 2 * i + 1][r] = static_cast<uint16_t>(ws[i] >> 16);
+                    }
+                }
+            }
+        } else {
+            for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+                const int r = e >> 6, c = e & 63;
+                if (r0 + r < n && c0 + c < m) tile[c][r] = in[(b * n + r0 + r) * m + c0 + c];
+            }
+        }
+        __syncthreads();
+        for (int e = threadIdx.x; e < 64 * 8; e += 256) {
+            const int c = e >> 3, r8 = (e & 7) * 8;
+            if (c0 + c >= m) continue;
+            uint16_t *dst = out + (b * m + c0 + c) * n + r0 + r8;
+            if (VEC && r0 + r8 + 8 <= n && ((reinterpret_cast<uintptr_t>(dst) & 15) == 0)) {
+                uint4 w;
+                w.x = tile[c][r8] | (static_cast<uint32_t>(tile[c][r8 + 1]) << 16);
+                w.y = tile[c][r8 + 2] | (static_cast<uint32_t>(tile[c][r8 + 3]) << 16);
+                w.z = tile[c][r8 + 4] | (static_cast<uint32_t>(tile[c][r8 + 5]) << 16);
+                w.w = tile[c][r8 + 6] | (static_cast<uint32_t>(tile[c][r8 + 7]) << 16);
+                *reinterpret_cast<uint4 *>(dst) = w;
+            } else {
+                for (int i = 0; i < 8 && r0 + r8 + i < n; i++) dst[i] = tile[c][r8 + i];
+            }
+        }
+        __syncthreads();  // the tile is refilled for the next item of the stride
+    }
+}
+
+// unit = b*m + h reads column h of head b: with stride m from the codes as given
+// ([bh][n][m], `transposed` false), or contiguous from codes_t_kernel's copy.
 template <int NT>
 __global__ __launch_bounds__(NT) void sort_kernel(const uint16_t *__restrict__ qcodes,
                                                             const uint16_t *__restrict__ kcodes, int m,
-                                                            int64_t n_q, int64_t n_k, int tau, bool stage,
+                                                            int64_t n_q, int64_t n_k, int tau, bool transposed,
+                                                            bool stage_codes, bool stage_ent,
                                                             int32_t *__restrict__ qoff, int32_t *__restrict__ koff,
                                                             uint32_t *__restrict__ qent,
                                                             uint32_t *__restrict__ kent) {
     // [NW][buckets] per-wave counts, then per-wave cursors; + [NT]
-    // scan scratch; + [placing waves][buckets] 64-bit lane masks; when `stage`, the
-    // column's codes (read from memory once, with stride m) and the sorted entries,
-    // which are then written out whole (single scattered 4-byte stores would each
-    // cost a partial-line write)
+    // scan scratch; + [placing waves][buckets] 64-bit lane masks; when `stage_ent`,
+    // the sorted entries, which are then written out whole (single scattered 4-byte
+    // stores would each cost a partial-line write); when `stage_codes`, the column's
+    // codes (read from memory once)
     constexpr int NW = NT / 64;
     extern __shared__ int32_t hist[];
     const int B = 1 << tau;
@@ -130,8 +192,9 @@ __global__ __launch_bounds__(NT) void sort_kernel(const uint16_t *__restrict__ q
     const int64_t b = unit / m;
     const int h = static_cast<int>(unit - b * m);
     const int64_t n = kside ? n_k : n_q;
-    uint16_t *cst = reinterpret_cast<uint16_t *>(est + (stage ? (kside ? n_k : n_q) : 0));
-    const uint16_t *codes = (kside ? kcodes : qcodes) + b * n * m + h;
+    uint16_t *cst = reinterpret_cast<uint16_t *>(est + (stage_ent ? n : 0));
+    const uint16_t *codes = (kside ? kcodes : qcodes) + (transposed ? (b * m + h) * n : b * n * m + h);
+    const int64_t cstride = transposed ? 1 : m;
     int32_t *off = (kside ? koff : qoff) + unit * (B + 1);
     uint32_t *ent = (kside ? kent : qent) + unit * ent_stride(n);
     const int tid = threadIdx.x, lane = tid & 63;
@@ -145,23 +208,23 @@ __global__ __launch_bounds__(NT) void sort_kernel(const uint16_t *__restrict__ q
     for (int c = tid; c < pw * B; c += NT) masks[c] = 0ull;
     __syncthreads();
     {
-        // sixteen codes per lane in flight before their counts are added (the codes
-        // come with stride m, one 64-byte segment each; one at a time, every load's
-        // latency was paid in turn); rows past r1 read row r1 - 1 and are not counted
+        // sixteen codes per lane in flight before their counts are added (one at a
+        // time, every load's latency was paid in turn); rows past r1 read row r1 - 1
+        // and are not counted
         constexpr int U = 16;
         for (int64_t i0 = r0 + lane; i0 < r1; i0 += 64 * U) {
             uint32_t cc[U];
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const int64_t i = i0 + 64 * u;
-                cc[u] = codes[(i < r1 ? i : r1 - 1) * m];
+                cc[u] = codes[(i < r1 ? i : r1 - 1) * cstride];
             }
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const int64_t i = i0 + 64 * u;
                 if (i < r1) {
                     const int c = static_cast<int>(cc[u]) & (B - 1);
-                    if (stage) cst[i] = static_cast<uint16_t>(c);
+                    if (stage_codes) cst[i] = static_cast<uint16_t>(c);
                     atomicAdd(&hist[wave * B + c], 1);
                 }
             }
@@ -211,14 +274,14 @@ __global__ __launch_bounds__(NT) void sort_kernel(const uint16_t *__restrict__ q
             const int64_t i = base + lane;
             const bool valid = i < r1;
             const int64_t ic = valid ? i : r1 - 1;
-            const uint32_t c = stage ? cst[ic] : codes[ic * m] & (B - 1);
+            const uint32_t c = stage_codes ? cst[ic] : codes[ic * cstride] & (B - 1);
             if (valid) atomicOr(&mk[c], 1ull << lane);
             const unsigned long long mask = mk[c];
             const int32_t first = cur[c];
             const int rank = __popcll(mask & ((1ull << lane) - 1ull));
             if (valid) {
                 const uint32_t e = (c << 16) | static_cast<uint32_t>(i);
-                if (stage)
+                if (stage_ent)
                     est[first + rank] = e;
                 else
                     ent[first + rank] = e;
@@ -229,7 +292,7 @@ __global__ __launch_bounds__(NT) void sort_kernel(const uint16_t *__restrict__ q
             }
         }
     }
-    if (stage) {
+    if (stage_ent) {
         __syncthreads();
         // the entries, then the sentinels, 16 bytes per thread (ent_stride is a
         // multiple of 4 and the unit's entry array starts 16-byte aligned)
@@ -1749,6 +1812,8 @@ BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, 
     L.koff = o; o = align_up(o + units * nb * 4);
     L.qent = o; o = align_up(o + units * ent_stride(n_q) * 4);
     L.kent = o; o = align_up(o + units * ent_stride(n_k) * 4);
+    L.qct = o; o = align_up(o + static_cast<size_t>(units) * n_q * 2);
+    L.kct = o; o = align_up(o + static_cast<size_t>(units) * n_k * 2);
     L.qs = o; o = align_up(o + static_cast<size_t>(bh) * n_q * D * 4);
     L.dys = o; o = align_up(o + static_cast<size_t>(bh) * n_q * D * 4);
     L.ks = o; o = align_up(o + static_cast<size_t>(bh) * n_k * D * 4);
@@ -1790,23 +1855,47 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
     }
 
     {
+        // Sort modes, by what fits in a workgroup's LDS: (1) the column's codes (read
+        // once, with stride m) and its sorted entries staged, 6 bytes per row; (2) the
+        // codes transposed to [bh][m][n] first (each block then reads its column
+        // contiguously) and the entries staged, 4 bytes per row; (3) transposed codes,
+        // entries stored straight to memory (eight waves when tau <= 10).
         size_t sort_lds = sort_base_lds(kSortThreads, tau);
-        // stage the column's codes and entries in LDS when they fit (6 bytes per row)
         const int64_t n_max = n_q > n_k ? n_q : n_k;
-        const bool stage = sort_lds + static_cast<size_t>(n_max) * 6 <= kSortStageLds;
-        if (stage) sort_lds += static_cast<size_t>(n_max) * 6;
-        const bool wide = !stage && tau <= 10;
+        const bool stage_codes = sort_lds + static_cast<size_t>(n_max) * 6 <= kSortStageLds;
+        const bool stage_ent = stage_codes || sort_lds + static_cast<size_t>(n_max) * 4 <= kSortEntLds;
+        const bool transposed = !stage_codes;
+        sort_lds += stage_codes ? static_cast<size_t>(n_max) * 6 : stage_ent ? static_cast<size_t>(n_max) * 4 : 0;
+        const bool wide = !stage_ent && tau <= 10;
+        uint16_t *qct = reinterpret_cast<uint16_t *>(ws + L.qct), *kct = reinterpret_cast<uint16_t *>(ws + L.kct);
+        if (transposed) {
+            for (int side = 0; side < 2; side++) {
+                const int64_t n = side ? n_k : n_q;
+                const int64_t items = bh * ((n + 63) / 64) * ((m + 63) / 64);
+                const unsigned blocks = static_cast<unsigned>(items < 65536 ? items : 65536);
+                KernelTimer timer("codes_t_kernel", stream);
+                const uint16_t *src = side ? kcodes : qcodes;
+                if (m % 8 == 0 && (reinterpret_cast<uintptr_t>(src) & 15) == 0)
+                    hipLaunchKernelGGL(codes_t_kernel<true>, dim3(blocks), dim3(256), 0, stream,
+                                       side ? kcodes : qcodes, side ? kct : qct, bh, n, m);
+                else
+                    hipLaunchKernelGGL(codes_t_kernel<false>, dim3(blocks), dim3(256), 0, stream,
+                                       side ? kcodes : qcodes, side ? kct : qct, bh, n, m);
+                if ((e = hipGetLastError()) != hipSuccess) return e;
+            }
+        }
+        const uint16_t *qsrc = transposed ? qct : qcodes, *ksrc = transposed ? kct : kcodes;
         KernelTimer timer("sort_kernel", stream);
         const dim3 grid(static_cast<unsigned>(2 * units));
         int32_t *qo = reinterpret_cast<int32_t *>(ws + L.qoff), *ko = reinterpret_cast<int32_t *>(ws + L.koff);
         uint32_t *qe = reinterpret_cast<uint32_t *>(ws + L.qent), *ke = reinterpret_cast<uint32_t *>(ws + L.kent);
         if (wide)
             hipLaunchKernelGGL(sort_kernel<kSortThreadsWide>, grid, dim3(kSortThreadsWide),
-                               sort_base_lds(kSortThreadsWide, tau), stream, qcodes, kcodes, m, n_q, n_k, tau, false,
-                               qo, ko, qe, ke);
+                               sort_base_lds(kSortThreadsWide, tau), stream, qsrc, ksrc, m, n_q, n_k, tau, transposed,
+                               false, false, qo, ko, qe, ke);
         else
-            hipLaunchKernelGGL(sort_kernel<kSortThreads>, grid, dim3(kSortThreads), sort_lds, stream, qcodes, kcodes,
-                               m, n_q, n_k, tau, stage, qo, ko, qe, ke);
+            hipLaunchKernelGGL(sort_kernel<kSortThreads>, grid, dim3(kSortThreads), sort_lds, stream, qsrc, ksrc, m,
+                               n_q, n_k, tau, transposed, stage_codes, stage_ent, qo, ko, qe, ke);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
 

@@ -166,7 +166,7 @@ def test_backward_star_workspace():
     partials = bh * (nq + nk) * mh * (64 * 3 + 1)          # 24-bit rows + exponents
     index = bh * mh * (2 * (2 ** (tau - 1) + 1) * 4 + (nq + 16 + nk + 16) * 4)
     split = 4 * bh * (nq + nk) // 2 * 64 * 4
-    codes = bh * (nq + nk) * mh * 2
+    codes = 2 * bh * (nq + nk) * mh * 2                    # the derived codes, then transposed
     need = partials + index + split + codes
     assert need <= star < 1.02 * need + (1 << 16)
 
@@ -180,14 +180,14 @@ def test_empty_tensors_need_no_pointers(L):
 
 
 def test_workspace_sizes():
-    # backward workspace: bucket offsets + sorted entries, the fp16 (hi, lo) copies of
-    # Q, K, V, dY (4 bytes per element) and one partial row per (row, hash) for dq and
-    # dk in 24-bit fixed point (64 int16 high parts, 64 low bytes and one exponent
-    # byte), the same for both storage types
+    # backward workspace: bucket offsets + sorted entries, the codes transposed for the
+    # sort, the fp16 (hi, lo) copies of Q, K, V, dY (4 bytes per element) and one
+    # partial row per (row, hash) for dq and dk in 24-bit fixed point (64 int16 high
+    # parts, 64 low bytes and one exponent byte), the same for both storage types
     f32 = Y.yoso_workspace_bytes(Y.OP_BACKWARD, 32, 4096, 4096, 64, 32, 8, Y.F32)
     bf = Y.yoso_workspace_bytes(Y.OP_BACKWARD, 32, 4096, 4096, 64, 32, 8, Y.BF16)
     units = 32 * 32
-    index = units * (2 * 257 * 4 + 2 * 4096 * 4)
+    index = units * (2 * 257 * 4 + 2 * 4096 * 4 + 2 * 4096 * 2)
     split = 4 * 32 * 4096 * 64 * 4
     partials = 2 * 32 * 4096 * 32 * (64 * 3 + 1)
     assert f32 >= index + split + partials
