@@ -663,6 +663,8 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
                                            int8_t *ex_lds, bool ex_in_lds, int m, const uint32_t *tile_ent,
                                            int nvalid, int q, int cl, int g, int c, const floatx4 outT[4],
                                            float orow) {
+    // nothing to store when every row of the tile takes the table form (wave-uniform)
+    if (__builtin_amdgcn_ballot_w64(c < nvalid && (tile_ent[c] >> 16) != kSkipCode) == 0) return;
     // max |value| of row c over this lane's 16 values (a chain of 3-input maxima),
     // then over the row's 4 lanes
     float mx = 0.f;
