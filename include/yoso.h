@@ -43,10 +43,12 @@
  *     the largest power of two keeping 2^k_d (1 + 2^-10) times that dim's sum of
  *     |value| over the n_src source rows below 2^30; everything after that
  *     rounding is exact.  dQ and dK use fp32 accumulation of products formed
- *     from fp16 (hi, lo) pairs (about 22 significant bits); the contribution of
- *     each hash to a row is kept in 24-bit fixed point (one power-of-two
- *     exponent per row, exact to 2^-23 of that row's largest value), and the m
- *     contributions are summed in hash order in fp32.
+ *     from fp16 (hi, lo) pairs (about 22 significant bits; bf16 inputs are
+ *     exact as the hi halves alone wherever they lie within 2^27 of their head's
+ *     largest value); the contribution of each hash to a row is kept in 24-bit
+ *     fixed point (one power-of-two exponent per row, exact to 2^-23 of that
+ *     row's largest value; 16-bit, exact to 2^-15, for bf16 outputs, whose own
+ *     rounding is 2^-9), and the m contributions are summed in hash order in fp32.
  *   - Reproducibility.  Every accumulation order is fixed (integer tables, a
  *     stable bucket order, partial rows summed in hash order), so repeating a
  *     call on the same inputs gives bitwise identical outputs on any stream.
@@ -176,9 +178,10 @@ yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const v
  * q, dy, dq [bh][n_q][d];  k, v, dk, dv [bh][n_k][d]  (dtype).
  * workspace: yoso_workspace_bytes(YOSO_OP_BACKWARD, ...) bytes of scratch: the
  * per-hash bucket orders, the per-head maxima of |q|, |k|, |v|, |dy|, fp16
- * (hi, lo) copies of q, k, v, dy, and one 24-bit fixed-point partial row per
- * (row, hash) for dq and dk, the codes transposed to [bh][m][n] for the bucket
- * sort: about (3*m*d + 7*m + 8*d) * (n_q + n_k) * bh bytes.
+ * (hi, lo) copies of q, k, v, dy, and one 24-bit (bf16: 16-bit) fixed-point
+ * partial row per (row, hash) for dq and dk, the codes transposed to [bh][m][n]
+ * for the bucket sort: about (3*m*d + 7*m + 8*d) * (n_q + n_k) * bh bytes
+ * (bf16: (2*m*d + 7*m + 8*d) * (n_q + n_k) * bh).
  * A bucket with b_q queries and b_k keys whose sizes pass
  * yoso_backward_table_threshold() is summed in the table form of Sec. 3.3
  * restricted to that bucket (one d x d matrix per side and bucket, applied to the

@@ -385,6 +385,7 @@ struct PassArgs {
     int m, tau;
     float scale;                     // tau / (2m)
     int tab_t;                       // table form for buckets with b_q b_k > tab_t (b_q + b_k); 0: none
+    bool p16;                        // 16-bit partial rows (bf16 outputs): no low parts
 };
 
 // ---- the wave's LDS tile
@@ -660,7 +661,7 @@ __device__ __forceinline__ uint32_t low_off(int r, int w) {
 // rows whose entry carries kSkipCode (their bucket takes the table form) are not
 // stored.
 __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, uint8_t *plow, int8_t *pexp,
-                                           int8_t *ex_lds, bool ex_in_lds, int m, const uint32_t *tile_ent,
+                                           int8_t *ex_lds, bool ex_in_lds, int m, bool p16, const uint32_t *tile_ent,
                                            int nvalid, int q, int cl, int g, int c, const floatx4 outT[4],
                                            float orow) {
     // nothing to store when every row of the tile takes the table form (wave-uniform)
@@ -686,10 +687,13 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
     // 2^(23 - e) stays a normal float
     const float mxs = mx * orow;
     const int e = min(max(static_cast<int>((__float_as_uint(mxs) >> 23) & 0xFFu) - 126, -100), 100);
-    // value * 2^(23 - e) lies in (-2^23, 2^23): a power-of-two scaling of the
-    // rounded product value * orow, so the row maximum stays below 2^23 before
-    // rounding (and at most 2^23 after, hence the clamp)
-    const float sc = mx > 0.f ? __uint_as_float(static_cast<uint32_t>(127 + 23 - e) << 23) * orow : 0.f;
+    // value * 2^(fb - e) lies in (-2^fb, 2^fb): a power-of-two scaling of the
+    // rounded product value * orow, so the row maximum stays below 2^fb before
+    // rounding (and at most 2^fb after, hence the clamp).  fb = 23 (24-bit rows), or
+    // 15 with p16 (16-bit rows: bf16 outputs, whose own rounding is 2^-9)
+    const int fb = p16 ? 15 : 23;
+    const int mmax = (1 << fb) - 1;
+    const float sc = mx > 0.f ? __uint_as_float(static_cast<uint32_t>(127 + fb - e) << 23) * orow : 0.f;
     if (g == 0 && c < nvalid && (tile_ent[c] >> 16) != kSkipCode) {
         const uint32_t row = tile_ent[c] & 0xFFFFu;
         if (ex_in_lds) ex_lds[row] = static_cast<int8_t>(e);
@@ -701,18 +705,22 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
     for (int dt = 0; dt < 4; dt++) {
         int mm[4];
 #pragma unroll
-        for (int j = 0; j < 4; j++) mm[j] = min(max(__float2int_rn(outT[dt][j] * sc), -0x7FFFFF), 0x7FFFFF);
+        for (int j = 0; j < 4; j++) mm[j] = min(max(__float2int_rn(outT[dt][j] * sc), -mmax), mmax);
         // byte permutes: the high parts are bytes 1-2 of each M, the low part byte 0
         // (v_perm_b32 picks any bytes of a register pair: {first operand : second})
         const uint32_t u[4] = {static_cast<uint32_t>(mm[0]), static_cast<uint32_t>(mm[1]),
                                static_cast<uint32_t>(mm[2]), static_cast<uint32_t>(mm[3])};
+        // (p16: the low 16 bits of each M)
+        const uint32_t hsel = p16 ? 0x05040100u : 0x06050201u;
         uint2v w;
-        w.x = __builtin_amdgcn_perm(u[1], u[0], 0x06050201u);
-        w.y = __builtin_amdgcn_perm(u[3], u[2], 0x06050201u);
+        w.x = __builtin_amdgcn_perm(u[1], u[0], hsel);
+        w.y = __builtin_amdgcn_perm(u[3], u[2], hsel);
         lds_st(tile, mant_off(sw, 4 * dt + g), w);
-        const uint32_t lo01 = __builtin_amdgcn_perm(u[1], u[0], 0x0C0C0400u);  // [b0 of M0, b0 of M1, 0, 0]
-        const uint32_t lo23 = __builtin_amdgcn_perm(u[3], u[2], 0x0C0C0400u);
-        lds_st(tile, low_off(c, 4 * dt + g), __builtin_amdgcn_perm(lo23, lo01, 0x05040100u));
+        if (!p16) {
+            const uint32_t lo01 = __builtin_amdgcn_perm(u[1], u[0], 0x0C0C0400u);  // [b0 of M0, b0 of M1, 0, 0]
+            const uint32_t lo23 = __builtin_amdgcn_perm(u[3], u[2], 0x0C0C0400u);
+            lds_st(tile, low_off(c, 4 * dt + g), __builtin_amdgcn_perm(lo23, lo01, 0x05040100u));
+        }
     }
     // rows 4q + i: this lane's chunk cl of each high-part row, then the four stores
     uint2v w[4];
@@ -720,8 +728,10 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
 #pragma unroll
     for (int i = 0; i < 4; i++) w[i] = lds_ld<uint2v>(tile, mant_off(mant_slot(4 * q + i), cl));
     // rows 4i + q: dword cl of each low-part row
+    if (!p16) {
 #pragma unroll
-    for (int i = 0; i < 4; i++) lw[i] = lds_ld<uint32_t>(tile, low_off(4 * i + q, cl));
+        for (int i = 0; i < 4; i++) lw[i] = lds_ld<uint32_t>(tile, low_off(4 * i + q, cl));
+    }
     const uint4 e4 = reinterpret_cast<const uint4 *>(tile_ent)[q];
     const uint32_t re[4] = {e4.x, e4.y, e4.z, e4.w};
     // (row, hash) record index row * m by a full-rate 24-bit multiply (row < 2^16,
@@ -737,11 +747,13 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
         if (4 * q + i < nvalid && (re[i] >> 16) != kSkipCode)
             __builtin_nontemporal_store(w[i], reinterpret_cast<uint2v *>(part + rec(re[i] & 0xFFFFu) * D) + cl);
     }
+    if (!p16) {
 #pragma unroll
-    for (int i = 0; i < 4; i++) {
-        const uint32_t le = tile_ent[4 * i + q];
-        if (4 * i + q < nvalid && (le >> 16) != kSkipCode)
-            __builtin_nontemporal_store(lw[i], reinterpret_cast<uint32_t *>(plow + rec(le & 0xFFFFu) * D) + cl);
+        for (int i = 0; i < 4; i++) {
+            const uint32_t le = tile_ent[4 * i + q];
+            if (4 * i + q < nvalid && (le >> 16) != kSkipCode)
+                __builtin_nontemporal_store(lw[i], reinterpret_cast<uint32_t *>(plow + rec(le & 0xFFFFu) * D) + cl);
+        }
     }
 }
 
@@ -903,7 +915,8 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
         auto zero_tiles = [&](int ta, int tb) {
             const floatx4 z[4] = {};
             for (int t = ta; t < tb; t++)
-                store_tile(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, tile_ents(t), row_count(t), q, cl, g, c, z, 0.f);
+                store_tile(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, a.p16, tile_ents(t), row_count(t), q, cl, g,
+                           c, z, 0.f);
         };
         // sub-tile j of the run: its tile (searched forward from t) and first partner
         auto tile_of = [&](int j, int t) {
@@ -980,7 +993,7 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
                 compute_sub<STAR, HI1>(tile, cur.pe, rh, rl, rbh, rbl, xscale, static_cast<int>(row_entry(cur.t) >> 16),
                                   ldexpf(1.0f, -2 - erow), g, c, outT);
                 if (newtile) {
-                    store_tile(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, tile_ents(cur.t), row_count(cur.t), q, cl,
+                    store_tile(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, a.p16, tile_ents(cur.t), row_count(cur.t), q, cl,
                                g, c, outT, ldexpf(oscale, erow));
 #pragma unroll
                     for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -1289,7 +1302,7 @@ __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
 #pragma unroll
                 for (int dt = 0; dt < 4; dt++)
                     outT[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(mtl[dt][kb], rh[kb], outT[dt], 0, 0, 0);
-            store_tile(st, part, plow, pexp, nullptr, false, a.m, tent, nvalid, q, cl, g, c, outT, orow);
+            store_tile(st, part, plow, pexp, nullptr, false, a.m, a.p16, tent, nvalid, q, cl, g, c, outT, orow);
             return t + 1 < ntile;
         };
         for (int t = 0;; t += 3) {
@@ -1363,15 +1376,17 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *_
     float s[8];
 #pragma unroll
     for (int i = 0; i < 8; i++) s[i] = 0.f;
+    // 24-bit rows: M = high * 256 + low, value = M 2^(e - 23); bf16 outputs take
+    // 16-bit rows (no low parts): value = high 2^(e - 15)
     auto add = [&](const uint4v &v, const uint2v &l, int e) {
-        const float sc = ldexpf(1.0f, e - 23);
+        const float sc = ldexpf(1.0f, e - (BF16 ? 15 : 23));
         const uint32_t w[4] = {v.x, v.y, v.z, v.w};
         const uint32_t lb[2] = {l.x, l.y};
 #pragma unroll
         for (int i = 0; i < 8; i++) {
             const int hi = static_cast<int16_t>((w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
-            const int lo = static_cast<int>((lb[i >> 2] >> (8 * (i & 3))) & 0xFFu);
-            s[i] = fmaf(static_cast<float>(hi * 256 + lo), sc, s[i]);  // |M| < 2^23: exact in fp32
+            const int lo = BF16 ? 0 : static_cast<int>((lb[i >> 2] >> (8 * (i & 3))) & 0xFFu);
+            s[i] = fmaf(static_cast<float>(BF16 ? hi : hi * 256 + lo), sc, s[i]);  // |M| < 2^23: exact in fp32
         }
     };
     // groups of eight hashes, double-buffered: group g+1 is loaded while g is added
@@ -1381,8 +1396,10 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *_
     auto load = [&](uint4v w[8], uint2v lw[8], int f[8], int h0) {
 #pragma unroll
         for (int u = 0; u < 8; u++) w[u] = __builtin_nontemporal_load(src + (h0 + u) * (D / 8));
+        if constexpr (!BF16) {
 #pragma unroll
-        for (int u = 0; u < 8; u++) lw[u] = __builtin_nontemporal_load(srl + (h0 + u) * (D / 8));
+            for (int u = 0; u < 8; u++) lw[u] = __builtin_nontemporal_load(srl + (h0 + u) * (D / 8));
+        }
 #pragma unroll
         for (int u = 0; u < 8; u++) f[u] = ex[(h0 + u) * n];
     };
@@ -1400,7 +1417,8 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *_
     }
     int h = 8 * ng;
     for (; h < m; h++)
-        add(__builtin_nontemporal_load(src + h * (D / 8)), __builtin_nontemporal_load(srl + h * (D / 8)), ex[h * n]);
+        add(__builtin_nontemporal_load(src + h * (D / 8)), BF16 ? uint2v{0u, 0u} : __builtin_nontemporal_load(srl + h * (D / 8)),
+            ex[h * n]);
     if constexpr (BF16) {
         uint4 o;
         o.x = static_cast<uint32_t>(f32_to_bf16(s[0])) | (static_cast<uint32_t>(f32_to_bf16(s[1])) << 16);
@@ -1822,8 +1840,10 @@ BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, 
     L.vs = o; o = align_up(o + static_cast<size_t>(bh) * n_k * D * 4);
     L.pq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m * D * 2);
     L.pk = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m * D * 2);
-    L.lq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m * D);
-    L.lk = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m * D);
+    // the low parts of the 24-bit partial rows (bf16 outputs take 16-bit rows: none)
+    const size_t low = bf16 ? 0 : static_cast<size_t>(D);
+    L.lq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m * low);
+    L.lk = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m * low);
     L.eq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m);
     L.ek = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m);
     L.pmax = o; o = align_up(o + static_cast<size_t>(bh) * 4 * kMaxParts * 4);
@@ -1967,6 +1987,7 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
     a.bh = bh; a.m = m; a.tau = tau;
     a.scale = scale;
     a.tab_t = star ? 0 : kTableT;
+    a.p16 = bf16;
     e = launch_pass(a, units, star, bf16, stream);
     if (e != hipSuccess) return e;
     if (bf16) {

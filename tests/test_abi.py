@@ -183,7 +183,8 @@ def test_workspace_sizes():
     # backward workspace: bucket offsets + sorted entries, the codes transposed for the
     # sort, the fp16 (hi, lo) copies of Q, K, V, dY (4 bytes per element) and one
     # partial row per (row, hash) for dq and dk in 24-bit fixed point (64 int16 high
-    # parts, 64 low bytes and one exponent byte), the same for both storage types
+    # parts, 64 low bytes and one exponent byte); bf16 outputs take 16-bit rows
+    # (no low bytes)
     f32 = Y.yoso_workspace_bytes(Y.OP_BACKWARD, 32, 4096, 4096, 64, 32, 8, Y.F32)
     bf = Y.yoso_workspace_bytes(Y.OP_BACKWARD, 32, 4096, 4096, 64, 32, 8, Y.BF16)
     units = 32 * 32
@@ -192,7 +193,8 @@ def test_workspace_sizes():
     partials = 2 * 32 * 4096 * 32 * (64 * 3 + 1)
     assert f32 >= index + split + partials
     assert f32 < 1.05 * (index + split + partials) + (1 << 20)
-    assert bf == f32
+    low = 2 * 32 * 4096 * 32 * 64
+    assert f32 - low - (1 << 12) <= bf <= f32 - low
     assert Y.yoso_workspace_bytes(Y.OP_HASH, 32, 4096, 4096, 64, 32, 8, Y.F32) == 0
     assert Y.yoso_workspace_bytes(Y.OP_FORWARD, 32, 4096, 4096, 64, 32, 8, Y.F32) == 0
     with pytest.raises(Y.YosoError):
