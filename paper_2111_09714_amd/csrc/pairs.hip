@@ -98,7 +98,7 @@ constexpr uint32_t kSkipCode = 0xFFFEu;
 // better than the masked 16 x 16 pair tiles, so the bucket switches over at a
 // threshold below d / 2.  kTableT >= 16 keeps every table bucket above 16 rows on
 // both sides, so within a 16-row tile its rows are a prefix and/or a suffix.
-constexpr int kTableT = 32;
+constexpr int kTableT = 24;
 static_assert(kTableT >= 16, "table buckets must span more than one row tile");
 
 __device__ __forceinline__ bool table_bucket(int32_t bq, int32_t bk, int t) {
