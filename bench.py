@@ -16,8 +16,9 @@ One JSON line is printed on stdout.
 Per-kernel durations come from HIP events that the library records around each
 of its launches on the launch stream (yoso_timing_enable); the roofline object
 describes the kernel with the largest total time.  For the dQ, dK pair kernel that
-is a matrix-unit roofline (3d multiply-adds per colliding pair, fp32 peak), with
-its HBM figures alongside.  The CPU baseline is the fp64
+is a matrix-unit roofline (3d multiply-adds per colliding pair, at the matrix
+peak of the input type: fp32, or bf16 for bf16 inputs), with its HBM figures
+alongside.  The CPU baseline is the fp64
 oracle, timed on this machine's host cores on a stated sample of heads.
 
 The `configs` object repeats the step measurement (graph replay, fewer steps for
@@ -99,7 +100,7 @@ KERNEL_SOURCES = {
     "hash_kernel": ["paper_2111_09714_amd/csrc/hash.hip", "paper_2111_09714_amd/csrc/common.h"],
     "table_kernel": ["paper_2111_09714_amd/csrc/tables.hip", "paper_2111_09714_amd/csrc/common.h"],
     **{k: _PAIRS for k in ("codes_t_kernel", "sort_kernel", "absmax_kernel", "split_kernel", "pass_kernel", "bucket_kernel",
-                           "reduce_kernel", "dense_kernel")},
+                           "reduce_kernel", "dense_kernel", "dense_fwd_kernel")},
 }
 
 
@@ -156,7 +157,7 @@ def cpu_baseline(w, inp, heads, min_wall: float = 10.0):
 STEP_KERNELS = ("hash_kernel", "table_kernel", "codes_t_kernel", "sort_kernel", "absmax_kernel", "split_kernel",
                 "pass_kernel",
                 "bucket_kernel",
-                "reduce_kernel", "dense_kernel", "zero_kernel")
+                "reduce_kernel", "dense_kernel", "dense_fwd_kernel", "zero_kernel")
 
 
 def make_step(Y, torch, w, inp, dev):
@@ -236,8 +237,9 @@ def time_step(Y, torch, step, steps, warmup):
 
 def dominant_roofline(w, kernels, qc, kc):
     """Roofline of the kernel with the largest time per step: HBM for the streaming
-    kernels, the fp32 matrix peak for the pair kernel (3d multiply-adds per colliding
-    pair, counted exactly from the codes) with its HBM figures alongside."""
+    kernels, the matrix peak of the input type for the dQ/dK kernels (3d multiply-adds
+    per colliding pair, 2d^2 per table row and side, counted exactly from the codes)
+    with their HBM figures alongside."""
     dominant = max(kernels, key=lambda kname: kernels[kname]["avg_us"] * kernels[kname]["launches_per_step"])
     alg = kernel_algorithmic(w, dominant)
     avg_s = kernels[dominant]["avg_us"] * 1e-6
@@ -247,8 +249,12 @@ def dominant_roofline(w, kernels, qc, kc):
         roofline = {"kernel": dominant, "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
                     "algorithmic_bytes_per_launch": alg, "avg_launch_us": round(kernels[dominant]["avg_us"], 2)}
+    # A contraction is priced at the matrix peak of its own input type: fp32 inputs
+    # against the fp32 peak (they run as three fp16 products), bf16 inputs against
+    # the dense bf16/fp16 peak (bf16 values are exact fp16 operands there).
+    peak = FP16_MFMA_PEAK_TFLOPS if w.dtype == "bf16" else FP32_PEAK_TFLOPS
     if dominant in ("pass_kernel", "bucket_kernel"):
-        # dQ, dK are dense per-bucket contractions, bound by the matrix units, in fp32.
+        # dQ, dK are dense per-bucket contractions, bound by the matrix units.
         # Pair form (pass_kernel): per colliding (query, key) pair 3d multiply-adds
         # (dy.v once, then its share of dQ and of dK).  Table form (bucket_kernel): per
         # row of a table bucket and side 2 d^2 (its share of M = sum a' b^T, then its
@@ -258,8 +264,8 @@ def dominant_roofline(w, kernels, qc, kc):
         flops = 6 * w.d * pair_form if dominant == "pass_kernel" else 4 * w.d * w.d * table_rows
         tf = flops / avg_s / 1e12
         hbm = roofline
-        roofline = {"kernel": dominant, "bound": "mfma", "achieved": round(tf, 2), "peak": FP32_PEAK_TFLOPS,
-                    "unit": "TFLOP/s", "frac": round(tf / FP32_PEAK_TFLOPS, 4), "traffic": None,
+        roofline = {"kernel": dominant, "bound": "mfma", "achieved": round(tf, 2), "peak": peak,
+                    "unit": "TFLOP/s", "frac": round(tf / peak, 4), "traffic": None,
                     "algorithmic_flops_per_launch": flops, "colliding_pairs_per_launch": pairs,
                     "pair_form_pairs_per_launch": pair_form, "table_form_rows_per_launch": table_rows,
                     "avg_launch_us": round(kernels[dominant]["avg_us"], 2)}
@@ -269,11 +275,11 @@ def dominant_roofline(w, kernels, qc, kc):
     if dominant == "dense_kernel":
         # short sequences: dQ, dK and dV as dense blocks over every (query, key) pair,
         # 5 d multiply-adds per pair (dy.v once for each of the two sides, then its
-        # shares of dQ, dK and the count-weighted dV), in fp32
+        # shares of dQ, dK and the count-weighted dV)
         flops = 10 * w.d * w.n * w.n * w.bh
         tf = flops / avg_s / 1e12
-        roofline = {"kernel": dominant, "bound": "mfma", "achieved": round(tf, 2), "peak": FP32_PEAK_TFLOPS,
-                    "unit": "TFLOP/s", "frac": round(tf / FP32_PEAK_TFLOPS, 4), "traffic": None,
+        roofline = {"kernel": dominant, "bound": "mfma", "achieved": round(tf, 2), "peak": peak,
+                    "unit": "TFLOP/s", "frac": round(tf / peak, 4), "traffic": None,
                     "algorithmic_flops_per_launch": flops, "avg_launch_us": round(kernels[dominant]["avg_us"], 2)}
     if roofline is not None:
         roofline["traffic"] = measured_traffic(dominant, w.name)

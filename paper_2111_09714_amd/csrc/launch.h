@@ -61,6 +61,12 @@ hipError_t launch_expect_backward(const void *q, const void *k, const void *v, c
 // T of the backward's rule: a bucket takes the table form when b_q b_k > T (b_q + b_k).
 int backward_table_threshold();
 
+// Short sequences over many heads (both sides at most 1024 rows): the forward as
+// Y = (1/m) C V over every (query, key) pair, C counted from the codes; no workspace.
+bool dense_forward_applies(int64_t bh, int64_t n_q, int64_t n_k, int m, int tau);
+hipError_t launch_dense_forward(const uint16_t *qcodes, const uint16_t *kcodes, const void *v, void *y, bool bf16,
+                                int64_t bh, int64_t n_q, int64_t n_k, int m, int tau, hipStream_t stream);
+
 hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
                            const void *v, const void *dy, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m,
                            int tau, void *dq, void *dk, void *dv, void *workspace, hipStream_t stream);

@@ -1741,6 +1741,265 @@ __global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
     }
 }
 
+// ---------------------------------------------------------------- dense forward (short sequences)
+// Y = (1/m) sum_h B_h V (Sec. 3.1, 3.2) with the hashes summed first: Y = (1/m) C V,
+// C_ij the number of hashes under which q_i and k_j collide, every (query, key)
+// pair of a head visited once.  C is counted from the two rows' codes and C V runs
+// on 16 x 16 MFMA blocks (C is an exact fp16 integer, V an fp16 (hi, lo) pair).  At
+// a few rows per bucket the bucket tables cost a fixed amount per table and feature
+// slice that this form does not have; it does n_q n_k (~1.5 tau + 1 compares + 2d
+// multiply-adds) of work per head.
+//
+// Codes as bit planes: plane t of a row is the bit vector over its hashes of bit t
+// of each code (one 32-bit word per 32 hashes), so that for a (query, key) pair the
+// hashes on which the codes differ are OR_t (plane_t(q) ^ plane_t(k)) and
+// C = m - popcount of that.  A tile's codes are copied into LDS as they lie in
+// memory (one coalesced run) and each thread assembles whole plane words of a row.
+//
+// One workgroup (4 waves) per (head, 64 queries): wave w owns queries 16w .. 16w+15,
+// lane (g, c) query 16w + c.  Keys stream through LDS in tiles of 64 (V rows split
+// into fp16 (hi, lo) under the tile's power-of-two scale; planes); per 16-key block
+// lane (g, c) counts C for its query against keys 4g .. 4g+3 and out^T += V^T C.
+constexpr int kDenseFwdMaxN = 1024;   // both sides at most this many rows: dense forward
+
+// Plane row stride in words: tau * PW words rounded up to a 16-byte multiple, plus
+// 16 bytes (the words between are zero)
+__host__ __device__ constexpr int plane_stride(int tau, int pw) { return (tau * pw + 3) / 4 * 4 + 4; }
+
+// Raw codes of rows [r0, r0 + 64) of a [rows][m] array (64 m contiguous uint16, one
+// coalesced run): thread t loads elements t + 256 i, clamped to the array.
+template <int PW>
+struct RawCodes {
+    uint32_t c[8 * PW];
+};
+
+template <int PW>
+__device__ __forceinline__ void load_raw_codes(RawCodes<PW> &rc, const uint16_t *codes, int r0, int nrows, int m,
+                                               int tid) {
+    const int last = nrows * m - 1, base = r0 * m;
+#pragma unroll
+    for (int i = 0; i < 8 * PW; i++) rc.c[i] = codes[min(base + tid + 256 * i, last)];
+}
+
+// LDS copy of the raw codes: row r at uint16 offset r * raw_stride (16-byte
+// aligned rows whose 16-byte reads by 16 consecutive rows hit distinct banks).
+template <int PW>
+__host__ __device__ constexpr int raw_stride() { return 64 * PW + 8; }
+
+template <int PW>
+__device__ __forceinline__ void store_raw_codes(const RawCodes<PW> &rc, uint16_t *dst, int m, float inv_m, int tid) {
+#pragma unroll
+    for (int i = 0; i < 8 * PW; i++) {
+        const int e = tid + 256 * i;
+        if (e < 64 * m) {
+            // e / m, exact: (e + 1/2) / m lies at least 1/(2m) from an integer and the
+            // product's rounding error is below 2^-16 for e < 2^12
+            const int r = static_cast<int>((static_cast<float>(e) + 0.5f) * inv_m);
+            dst[r * raw_stride<PW>() + (e - r * m)] = static_cast<uint16_t>(rc.c[i]);
+        }
+    }
+}
+
+// Planes of the 64 rows in LDS (row stride `ps` words: word t*PW + w of a row holds
+// bits [32w, 32w + 32) of plane t).  Thread t builds planes (t >> 6) + 4k of row
+// t & 63 from the row's codes, two operations per code and plane.
+template <int PW>
+__device__ __forceinline__ void build_planes(const uint16_t *raw, int m, int tau, int ps, uint32_t *dst, int tid) {
+    const int r = tid & 63, p0 = tid >> 6;
+    const uint4 *src = reinterpret_cast<const uint4 *>(raw + r * raw_stride<PW>());
+#pragma unroll
+    for (int w = 0; w < PW; w++) {
+        uint32_t cw[16];  // codes 32w .. 32w + 31, two per word
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const uint4 q4 = src[4 * w + j];
+            cw[4 * j] = q4.x;
+            cw[4 * j + 1] = q4.y;
+            cw[4 * j + 2] = q4.z;
+            cw[4 * j + 3] = q4.w;
+        }
+        // hashes past m (the rest of the row's LDS slot) are masked out
+        const int valid = m - 32 * w;
+        const uint32_t keep = valid >= 32 ? 0xFFFFFFFFu : valid <= 0 ? 0u : (1u << valid) - 1u;
+#pragma unroll
+        for (int k = 0; k < 3; k++) {
+            const int t = p0 + 4 * k;
+            if (t < tau) {
+                uint32_t word = 0u;
+#pragma unroll
+                for (int j = 0; j < 16; j++) {
+                    word |= __builtin_amdgcn_ubfe(cw[j], t, 1) << (2 * j);
+                    word |= __builtin_amdgcn_ubfe(cw[j], 16 + t, 1) << (2 * j + 1);
+                }
+                dst[r * ps + t * PW + w] = word & keep;
+            }
+        }
+    }
+}
+
+template <bool BF16, int PW>
+__global__ __launch_bounds__(256) void dense_fwd_kernel(const uint16_t *__restrict__ qcodes,
+                                                        const uint16_t *__restrict__ kcodes,
+                                                        const void *__restrict__ v, void *__restrict__ y, int64_t bh,
+                                                        int n_q, int n_k, int m, int tau) {
+    constexpr int NW = 12 * PW;  // plane words per row at most (tau <= 12)
+    __shared__ __align__(16) unsigned char v_lds[kDenseTile * 256];
+    __shared__ __align__(16) uint32_t kp_lds[kDenseTile * plane_stride(12, PW)];
+    __shared__ __align__(16) uint32_t qp_lds[kDenseRows * plane_stride(12, PW)];
+    __shared__ __align__(16) uint16_t raw_lds[64 * raw_stride<PW>()];
+    __shared__ float tmax[4];
+
+    const int64_t tiles = (n_q + kDenseRows - 1) / kDenseRows;
+    const int64_t blk = xcd_remap(blockIdx.x, bh * tiles);
+    const int64_t b = blk / tiles;
+    const int r0 = static_cast<int>(blk - b * tiles) * kDenseRows;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = lane >> 4, c = lane & 15;
+    const int ps = plane_stride(tau, PW);
+    const int nw = tau * PW;  // plane words per row
+    const float inv_m = 1.0f / static_cast<float>(m);
+    const uint16_t *kc = kcodes + b * n_k * m;
+
+    // plane words past tau * PW are read as zeros and never written
+    for (int i = tid; i < kDenseTile * plane_stride(12, PW); i += 256) kp_lds[i] = qp_lds[i] = 0u;
+
+    // staging of V: lane l of wave w stages row 16w + (l & 15), dims 16 (l >> 4) + [0, 16)
+    const int lrow = 16 * wave + (lane & 15), lq = lane >> 4;
+    // a key tile's V rows and raw codes, loaded together (rows clamped: the prefetch
+    // past the last tile reads the last rows again and is never used)
+    auto load_tile = [&](int c0, RawCodes<PW> &rc, float (&x)[16]) {
+        const int64_t off = (b * n_k + min(c0 + lrow, n_k - 1)) * D + 16 * lq;
+        load8<BF16>(v, off, x);
+        load8<BF16>(v, off + 8, x + 8);
+        load_raw_codes<PW>(rc, kc, c0, n_k, m, tid);
+    };
+    RawCodes<PW> kca, kcb;
+    float xa[16], xb[16];
+    if (n_k > 0) load_tile(0, kca, xa);
+
+    // ---- the workgroup's queries as planes; lane (g, c) keeps query 16 wave + c's
+    uint32_t qp[NW];
+    {
+        RawCodes<PW> rc;
+        load_raw_codes<PW>(rc, qcodes + b * n_q * m, r0, n_q, m, tid);
+        store_raw_codes<PW>(rc, raw_lds, m, inv_m, tid);
+        __syncthreads();
+        build_planes<PW>(raw_lds, m, tau, ps, qp_lds, tid);
+        __syncthreads();
+        const uint4 *src = reinterpret_cast<const uint4 *>(qp_lds + (16 * wave + c) * ps);
+#pragma unroll
+        for (int j = 0; j < NW / 4; j++) {
+            const uint4 w4 = j * 4 < nw ? src[j] : make_uint4(0u, 0u, 0u, 0u);
+            qp[4 * j] = w4.x;
+            qp[4 * j + 1] = w4.y;
+            qp[4 * j + 2] = w4.z;
+            qp[4 * j + 3] = w4.w;
+        }
+    }
+
+    const int pr = 4 * g + (c >> 2), a4 = c & 3;
+    const floatx4 z4 = {0.f, 0.f, 0.f, 0.f};
+    floatx4 out[4];
+#pragma unroll
+    for (int dt = 0; dt < 4; dt++) out[dt] = z4;
+    int ev = 0;
+    // one key tile from (rc, x), the next one's loads into (rn, xn) (two register
+    // sets, swapped by unrolling the loop twice: copying registers a load is still
+    // filling would wait for it)
+    auto do_tile = [&](int c0, RawCodes<PW> &rc, float (&x)[16], RawCodes<PW> &rn, float (&xn)[16]) {
+        __syncthreads();  // the previous tile (and the query planes' raw codes) have been read
+        store_raw_codes<PW>(rc, raw_lds, m, inv_m, tid);
+        float mx = 0.f;
+        {
+            const bool ok = c0 + lrow < n_k;
+#pragma unroll
+            for (int i = 0; i < 16; i++) {
+                x[i] = ok ? x[i] : 0.f;
+                mx = fmaxf(mx, fabsf(x[i]));
+            }
+        }
+        mx = wave_max(mx);
+        if (lane == 0) tmax[wave] = mx;
+        __syncthreads();
+        // planes of the tile's keys (keys past n_k have zero V rows, so their codes,
+        // clamped copies of the last key's, do not matter)
+        build_planes<PW>(raw_lds, m, tau, ps, kp_lds, tid);
+        const int ev_new = pow2_above(fmaxf(fmaxf(tmax[0], tmax[1]), fmaxf(tmax[2], tmax[3])));
+        {
+            half8 h[2], l[2];
+            const float sc = ldexpf(1.0f, 13 - ev_new);
+            split8(x, sc, h[0], l[0]);
+            split8(x + 8, sc, h[1], l[1]);
+#pragma unroll
+            for (int u = 0; u < 2; u++) {
+                *reinterpret_cast<half8 *>(v_lds + swz(lrow, 2 * lq + u, 256)) = h[u];
+                *reinterpret_cast<half8 *>(v_lds + swz(lrow, 8 + 2 * lq + u, 256)) = l[u];
+            }
+        }
+        if (c0 > 0) {
+            const float f = ldexpf(1.0f, ev - ev_new);
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) out[dt] *= f;
+        }
+        ev = ev_new;
+        load_tile(c0 + kDenseTile, rn, xn);
+        __syncthreads();
+#pragma unroll 1
+        for (int cb = 0; cb < kDenseTile / 16; cb++) {
+            if (c0 + 16 * cb >= n_k) break;
+            // C for the lane's query against keys 16cb + 4g + i
+            half4 ch;
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                const uint4 *src = reinterpret_cast<const uint4 *>(kp_lds + (16 * cb + 4 * g + i) * ps);
+                uint32_t d0 = 0u, d1 = 0u;
+#pragma unroll
+                for (int j = 0; j < NW / 4; j++) {
+                    if (j * 4 < nw) {
+                        const uint4 w4 = src[j];
+                        const uint32_t kw[4] = {w4.x, w4.y, w4.z, w4.w};
+#pragma unroll
+                        for (int u = 0; u < 4; u++) {
+                            // word 4j + u: plane (4j + u) / PW, hash word (4j + u) % PW
+                            const uint32_t dx = qp[4 * j + u] ^ kw[u];
+                            if (PW == 1 || (u & 1) == 0)
+                                d0 |= dx;
+                            else
+                                d1 |= dx;
+                        }
+                    }
+                }
+                const int cnt = m - static_cast<int>(__builtin_popcount(d0) + __builtin_popcount(d1));
+                ch[i] = static_cast<_Float16>(static_cast<float>(cnt));
+            }
+            // V^T of the block as the A operand (lane (g, c): dim 16dt + c, keys 4g .. 4g+3)
+            half4 vh[4], vl[4];
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) {
+                vh[dt] = tr_load(v_lds + swz(16 * cb + pr, 2 * dt + (a4 >> 1), 256) + 8 * (a4 & 1));
+                vl[dt] = tr_load(v_lds + swz(16 * cb + pr, 8 + 2 * dt + (a4 >> 1), 256) + 8 * (a4 & 1));
+            }
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) out[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(vh[dt], ch, out[dt], 0, 0, 0);
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) out[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(vl[dt], ch, out[dt], 0, 0, 0);
+        }
+    };
+    for (int c0 = 0; c0 < n_k; c0 += 2 * kDenseTile) {
+        do_tile(c0, kca, xa, kcb, xb);
+        if (c0 + kDenseTile < n_k) do_tile(c0 + kDenseTile, kcb, xb, kca, xa);
+    }
+
+    // Y = out 2^(e_v - 13) / m; lane (g, c) holds out[query c][16dt + 4g + i]
+    const int frow = r0 + 16 * wave + c;
+    if (frow < n_q) {
+        const float sc = ldexpf(1.0f, ev - 13) / static_cast<float>(m);
+#pragma unroll
+        for (int dt = 0; dt < 4; dt++) dense_store<BF16>(y, (b * n_q + frow) * D + 16 * dt + 4 * g, out[dt], sc);
+    }
+}
+
 unsigned elementwise_grid(int64_t count) {
     const int64_t blocks = (count + 255) / 256;
     return static_cast<unsigned>(blocks < 8192 ? (blocks > 0 ? blocks : 1) : 8192);
@@ -2001,6 +2260,30 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
 }  // namespace
 
 int backward_table_threshold() { return kTableT; }
+
+// The dense forward's work grows as n_q n_k, the tables' as (n_q + n_k) plus a cost
+// per table of 2^tau m rows; measured on 16-row to 1024-row sequences, the dense
+// form is faster where it fills the chip (a workgroup per head and 64 queries: at
+// least two per CU) and n_q n_k stays below 2^19 per 8192 table rows per head.
+bool dense_forward_applies(int64_t bh, int64_t n_q, int64_t n_k, int m, int tau) {
+    if (n_q > kDenseFwdMaxN || n_k > kDenseFwdMaxN) return false;
+    if (bh * ((n_q + kDenseRows - 1) / kDenseRows) < 512) return false;
+    const int64_t per = (int64_t{1} << tau) * m / 8192;
+    return n_q * n_k <= (int64_t{1} << 19) * (per > 1 ? per : 1);
+}
+
+hipError_t launch_dense_forward(const uint16_t *qcodes, const uint16_t *kcodes, const void *v, void *y, bool bf16,
+                                int64_t bh, int64_t n_q, int64_t n_k, int m, int tau, hipStream_t stream) {
+    const int64_t blocks = bh * ((n_q + kDenseRows - 1) / kDenseRows);
+    if (blocks == 0) return hipSuccess;
+    KernelTimer timer("dense_fwd_kernel", stream);
+    const int nq = static_cast<int>(n_q), nk = static_cast<int>(n_k);
+    auto kernel = bf16 ? (m > 32 ? dense_fwd_kernel<true, 2> : dense_fwd_kernel<true, 1>)
+                       : (m > 32 ? dense_fwd_kernel<false, 2> : dense_fwd_kernel<false, 1>);
+    hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, qcodes, kcodes, v, y, bh,
+                       nq, nk, m, tau);
+    return hipGetLastError();
+}
 
 hipError_t launch_backward(const uint16_t *qcodes, const uint16_t *kcodes, const void *q, const void *k,
                            const void *v, const void *dy, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m,

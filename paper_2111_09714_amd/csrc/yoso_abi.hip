@@ -80,7 +80,8 @@ yoso_status check_ptr(const void *p, int64_t elems, const char *name) {
 size_t required_workspace(yoso_op op, bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int32_t m, int32_t tau) {
     switch (op) {
         case YOSO_OP_HASH: return 0;
-        case YOSO_OP_FORWARD: return yoso::table_workspace_bytes(bf16, bh, n_q, m, tau);
+        case YOSO_OP_FORWARD:
+            return yoso::dense_forward_applies(bh, n_q, n_k, m, tau) ? 0 : yoso::table_workspace_bytes(bf16, bh, n_q, m, tau);
         case YOSO_OP_BACKWARD: return yoso::backward_layout(bf16, bh, n_q, n_k, m, tau).total;
         case YOSO_OP_BACKWARD_STAR: return yoso::backward_star_layout(bf16, bh, n_q, n_k, m, tau).total;
     }
@@ -215,6 +216,10 @@ yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const v
     YOSO_TRY(check_ptr(y, bh * n_q * d, "y"));
     const bool bf16 = dtype == YOSO_BF16;
     YOSO_TRY(check_workspace(workspace, workspace_bytes, required_workspace(YOSO_OP_FORWARD, bf16, bh, n_q, n_k, m, tau)));
+    if (yoso::dense_forward_applies(bh, n_q, n_k, m, tau))
+        return device_status(yoso::launch_dense_forward(qcodes, kcodes, v, y, bf16, bh, n_q, n_k, m, tau,
+                                                        static_cast<hipStream_t>(stream)),
+                             "yoso_forward");
     return device_status(yoso::launch_table(kcodes, v, qcodes, y, bf16, bh, n_k, n_q, m, tau, workspace,
                                             static_cast<hipStream_t>(stream)),
                          "yoso_forward");

@@ -99,12 +99,25 @@ def test_forward_rejects(L, kw, status):
 
 
 def test_forward_workspace_checks(L):
-    # tau = 12, m = 64 needs several hash groups, and bf16 output needs an fp32 accumulator
-    need = Y.yoso_workspace_bytes(Y.OP_FORWARD, 2, 128, 128, 64, 32, 12, Y.BF16)
+    # past the dense form's 1024 rows, tau = 12 needs several hash groups of tables,
+    # and bf16 output needs an fp32 accumulator
+    need = Y.yoso_workspace_bytes(Y.OP_FORWARD, 2, 2048, 2048, 64, 32, 12, Y.BF16)
     assert need > 0
-    assert _fwd(L, dtype=1, tau=12, ws=None, wsb=0) == 6
-    assert _fwd(L, dtype=1, tau=12, ws=FAKE, wsb=need - 1) == 6
-    assert _fwd(L, dtype=1, tau=12, ws=FAKE + 4, wsb=need) == 5
+    big = dict(dtype=1, tau=12, nq=2048, nk=2048)
+    assert _fwd(L, ws=None, wsb=0, **big) == 6
+    assert _fwd(L, ws=FAKE, wsb=need - 1, **big) == 6
+    assert _fwd(L, ws=FAKE + 4, wsb=need, **big) == 5
+
+
+def test_dense_forward_needs_no_workspace(L):
+    # many heads of short sequences: the forward counts collisions pair by pair and
+    # needs no workspace; over few heads it takes the tables, and bf16 output with
+    # several groups of tau = 12 tables needs an fp32 accumulator
+    for n_q, n_k in ((1, 1), (100, 1024), (512, 512), (1024, 1)):
+        for tau, m, dt in ((12, 32, Y.BF16), (8, 64, Y.F32), (1, 1, Y.F32)):
+            assert Y.yoso_workspace_bytes(Y.OP_FORWARD, 1024, n_q, n_k, 64, m, tau, dt) == 0
+    assert Y.yoso_workspace_bytes(Y.OP_FORWARD, 4, 512, 512, 64, 32, 12, Y.BF16) > 0
+    assert Y.yoso_workspace_bytes(Y.OP_FORWARD, 1024, 1025, 1024, 64, 32, 12, Y.BF16) > 0
 
 
 @pytest.mark.parametrize("kw,status", [

@@ -96,6 +96,46 @@ def test_small_shapes(bh, nq, nk, m, tau, dtype):
     run_case(bh, nq, nk, m, tau, dtype)
 
 
+FORWARD_FORMS = [
+    # (bh, n_q, n_k, m, tau, dtype, kernel): many heads of short sequences take the
+    # dense forward (ragged tiles, one and two words of hashes, tau 1 to 12); few
+    # heads, or n_q n_k past the rule's bound, take the bucket tables
+    (512, 37, 50, 5, 3, "f32", "dense_fwd_kernel"),
+    (160, 200, 333, 32, 8, "f32", "dense_fwd_kernel"),
+    (96, 400, 1024, 64, 6, "f32", "dense_fwd_kernel"),
+    (128, 300, 1000, 33, 12, "bf16", "dense_fwd_kernel"),
+    (256, 129, 65, 17, 9, "bf16", "dense_fwd_kernel"),
+    (520, 1, 1, 1, 1, "f32", "dense_fwd_kernel"),
+    (8, 512, 512, 32, 8, "f32", "table_kernel"),
+    (64, 1024, 1000, 32, 8, "f32", "table_kernel"),
+]
+
+
+@pytest.mark.parametrize("bh,nq,nk,m,tau,dtype,kernel", FORWARD_FORMS)
+def test_forward_forms(bh, nq, nk, m, tau, dtype, kernel):
+    """The forward's two forms (dense counts C V, or bucket tables) against the
+    oracle on every head; the library's kernel timer confirms which form ran."""
+    name = f"fwd_bh{bh}_nq{nq}_nk{nk}_m{m}_tau{tau}_{dtype}"
+    log(f"[{name}] start")
+    w = workloads.Workload(name, 1, bh, nq, 64, tau, m, dtype, "gauss", 4321 + nq + 7 * nk + m + tau)
+    inp = make_inputs(w, n=nq, n_k=nk)
+    q, k, v = (to_dev(inp[s], dtype) for s in ("q", "k", "v"))
+    R = torch.from_numpy(inp["R"]).cuda()
+    qc, kc = Y.hash_qk(q, k, R, m, tau)
+    torch.cuda.synchronize()
+    Y.yoso_timing_enable(64)
+    Y.yoso_timing_reset()
+    try:
+        y = Y.forward(qc, kc, v, m, tau, n_q=nq)
+        torch.cuda.synchronize()
+        launches = {kn: Y.yoso_timing_query(kn)[1] for kn in ("dense_fwd_kernel", "table_kernel")}
+    finally:
+        Y.yoso_timing_enable(0)
+    assert launches[kernel] >= 1 and sum(launches.values()) == launches[kernel], launches
+    ref = oracle.forward(codes_np(qc), codes_np(kc), inp["v"], m, tau)
+    check_all(name, [("y", y.float().cpu().numpy().astype(np.float64), ref)], TOL[dtype])
+
+
 @pytest.mark.parametrize("bh,nq,nk,m,tau,dtype", [(1, 65536, 65536, 3, 10, "f32"), (1, 65535, 65536, 2, 12, "bf16")])
 def test_maximum_length(bh, nq, nk, m, tau, dtype):
     """Sequences at the library's limit of 65536 rows (the most that the 16-bit row
