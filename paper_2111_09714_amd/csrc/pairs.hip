@@ -58,6 +58,13 @@ namespace {
 // and tau <= 10 (the larger tables and masks of tau 11-12 do not fit twice).
 constexpr int kSortThreads = 256;
 constexpr int kSortThreadsWide = 512;
+// Short sequences over many heads: one wave per (head, hash, side).  The work of a
+// workgroup is then a few 64-row steps and its fixed cost (zeroing, scan, barriers)
+// is paid by one wave, with many more workgroups resident per CU (384 x 512: 90 ->
+// 56 us; at 4096 rows four waves are faster, and a single head gains nothing).
+constexpr int kSortThreadsNarrow = 64;
+constexpr int64_t kSortNarrowN = 1024;
+constexpr int64_t kSortNarrowBlocks = 2048;
 
 // Waves of a sort workgroup that place rows: each needs a 64-bit lane mask per bucket.
 __host__ __device__ constexpr int sort_placing_waves(int tau, int waves) { return tau <= 10 ? waves : 1; }
@@ -2140,9 +2147,11 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
         // once, with stride m) and its sorted entries staged, 6 bytes per row; (2) the
         // codes transposed to [bh][m][n] first (each block then reads its column
         // contiguously) and the entries staged, 4 bytes per row; (3) transposed codes,
-        // entries stored straight to memory (eight waves when tau <= 10).
-        size_t sort_lds = sort_base_lds(kSortThreads, tau);
+        // entries stored straight to memory (eight waves when tau <= 10).  Short
+        // sequences take mode (1) with one wave per block.
         const int64_t n_max = n_q > n_k ? n_q : n_k;
+        const bool narrow = n_max <= kSortNarrowN && 2 * units >= kSortNarrowBlocks;
+        size_t sort_lds = sort_base_lds(narrow ? kSortThreadsNarrow : kSortThreads, tau);
         const bool stage_codes = sort_lds + static_cast<size_t>(n_max) * 6 <= kSortStageLds;
         const bool stage_ent = stage_codes || sort_lds + static_cast<size_t>(n_max) * 4 <= kSortEntLds;
         const bool transposed = !stage_codes;
@@ -2170,7 +2179,10 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
         const dim3 grid(static_cast<unsigned>(2 * units));
         int32_t *qo = reinterpret_cast<int32_t *>(ws + L.qoff), *ko = reinterpret_cast<int32_t *>(ws + L.koff);
         uint32_t *qe = reinterpret_cast<uint32_t *>(ws + L.qent), *ke = reinterpret_cast<uint32_t *>(ws + L.kent);
-        if (wide)
+        if (narrow)
+            hipLaunchKernelGGL(sort_kernel<kSortThreadsNarrow>, grid, dim3(kSortThreadsNarrow), sort_lds, stream, qsrc,
+                               ksrc, m, n_q, n_k, tau, transposed, stage_codes, stage_ent, qo, ko, qe, ke);
+        else if (wide)
             hipLaunchKernelGGL(sort_kernel<kSortThreadsWide>, grid, dim3(kSortThreadsWide),
                                sort_base_lds(kSortThreadsWide, tau), stream, qsrc, ksrc, m, n_q, n_k, tau, transposed,
                                false, false, qo, ko, qe, ke);

@@ -85,6 +85,10 @@ SMALL = [
     (1, 200, 150, 32, 12, "bf16"),
     (2, 1, 1, 8, 4, "f32"),
     (1, 17, 33, 7, 2, "bf16"),
+    # many heads of short sequences: the bucket sort's one-wave blocks, the dense
+    # forward and the dense backward
+    (40, 300, 257, 32, 8, "f32"),
+    (32, 129, 1000, 33, 12, "bf16"),
     # above 1024 rows on a side the pair passes serve dQ, dK (below, the dense form)
     (1, 1025, 1100, 7, 5, "f32"),
     (2, 1500, 1030, 16, 8, "bf16"),
