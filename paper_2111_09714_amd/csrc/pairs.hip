@@ -1531,6 +1531,21 @@ __global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
     const int stride = dense_stride(a.n_s);
     const int nf = static_cast<int>(a.n_f), ns = static_cast<int>(a.n_s);
 
+    // the streamed side's rows: lane l of wave w loads row 16w + (l & 15), dims
+    // 16 (l >> 4) + [0, 16) of a tile (rows clamped: the prefetch past the last tile
+    // reads the last rows again and is never used).  The first tile's loads are in
+    // flight while the counts are built.
+    const int lrow = 16 * wave + (lane & 15), lq = lane >> 4;
+    auto load_tile = [&](int c0, float (&xg)[16], float (&xy)[16]) {
+        const int64_t off = (b * a.n_s + min(c0 + lrow, ns - 1)) * D + 16 * lq;
+        load8<BF16>(a.sg, off, xg);
+        load8<BF16>(a.sg, off + 8, xg + 8);
+        load8<BF16>(a.sy, off, xy);
+        load8<BF16>(a.sy, off + 8, xy + 8);
+    };
+    float xga[16], xya[16], xgb[16], xyb[16];
+    load_tile(0, xga, xya);
+
     // ---- 1. collision counts.  Items (fixed row, hash) in groups of eight per
     // thread: their codes, then their bucket ranges, then the entries, each stage's
     // loads all in flight before the next stage uses them.
@@ -1604,21 +1619,6 @@ __global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
 
     // ---- 3. streamed tiles.  Staging: lane l of wave w stages row 16w + (l & 15),
     // dims 16 (l >> 4) + [0, 16) (a quarter-wave writes 16 rows at one chunk).
-    const int lrow = 16 * wave + (lane & 15), lq = lane >> 4;
-    auto load_row = [&](const void *src, int c0, float x[16]) {
-        const int row = c0 + lrow;
-        const int64_t off = (b * a.n_s + min(row, ns - 1)) * D + 16 * lq;
-        load8<BF16>(src, off, x);
-        load8<BF16>(src, off + 8, x + 8);
-        const bool ok = row < ns;
-        float mx = 0.f;
-#pragma unroll
-        for (int i = 0; i < 16; i++) {
-            x[i] = ok ? x[i] : 0.f;
-            mx = fmaxf(mx, fabsf(x[i]));
-        }
-        return mx;
-    };
     auto put_row = [&](unsigned char *dst, const float x[16], float scale) {
         half8 h[2], l[2];
         split8(x, scale, h[0], l[0]);
@@ -1628,6 +1628,17 @@ __global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
             *reinterpret_cast<half8 *>(dst + swz(lrow, 2 * lq + u, 256)) = h[u];
             *reinterpret_cast<half8 *>(dst + swz(lrow, 8 + 2 * lq + u, 256)) = l[u];
         }
+    };
+    // rows past n_s become zeros when the tile is staged
+    auto row_max = [&](int c0, float x[16]) {
+        const bool ok = c0 + lrow < ns;
+        float mx = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; i++) {
+            x[i] = ok ? x[i] : 0.f;
+            mx = fmaxf(mx, fabsf(x[i]));
+        }
+        return mx;
     };
     const int pr = 4 * g + (c >> 2), a4 = c & 3;
     const floatx4 z4 = {0.f, 0.f, 0.f, 0.f};
@@ -1644,11 +1655,13 @@ __global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
     const bool with_dv = a.out2 != nullptr;
     const uint32_t *crow = cnt + (16 * wave + c) * stride;  // the lane's fixed row of counts
     int eg = 0, ey = 0;
-    for (int c0 = 0; c0 < ns; c0 += kDenseTile) {
+    // one streamed tile from (xg, xy), the next one's loads into (gn, yn) (two
+    // register sets, swapped by unrolling the loop twice: copying registers a load
+    // is still filling would wait for it)
+    auto do_tile = [&](int c0, float (&xg)[16], float (&xy)[16], float (&gn)[16], float (&yn)[16]) {
         __syncthreads();  // counts complete (first tile); the previous tile has been read
-        float xg[16], xy[16];
-        float mg = load_row(a.sg, c0, xg);
-        float my = load_row(a.sy, c0, xy);
+        float mg = row_max(c0, xg);
+        float my = row_max(c0, xy);
         mg = wave_max(mg);
         my = wave_max(my);
         if (lane == 0) {
@@ -1670,6 +1683,7 @@ __global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
         }
         eg = eg_new;
         ey = ey_new;
+        load_tile(c0 + kDenseTile, gn, yn);
         __syncthreads();
 #pragma unroll 1
         for (int cb = 0; cb < kDenseTile / 16; cb++) {
@@ -1732,6 +1746,10 @@ __global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
                     out2[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(gl[dt], vh, out2[dt], 0, 0, 0);
             }
         }
+    };
+    for (int c0 = 0; c0 < ns; c0 += 2 * kDenseTile) {
+        do_tile(c0, xga, xya, xgb, xyb);
+        if (c0 + kDenseTile < ns) do_tile(c0 + kDenseTile, xgb, xyb, xga, xya);
     }
 
     // ---- 4. out = acc 2^(16 + k) (a row 2^(13 - e_a)) (g tile 2^(13 - e_g)) (y tile 2^(13 - e_y));
