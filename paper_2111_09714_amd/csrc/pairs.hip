@@ -392,7 +392,7 @@ struct PassArgs {
     int m, tau;
     float scale;                     // tau / (2m)
     int tab_t;                       // table form for buckets with b_q b_k > tab_t (b_q + b_k); 0: none
-    bool p16;                        // 16-bit partial rows (bf16 outputs): no low parts
+    bool p16;                        // 16-bit partial rows carrying their exponents (bf16 outputs)
 };
 
 // ---- the wave's LDS tile
@@ -664,13 +664,18 @@ __device__ __forceinline__ uint32_t low_off(int r, int w) {
 // the partials are read once, by the reduction, and should not evict the operands
 // from L2.  Exponents go to the block's LDS copy of its exponent row when it fits
 // (written out whole at the end: single-byte stores scattered over the row would
-// each cost a partial-line write), else straight to memory.  Rows past nvalid and
-// rows whose entry carries kSkipCode (their bucket takes the table form) are not
-// stored.
+// each cost a partial-line write), else straight to memory.  p16 (bf16 outputs):
+// 16-bit rows that carry their own exponent (below).  Rows past nvalid and rows
+// whose entry carries kSkipCode (their bucket takes the table form) are not stored.
+// (P16 fixes p16 at compile time for the bf16 kernels; the fp32 kernels pass it as
+// the run-time value it is, false: compiled as a constant there, the code around
+// it was scheduled 4-11% slower, measured on the pair and table kernels)
+template <bool P16>
 __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, uint8_t *plow, int8_t *pexp,
-                                           int8_t *ex_lds, bool ex_in_lds, int m, bool p16, const uint32_t *tile_ent,
-                                           int nvalid, int q, int cl, int g, int c, const floatx4 outT[4],
-                                           float orow) {
+                                           int8_t *ex_lds, bool ex_in_lds, int m, bool rt_p16,
+                                           const uint32_t *tile_ent, int nvalid, int q, int cl, int g, int c,
+                                           const floatx4 outT[4], float orow) {
+    const bool p16 = P16 || rt_p16;
     // nothing to store when every row of the tile takes the table form (wave-uniform)
     if (__builtin_amdgcn_ballot_w64(c < nvalid && (tile_ent[c] >> 16) != kSkipCode) == 0) return;
     // max |value| of row c over this lane's 16 values (a chain of 3-input maxima),
@@ -701,7 +706,7 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
     const int fb = p16 ? 15 : 23;
     const int mmax = (1 << fb) - 1;
     const float sc = mx > 0.f ? __uint_as_float(static_cast<uint32_t>(127 + fb - e) << 23) * orow : 0.f;
-    if (g == 0 && c < nvalid && (tile_ent[c] >> 16) != kSkipCode) {
+    if (!p16 && g == 0 && c < nvalid && (tile_ent[c] >> 16) != kSkipCode) {
         const uint32_t row = tile_ent[c] & 0xFFFFu;
         if (ex_in_lds) ex_lds[row] = static_cast<int8_t>(e);
         else pexp[row] = static_cast<int8_t>(e);
@@ -713,6 +718,19 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
         int mm[4];
 #pragma unroll
         for (int j = 0; j < 4; j++) mm[j] = min(max(__float2int_rn(outT[dt][j] * sc), -mmax), mmax);
+        if (p16 && dt == 0 && g == 0) {
+            // 16-bit rows carry their exponent in the record: the two low bits of
+            // values 0 .. 3 (held by this lane) are bits 2j, 2j+1 of e, and those four
+            // values keep 14 bits (2^-13 of the row's largest value); the row is then
+            // one whole 128-byte line with nothing stored beside it
+            const uint32_t eb = static_cast<uint32_t>(e) & 0xFFu;
+#pragma unroll
+            for (int j = 0; j < 4; j++)
+                mm[j] = static_cast<int>(static_cast<uint32_t>(min(max(__float2int_rn(outT[0][j] * sc * 0.25f), -8191),
+                                                                   8191))
+                                         << 2) |
+                        static_cast<int>((eb >> (2 * j)) & 3u);
+        }
         // byte permutes: the high parts are bytes 1-2 of each M, the low part byte 0
         // (v_perm_b32 picks any bytes of a register pair: {first operand : second})
         const uint32_t u[4] = {static_cast<uint32_t>(mm[0]), static_cast<uint32_t>(mm[1]),
@@ -818,7 +836,7 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
     const int esum = head_exp(a.pmax, b, kside ? 3 : 1) + head_exp(a.pmax, b, kside ? 1 : 3) +
                      head_exp(a.pmax, b, kside ? 0 : 2);
     const float oscale = ldexpf(a.scale, esum - 39 + 2);
-    const bool ex_in_lds = n_r <= kExpLds;
+    const bool ex_in_lds = !a.p16 && n_r <= kExpLds;  // (16-bit rows carry their exponents)
 
     // buckets in the table form (bucket_kernel writes their rows' partials): the
     // plan leaves their rows out of every tile's partner range and the run's copy
@@ -922,7 +940,7 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
         auto zero_tiles = [&](int ta, int tb) {
             const floatx4 z[4] = {};
             for (int t = ta; t < tb; t++)
-                store_tile(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, a.p16, tile_ents(t), row_count(t), q, cl, g,
+                store_tile<HI1>(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, a.p16, tile_ents(t), row_count(t), q, cl, g,
                            c, z, 0.f);
         };
         // sub-tile j of the run: its tile (searched forward from t) and first partner
@@ -1000,7 +1018,7 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
                 compute_sub<STAR, HI1>(tile, cur.pe, rh, rl, rbh, rbl, xscale, static_cast<int>(row_entry(cur.t) >> 16),
                                   ldexpf(1.0f, -2 - erow), g, c, outT);
                 if (newtile) {
-                    store_tile(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, a.p16, tile_ents(cur.t), row_count(cur.t), q, cl,
+                    store_tile<HI1>(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, a.p16, tile_ents(cur.t), row_count(cur.t), q, cl,
                                g, c, outT, ldexpf(oscale, erow));
 #pragma unroll
                     for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -1309,7 +1327,7 @@ __global__ __launch_bounds__(kPassThreads, 2) void bucket_kernel(PassArgs a) {
 #pragma unroll
                 for (int dt = 0; dt < 4; dt++)
                     outT[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(mtl[dt][kb], rh[kb], outT[dt], 0, 0, 0);
-            store_tile(st, part, plow, pexp, nullptr, false, a.m, a.p16, tent, nvalid, q, cl, g, c, outT, orow);
+            store_tile<HI1>(st, part, plow, pexp, nullptr, false, a.m, a.p16, tent, nvalid, q, cl, g, c, outT, orow);
             return t + 1 < ntile;
         };
         for (int t = 0;; t += 3) {
@@ -1383,15 +1401,23 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *_
     float s[8];
 #pragma unroll
     for (int i = 0; i < 8; i++) s[i] = 0.f;
-    // 24-bit rows: M = high * 256 + low, value = M 2^(e - 23); bf16 outputs take
-    // 16-bit rows (no low parts): value = high 2^(e - 15)
+    // 24-bit rows: M = high * 256 + low, value = M 2^(e - 23), e from the exponent
+    // array.  bf16 outputs take 16-bit rows (no low parts): value = high 2^(e - 15),
+    // except values 0 .. 3, whose two low bits hold bits 2j, 2j+1 of e and whose
+    // value is (high >> 2) 2^(e - 13); the thread of a row holding values 0 .. 7
+    // decodes e and the row's other seven threads take it from there
     auto add = [&](const uint4v &v, const uint2v &l, int e) {
-        const float sc = ldexpf(1.0f, e - (BF16 ? 15 : 23));
         const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+        if constexpr (BF16) {
+            const uint32_t eb = (w[0] & 3u) | ((w[0] >> 14) & 0xCu) | ((w[1] & 3u) << 4) | ((w[1] >> 10) & 0xC0u);
+            e = __shfl(static_cast<int>(static_cast<int8_t>(eb)), 0, 8);
+        }
+        const float sc = ldexpf(1.0f, e - (BF16 ? 15 : 23));
         const uint32_t lb[2] = {l.x, l.y};
 #pragma unroll
         for (int i = 0; i < 8; i++) {
-            const int hi = static_cast<int16_t>((w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+            int hi = static_cast<int16_t>((w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
+            if (BF16 && i < 4 && q == 0) hi = (hi >> 2) * 4;  // the exponent bits out, the 14-bit value scaled to 16
             const int lo = BF16 ? 0 : static_cast<int>((lb[i >> 2] >> (8 * (i & 3))) & 0xFFu);
             s[i] = fmaf(static_cast<float>(BF16 ? hi : hi * 256 + lo), sc, s[i]);  // |M| < 2^23: exact in fp32
         }
@@ -1408,7 +1434,7 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *_
             for (int u = 0; u < 8; u++) lw[u] = __builtin_nontemporal_load(srl + (h0 + u) * (D / 8));
         }
 #pragma unroll
-        for (int u = 0; u < 8; u++) f[u] = ex[(h0 + u) * n];
+        for (int u = 0; u < 8; u++) f[u] = BF16 ? 0 : ex[(h0 + u) * n];
     };
     const int ng = m >> 3;
     if (ng > 0) load(v[0], l[0], e[0], 0);
@@ -1425,7 +1451,7 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *_
     int h = 8 * ng;
     for (; h < m; h++)
         add(__builtin_nontemporal_load(src + h * (D / 8)), BF16 ? uint2v{0u, 0u} : __builtin_nontemporal_load(srl + h * (D / 8)),
-            ex[h * n]);
+            BF16 ? 0 : ex[h * n]);
     if constexpr (BF16) {
         uint4 o;
         o.x = static_cast<uint32_t>(f32_to_bf16(s[0])) | (static_cast<uint32_t>(f32_to_bf16(s[1])) << 16);
@@ -2128,8 +2154,10 @@ BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, 
     const size_t low = bf16 ? 0 : static_cast<size_t>(D);
     L.lq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m * low);
     L.lk = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m * low);
-    L.eq = o; o = align_up(o + static_cast<size_t>(bh) * n_q * m);
-    L.ek = o; o = align_up(o + static_cast<size_t>(bh) * n_k * m);
+    // exponents of 24-bit rows (16-bit rows carry theirs)
+    const size_t ex = bf16 ? 0 : 1;
+    L.eq = o; o = align_up(o + ex * bh * n_q * m);
+    L.ek = o; o = align_up(o + ex * bh * n_k * m);
     L.pmax = o; o = align_up(o + static_cast<size_t>(bh) * 4 * kMaxParts * 4);
     L.table = o; o = align_up(o + table_workspace_bytes(bf16, bh, n_k, m, tau));
     L.total = o;

@@ -206,8 +206,10 @@ def test_workspace_sizes():
     partials = 2 * 32 * 4096 * 32 * (64 * 3 + 1)
     assert f32 >= index + split + partials
     assert f32 < 1.05 * (index + split + partials) + (1 << 20)
+    # bf16: no low parts and no exponent arrays (16-bit rows carry their exponents)
     low = 2 * 32 * 4096 * 32 * 64
-    assert f32 - low - (1 << 12) <= bf <= f32 - low
+    exps = 2 * 32 * 4096 * 32
+    assert f32 - low - exps - (1 << 12) <= bf <= f32 - low - exps
     assert Y.yoso_workspace_bytes(Y.OP_HASH, 32, 4096, 4096, 64, 32, 8, Y.F32) == 0
     assert Y.yoso_workspace_bytes(Y.OP_FORWARD, 32, 4096, 4096, 64, 32, 8, Y.F32) == 0
     with pytest.raises(Y.YosoError):
