@@ -161,8 +161,13 @@ yoso_status yoso_fast_hash(const void *x, yoso_dtype dtype, int64_t bh, int64_t 
  * qcodes [bh][n_q][m], kcodes [bh][n_k][m]  from yoso_hash with the same R.
  * v      [bh][n_k][d],  y [bh][n_q][d]  (dtype).  Queries whose buckets are empty
  * get 0 (no renormalisation).
- * workspace: yoso_workspace_bytes(YOSO_OP_FORWARD, ...) bytes (0 for every shape
- * whose tables fit in one LDS pass; then workspace may be NULL).
+ * Many heads of short sequences (both sides at most 1024 rows, enough heads to
+ * fill the GPU) take the same sum as y = (1/m) C v, C[i][j] the number of hashes
+ * under which query i and key j collide, counted pair by pair from the codes; the
+ * result differs from the tables' only in the rounding of the additions.
+ * workspace: yoso_workspace_bytes(YOSO_OP_FORWARD, ...) bytes (0 for that form
+ * and for every shape whose tables fit in one LDS pass; then workspace may be
+ * NULL).
  */
 yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const void *v,
                          yoso_dtype dtype, int64_t bh, int64_t n_q, int64_t n_k, int32_t d,

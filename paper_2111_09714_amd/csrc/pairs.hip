@@ -15,6 +15,8 @@
 // the same bucket with vectors a'_y and b_y, out_x = s sum_y (a_x . a'_y) b_y.
 //
 // Kernels:
+//   codes_t_kernel long sequences: the codes transposed to [bh][m][n], so that the
+//                  sort reads each (head, hash) column contiguously.
 //   sort_kernel    one workgroup per (head, hash, side): histogram of the codes,
 //                  exclusive scan -> bucket offsets, then the rows in bucket order
 //                  as packed entries (code << 16 | row): a stable counting sort in
@@ -24,7 +26,7 @@
 //                  consumer derives the same power-of-two scale per (head, tensor).
 //   split_kernel   Q, K, V, dY -> fp16 (hi, lo) rows, each head's tensor scaled by
 //                  2^(13 - e) with max|x| < 2^e, so that hi and lo stay normal fp16
-//                  numbers whatever the data's magnitude.
+//                  numbers whatever the data's magnitude (bf16 inputs: hi only).
 //   pass_kernel    one workgroup per (head, hash, side).  Each wave walks 16-row
 //                  tiles of sorted rows; the partners that can collide with a tile
 //                  form one contiguous range of sorted partners, visited 16 at a
@@ -34,10 +36,19 @@
 //                  transposed through a per-wave LDS tile.  The finished tile is the
 //                  hash's share of out for those rows; it is stored, not added, into a
 //                  partial buffer (each row of each hash is written exactly once, so no
-//                  atomics are needed) as a 24-bit fixed-point row: one power-of-two
-//                  exponent per row, 16 high bits and 8 low bits per value.
+//                  atomics are needed) as a fixed-point row with one power-of-two
+//                  exponent: 24 bits per value (16 high, 8 low), or 16 bits for bf16
+//                  outputs.  With *YOSO's weights (STAR) it runs over the m tau
+//                  derived hashes of drop_bit_kernel.
+//   bucket_kernel  the buckets large enough for the table form: per bucket and side
+//                  M = sum_y a'_y b_y^T (64 x 64), then out_x = s a_x^T M for its rows,
+//                  stored as the same partial rows (the pass kernel skips them).
 //   reduce_kernel  out[b][x] = sum over the m hashes of the partial rows, in hash
 //                  order (deterministic), written as fp32 or bf16.
+//   dense_kernel   short sequences: C = sum_h B_h from the sorted bucket lists, then
+//                  dQ, dK and dV as dense masked MFMA blocks, no partial rows.
+//   dense_fwd_kernel  the forward for many heads of short sequences, Y = (1/m) C V,
+//                  C counted from bit planes of the codes.
 // gfx950's global fp32 atomics sustain roughly 1.3 TB/s of payload, so a plain
 // store of every partial plus one coalesced reduction beats accumulating with
 // atomics.  Every fp32 product uses three fp16 MFMAs (hi*hi + hi*lo + lo*hi).
@@ -53,9 +64,10 @@ namespace yoso {
 
 namespace {
 
-// Sort workgroups: four waves when the column is staged in LDS; eight when it is
-// not (long sequences: more rows per workgroup to place, 89 -> 72 us at n = 32768)
-// and tau <= 10 (the larger tables and masks of tau 11-12 do not fit twice).
+// Sort workgroups: four waves when the column or the entries are staged in LDS;
+// eight when neither is (long sequences: more rows per workgroup to place, 89 ->
+// 72 us at n = 32768) and tau <= 10 (the larger tables and masks of tau 11-12 do not
+// fit twice); one for short sequences over many heads (below).
 constexpr int kSortThreads = 256;
 constexpr int kSortThreadsWide = 512;
 // Short sequences over many heads: one wave per (head, hash, side).  The work of a
