@@ -82,6 +82,39 @@ def bucket_work(qc, kc, tau: int, t: int):
     return int(prod.sum()), int(prod[~tab].sum()), int((hq + hk)[tab].sum())
 
 
+# upper bounds of the bucket-size classes of bucket_load's histogram (rows of one
+# side in one (head, hash, bucket)); the last class is everything above
+LOAD_CLASSES = (16, 64, 256, 1024)
+
+
+def bucket_load(qc, kc, tau: int):
+    """How the rows fall into buckets, from the codes on the host: per side the mean
+    rows per (head, hash, bucket) (n / 2^tau), the largest bucket and their ratio, and
+    the share of rows in buckets of each size class (up to 16, 64, 256, 1024 rows, and
+    more)."""
+    import numpy as np
+    B = 1 << tau
+    out = {}
+    for side, c in (("queries", qc), ("keys", kc)):
+        x = c.cpu().numpy().astype(np.int64) & (B - 1)  # [bh, n, m]
+        bh, n, m = x.shape
+        unit = (np.arange(bh)[:, None, None] * m + np.arange(m)[None, None, :]) * B
+        cnt = np.bincount((unit + x).ravel(), minlength=bh * m * B)
+        mean = n / B
+        rows = np.zeros(len(LOAD_CLASSES) + 1)
+        lo = 0
+        for i, hi in enumerate(LOAD_CLASSES + (None,)):
+            sel = (cnt > lo) if hi is None else ((cnt > lo) & (cnt <= hi))
+            rows[i] = cnt[sel].sum()
+            lo = hi if hi is not None else lo
+        total = max(rows.sum(), 1)
+        labels = [f"<={hi}" for hi in LOAD_CLASSES] + [f">{LOAD_CLASSES[-1]}"]
+        out[side] = {"mean_rows": round(mean, 3), "max_rows": int(cnt.max()) if cnt.size else 0,
+                     "max_over_mean": round(float(cnt.max()) / mean, 2) if cnt.size and mean > 0 else None,
+                     "row_share_by_bucket_rows": {lab: round(float(r / total), 4) for lab, r in zip(labels, rows)}}
+    return out
+
+
 COPY_BYTES = 256 << 20
 
 
@@ -309,6 +342,7 @@ def measure_configs(Y, torch, dev, cpu: bool):
                  "tokens_per_s": round(w.tokens / (ms * 1e-3), 1),
                  "hbm_roofline_frac": round(alg / (ms * 1e-3) / (HBM_PEAK_GBS * 1e9), 4),
                  "roofline": dominant_roofline(w, kernels, t["qc"], t["kc"]),
+                 "bucket_load": bucket_load(t["qc"], t["kc"], w.tau),
                  "kernels": {kn: {"launches_per_step": round(kv["launches_per_step"], 2),
                                   "avg_us": round(kv["avg_us"], 2)} for kn, kv in kernels.items()}}
         del t, step
@@ -566,6 +600,7 @@ def main() -> int:
         "hbm_roofline_frac_of_copy": round(copy_frac, 4),
         "algorithmic_bytes_per_step": alg_step_bytes,
         "roofline": roofline,
+        "bucket_load": bucket_load(qc, kc, w.tau),
         "kernels": {kn: {kk: round(vv, 3) for kk, vv in kv.items()} for kn, kv in kernels.items()},
         "cpu_baseline": cpu,
         "l2_normalize": l2,

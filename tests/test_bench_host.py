@@ -50,3 +50,21 @@ def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True, text=True,
                        timeout=300)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_bucket_load_by_hand():
+    # tau = 2 (4 buckets), one head, one hash: queries fill bucket 1 with 20 rows and
+    # bucket 3 with 4; keys put all 24 rows in bucket 0
+    q = torch.tensor([1] * 20 + [3] * 4, dtype=torch.int16).reshape(1, 24, 1)
+    k = torch.zeros((1, 24, 1), dtype=torch.int16)
+    load = bench.bucket_load(q, k, 2)
+    assert load["queries"]["mean_rows"] == 6.0
+    assert load["queries"]["max_rows"] == 20 and load["queries"]["max_over_mean"] == round(20 / 6, 2)
+    assert load["queries"]["row_share_by_bucket_rows"]["<=16"] == round(4 / 24, 4)
+    assert load["queries"]["row_share_by_bucket_rows"]["<=64"] == round(20 / 24, 4)
+    assert load["keys"]["max_rows"] == 24 and load["keys"]["row_share_by_bucket_rows"]["<=64"] == 1.0
+    # every row is counted once, whatever the high bits above tau hold
+    g = np.random.default_rng(3)
+    r = torch.from_numpy(g.integers(0, 2**15, (3, 500, 7)).astype(np.int16))
+    shares = bench.bucket_load(r, r, 5)["queries"]["row_share_by_bucket_rows"]
+    assert abs(sum(shares.values()) - 1.0) < 1e-3
