@@ -358,6 +358,50 @@ def measure_configs(Y, torch, dev, cpu: bool):
     return out
 
 
+SCALING_N = (1024, 2048, 4096, 8192, 16384, 32768)
+
+
+def scaling_timing(Y, torch, dev, reps: int = 5):
+    """Time per token against sequence length at fixed heads, tau and m (Table 1:
+    the forward is linear in n; the backward, pairs per bucket growing with n, is
+    linear where the buckets take the table form): hash of Q and K, forward and
+    backward on 8 heads (4 x 2), tau = 8, m = 32, fp32, Gaussian inputs, each timed
+    with events around `reps` eager calls after one warm-up call."""
+    from workloads import Workload, make_inputs
+    rows = []
+    for n in SCALING_N:
+        w = Workload(f"scaling_n{n}", 4, 2, n, 64, 8, 32, "f32", "gauss", 2111_09714 + n)
+        inp = make_inputs(w)
+        q, k, v, dy = (torch.from_numpy(inp[s]).to(dev) for s in ("q", "k", "v", "dy"))
+        R = torch.from_numpy(inp["R"]).to(dev)
+        qc = torch.empty((w.bh, n, w.m), dtype=torch.int16, device=dev)
+        kc = torch.empty_like(qc)
+        y, dq, dk, dv = torch.empty_like(q), torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+        wsf = Y.workspace(Y.OP_FORWARD, q, w.m, w.tau)
+        wsb = Y.workspace(Y.OP_BACKWARD, q, w.m, w.tau)
+        calls = {"hash_ms": lambda: (Y.yoso_hash(q, R, w.m, w.tau, qc), Y.yoso_hash(k, R, w.m, w.tau, kc)),
+                 "forward_ms": lambda: Y.yoso_forward(qc, kc, v, w.m, w.tau, y, wsf),
+                 "backward_ms": lambda: Y.yoso_backward(qc, kc, q, k, v, dy, w.m, w.tau, dq, dk, dv, wsb)}
+        row = {"n": n}
+        for key, call in calls.items():
+            call()
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                call()
+            b.record()
+            torch.cuda.synchronize()
+            row[key] = round(a.elapsed_time(b) / reps, 4)
+        tokens = w.batch * n
+        for key in ("hash_ms", "forward_ms", "backward_ms"):
+            row[key.replace("_ms", "_ns_per_token")] = round(row[key] * 1e6 / tokens, 2)
+        rows.append(row)
+        del q, k, v, dy, R, qc, kc, y, dq, dk, dv, wsf, wsb, inp
+        torch.cuda.empty_cache()
+    return {"heads": 8, "batch": 4, "tau": 8, "hashes": 32, "dtype": "f32", "inputs": "gauss", "rows": rows}
+
+
 def star_timing(Y, torch, w, t, stream):
     """*YOSO's backward (yoso_backward_star) on the bench workload, outside the timed
     step: its pair kernel runs over the m*tau derived hashes (pairs whose codes agree
@@ -417,8 +461,9 @@ def main() -> int:
     ap.add_argument("--cpu-heads", type=int, default=-1, help="heads in the oracle sample (-1: all)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-configs", action="store_true", help="skip the per-workload `configs` object")
-    ap.add_argument("--parts", default="star,l2,yoso_e,fast_hash",
-                    help="measurements besides the step (comma list of star, l2, yoso_e, fast_hash; 'none' for none), "
+    ap.add_argument("--parts", default="star,l2,yoso_e,fast_hash,scaling",
+                    help="measurements besides the step (comma list of star, l2, yoso_e, fast_hash, scaling; 'none' "
+                         "for none), "
                          "e.g. to profile the step's kernels alone")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, run a plain 256 MiB device copy (read + write) three times, "
@@ -608,8 +653,13 @@ def main() -> int:
         "fast_hash": fast,
         "yoso_star": star,
     }
-    if not args.no_configs:
+    if "scaling" in parts:
         del t, step, q, k, v, dy, qc, kc
+        torch.cuda.empty_cache()
+        out["scaling"] = scaling_timing(Y, torch, dev)
+    if not args.no_configs:
+        if "scaling" not in parts:
+            del t, step, q, k, v, dy, qc, kc
         torch.cuda.empty_cache()
         out["configs"] = measure_configs(Y, torch, dev, cpu=not args.no_cpu_baseline)
     print(json.dumps(out), flush=True)
