@@ -140,6 +140,36 @@ def test_forward_forms(bh, nq, nk, m, tau, dtype, kernel):
     check_all(name, [("y", y.float().cpu().numpy().astype(np.float64), ref)], TOL[dtype])
 
 
+def test_dense_forward_without_keys():
+    """Many heads with no keys at all: the dense forward runs (enough workgroups) and
+    every query reads empty buckets, so Y is exactly zero; one key per head gives
+    Y_i = (C_i0 / m) V_0 with C_i0 counted from the codes."""
+    bh, nq, m, tau = 600, 10, 4, 3
+    g = torch.Generator().manual_seed(5)
+    q = torch.nn.functional.normalize(torch.randn(bh, nq, 64, generator=g), dim=-1).cuda()
+    R = torch.randn(64, m * tau, generator=g).cuda()
+    for nk in (0, 1):
+        k = torch.nn.functional.normalize(torch.randn(bh, nk, 64, generator=g), dim=-1).cuda()
+        v = torch.randn(bh, nk, 64, generator=g).cuda()
+        qc, kc = Y.hash_qk(q, k, R, m, tau)
+        torch.cuda.synchronize()
+        Y.yoso_timing_enable(64)
+        Y.yoso_timing_reset()
+        try:
+            y = Y.forward(qc, kc, v, m, tau, n_q=nq)
+            torch.cuda.synchronize()
+            dense = Y.yoso_timing_query("dense_fwd_kernel")[1]
+        finally:
+            Y.yoso_timing_enable(0)
+        assert dense == 1
+        if nk == 0:
+            assert float(y.abs().max()) == 0.0
+        else:
+            c = (qc.long() == kc.long()).sum(-1, keepdim=True).float()  # [bh, nq, 1]
+            ref = c / m * v[:, :1, :]
+            assert torch.allclose(y, ref, rtol=1e-6, atol=1e-6)
+
+
 @pytest.mark.parametrize("bh,nq,nk,m,tau,dtype", [(1, 65536, 65536, 3, 10, "f32"), (1, 65535, 65536, 2, 12, "bf16")])
 def test_maximum_length(bh, nq, nk, m, tau, dtype):
     """Sequences at the library's limit of 65536 rows (the most that the 16-bit row
