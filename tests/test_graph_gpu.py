@@ -22,7 +22,10 @@ def log(msg):
     sys.stdout.flush()
 
 
-@pytest.mark.parametrize("wname,n", [("single_head_n512", 700), ("lra_n4096", None)])
+# (one head of 700 rows: the tables and the dense backward; all 384 heads of 512 rows:
+# the dense forward, the one-wave sort and the dense backward; the bench workload:
+# the tables, the pair passes, the table form and the reductions)
+@pytest.mark.parametrize("wname,n", [("single_head_n512", 700), ("bert_base_n512", None), ("lra_n4096", None)])
 def test_step_graph_replays_match_eager(wname, n):
     assert torch.cuda.is_available(), "GPU tests need a GPU"
     w = WORKLOADS[wname]
