@@ -158,6 +158,18 @@ def measured_traffic(kernel: str, workload: str):
         return None
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), or "unknown"."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, inp, heads, min_wall: float = 10.0):
     """Time the oracle (hash + forward + backward) on `heads`, one head per thread,
     repeating the sample until `min_wall` seconds have been spent (at most 30 s)."""
@@ -181,6 +193,7 @@ def cpu_baseline(w, inp, heads, min_wall: float = 10.0):
         "value": w.tokens / step_equiv,
         "unit": "tokens/s",
         "cores": threads,
+        "cpu_model": cpu_model(),
         "kind": "oracle",
         "sample": f"{len(heads)} of {w.bh} heads of the same workload (hash+forward+backward, fp64 C oracle, "
                   f"one head per thread), {reps} repetitions in {wall:.2f} s wall, scaled by {w.bh}/{len(heads)}",
