@@ -1545,11 +1545,13 @@ __device__ __forceinline__ void dense_store(void *dst, int64_t off, const floatx
     }
 }
 
-template <bool BF16>
-__global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
+template <bool BF16, int TILE>
+__global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArgs args) {
+    // staging: RPW rows per wave, LPR lanes per row, DPL dims per lane
+    constexpr int RPW = TILE / 4, LPR = 64 / RPW, DPL = D / LPR;
     extern __shared__ __align__(16) uint32_t cnt[];  // [kDenseRows][dense_stride(n_s)]
-    __shared__ __align__(16) unsigned char g_lds[kDenseTile * 256];
-    __shared__ __align__(16) unsigned char y_lds[kDenseTile * 256];
+    __shared__ __align__(16) unsigned char g_lds[TILE * 256];
+    __shared__ __align__(16) unsigned char y_lds[TILE * 256];
     __shared__ float tmax[8];
 
     // blocks of side 0, then side 1 (both sides' tile counts)
@@ -1569,19 +1571,20 @@ __global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
     const int stride = dense_stride(a.n_s);
     const int nf = static_cast<int>(a.n_f), ns = static_cast<int>(a.n_s);
 
-    // the streamed side's rows: lane l of wave w loads row 16w + (l & 15), dims
-    // 16 (l >> 4) + [0, 16) of a tile (rows clamped: the prefetch past the last tile
-    // reads the last rows again and is never used).  The first tile's loads are in
-    // flight while the counts are built.
-    const int lrow = 16 * wave + (lane & 15), lq = lane >> 4;
-    auto load_tile = [&](int c0, float (&xg)[16], float (&xy)[16]) {
-        const int64_t off = (b * a.n_s + min(c0 + lrow, ns - 1)) * D + 16 * lq;
-        load8<BF16>(a.sg, off, xg);
-        load8<BF16>(a.sg, off + 8, xg + 8);
-        load8<BF16>(a.sy, off, xy);
-        load8<BF16>(a.sy, off + 8, xy + 8);
+    // the streamed side's rows: lane l of wave w loads row RPW w + (l % RPW), dims
+    // DPL (l / RPW) + [0, DPL) of a tile (rows clamped: the prefetch past the last
+    // tile reads the last rows again and is never used).  The first tile's loads are
+    // in flight while the counts are built.
+    const int lrow = RPW * wave + (lane % RPW), lq = lane / RPW;
+    auto load_tile = [&](int c0, float (&xg)[DPL], float (&xy)[DPL]) {
+        const int64_t off = (b * a.n_s + min(c0 + lrow, ns - 1)) * D + DPL * lq;
+#pragma unroll
+        for (int u = 0; u < DPL / 8; u++) {
+            load8<BF16>(a.sg, off + 8 * u, xg + 8 * u);
+            load8<BF16>(a.sy, off + 8 * u, xy + 8 * u);
+        }
     };
-    float xga[16], xya[16], xgb[16], xyb[16];
+    float xga[DPL], xya[DPL], xgb[DPL], xyb[DPL];
     load_tile(0, xga, xya);
 
     // ---- 1. collision counts.  Items (fixed row, hash) in groups of eight per
@@ -1655,24 +1658,24 @@ __global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
         for (int kb = 0; kb < 2; kb++) split8(y[kb], ldexpf(1.0f, 13 - ea), arh[kb], arl[kb]);
     }
 
-    // ---- 3. streamed tiles.  Staging: lane l of wave w stages row 16w + (l & 15),
-    // dims 16 (l >> 4) + [0, 16) (a quarter-wave writes 16 rows at one chunk).
-    auto put_row = [&](unsigned char *dst, const float x[16], float scale) {
-        half8 h[2], l[2];
-        split8(x, scale, h[0], l[0]);
-        split8(x + 8, scale, h[1], l[1]);
+    // ---- 3. streamed tiles of TILE rows (32 rows, two 16 x 16 blocks, where there are
+    // enough workgroups to fill the GPU: smaller tiles and fewer prefetch registers
+    // leave room for three workgroups per CU; else 64).  Staging as the loads.
+    auto put_row = [&](unsigned char *dst, const float x[DPL], float scale) {
 #pragma unroll
-        for (int u = 0; u < 2; u++) {
-            *reinterpret_cast<half8 *>(dst + swz(lrow, 2 * lq + u, 256)) = h[u];
-            *reinterpret_cast<half8 *>(dst + swz(lrow, 8 + 2 * lq + u, 256)) = l[u];
+        for (int u = 0; u < DPL / 8; u++) {
+            half8 h, l;
+            split8(x + 8 * u, scale, h, l);
+            *reinterpret_cast<half8 *>(dst + swz(lrow, (DPL / 8) * lq + u, 256)) = h;
+            *reinterpret_cast<half8 *>(dst + swz(lrow, 8 + (DPL / 8) * lq + u, 256)) = l;
         }
     };
     // rows past n_s become zeros when the tile is staged
-    auto row_max = [&](int c0, float x[16]) {
+    auto row_max = [&](int c0, float x[DPL]) {
         const bool ok = c0 + lrow < ns;
         float mx = 0.f;
 #pragma unroll
-        for (int i = 0; i < 16; i++) {
+        for (int i = 0; i < DPL; i++) {
             x[i] = ok ? x[i] : 0.f;
             mx = fmaxf(mx, fabsf(x[i]));
         }
@@ -1696,7 +1699,7 @@ __global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
     // one streamed tile from (xg, xy), the next one's loads into (gn, yn) (two
     // register sets, swapped by unrolling the loop twice: copying registers a load
     // is still filling would wait for it)
-    auto do_tile = [&](int c0, float (&xg)[16], float (&xy)[16], float (&gn)[16], float (&yn)[16]) {
+    auto do_tile = [&](int c0, float (&xg)[DPL], float (&xy)[DPL], float (&gn)[DPL], float (&yn)[DPL]) {
         __syncthreads();  // counts complete (first tile); the previous tile has been read
         float mg = row_max(c0, xg);
         float my = row_max(c0, xy);
@@ -1721,10 +1724,10 @@ __global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
         }
         eg = eg_new;
         ey = ey_new;
-        load_tile(c0 + kDenseTile, gn, yn);
+        load_tile(c0 + TILE, gn, yn);
         __syncthreads();
 #pragma unroll 1
-        for (int cb = 0; cb < kDenseTile / 16; cb++) {
+        for (int cb = 0; cb < TILE / 16; cb++) {
             if (c0 + 16 * cb >= ns) break;
             // G^T block: lane (g, c) = (g row c0 + 16cb + 4g + i) . (a row c)
             half8 bh[2], bl[2];
@@ -1785,9 +1788,9 @@ __global__ __launch_bounds__(256, 2) void dense_kernel(DenseArgs args) {
             }
         }
     };
-    for (int c0 = 0; c0 < ns; c0 += 2 * kDenseTile) {
+    for (int c0 = 0; c0 < ns; c0 += 2 * TILE) {
         do_tile(c0, xga, xya, xgb, xyb);
-        if (c0 + kDenseTile < ns) do_tile(c0 + kDenseTile, xgb, xyb, xga, xya);
+        if (c0 + TILE < ns) do_tile(c0 + TILE, xgb, xyb, xga, xya);
     }
 
     // ---- 4. out = acc 2^(16 + k) (a row 2^(13 - e_a)) (g tile 2^(13 - e_g)) (y tile 2^(13 - e_y));
@@ -2270,10 +2273,12 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
         const int64_t blocks = bh * ((n_q + kDenseRows - 1) / kDenseRows + (n_k + kDenseRows - 1) / kDenseRows);
         const size_t lds = static_cast<size_t>(kDenseRows) * dense_stride(n_q > n_k ? n_q : n_k) * 4;
         KernelTimer timer("dense_kernel", stream);
-        if (bf16)
-            hipLaunchKernelGGL(dense_kernel<true>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, stream, d);
-        else
-            hipLaunchKernelGGL(dense_kernel<false>, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, stream, d);
+        // 32-row streamed tiles where the blocks fill the GPU at three per CU (384 x
+        // 512: 618 -> 515 us), 64-row ones for a few blocks (fewer barriers per row)
+        const bool t32 = blocks >= 512;
+        auto kernel = bf16 ? (t32 ? dense_kernel<true, 32> : dense_kernel<true, 64>)
+                           : (t32 ? dense_kernel<false, 32> : dense_kernel<false, 64>);
+        hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, stream, d);
         return hipGetLastError();
     }
 
