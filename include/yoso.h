@@ -31,9 +31,10 @@
  *     for two feature dims take 2^tau x 8 bytes, 32 KiB at tau = 12, and the
  *     bucket sort keeps 2^tau counters and 64-bit lane masks per wave; with at
  *     most 65536 rows, tau > 12 would leave almost every bucket with 0 or 1 key.
- *   - Inputs must be finite.  The hash stages rows through fp16 pairs after a
- *     2^8 scaling, so |x| must stay below 255 (unit rows always do) and |R| below
- *     65504.  The backward and YOSO-E scale every operand by a power of two
+ *   - Inputs must be finite.  The hash scales each row of x by a power of two
+ *     before staging it through fp16 pairs, so rows may have any finite
+ *     magnitude; R is staged unscaled, so |R| must stay below 65504 (Gaussian
+ *     entries below about 2^-3 keep their value to 2^-24 absolute).  The backward and YOSO-E scale every operand by a power of two
  *     before it is split into fp16 (hi, lo) pairs (per head and tensor, per row,
  *     or per 64-row tile), so V, dY, Q, K may have any magnitude between about
  *     2^-40 and 2^40; values more than about 2^20 below the largest of their

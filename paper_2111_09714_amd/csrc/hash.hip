@@ -9,8 +9,12 @@
 // The product runs on v_mfma_f32_16x16x32_f16.  Each fp32 operand is split into
 // an fp16 pair (hi + lo, ~21 significant bits, both truncated) and the three
 // products hi*hi, hi*lo, lo*hi are accumulated in fp32, so a projection is off by
-// at most about 2^-20 |x| |R[:, c]| (rows are scaled by 2^8 first so that lo parts
-// of unit-vector entries stay normal fp16 numbers; the scaling changes no sign).
+// at most about 2^-20 |x| |R[:, c]|.  Each row is first scaled by the power of two
+// 2^(13 - e), max |x_i| < 2^e, so that its entries lie below 2^13 and their hi and
+// lo parts are normal fp16 numbers whatever the row's magnitude (a positive scale
+// changes no sign).  A bf16 row so scaled is exact as its hi parts (8 significant
+// bits, within fp16's normal range down to 2^-27 of its largest entry), so bf16
+// inputs take two products, hi*hi and hi*lo of R.
 //
 // Work split: a workgroup of 8 or 16 waves (two or one per CU, as LDS allows)
 // converts R once into fp16 MFMA B-fragments in LDS and then walks tiles of 32
@@ -144,9 +148,24 @@ __global__ __launch_bounds__(64 * WAVES) void hash_kernel(const void *__restrict
         const int64_t base = tile * kHashRowsPerTile + wave * kHashWaveRows;
         half8 ah[kHashRT][2], al[kHashRT][2];
 #pragma unroll
-        for (int t = 0; t < kHashRT; t++)
+        for (int t = 0; t < kHashRT; t++) {
+            // the row's largest |entry| (its 64 entries sit in the lanes L, L ^ 16,
+            // L ^ 32, L ^ 48), then the power of two that brings it below 2^13
+            float mx = 0.f;
 #pragma unroll
-            for (int kb = 0; kb < 2; kb++) split8_rtz(xv[t][kb], 256.0f, ah[t][kb], al[t][kb]);
+            for (int kb = 0; kb < 2; kb++)
+#pragma unroll
+                for (int i = 0; i < 8; i++) mx = fmaxf(mx, fabsf(xv[t][kb][i]));
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            // (max |x_i| = f 2^e, f in [0.5, 1); the scale stays a normal fp32 number
+            // for every finite row, at most 2^126)
+            int e = 0;
+            if (mx > 0.f) frexpf(mx, &e);
+            const float sc = ldexpf(1.0f, min(13 - e, 126));
+#pragma unroll
+            for (int kb = 0; kb < 2; kb++) split8_rtz(xv[t][kb], sc, ah[t][kb], al[t][kb]);
+        }
         const int64_t next = tile + gridDim.x;
         if (next < num_tiles)
             hash_load_rows<BF16>(x, rows, next * kHashRowsPerTile + wave * kHashWaveRows, lane, xv);
@@ -163,8 +182,15 @@ __global__ __launch_bounds__(64 * WAVES) void hash_kernel(const void *__restrict
                     const half8 bh = frag[((nt * 2 + kb) * 2 + 0) * 64 + lane];
                     const half8 bl = frag[((nt * 2 + kb) * 2 + 1) * 64 + lane];
 #pragma unroll
-                    for (int t = 0; t < kHashRT; t++)
-                        acc[j][t] = mfma3_16x16x32(ah[t][kb], al[t][kb], bh, bl, acc[j][t]);
+                    for (int t = 0; t < kHashRT; t++) {
+                        if constexpr (BF16) {
+                            // (the lo parts of a scaled bf16 row are zero)
+                            acc[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[t][kb], bh, acc[j][t], 0, 0, 0);
+                            acc[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[t][kb], bl, acc[j][t], 0, 0, 0);
+                        } else {
+                            acc[j][t] = mfma3_16x16x32(ah[t][kb], al[t][kb], bh, bl, acc[j][t]);
+                        }
+                    }
                 }
             }
             // acc[j][t][i] of lane L is P[row 16t + 4*(L>>4) + i][col (g0+j)*16 + (L&15)].

@@ -351,6 +351,32 @@ def test_golden_worked_example(golden):
         assert not got[:, 2:].any()
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_hash_rows_of_any_magnitude(dtype):
+    """Rows scaled by powers of ten from 1e-30 to 1e30 (each row its own): the hash
+    scales every row by a power of two before its fp16 split, so its codes equal the
+    oracle's wherever every projection of the hash exceeds 1e-4 |x| |R[:, c]|."""
+    g = np.random.default_rng(11)
+    bh, n, m, tau = 2, 300, 8, 9
+    x = g.standard_normal((bh, n, 64)) * 10.0 ** g.uniform(-30, 30, size=(bh, n, 1))
+    x = x.astype(np.float32)
+    if dtype == "bf16":
+        x = workloads.bf16_round(x)
+    R = g.standard_normal((64, m * tau)).astype(np.float32)
+    codes = torch.empty((bh, n, m), dtype=torch.int16, device="cuda")
+    Y.yoso_hash(to_dev(x, dtype), torch.from_numpy(R).cuda(), m, tau, codes)
+    got = codes_np(codes)  # [bh, m, n]
+    ref = oracle.hash_codes(x.astype(np.float64), R, m, tau)
+    proj = np.einsum("bnd,dc->bnc", x.astype(np.float64), R.astype(np.float64))
+    rel = np.abs(proj) / (np.linalg.norm(x.astype(np.float64), axis=-1, keepdims=True) *
+                          np.linalg.norm(R.astype(np.float64), axis=0))
+    sure = rel.reshape(bh, n, m, tau).min(-1).transpose(0, 2, 1) > 1e-4  # [bh, m, n]
+    mism = (got != ref) & sure
+    log(f"[hash any magnitude {dtype}] {sure.size} codes, excluded {1 - sure.mean():.2e}, mismatches {int(mism.sum())}")
+    assert sure.mean() > 0.95
+    assert not mism.any()
+
+
 def test_golden_hash_example(golden):
     g = golden["hash"]
     m, tau = g["m"], g["tau"]
