@@ -37,8 +37,9 @@
  *     below about 2^-3 keep their value to 2^-24 absolute).  The backward and
  *     YOSO-E scale every operand by a power of two before it is split into
  *     fp16 (hi, lo) pairs (per head and tensor, per row, or per 64-row tile),
- *     so V, dY, Q, K may have any magnitude between about 2^-40 and 2^40; values more than about 2^20 below the largest of their
- *     head (backward) or tile (YOSO-E) keep less than 22 significant bits.
+ *     so V, dY, Q, K may have any magnitude between about 2^-40 and 2^40;
+ *     values more than about 2^20 below the largest of their head (backward)
+ *     or tile (YOSO-E) keep less than 22 significant bits.
  *   - Precision.  Y and dV are accumulated as exact fixed-point integers: each
  *     value of feature dim d is rounded to a multiple of 2^-k_d, where 2^k_d is
  *     the largest power of two keeping 2^k_d (1 + 2^-10) times that dim's sum of
