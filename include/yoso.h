@@ -48,7 +48,7 @@
  *     from fp16 (hi, lo) pairs (about 22 significant bits; bf16 inputs are
  *     exact as the hi halves alone wherever they lie within 2^27 of their head's
  *     largest value); the contribution of each hash to a row is kept in 24-bit
- *     fixed point (one power-of-two exponent per row, exact to 2^-23 of that
+ *     fixed point (one power-of-two exponent per row, exact to 2^-22 of that
  *     row's largest value; 16-bit, exact to 2^-15, for bf16 outputs, whose own
  *     rounding is 2^-9, four values of each row keeping 14 bits, 2^-13, beside
  *     the row's exponent), and the m contributions are summed in hash order in
@@ -189,8 +189,9 @@ yoso_status yoso_forward(const uint16_t *qcodes, const uint16_t *kcodes, const v
  * per-hash bucket orders, the per-head maxima of |q|, |k|, |v|, |dy|, fp16
  * (hi, lo) copies of q, k, v, dy, and one 24-bit (bf16: 16-bit) fixed-point
  * partial row per (row, hash) for dq and dk, the codes transposed to [bh][m][n]
- * for the bucket sort: about (3*m*d + 7*m + 8*d) * (n_q + n_k) * bh bytes
- * (bf16: (2*m*d + 6*m + 8*d) * (n_q + n_k) * bh).
+ * for the bucket sort, one exponent byte per row of dy and v: about
+ * (3*m*d + 7*m + 8*d + 1) * (n_q + n_k) * bh bytes
+ * (bf16: (2*m*d + 6*m + 8*d + 1) * (n_q + n_k) * bh).
  * A bucket with b_q queries and b_k keys whose sizes pass
  * yoso_backward_table_threshold() is summed in the table form of Sec. 3.3
  * restricted to that bucket (one d x d matrix per side and bucket, applied to the

@@ -25,7 +25,7 @@ size_t table_workspace_bytes(bool bf16, int64_t bh, int64_t n_dst, int m, int ta
 size_t hash_lds_bytes(int m, int tau);
 
 struct BackwardLayout {
-    size_t qoff, koff, qent, kent, qct, kct, qs, dys, ks, vs, pq, pk, lq, lk, eq, ek, pmax, table, total;
+    size_t qoff, koff, qent, kent, qct, kct, qs, dys, ks, vs, pq, pk, lq, lk, eq, ek, rexq, rexk, pmax, table, total;
 };
 BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, int m, int tau);
 

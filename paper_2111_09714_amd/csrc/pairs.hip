@@ -400,6 +400,9 @@ struct PassArgs {
     int16_t *pq, *pk;                // partials [bh][n][m][64]: high 16 bits of the 24-bit mantissas
     uint8_t *lq, *lk;                // [bh][n][m][64]: their low 8 bits
     int8_t *eq, *ek;                 // their exponents [bh][m][n] (one block writes one n-byte run)
+    // per row of dY (the dQ side's rows) and of V (the dK side's): e with ||a|| < 2^e
+    // for the fp16 pairs above [bh][n] (split_kernel)
+    const int8_t *rexq, *rexk;
     int64_t bh;
     int m, tau;
     float scale;                     // tau / (2m)
@@ -481,11 +484,9 @@ __device__ __forceinline__ void load_row_tile(uint4 r[4], const uint4 &re4, cons
 }
 
 // Rows through the tile into the MFMA B-operand layout of S^T: lane (g, c) gets
-// row c, dims kb*32 + 8g + [0, 8) (hi and lo; HI1: hi, and lo is zero).  Returns
-// e_c with ||a_c|| < 2^e_c for the lane's row c (from the fp16 pairs the products
-// use; the row's other three quarters sit in the lanes 16, 32 and 48 away).
+// row c, dims kb*32 + 8g + [0, 8) (hi and lo; HI1: hi, and lo is zero).
 template <bool HI1>
-__device__ __forceinline__ int stage_rows(const uint4 r[4], unsigned char *tile, int q, int cl, int g, int c,
+__device__ __forceinline__ void stage_rows(const uint4 r[4], unsigned char *tile, int q, int cl, int g, int c,
                                           half8 rh[2], half8 rl[2]) {
 #pragma unroll
     for (int i = 0; i < (HI1 ? 2 : 4); i++) lds_st(tile, swz(slot_row<HI1>(q, cl, i), slot_chunk<HI1>(cl), 256), r[i]);
@@ -497,27 +498,6 @@ __device__ __forceinline__ int stage_rows(const uint4 r[4], unsigned char *tile,
         else
             rl[kb] = lds_ld<half8>(tile, swz(c, 8 + kb * 4 + g, 256));
     }
-    float ss = 0.f;
-#pragma unroll
-    for (int kb = 0; kb < 2; kb++)
-#pragma unroll
-        for (int i = 0; i < 8; i++) {
-            const float x = static_cast<float>(rh[kb][i]) + static_cast<float>(rl[kb][i]);
-            ss = fmaf(x, x, ss);
-        }
-    {
-        const auto t = __builtin_amdgcn_permlane16_swap(__float_as_uint(ss), __float_as_uint(ss), false, false);
-        ss = __uint_as_float(t[0]) + __uint_as_float(t[1]);
-    }
-    {
-        const auto t = __builtin_amdgcn_permlane32_swap(__float_as_uint(ss), __float_as_uint(ss), false, false);
-        ss = __uint_as_float(t[0]) + __uint_as_float(t[1]);
-    }
-    // ss < 2^e2  ->  ||a|| < 2^ceil(e2 / 2); the sum's rounding (far below one part in
-    // 2^20) is covered by the factor 4 of slack in the 2^14 bound of S
-    int e2 = 0;
-    if (ss > 0.f) frexpf(ss, &e2);
-    return (e2 + 1) >> 1;
 }
 
 // The rows' own b vectors (the q of a query row, the k of a key row; used by
@@ -666,9 +646,14 @@ __device__ __forceinline__ uint32_t low_off(int r, int w) {
 // Write the partial rows of a finished tile: lane (g, c) holds out[row c][16dt +
 // 4g + (0..3)] / orow, orow being the lane's row factor.  A partial row is stored
 // as 24-bit fixed point: one exponent e with max|value| < 2^e, and per value the
-// integer M = round(value * 2^(23 - e)), |M| < 2^23, kept as its high 16 bits
-// (M >> 8, int16) and its low 8 bits (M & 255); value = M 2^(e - 23) (rounding
-// error at most 2^(e - 24), i.e. below 2^-23 of the row's largest value).  The row
+// integer M = round(value * 2^(22 - e)), |M| <= 2^22, kept in offset binary as
+// U = M + 2^22 (0 <= U <= 2^23): its high 16 bits (U >> 8) and its low 8 bits
+// (U & 255); value = (U - 2^22) 2^(e - 22) (rounding error at most 2^(e - 23),
+// i.e. below 2^-22 of the row's largest value).  U comes from one fused
+// multiply-add: value * 2^(22 - e) + 1.5 * 2^23 lies in (2^23, 2^24), where fp32
+// numbers are the integers, so the sum rounded to nearest (ties to even, as M is
+// rounded) is 1.5 * 2^23 + M, whose low 24 bits are U (2^24 itself, M = 2^22, has
+// low bits 2^23 = U as well).  The row
 // maximum and M are computed where the MFMA leaves the values (16 per lane, the
 // rest of the row in the lanes 16, 32 and 48 away: two permlane swaps); both parts
 // then go through the tile so that each quarter-wave stores one whole 128-byte
@@ -713,9 +698,10 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
     const int e = min(max(static_cast<int>((__float_as_uint(mxs) >> 23) & 0xFFu) - 126, -100), 100);
     // value * 2^(fb - e) lies in (-2^fb, 2^fb): a power-of-two scaling of the
     // rounded product value * orow, so the row maximum stays below 2^fb before
-    // rounding (and at most 2^fb after, hence the clamp).  fb = 23 (24-bit rows), or
-    // 15 with p16 (16-bit rows: bf16 outputs, whose own rounding is 2^-9)
-    const int fb = p16 ? 15 : 23;
+    // rounding (and at most 2^fb after, hence the clamp of 16-bit values).  fb = 22
+    // (24-bit rows), or 15 with p16 (16-bit rows: bf16 outputs, whose own rounding
+    // is 2^-9)
+    const int fb = p16 ? 15 : 22;
     const int mmax = (1 << fb) - 1;
     const float sc = mx > 0.f ? __uint_as_float(static_cast<uint32_t>(127 + fb - e) << 23) * orow : 0.f;
     if (!p16 && g == 0 && c < nvalid && (tile_ent[c] >> 16) != kSkipCode) {
@@ -728,8 +714,13 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
 #pragma unroll
     for (int dt = 0; dt < 4; dt++) {
         int mm[4];
+        if (p16) {
 #pragma unroll
-        for (int j = 0; j < 4; j++) mm[j] = min(max(__float2int_rn(outT[dt][j] * sc), -mmax), mmax);
+            for (int j = 0; j < 4; j++) mm[j] = min(max(__float2int_rn(outT[dt][j] * sc), -mmax), mmax);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 4; j++) mm[j] = __float_as_int(fmaf(outT[dt][j], sc, 12582912.0f));  // 1.5 * 2^23
+        }
         if (p16 && dt == 0 && g == 0) {
             // 16-bit rows carry their exponent in the record: the two low bits of
             // values 0 .. 3 (held by this lane) are bits 2j, 2j+1 of e, and those four
@@ -743,7 +734,7 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
                                          << 2) |
                         static_cast<int>((eb >> (2 * j)) & 3u);
         }
-        // byte permutes: the high parts are bytes 1-2 of each M, the low part byte 0
+        // byte permutes: the high parts are bytes 1-2 of each U, the low part byte 0
         // (v_perm_b32 picks any bytes of a register pair: {first operand : second})
         const uint32_t u[4] = {static_cast<uint32_t>(mm[0]), static_cast<uint32_t>(mm[1]),
                                static_cast<uint32_t>(mm[2]), static_cast<uint32_t>(mm[3])};
@@ -827,6 +818,7 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
     const _Float16 *apar = (kside ? a.dys : a.vs) + b * n_p * (2 * D);
     const _Float16 *bpar = (kside ? a.qs : a.ks) + b * n_p * (2 * D);
     const _Float16 *brow = (kside ? a.ks : a.qs) + b * n_r * (2 * D);  // *YOSO only
+    const int8_t *rexp = (kside ? a.rexk : a.rexq) + b * n_r;         // ||a_r|| < 2^rexp[r]
     // *YOSO: x = (q 2^(13 - e_Q)) . (k 2^(13 - e_K)) * xscale
     const float xscale = STAR ? ldexpf(1.0f, head_exp(a.pmax, b, 0) + head_exp(a.pmax, b, 2) - 26) : 0.f;
     // partial row (row r, hash h) starts r*m*64 elements past these bases, its
@@ -976,11 +968,13 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
                 uint4 pe;     // entries of its partners 4q .. 4q+3
                 uint4 rw[4];  // its tile's rows, loaded when the tile starts here
                 uint4 rb[4];  // (*YOSO) the same rows' own b vectors
+                int ex;       // e_c with ||a_c|| < 2^e_c for the lane's row c of the tile
             };
             auto fill = [&](Slot &sl, int t, int y, bool new_tile) {
                 sl.t = t;
                 sl.pe = pent4(y);
                 if (new_tile) {
+                    sl.ex = rexp[row_entry(t) & 0xFFFFu];  // (sentinel rows read row 0)
                     load_row_tile<HI1>(sl.rw, row_entries4(t), arow, cl);
                     if constexpr (STAR) load_row_tile<HI1>(sl.rb, row_entries4(t), brow, cl);
                 }
@@ -1004,7 +998,8 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
                 cursor_at(t1);
             }
             half8 rh[2], rl[2], rbh[2], rbl[2];
-            int erow = stage_rows<HI1>(A.rw, tile, q, cl, g, c, rh, rl);  // ||a_c|| < 2^erow
+            stage_rows<HI1>(A.rw, tile, q, cl, g, c, rh, rl);
+            int erow = A.ex;  // ||a_c|| < 2^erow
             if constexpr (STAR) stage_rows_b<HI1>(A.rb, tile, q, cl, g, c, rbh, rbl);
             // one operand buffer: a sub-tile's registers are reloaded with the next
             // sub-tile as soon as they have been written to the tile
@@ -1036,7 +1031,8 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
                     for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
                     zero_tiles(cur.t + 1, has1 ? nxt.t : thi);
                     if (has1) {
-                        erow = stage_rows<HI1>(nxt.rw, tile, q, cl, g, c, rh, rl);
+                        stage_rows<HI1>(nxt.rw, tile, q, cl, g, c, rh, rl);
+                        erow = nxt.ex;
                         if constexpr (STAR) stage_rows_b<HI1>(nxt.rb, tile, q, cl, g, c, rbh, rbl);
                     }
                 }
@@ -1359,6 +1355,7 @@ __global__ __launch_bounds__(256) void split_kernel(const void *__restrict__ q, 
                                                     const void *__restrict__ v, const void *__restrict__ dy,
                                                     _Float16 *__restrict__ qs, _Float16 *__restrict__ ks,
                                                     _Float16 *__restrict__ vs, _Float16 *__restrict__ dys,
+                                                    int8_t *__restrict__ rexq, int8_t *__restrict__ rexk,
                                                     const float *__restrict__ pmax, int64_t bh, int64_t n_q,
                                                     int64_t n_k) {
     const int64_t rows_q = bh * n_q, rows_k = bh * n_k;
@@ -1388,11 +1385,30 @@ __global__ __launch_bounds__(256) void split_kernel(const void *__restrict__ q, 
         // bf16 inputs: the lo halves are zero (wherever the scaled value is a normal
         // fp16 number) and the pair passes read hi halves only
         if constexpr (!BF16) *reinterpret_cast<half8 *>(dst + row * (2 * D) + D + o) = lo;
+        // rows of dY and V (the rows a of the pair passes): e with ||a|| < 2^e, from the
+        // fp16 pairs the products use.  A row is 8 consecutive threads (every tensor
+        // and the grid stride are multiples of 8 threads, so the 8 are all active).
+        float ss = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; i++) {
+            const float xv = static_cast<float>(hi[i]) + (BF16 ? 0.f : static_cast<float>(lo[i]));
+            ss = fmaf(xv, xv, ss);
+        }
+        ss += __shfl_xor(ss, 1, 8);
+        ss += __shfl_xor(ss, 2, 8);
+        ss += __shfl_xor(ss, 4, 8);
+        if ((which & 1) && o == 0) {
+            // ss < 2^e2  ->  ||a|| < 2^ceil(e2 / 2); the sum's rounding (far below one
+            // part in 2^20) is covered by the factor 4 of slack in the 2^14 bound of S
+            int e2 = 0;
+            if (ss > 0.f) frexpf(ss, &e2);
+            (which == 1 ? rexq : rexk)[row] = static_cast<int8_t>((e2 + 1) >> 1);
+        }
     }
 }
 
-// out[r][:] = sum_h M[r][h][:] * 2^(e[r][h] - 23), M = (high part) * 256 + (low byte),
-// in hash order; 8 lanes per row, 8 values each.  The hashes go in groups of
+// out[r][:] = sum_h M[r][h][:] * 2^(e[r][h] - 22), M = (high part) * 256 + (low byte)
+// - 2^22, in hash order; 8 lanes per row, 8 values each.  The hashes go in groups of
 // eight, each group's loads issued before the previous group is added, so that a
 // lane keeps up to 384 bytes in flight.
 template <bool BF16>
@@ -1413,7 +1429,7 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *_
     float s[8];
 #pragma unroll
     for (int i = 0; i < 8; i++) s[i] = 0.f;
-    // 24-bit rows: M = high * 256 + low, value = M 2^(e - 23), e from the exponent
+    // 24-bit rows: M = high * 256 + low - 2^22, value = M 2^(e - 22), e from the exponent
     // array.  bf16 outputs take 16-bit rows (no low parts): value = high 2^(e - 15),
     // except values 0 .. 3, whose two low bits hold bits 2j, 2j+1 of e and whose
     // value is (high >> 2) 2^(e - 13); the thread of a row holding values 0 .. 7
@@ -1424,14 +1440,19 @@ __global__ __launch_bounds__(kReduceThreads) void reduce_kernel(const int16_t *_
             const uint32_t eb = (w[0] & 3u) | ((w[0] >> 14) & 0xCu) | ((w[1] & 3u) << 4) | ((w[1] >> 10) & 0xC0u);
             e = __shfl(static_cast<int>(static_cast<int8_t>(eb)), 0, 8);
         }
-        const float sc = ldexpf(1.0f, e - (BF16 ? 15 : 23));
+        const float sc = ldexpf(1.0f, e - (BF16 ? 15 : 22));
         const uint32_t lb[2] = {l.x, l.y};
 #pragma unroll
         for (int i = 0; i < 8; i++) {
-            int hi = static_cast<int16_t>((w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu);
-            if (BF16 && i < 4 && q == 0) hi = (hi >> 2) * 4;  // the exponent bits out, the 14-bit value scaled to 16
-            const int lo = BF16 ? 0 : static_cast<int>((lb[i >> 2] >> (8 * (i & 3))) & 0xFFu);
-            s[i] = fmaf(static_cast<float>(BF16 ? hi : hi * 256 + lo), sc, s[i]);  // |M| < 2^23: exact in fp32
+            const uint32_t hu = (w[i >> 1] >> (16 * (i & 1))) & 0xFFFFu;
+            int mv;
+            if constexpr (BF16) {
+                mv = static_cast<int16_t>(hu);
+                if (i < 4 && q == 0) mv = (mv >> 2) * 4;  // the exponent bits out, the 14-bit value scaled to 16
+            } else {
+                mv = static_cast<int>((hu << 8) | ((lb[i >> 2] >> (8 * (i & 3))) & 0xFFu)) - (1 << 22);
+            }
+            s[i] = fmaf(static_cast<float>(mv), sc, s[i]);  // |M| <= 2^22: exact in fp32
         }
     };
     // groups of eight hashes, double-buffered: group g+1 is loaded while g is added
@@ -2173,6 +2194,8 @@ BackwardLayout backward_layout(bool bf16, int64_t bh, int64_t n_q, int64_t n_k, 
     const size_t ex = bf16 ? 0 : 1;
     L.eq = o; o = align_up(o + ex * bh * n_q * m);
     L.ek = o; o = align_up(o + ex * bh * n_k * m);
+    L.rexq = o; o = align_up(o + static_cast<size_t>(bh) * n_q);
+    L.rexk = o; o = align_up(o + static_cast<size_t>(bh) * n_k);
     L.pmax = o; o = align_up(o + static_cast<size_t>(bh) * 4 * kMaxParts * 4);
     L.table = o; o = align_up(o + table_workspace_bytes(bf16, bh, n_k, m, tau));
     L.total = o;
@@ -2285,6 +2308,7 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
     _Float16 *qs = reinterpret_cast<_Float16 *>(ws + L.qs), *ks = reinterpret_cast<_Float16 *>(ws + L.ks);
     _Float16 *vs = reinterpret_cast<_Float16 *>(ws + L.vs), *dys = reinterpret_cast<_Float16 *>(ws + L.dys);
     float *pmax = reinterpret_cast<float *>(ws + L.pmax);
+    int8_t *rexq = reinterpret_cast<int8_t *>(ws + L.rexq), *rexk = reinterpret_cast<int8_t *>(ws + L.rexk);
     {
         KernelTimer timer("absmax_kernel", stream);
         const dim3 grid(static_cast<unsigned>(bh * 4 * kMaxParts));
@@ -2300,10 +2324,10 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
         KernelTimer timer("split_kernel", stream);
         if (bf16)
             hipLaunchKernelGGL(split_kernel<true>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, q, k, v,
-                               dy, qs, ks, vs, dys, pmax, bh, n_q, n_k);
+                               dy, qs, ks, vs, dys, rexq, rexk, pmax, bh, n_q, n_k);
         else
             hipLaunchKernelGGL(split_kernel<false>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, q, k,
-                               v, dy, qs, ks, vs, dys, pmax, bh, n_q, n_k);
+                               v, dy, qs, ks, vs, dys, rexq, rexk, pmax, bh, n_q, n_k);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
@@ -2312,6 +2336,7 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
     a.k = Side{reinterpret_cast<const uint32_t *>(ws + L.kent), reinterpret_cast<const int32_t *>(ws + L.koff), n_k};
     a.qs = qs; a.ks = ks; a.vs = vs; a.dys = dys;
     a.pmax = pmax;
+    a.rexq = rexq; a.rexk = rexk;
     a.pq = reinterpret_cast<int16_t *>(ws + L.pq);
     a.pk = reinterpret_cast<int16_t *>(ws + L.pk);
     a.lq = reinterpret_cast<uint8_t *>(ws + L.lq);
