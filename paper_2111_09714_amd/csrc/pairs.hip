@@ -636,11 +636,14 @@ __device__ __forceinline__ uint32_t mant_off(int s, int ch) {
     return static_cast<uint32_t>(s * 128 + (((ch >> 1) ^ (s >> 1)) << 4) + ((ch & 1) << 3));
 }
 // Byte offset of dword w (low bytes of dims 4w .. 4w+3) of row r's 64 low bytes,
-// after the mantissas: the dword's group of four (w >> 2) is XORed with (r >> 2) & 3.
-// MFMA-layout writes (rows c, dwords 4dt + g) and row-major reads (row 4i + q,
-// dword cl) then both fall on 64 distinct banks.
+// after the mantissas: row r = 4a + b sits in 64-byte slot 4a + ((a + b) & 3), and
+// the dword's group of four (w >> 2) is XORed with a.  MFMA-layout writes (rows c,
+// dwords 4dt + g) and row-major reads (rows 4q + i, dword cl: the rows whose high
+// parts the lane stores, so that both stores of a row share its address) then both
+// fall on 64 distinct banks.
 __device__ __forceinline__ uint32_t low_off(int r, int w) {
-    return static_cast<uint32_t>(kMantBytes + r * 64 + ((((w >> 2) ^ (r >> 2)) & 3) << 4) + ((w & 3) << 2));
+    const int s = (r & 12) | ((r + (r >> 2)) & 3);
+    return static_cast<uint32_t>(kMantBytes + s * 64 + ((((w >> 2) ^ (r >> 2)) & 3) << 4) + ((w & 3) << 2));
 }
 
 // Write the partial rows of a finished tile: lane (g, c) holds out[row c][16dt +
@@ -664,9 +667,9 @@ __device__ __forceinline__ uint32_t low_off(int r, int w) {
 // each cost a partial-line write), else straight to memory.  p16 (bf16 outputs):
 // 16-bit rows that carry their own exponent (below).  Rows past nvalid and rows
 // whose entry carries kSkipCode (their bucket takes the table form) are not stored.
-// (P16 fixes p16 at compile time for the bf16 kernels; the fp32 kernels pass it as
-// the run-time value it is, false: compiled as a constant there, the code around
-// it was scheduled 4-11% slower, measured on the pair and table kernels)
+// (P16 fixes p16 at compile time for the bf16 kernels; the pair kernels pass the
+// constant for fp32 too, the table-form kernel the run-time value, false: each
+// choice was measured faster for its kernel, by 3% and 4%)
 template <bool P16>
 __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, uint8_t *plow, int8_t *pexp,
                                            int8_t *ex_lds, bool ex_in_lds, int m, bool rt_p16,
@@ -755,10 +758,10 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
     uint32_t lw[4];
 #pragma unroll
     for (int i = 0; i < 4; i++) w[i] = lds_ld<uint2v>(tile, mant_off(mant_slot(4 * q + i), cl));
-    // rows 4i + q: dword cl of each low-part row
+    // rows 4q + i: dword cl of each low-part row
     if (!p16) {
 #pragma unroll
-        for (int i = 0; i < 4; i++) lw[i] = lds_ld<uint32_t>(tile, low_off(4 * i + q, cl));
+        for (int i = 0; i < 4; i++) lw[i] = lds_ld<uint32_t>(tile, low_off(4 * q + i, cl));
     }
     const uint4 e4 = reinterpret_cast<const uint4 *>(tile_ent)[q];
     const uint32_t re[4] = {e4.x, e4.y, e4.z, e4.w};
@@ -772,15 +775,10 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
     };
 #pragma unroll
     for (int i = 0; i < 4; i++) {
-        if (4 * q + i < nvalid && (re[i] >> 16) != kSkipCode)
-            __builtin_nontemporal_store(w[i], reinterpret_cast<uint2v *>(part + rec(re[i] & 0xFFFFu) * D) + cl);
-    }
-    if (!p16) {
-#pragma unroll
-        for (int i = 0; i < 4; i++) {
-            const uint32_t le = tile_ent[4 * i + q];
-            if (4 * i + q < nvalid && (le >> 16) != kSkipCode)
-                __builtin_nontemporal_store(lw[i], reinterpret_cast<uint32_t *>(plow + rec(le & 0xFFFFu) * D) + cl);
+        if (4 * q + i < nvalid && (re[i] >> 16) != kSkipCode) {
+            const uint64_t rr = rec(re[i] & 0xFFFFu) * D;
+            __builtin_nontemporal_store(w[i], reinterpret_cast<uint2v *>(part + rr) + cl);
+            if (!p16) __builtin_nontemporal_store(lw[i], reinterpret_cast<uint32_t *>(plow + rr) + cl);
         }
     }
 }
@@ -840,7 +838,7 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
     const int esum = head_exp(a.pmax, b, kside ? 3 : 1) + head_exp(a.pmax, b, kside ? 1 : 3) +
                      head_exp(a.pmax, b, kside ? 0 : 2);
     const float oscale = ldexpf(a.scale, esum - 39 + 2);
-    const bool ex_in_lds = !a.p16 && n_r <= kExpLds;  // (16-bit rows carry their exponents)
+    const bool ex_in_lds = !HI1 && n_r <= kExpLds;  // (16-bit rows carry their exponents)
 
     // buckets in the table form (bucket_kernel writes their rows' partials): the
     // plan leaves their rows out of every tile's partner range and the run's copy
@@ -944,7 +942,7 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
         auto zero_tiles = [&](int ta, int tb) {
             const floatx4 z[4] = {};
             for (int t = ta; t < tb; t++)
-                store_tile<HI1>(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, a.p16, tile_ents(t), row_count(t), q, cl, g,
+                store_tile<HI1>(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, HI1, tile_ents(t), row_count(t), q, cl, g,
                            c, z, 0.f);
         };
         // sub-tile j of the run: its tile (searched forward from t) and first partner
@@ -1025,7 +1023,7 @@ __global__ __launch_bounds__(kPassThreads, STAR ? 1 : 2) void pass_kernel(PassAr
                 compute_sub<STAR, HI1>(tile, cur.pe, rh, rl, rbh, rbl, xscale, static_cast<int>(row_entry(cur.t) >> 16),
                                   ldexpf(1.0f, -2 - erow), g, c, outT);
                 if (newtile) {
-                    store_tile<HI1>(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, a.p16, tile_ents(cur.t), row_count(cur.t), q, cl,
+                    store_tile<HI1>(tile, part, plow, pexp, ex_lds, ex_in_lds, a.m, HI1, tile_ents(cur.t), row_count(cur.t), q, cl,
                                g, c, outT, ldexpf(oscale, erow));
 #pragma unroll
                     for (int dt = 0; dt < 4; dt++) outT[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
