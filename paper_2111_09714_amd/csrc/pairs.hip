@@ -1713,6 +1713,9 @@ __global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArg
     const float wgd = static_cast<float>(tau) / (2.0f * static_cast<float>(m)) * ldexpf(1.0f, -(16 + k2));
     const float wvd = 32768.0f / static_cast<float>(m);
     const bool with_dv = a.out2 != nullptr;
+    // for m a power of two the weight C 2^15 / m (C <= m) is an exact fp16 number: its
+    // lo half is zero and so is the product with it
+    const bool wv_exact = (m & (m - 1)) == 0;
     const uint32_t *crow = cnt + (16 * wave + c) * stride;  // the lane's fixed row of counts
     int eg = 0, ey = 0;
     // one streamed tile from (xg, xy), the next one's loads into (gn, yn) (two
@@ -1733,7 +1736,8 @@ __global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArg
         const int ey_new = pow2_above(fmaxf(fmaxf(tmax[4], tmax[5]), fmaxf(tmax[6], tmax[7])));
         put_row(g_lds, xg, ldexpf(1.0f, 13 - eg_new));
         put_row(y_lds, xy, ldexpf(1.0f, 13 - ey_new));
-        if (c0 > 0) {
+        // (rescaled only when a tile scale changed: a factor of 1 would change nothing)
+        if (c0 > 0 && (eg != eg_new || ey != ey_new)) {
             const float f = ldexpf(1.0f, eg + ey - eg_new - ey_new), f2 = ldexpf(1.0f, eg - eg_new);
 #pragma unroll
             for (int dt = 0; dt < 4; dt++) {
@@ -1788,7 +1792,12 @@ __global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArg
 #pragma unroll
                 for (int i = 0; i < 4; i++) wv[i] = static_cast<float>((cw >> (8 * i)) & 0xFFu) * wvd;
                 half4 vh, vl;
-                split4(wv, 1.0f, vh, vl);
+                if (wv_exact) {
+#pragma unroll
+                    for (int i = 0; i < 4; i++) vh[i] = static_cast<_Float16>(wv[i]);
+                } else {
+                    split4(wv, 1.0f, vh, vl);
+                }
                 half4 gh[4], gl[4];
 #pragma unroll
                 for (int dt = 0; dt < 4; dt++) {
@@ -1798,9 +1807,11 @@ __global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArg
 #pragma unroll
                 for (int dt = 0; dt < 4; dt++)
                     out2[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(gh[dt], vh, out2[dt], 0, 0, 0);
+                if (!wv_exact) {
 #pragma unroll
-                for (int dt = 0; dt < 4; dt++)
-                    out2[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(gh[dt], vl, out2[dt], 0, 0, 0);
+                    for (int dt = 0; dt < 4; dt++)
+                        out2[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(gh[dt], vl, out2[dt], 0, 0, 0);
+                }
 #pragma unroll
                 for (int dt = 0; dt < 4; dt++)
                     out2[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(gl[dt], vh, out2[dt], 0, 0, 0);
