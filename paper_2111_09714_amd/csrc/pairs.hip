@@ -614,14 +614,25 @@ __device__ __forceinline__ void compute_sub(const unsigned char *tile, const uin
         split4(sv, sfac, sh, sl);  // sv carries the weight, a product of its own
     else
         split4_pow2(sv, sfac, sh, sl);
-    // out^T += B_y^T S^T (hi*hi + hi*lo + lo*hi), the four dim blocks interleaved
+    // out^T += B_y^T S^T (hi*hi + hi*lo + lo*hi), the four dim blocks interleaved.
+    // The general form takes hi*lo + lo*hi in one 16x16x32 product over the
+    // concatenated operands [B hi | B lo] and [S lo ; S hi] (a contraction does not
+    // depend on the order of its k index, only on both operands using the same one),
+    // then hi*hi in a 16x16x16 product.
+    if constexpr (HI1) {
 #pragma unroll
-    for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(bth[dt], sh, outT[dt], 0, 0, 0);
+        for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(bth[dt], sh, outT[dt], 0, 0, 0);
 #pragma unroll
-    for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(bth[dt], sl, outT[dt], 0, 0, 0);
-    if constexpr (!HI1) {
+        for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(bth[dt], sl, outT[dt], 0, 0, 0);
+    } else {
+        const half8 slh = __builtin_shufflevector(sl, sh, 0, 1, 2, 3, 4, 5, 6, 7);
 #pragma unroll
-        for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(btl[dt], sh, outT[dt], 0, 0, 0);
+        for (int dt = 0; dt < 4; dt++) {
+            const half8 bt = __builtin_shufflevector(bth[dt], btl[dt], 0, 1, 2, 3, 4, 5, 6, 7);
+            outT[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(bt, slh, outT[dt], 0, 0, 0);
+        }
+#pragma unroll
+        for (int dt = 0; dt < 4; dt++) outT[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(bth[dt], sh, outT[dt], 0, 0, 0);
     }
 }
 
@@ -1780,12 +1791,16 @@ __global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArg
                 yh[dt] = tr_load(y_lds + swz(16 * cb + pr, 2 * dt + (a4 >> 1), 256) + 8 * (a4 & 1));
                 yl[dt] = tr_load(y_lds + swz(16 * cb + pr, 8 + 2 * dt + (a4 >> 1), 256) + 8 * (a4 & 1));
             }
+            // hi*lo + lo*hi as one 16x16x32 product over [y hi | y lo] and [w lo ; w hi],
+            // then hi*hi
+            const half8 wlh = __builtin_shufflevector(wl, wh, 0, 1, 2, 3, 4, 5, 6, 7);
+#pragma unroll
+            for (int dt = 0; dt < 4; dt++) {
+                const half8 yt = __builtin_shufflevector(yh[dt], yl[dt], 0, 1, 2, 3, 4, 5, 6, 7);
+                out[dt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(yt, wlh, out[dt], 0, 0, 0);
+            }
 #pragma unroll
             for (int dt = 0; dt < 4; dt++) out[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(yh[dt], wh, out[dt], 0, 0, 0);
-#pragma unroll
-            for (int dt = 0; dt < 4; dt++) out[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(yh[dt], wl, out[dt], 0, 0, 0);
-#pragma unroll
-            for (int dt = 0; dt < 4; dt++) out[dt] = __builtin_amdgcn_mfma_f32_16x16x16f16(yl[dt], wh, out[dt], 0, 0, 0);
             if (with_dv) {
                 // dV^T += dY^T (C / m) 2^15: the staged g rows are dY on this side
                 float wv[4];
