@@ -42,9 +42,11 @@
  *     or tile (YOSO-E) keep less than 22 significant bits.
  *   - Precision.  Y and dV are accumulated as exact fixed-point integers: each
  *     value of feature dim d is rounded to a multiple of 2^-k_d, where 2^k_d is
- *     the largest power of two keeping 2^k_d (1 + 2^-10) times that dim's sum of
- *     |value| over the n_src source rows below 2^30; everything after that
- *     rounding is exact.  dQ and dK use fp32 accumulation of products formed
+ *     the largest power of two keeping 2^k_d (1 + 2^-10) times a bound on every
+ *     bucket sum of |value| of that dim below 2^30: the dim's sum of |value|
+ *     over the n_src source rows, or, for fp32 outputs with n_src > 8192, the
+ *     smaller of that sum and the largest bucket's row count times the dim's
+ *     largest |value|; everything after that rounding is exact.  dQ and dK use fp32 accumulation of products formed
  *     from fp16 (hi, lo) pairs (about 22 significant bits; bf16 inputs are
  *     exact as the hi halves alone wherever they lie within 2^27 of their head's
  *     largest value); the contribution of each hash to a row is kept in 24-bit

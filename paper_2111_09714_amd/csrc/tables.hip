@@ -16,10 +16,13 @@
 // atomic adds some 40x slower than integer ones, while a 64-bit integer add
 // carries two values at once.  Each value v of feature dim d is quantised to
 // q = rint(v 2^k_d) with one power-of-two scale per dim of the workgroup's
-// slice, chosen so that 2^k_d times that dim's sum of |v| over the source rows (a
-// bound on every bucket sum of the dim, and never above n_src max|v|) stays below
-// 2^30; a bucket sum of rounded values is then below 2^30 + n_src/2 in magnitude.
-// A dim of small values is thus resolved as finely as a dim of large ones.  Two adjacent dims
+// slice, chosen so that 2^k_d times a bound on every bucket sum of |v| of that dim
+// stays below 2^30: the dim's sum of |v| over the source rows, or (fp32 outputs of
+// more than 8192 source rows, where that sum grows with n_src and the rounding step
+// with it) the smaller of that sum and the count of the largest bucket times the
+// dim's largest |v|, the counts taken in LDS before the scatter.  A bucket sum of
+// rounded values is then below 2^30 + n_src/2 in magnitude.  A dim of small values
+// is thus resolved as finely as a dim of large ones.  Two adjacent dims
 // (q_lo, q_hi) are packed as the 64-bit integer q_hi 2^32 + q_lo; sums of packed
 // words never corrupt each other's field because |sum q_lo| < 2^31.  Integer
 // sums are exact and independent of the order of the atomics, so the tables (and
@@ -48,6 +51,9 @@ namespace {
 
 constexpr int kTableThreads = 512;
 constexpr int kTableWaves = kTableThreads / 64;
+// fp32 outputs with more source rows than this also bound the bucket sums by the
+// largest bucket count (a count pass over the codes before the scatter)
+constexpr int64_t kTableHistRows = 8192;
 
 template <bool BF16, int DS>
 __device__ __forceinline__ void load_slice(const void *base, int64_t off, float v[DS]) {
@@ -98,6 +104,7 @@ struct TableArgs {
     float *acc;                 // fp32 running sums when the hashes take several LDS passes
     int64_t bh, n_src, n_dst;
     int m, tau, G;              // G = hashes per LDS pass
+    int hist;                   // 1: bound the bucket sums by the largest bucket count too
 };
 
 // (lo, hi) of a packed word whose fields are signed and |field sums| < 2^31:
@@ -115,6 +122,9 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
     constexpr int S = D / DS;   // slices per head
     extern __shared__ __align__(16) unsigned long long tab[];  // [2^tau][G][P]
     __shared__ float wave_red[kTableWaves * DS];
+    __shared__ float wave_mx[kTableWaves * DS];
+    __shared__ float dim_sum[DS], dim_max[DS];  // per dim: sum and largest |v| over the source rows
+    __shared__ uint32_t wave_cnt[kTableWaves];
     __shared__ int scale_exp[DS];
 
     const int64_t blocks = a.bh * S;
@@ -128,13 +138,15 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
     const int64_t vbase = b * a.n_src * D + slice * DS;
 
     // ---- scale: for each dim of this slice, the sum of |v| over all source rows
-    // bounds every bucket sum of that dim; the largest of these sums -> exponent k.
+    // bounds every bucket sum of that dim -> exponent k.  With `hist` the count of
+    // the largest bucket times the dim's largest |v| bounds them too, and the smaller
+    // bound sets k (per pass of hashes, below).
     // (eight rows per thread in flight at once: the pass is latency-bound; rows past
     // the end re-read the last row and add nothing)
     {
-        float sa[DS];
+        float sa[DS], sm[DS];
 #pragma unroll
-        for (int d = 0; d < DS; d++) sa[d] = 0.f;
+        for (int d = 0; d < DS; d++) sa[d] = sm[d] = 0.f;
         constexpr int U = 8;
         const int64_t last = a.n_src - 1;
         for (int64_t j0 = tid; j0 < a.n_src; j0 += U * kTableThreads) {
@@ -148,20 +160,34 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
             for (int u = 0; u < U; u++) {
                 const bool in = j0 + u * kTableThreads < a.n_src;
 #pragma unroll
-                for (int d = 0; d < DS; d++) sa[d] += in ? fabsf(v[u][d]) : 0.f;
+                for (int d = 0; d < DS; d++) {
+                    sa[d] += in ? fabsf(v[u][d]) : 0.f;
+                    sm[d] = fmaxf(sm[d], in ? fabsf(v[u][d]) : 0.f);
+                }
             }
         }
 #pragma unroll
-        for (int d = 0; d < DS; d++) sa[d] = group_sum(sa[d], 64);
+        for (int d = 0; d < DS; d++) {
+            sa[d] = group_sum(sa[d], 64);
+            for (int o = 1; o < 64; o <<= 1) sm[d] = fmaxf(sm[d], __shfl_xor(sm[d], o));
+        }
         if (lane == 0) {
 #pragma unroll
-            for (int d = 0; d < DS; d++) wave_red[wave * DS + d] = sa[d];
+            for (int d = 0; d < DS; d++) {
+                wave_red[wave * DS + d] = sa[d];
+                wave_mx[wave * DS + d] = sm[d];
+            }
         }
         __syncthreads();
         if (tid < DS) {
             const int d = tid;
-            float t = 0.f;
-            for (int w = 0; w < kTableWaves; w++) t += wave_red[w * DS + d];
+            float t = 0.f, mx = 0.f;
+            for (int w = 0; w < kTableWaves; w++) {
+                t += wave_red[w * DS + d];
+                mx = fmaxf(mx, wave_mx[w * DS + d]);
+            }
+            dim_sum[d] = t;
+            dim_max[d] = mx;
             int k = 0;
             if (t > 0.f) {
                 // the fp32 sums are low by at most ~140 ulp-units relative (128 terms
@@ -180,6 +206,82 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
     int kd[DS];
 #pragma unroll
     for (int d = 0; d < DS; d++) kd[d] = __builtin_amdgcn_readfirstlane(scale_exp[d]);
+    // with `hist`, per pass of hashes: the bucket counts of its hashes (in the tables'
+    // LDS, before they are zeroed), the largest count c, and per dim the exponent k
+    // with 2^k (1 + 2^-10) min(sum |v|, c max |v|) < 2^30.  Every bucket sum of a dim
+    // is at most both bounds, so the argument of the sum bound holds as it is.
+    auto count_scales = [&](int h0, int gcount) {
+        uint32_t *cnt = reinterpret_cast<uint32_t *>(tab);  // [gcount][2^tau] (fits in the tables)
+        const int nb = cmask + 1;
+        for (int e = tid; e < gcount * nb; e += kTableThreads) cnt[e] = 0u;
+        __syncthreads();
+        // (key, hash) pairs in code order, eight per thread in flight; key = p / gcount
+        // from a float reciprocal (p < 2^22, exact as a float; off by at most one,
+        // corrected)
+        const int npairs = static_cast<int>(a.n_src) * gcount;
+        const uint16_t *hcodes = a.src_codes + b * a.n_src * a.m;
+        // all of a row's hashes in this pass, m a multiple of 8 and the codes 16-byte
+        // aligned: eight codes (one row's hashes 8v mod m .. +7) per 16-byte load
+        const bool vec = gcount == a.m && (a.m & 7) == 0 && (reinterpret_cast<uintptr_t>(hcodes) & 15) == 0;
+        const int nvec = vec ? npairs / 8 : 0;
+        for (int v0 = tid; v0 < nvec; v0 += 8 * kTableThreads) {
+            uint4 w[8];
+#pragma unroll
+            for (int u = 0; u < 8; u++) w[u] = reinterpret_cast<const uint4 *>(hcodes)[min(v0 + u * kTableThreads, nvec - 1)];
+#pragma unroll
+            for (int u = 0; u < 8; u++) {
+                const int vi = v0 + u * kTableThreads;
+                if (vi < nvec) {
+                    const int hb = (8 * vi) % a.m;
+                    const uint32_t ws[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+#pragma unroll
+                    for (int e = 0; e < 8; e++)
+                        atomicAdd(&cnt[(hb + e) * nb + ((ws[e >> 1] >> (16 * (e & 1))) & cmask)], 1u);
+                }
+            }
+        }
+        const float inv_g = 1.0f / static_cast<float>(gcount);
+        for (int p0 = vec ? npairs : tid; p0 < npairs; p0 += 8 * kTableThreads) {
+            uint32_t cc[8];
+            int hq[8];
+#pragma unroll
+            for (int u = 0; u < 8; u++) {
+                const int p = min(p0 + u * kTableThreads, npairs - 1);
+                int key = static_cast<int>(static_cast<float>(p) * inv_g);
+                if (key * gcount > p) key--;
+                if ((key + 1) * gcount <= p) key++;
+                hq[u] = p - key * gcount;
+                cc[u] = hcodes[key * a.m + h0 + hq[u]];
+            }
+#pragma unroll
+            for (int u = 0; u < 8; u++)
+                if (p0 + u * kTableThreads < npairs) atomicAdd(&cnt[hq[u] * nb + (cc[u] & cmask)], 1u);
+        }
+        __syncthreads();
+        uint32_t c = 0u;
+        for (int e = tid; e < gcount * nb; e += kTableThreads) c = max(c, cnt[e]);
+        for (int o = 1; o < 64; o <<= 1) c = max(c, static_cast<uint32_t>(__shfl_xor(static_cast<int>(c), o)));
+        if (lane == 0) wave_cnt[wave] = c;
+        __syncthreads();
+        if (tid < DS) {
+            const int d = tid;
+            uint32_t cm = 0u;
+            for (int w = 0; w < kTableWaves; w++) cm = max(cm, wave_cnt[w]);
+            // (c <= 65536 is exact in fp32 and the product rounds once: the margin
+            // 1 + 2^-10 covers it as it covers the rounding of the sums)
+            const float bound = fminf(dim_sum[d], static_cast<float>(cm) * dim_max[d]);
+            int k = 0;
+            if (bound > 0.f) {
+                int ev;
+                frexpf(bound * (1.0f + 0x1p-10f), &ev);
+                k = 30 - ev;
+            }
+            scale_exp[d] = k;
+        }
+        __syncthreads();  // (also: every count has been read before the tables are zeroed)
+#pragma unroll
+        for (int d = 0; d < DS; d++) kd[d] = __builtin_amdgcn_readfirstlane(scale_exp[d]);
+    };
 
     // lane roles
     // hashes rounded up to a power of two: fixed by (DS, KM) for the one- and
@@ -219,6 +321,7 @@ __global__ __launch_bounds__(kTableThreads) void table_kernel(TableArgs a) {
         __builtin_amdgcn_s_waitcnt(0x0F70);
         const int h0 = grp * G;
         const int gcount = min(G, a.m - h0);
+        if (a.hist) count_scales(h0, gcount);
         {
             const int words = (cmask + 1) * G * P;  // even
             ulonglong2 *t2 = reinterpret_cast<ulonglong2 *>(tab);
@@ -656,6 +759,9 @@ hipError_t launch_table(const uint16_t *src_codes, const void *values, const uin
     a.m = m;
     a.tau = tau;
     a.G = p.G;
+    // fp32 outputs of long sequences: the sum bound grows with n_src (its rounding
+    // step with it), the largest bucket count does not
+    a.hist = !bf16 && n_src > kTableHistRows ? 1 : 0;
     // the one- and two-key step forms also need one private dummy word per lane
     // (targets of lanes without a valid key) and per-wave staging of a chunk's
     // packed words (64 keys x DS/2 words); the general form needs neither (with 128
