@@ -706,10 +706,12 @@ __device__ __forceinline__ void store_tile(unsigned char *tile, int16_t *part, u
         mx = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
     }
     // e with max|value| < 2^e, from the biased exponent field of the scaled row
-    // maximum (0 gives a tiny e whose mantissas are all 0), clamped so that
-    // 2^(23 - e) stays a normal float
+    // maximum (0 gives a tiny e whose mantissas are all 0), clamped to [-100, 127]
+    // so that 2^(fb - e) and 2^(e - fb) stay normal floats (a row below 2^-100 only
+    // keeps fewer bits; one whose largest value reaches 2^127, next to fp32's
+    // overflow, is outside the format)
     const float mxs = mx * orow;
-    const int e = min(max(static_cast<int>((__float_as_uint(mxs) >> 23) & 0xFFu) - 126, -100), 100);
+    const int e = min(max(static_cast<int>((__float_as_uint(mxs) >> 23) & 0xFFu) - 126, -100), 127);
     // value * 2^(fb - e) lies in (-2^fb, 2^fb): a power-of-two scaling of the
     // rounded product value * orow, so the row maximum stays below 2^fb before
     // rounding (and at most 2^fb after, hence the clamp of 16-bit values).  fb = 22
