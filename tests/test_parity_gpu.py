@@ -186,6 +186,18 @@ def test_maximum_length(bh, nq, nk, m, tau, dtype):
         assert len(got) == 2 and max(got.values()) < 1e-5, got
 
 
+@pytest.mark.parametrize("bh,nq,nk,m,tau", [(1, 8193, 8200, 16, 9), (2, 9000, 8209, 7, 8)])
+def test_count_bound_lengths(bh, nq, nk, m, tau):
+    """Just past 8192 source rows (fp32) the tables' fixed-point scale also bounds the
+    bucket sums by the largest bucket count: with m = 16 the counts read a row's
+    codes 16 bytes at a time, with m = 7 one code at a time.  Ragged lengths on both
+    sides; every row checked, and Y, dV at the count bound's precision (1e-5)."""
+    run_case(bh, nq, nk, m, tau, "f32")
+    name = f"bh{bh}_nq{nq}_nk{nk}_m{m}_tau{tau}_f32"
+    got = {k: e for tag, k, f, e, tol in parity.RECORD if tag == name and k in ("y", "dv")}
+    assert len(got) == 2 and max(got.values()) < 1e-5, got
+
+
 def run_case(bh, nq, nk, m, tau, dtype, dist="gauss"):
     name = f"bh{bh}_nq{nq}_nk{nk}_m{m}_tau{tau}_{dtype}" + ("" if dist == "gauss" else f"_{dist}")
     log(f"[{name}] start")
