@@ -93,6 +93,10 @@ SMALL = [
     # above 1024 rows on a side the pair passes serve dQ, dK (below, the dense form)
     (1, 1025, 1100, 7, 5, "f32"),
     (2, 1500, 1030, 16, 8, "bf16"),
+    # the most hashes (m = 64) on the pair path: eight gather lanes per query in the
+    # tables, 64 partial rows per row in the hash sums
+    (1, 1100, 1500, 64, 8, "f32"),
+    (1, 2000, 1100, 64, 7, "bf16"),
 ]
 
 
