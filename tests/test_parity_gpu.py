@@ -202,6 +202,16 @@ def test_count_bound_lengths(bh, nq, nk, m, tau):
     assert len(got) == 2 and max(got.values()) < 1e-5, got
 
 
+@pytest.mark.parametrize("bh,nq,nk,m,tau,dtype", [(1, 1, 65536, 4, 10, "f32"), (2, 65536, 3, 5, 10, "f32"),
+                                                   (1, 3, 40000, 6, 9, "bf16")])
+def test_extreme_aspect(bh, nq, nk, m, tau, dtype):
+    """A handful of queries against the longest key sequence, and the reverse: one
+    side's pair pass has a single ragged row tile whose partners span a long sorted
+    range, the other side's rows have at most a few partners each; the tables sum
+    65536 source rows into a few destinations (and a few into many)."""
+    run_case(bh, nq, nk, m, tau, dtype)
+
+
 def run_case(bh, nq, nk, m, tau, dtype, dist="gauss"):
     name = f"bh{bh}_nq{nq}_nk{nk}_m{m}_tau{tau}_{dtype}" + ("" if dist == "gauss" else f"_{dist}")
     log(f"[{name}] start")
