@@ -133,7 +133,7 @@ KERNEL_SOURCES = {
     "hash_kernel": ["paper_2111_09714_amd/csrc/hash.hip", "paper_2111_09714_amd/csrc/common.h"],
     "table_kernel": ["paper_2111_09714_amd/csrc/tables.hip", "paper_2111_09714_amd/csrc/common.h"],
     **{k: _PAIRS for k in ("codes_t_kernel", "sort_kernel", "absmax_kernel", "split_kernel", "pass_kernel", "bucket_kernel",
-                           "reduce_kernel", "dense_kernel", "dense_fwd_kernel")},
+                           "reduce_kernel", "dense_kernel", "dense_sum_kernel", "dense_fwd_kernel")},
 }
 
 
@@ -203,7 +203,7 @@ def cpu_baseline(w, inp, heads, min_wall: float = 10.0):
 STEP_KERNELS = ("hash_kernel", "table_kernel", "codes_t_kernel", "sort_kernel", "absmax_kernel", "split_kernel",
                 "pass_kernel",
                 "bucket_kernel",
-                "reduce_kernel", "dense_kernel", "dense_fwd_kernel", "zero_kernel")
+                "reduce_kernel", "dense_kernel", "dense_sum_kernel", "dense_fwd_kernel", "zero_kernel")
 
 
 def make_step(Y, torch, w, inp, dev):

@@ -1538,6 +1538,11 @@ __global__ void zero_kernel(uint32_t *__restrict__ p, int64_t count) {
 //      fp16 products), W = G .* C tau/(2m) 2^-(16 + k), out^T += y^T W.  The
 //      accumulators are rescaled exactly when a tile's scales change.
 constexpr int kDenseRows = 64;     // fixed rows per workgroup (16 per wave)
+// Fewer fixed-row blocks than this and a longest side of at least kDenseSplitMinRows:
+// each block's streamed rows are shared among up to kDenseSplit workgroups.
+constexpr int64_t kDenseSplitBelow = 128;
+constexpr int64_t kDenseSplitMinRows = 256;
+constexpr int kDenseSplit = 8;
 constexpr int kDenseTile = 64;     // streamed rows per LDS tile
 constexpr int kDenseMaxN = 1024;   // streamed rows whose counts fit in LDS
 
@@ -1555,6 +1560,7 @@ struct DenseSide {
     const void *sg, *sy;     // streamed side's g rows and y rows [bh][n_s][64]
     void *out;               // [bh][n_f][64]: dQ or dK
     void *out2;              // [bh][n_f][64]: dV (key side), else nullptr
+    float *pout, *pout2;     // split > 1: fp32 partial outputs [split][bh][n_f][64] of out, out2
     int64_t n_f, n_s;
 };
 
@@ -1562,6 +1568,7 @@ struct DenseArgs {
     DenseSide side[2];       // 0: dQ (queries fixed), 1: dK and dV (keys fixed)
     int64_t bh;
     int m, tau;
+    int split;               // workgroups per fixed-row block, each streaming a contiguous share of the rows
 };
 
 template <bool BF16>
@@ -1589,7 +1596,10 @@ __global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArg
     // blocks of side 0, then side 1 (both sides' tile counts)
     const int64_t t0 = (args.side[0].n_f + kDenseRows - 1) / kDenseRows;
     const int64_t t1 = (args.side[1].n_f + kDenseRows - 1) / kDenseRows;
-    const int64_t blk = xcd_remap(blockIdx.x, args.bh * (t0 + t1));
+    const int split = args.split;
+    const int64_t blk0 = xcd_remap(blockIdx.x, args.bh * (t0 + t1) * split);
+    const int sp = static_cast<int>(blk0 % split);
+    const int64_t blk = blk0 / split;
     const bool kside = blk >= args.bh * t0;
     const DenseSide a = args.side[kside ? 1 : 0];
     const int64_t tiles_f = kside ? t1 : t0;
@@ -1602,6 +1612,10 @@ __global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArg
     const int g = lane >> 4, c = lane & 15;
     const int stride = dense_stride(a.n_s);
     const int nf = static_cast<int>(a.n_f), ns = static_cast<int>(a.n_s);
+    // the streamed rows of this workgroup: [cs0, cs1), whole tiles (split > 1: a share of
+    // them, the fp32 partial outputs summed afterwards by dense_sum_kernel)
+    const int slen = ((ns + split - 1) / split + TILE - 1) / TILE * TILE;
+    const int cs0 = min(ns, sp * slen), cs1 = min(ns, cs0 + slen);
 
     // the streamed side's rows: lane l of wave w loads row RPW w + (l % RPW), dims
     // DPL (l / RPW) + [0, DPL) of a tile (rows clamped: the prefetch past the last
@@ -1617,7 +1631,7 @@ __global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArg
         }
     };
     float xga[DPL], xya[DPL], xgb[DPL], xyb[DPL];
-    load_tile(0, xga, xya);
+    load_tile(cs0, xga, xya);
 
     // ---- 1. collision counts.  Items (fixed row, hash) in groups of eight per
     // thread: their codes, then their bucket ranges, then the entries, each stage's
@@ -1702,9 +1716,9 @@ __global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArg
             *reinterpret_cast<half8 *>(dst + swz(lrow, 8 + (DPL / 8) * lq + u, 256)) = l;
         }
     };
-    // rows past n_s become zeros when the tile is staged
+    // rows past the range become zeros when the tile is staged
     auto row_max = [&](int c0, float x[DPL]) {
-        const bool ok = c0 + lrow < ns;
+        const bool ok = c0 + lrow < cs1;
         float mx = 0.f;
 #pragma unroll
         for (int i = 0; i < DPL; i++) {
@@ -1750,7 +1764,7 @@ __global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArg
         put_row(g_lds, xg, ldexpf(1.0f, 13 - eg_new));
         put_row(y_lds, xy, ldexpf(1.0f, 13 - ey_new));
         // (rescaled only when a tile scale changed: a factor of 1 would change nothing)
-        if (c0 > 0 && (eg != eg_new || ey != ey_new)) {
+        if (c0 > cs0 && (eg != eg_new || ey != ey_new)) {
             const float f = ldexpf(1.0f, eg + ey - eg_new - ey_new), f2 = ldexpf(1.0f, eg - eg_new);
 #pragma unroll
             for (int dt = 0; dt < 4; dt++) {
@@ -1764,7 +1778,7 @@ __global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArg
         __syncthreads();
 #pragma unroll 1
         for (int cb = 0; cb < TILE / 16; cb++) {
-            if (c0 + 16 * cb >= ns) break;
+            if (c0 + 16 * cb >= cs1) break;
             // G^T block: lane (g, c) = (g row c0 + 16cb + 4g + i) . (a row c)
             half8 bh[2], bl[2];
 #pragma unroll
@@ -1835,9 +1849,9 @@ __global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArg
             }
         }
     };
-    for (int c0 = 0; c0 < ns; c0 += 2 * TILE) {
+    for (int c0 = cs0; c0 < cs1; c0 += 2 * TILE) {
         do_tile(c0, xga, xya, xgb, xyb);
-        if (c0 + TILE < ns) do_tile(c0 + TILE, xgb, xyb, xga, xya);
+        if (c0 + TILE < cs1) do_tile(c0 + TILE, xgb, xyb, xga, xya);
     }
 
     // ---- 4. out = acc 2^(16 + k) (a row 2^(13 - e_a)) (g tile 2^(13 - e_g)) (y tile 2^(13 - e_y));
@@ -1848,9 +1862,38 @@ __global__ __launch_bounds__(256, TILE == 32 ? 3 : 2) void dense_kernel(DenseArg
 #pragma unroll
         for (int dt = 0; dt < 4; dt++) {
             const int64_t off = (b * a.n_f + frow) * D + 16 * dt + 4 * g;
-            dense_store<BF16>(a.out, off, out[dt], sc);
-            if (with_dv) dense_store<BF16>(a.out2, off, out2[dt], sc2);
+            if (split == 1) {
+                dense_store<BF16>(a.out, off, out[dt], sc);
+                if (with_dv) dense_store<BF16>(a.out2, off, out2[dt], sc2);
+            } else {
+                const int64_t po = sp * (args.bh * a.n_f * D) + off;
+                *reinterpret_cast<floatx4 *>(a.pout + po) = out[dt] * sc;
+                if (with_dv) *reinterpret_cast<floatx4 *>(a.pout2 + po) = out2[dt] * sc2;
+            }
         }
+    }
+}
+
+// dQ, dK, dV = sums over the splits of their fp32 partial outputs, in split order
+// (four values per thread, the three outputs one after another), stored as fp32 or bf16.
+struct DenseSum {
+    const float *part[3];
+    void *out[3];
+    int64_t count4[3];  // four-value groups per output (a split's partials are count4 groups apart)
+    int split;
+};
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void dense_sum_kernel(DenseSum a) {
+    const int64_t total = a.count4[0] + a.count4[1] + a.count4[2];
+    for (int64_t t = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; t < total;
+         t += static_cast<int64_t>(gridDim.x) * 256) {
+        const int o = t < a.count4[0] ? 0 : (t < a.count4[0] + a.count4[1] ? 1 : 2);
+        const int64_t i = t - (o > 0 ? a.count4[0] : 0) - (o > 1 ? a.count4[1] : 0);
+        const float *part = o == 0 ? a.part[0] : (o == 1 ? a.part[1] : a.part[2]);
+        floatx4 acc = reinterpret_cast<const floatx4 *>(part)[i];
+        for (int sp = 1; sp < a.split; sp++) acc += reinterpret_cast<const floatx4 *>(part)[sp * a.count4[o] + i];
+        dense_store<BF16>(o == 0 ? a.out[0] : (o == 1 ? a.out[1] : a.out[2]), 4 * i, acc, 1.0f);
     }
 }
 
@@ -2319,15 +2362,47 @@ hipError_t launch_pairs(const uint16_t *qcodes, const uint16_t *kcodes, const vo
             ds.n_s = side ? n_q : n_k;
         }
         d.bh = bh; d.m = m; d.tau = tau;
-        const int64_t blocks = bh * ((n_q + kDenseRows - 1) / kDenseRows + (n_k + kDenseRows - 1) / kDenseRows);
+        const int64_t blocks1 = bh * ((n_q + kDenseRows - 1) / kDenseRows + (n_k + kDenseRows - 1) / kDenseRows);
+        // Few fixed-row blocks (a head or two): each block's streamed rows are split
+        // among kDenseSplit workgroups, whose fp32 partial outputs go to the workspace
+        // after the partial-row sections' start (unused by this form) and are summed in
+        // split order.  Many blocks: one workgroup each, outputs stored directly.
+        int split = 1;
+        const size_t part_room = L.total - L.pq;
+        const size_t per_split = static_cast<size_t>(bh) * static_cast<size_t>(n_q + 2 * n_k) * D * sizeof(float);
+        if (blocks1 < kDenseSplitBelow && (n_q > n_k ? n_q : n_k) >= kDenseSplitMinRows)
+            while (split < kDenseSplit && per_split * (2 * split) <= part_room) split *= 2;
+        d.split = split;
+        float *pq0 = reinterpret_cast<float *>(ws + L.pq);
+        d.side[0].pout = pq0;
+        d.side[0].pout2 = nullptr;
+        d.side[1].pout = pq0 + static_cast<int64_t>(split) * bh * n_q * D;
+        d.side[1].pout2 = d.side[1].pout + static_cast<int64_t>(split) * bh * n_k * D;
+        const int64_t blocks = blocks1 * split;
         const size_t lds = static_cast<size_t>(kDenseRows) * dense_stride(n_q > n_k ? n_q : n_k) * 4;
-        KernelTimer timer("dense_kernel", stream);
-        // 32-row streamed tiles where the blocks fill the GPU at three per CU (384 x
-        // 512: 618 -> 515 us), 64-row ones for a few blocks (fewer barriers per row)
-        const bool t32 = blocks >= 512;
-        auto kernel = bf16 ? (t32 ? dense_kernel<true, 32> : dense_kernel<true, 64>)
-                           : (t32 ? dense_kernel<false, 32> : dense_kernel<false, 64>);
-        hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, stream, d);
+        {
+            KernelTimer timer("dense_kernel", stream);
+            // 32-row streamed tiles where the blocks fill the GPU at three per CU (384 x
+            // 512: 618 -> 515 us), 64-row ones for a few blocks (fewer barriers per row)
+            const bool t32 = blocks >= 512;
+            auto kernel = bf16 ? (t32 ? dense_kernel<true, 32> : dense_kernel<true, 64>)
+                               : (t32 ? dense_kernel<false, 32> : dense_kernel<false, 64>);
+            hipLaunchKernelGGL(kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), lds, stream, d);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        if (split == 1) return hipSuccess;
+        KernelTimer timer("dense_sum_kernel", stream);
+        DenseSum sa;
+        sa.part[0] = d.side[0].pout; sa.part[1] = d.side[1].pout; sa.part[2] = d.side[1].pout2;
+        sa.out[0] = dq; sa.out[1] = dk; sa.out[2] = dv;
+        sa.count4[0] = bh * n_q * D / 4; sa.count4[1] = sa.count4[2] = bh * n_k * D / 4;
+        sa.split = split;
+        const int64_t total = sa.count4[0] + 2 * sa.count4[1];
+        const int64_t grid = (total + 255) / 256 < 4096 ? (total + 255) / 256 : 4096;
+        if (bf16)
+            hipLaunchKernelGGL(dense_sum_kernel<true>, dim3(static_cast<unsigned>(grid)), dim3(256), 0, stream, sa);
+        else
+            hipLaunchKernelGGL(dense_sum_kernel<false>, dim3(static_cast<unsigned>(grid)), dim3(256), 0, stream, sa);
         return hipGetLastError();
     }
 
