@@ -54,6 +54,8 @@ constexpr int kTableWaves = kTableThreads / 64;
 // fp32 outputs with more source rows than this also bound the bucket sums by the
 // largest bucket count (a count pass over the codes before the scatter)
 constexpr int64_t kTableHistRows = 8192;
+// launches with fewer workgroups than this take narrower slices (down to two dims)
+constexpr int64_t kTableFewBlocks = 128;
 
 template <bool BF16, int DS>
 __device__ __forceinline__ void load_slice(const void *base, int64_t off, float v[DS]) {
@@ -746,7 +748,13 @@ hipError_t launch_table(const uint16_t *src_codes, const void *values, const uin
                         bool bf16, int64_t bh, int64_t n_src, int64_t n_dst, int m, int tau, void *workspace,
                         hipStream_t stream) {
     if (bh == 0 || n_dst == 0) return hipSuccess;
-    const TablePlan p = plan_table(m, tau);
+    TablePlan p = plan_table(m, tau);
+    // a head or two: narrower slices, so that more workgroups share the work (one head
+    // of 512 rows: 16 -> 32 workgroups, 15 -> 11.6 us); the hashes per pass stay
+    while (p.DS > 2 && bh * (D / p.DS) < kTableFewBlocks) {
+        p.DS /= 2;
+        p.lds /= 2;
+    }
     TableArgs a;
     a.src_codes = src_codes;
     a.values = values;
