@@ -20,8 +20,8 @@
 // converts R once into fp16 MFMA B-fragments in LDS and then walks tiles of 32
 // rows per wave (persistent when there are more tiles than resident
 // workgroups); each wave owns 32 rows of a tile (two 16-row MFMA tiles, so every
-// B-fragment read from LDS feeds two row tiles) and all ceil(m*tau/16) column
-// tiles.  The rows of a wave's next tile are loaded into registers while the
+// B-fragment read from LDS feeds two row tiles; 16 rows when the tiles would not
+// fill the resident workgroups) and all ceil(m*tau/16) column tiles.  The rows of a wave's next tile are loaded into registers while the
 // current one is computed; the first tile's loads are issued before the
 // conversion of R.  Signs are gathered with wave ballots: the four 64-bit
 // ballots of a 16 x 16 output tile hold the 16-column sign segments of its 16
@@ -37,8 +37,10 @@ namespace yoso {
 
 namespace {
 
-constexpr int kHashRT = 2;                   // 16-row MFMA tiles per wave
-constexpr int kHashWaveRows = 16 * kHashRT;  // rows per wave and tile
+// 16-row MFMA tiles per wave and tile: RT = 2 (32 rows) where the workgroups fill
+// the GPU, RT = 1 (16 rows, each wave's chain of products half as long) where they
+// do not (one head of 512 rows: 15 -> 10 us; 384 x 512 rows: 33 -> 32 us with 2)
+constexpr int kHashMaxRT = 2;
 
 // fp32 -> fp16 (hi, lo) pairs, truncating (v_cvt_pkrtz_f16_f32 converts two values
 // per instruction): hi = rtz(s), lo = rtz(s - hi), with s - hi exact in fp32;
@@ -58,11 +60,11 @@ __device__ __forceinline__ void split8_rtz(const float v[8], float scale, half8 
 
 // Lane L feeds the A operand of row 16t + (L & 15), elements kb*32 + (L >> 4)*8 + [0, 8).
 // Rows past the end load the last row (a valid address); their codes are not stored.
-template <bool BF16>
+template <bool BF16, int RT>
 __device__ __forceinline__ void hash_load_rows(const void *__restrict__ x, int64_t rows, int64_t base, int lane,
-                                               float (&v)[kHashRT][2][8]) {
+                                               float (&v)[RT][2][8]) {
 #pragma unroll
-    for (int t = 0; t < kHashRT; t++) {
+    for (int t = 0; t < RT; t++) {
         int64_t row = base + 16 * t + (lane & 15);
         row = row < rows ? row : rows - 1;
 #pragma unroll
@@ -70,11 +72,12 @@ __device__ __forceinline__ void hash_load_rows(const void *__restrict__ x, int64
     }
 }
 
-template <bool BF16, int WAVES>
+template <bool BF16, int WAVES, int RT>
 __global__ __launch_bounds__(64 * WAVES) void hash_kernel(const void *__restrict__ x, int64_t rows,
                                                             const float *__restrict__ R, int m, int tau,
                                                             uint16_t *__restrict__ codes, int64_t num_tiles) {
     constexpr int kHashThreads = 64 * WAVES;
+    constexpr int kHashWaveRows = 16 * RT;  // rows per wave and tile
     constexpr int kHashRowsPerTile = WAVES * kHashWaveRows;
     extern __shared__ __align__(16) unsigned char smem[];
     const int N = m * tau;               // columns of R
@@ -84,9 +87,9 @@ __global__ __launch_bounds__(64 * WAVES) void hash_kernel(const void *__restrict
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    // the wave's ballots: [kHashRT t][NT nt][4 i] uint64; bits [16g, 16g+16) of
+    // the wave's ballots: [RT t][NT nt][4 i] uint64; bits [16g, 16g+16) of
     // ballot (t, nt, i) are the signs of row 16t + 4g + i, columns 16nt .. 16nt+15
-    uint32_t *bal = reinterpret_cast<uint32_t *>(smem + (size_t)NT * 4096) + wave * kHashRT * NT * 8;
+    uint32_t *bal = reinterpret_cast<uint32_t *>(smem + (size_t)NT * 4096) + wave * RT * NT * 8;
     const uint16_t *seg = reinterpret_cast<const uint16_t *>(bal);
 
     // R -> fp16 B-fragments.  Fragment (nt, kb) lane L holds rows
@@ -112,9 +115,9 @@ __global__ __launch_bounds__(64 * WAVES) void hash_kernel(const void *__restrict
     };
     load_r(tid);
 
-    float xv[kHashRT][2][8];
+    float xv[RT][2][8];
     int64_t tile = blockIdx.x;
-    if (tile < num_tiles) hash_load_rows<BF16>(x, rows, tile * kHashRowsPerTile + wave * kHashWaveRows, lane, xv);
+    if (tile < num_tiles) hash_load_rows<BF16, RT>(x, rows, tile * kHashRowsPerTile + wave * kHashWaveRows, lane, xv);
 
     for (int s0 = tid; s0 < NT * 128; s0 += 4 * kHashThreads) {
         if (s0 != tid) load_r(s0);
@@ -146,9 +149,9 @@ __global__ __launch_bounds__(64 * WAVES) void hash_kernel(const void *__restrict
 
     for (; tile < num_tiles; tile += gridDim.x) {
         const int64_t base = tile * kHashRowsPerTile + wave * kHashWaveRows;
-        half8 ah[kHashRT][2], al[kHashRT][2];
+        half8 ah[RT][2], al[RT][2];
 #pragma unroll
-        for (int t = 0; t < kHashRT; t++) {
+        for (int t = 0; t < RT; t++) {
             // the row's largest |entry| (its 64 entries sit in the lanes L, L ^ 16,
             // L ^ 32, L ^ 48), then the power of two that brings it below 2^13
             float mx = 0.f;
@@ -168,21 +171,21 @@ __global__ __launch_bounds__(64 * WAVES) void hash_kernel(const void *__restrict
         }
         const int64_t next = tile + gridDim.x;
         if (next < num_tiles)
-            hash_load_rows<BF16>(x, rows, next * kHashRowsPerTile + wave * kHashWaveRows, lane, xv);
+            hash_load_rows<BF16, RT>(x, rows, next * kHashRowsPerTile + wave * kHashWaveRows, lane, xv);
 
         for (int g0 = 0; g0 < NT; g0 += 2) {
-            floatx4 acc[2][kHashRT];
+            floatx4 acc[2][RT];
 #pragma unroll
             for (int j = 0; j < 2; j++) {
                 const int nt = g0 + j;
 #pragma unroll
-                for (int t = 0; t < kHashRT; t++) acc[j][t] = floatx4{0.f, 0.f, 0.f, 0.f};
+                for (int t = 0; t < RT; t++) acc[j][t] = floatx4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int kb = 0; kb < 2; kb++) {
                     const half8 bh = frag[((nt * 2 + kb) * 2 + 0) * 64 + lane];
                     const half8 bl = frag[((nt * 2 + kb) * 2 + 1) * 64 + lane];
 #pragma unroll
-                    for (int t = 0; t < kHashRT; t++) {
+                    for (int t = 0; t < RT; t++) {
                         if constexpr (BF16) {
                             // (the lo parts of a scaled bf16 row are zero)
                             acc[j][t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(ah[t][kb], bh, acc[j][t], 0, 0, 0);
@@ -196,16 +199,16 @@ __global__ __launch_bounds__(64 * WAVES) void hash_kernel(const void *__restrict
             // acc[j][t][i] of lane L is P[row 16t + 4*(L>>4) + i][col (g0+j)*16 + (L&15)].
             // Ballot i collects, in bits [16g, 16g+16), the 16 column signs of row 16t + 4g + i.
             // The ballots are wave-uniform; lane 0 stores them.
-            uint64_t b[kHashRT][2][4];
+            uint64_t b[RT][2][4];
 #pragma unroll
-            for (int t = 0; t < kHashRT; t++)
+            for (int t = 0; t < RT; t++)
 #pragma unroll
                 for (int j = 0; j < 2; j++)
 #pragma unroll
                     for (int i = 0; i < 4; i++) b[t][j][i] = __ballot(acc[j][t][i] > 0.f);
             if (lane == 0) {
 #pragma unroll
-                for (int t = 0; t < kHashRT; t++) {
+                for (int t = 0; t < RT; t++) {
 #pragma unroll
                     for (int j = 0; j < 2; j++) {
                         uint4 *dst = reinterpret_cast<uint4 *>(bal + (t * NT + g0 + j) * 8);
@@ -257,7 +260,7 @@ struct HashShape {
 
 HashShape hash_shape(int m, int tau) {
     const int NT = ((m * tau + 31) >> 5) * 2;  // as in the kernel: column tiles rounded up to a pair
-    const size_t frag = (size_t)NT * 4096, bal = (size_t)kHashRT * NT * 32;
+    const size_t frag = (size_t)NT * 4096, bal = (size_t)kHashMaxRT * NT * 32;
     if (frag + 8 * bal <= 80 * 1024) return {8, 2, frag + 8 * bal};
     if (frag + 16 * bal <= 156 * 1024) return {16, 1, frag + 16 * bal};
     return {8, 1, frag + 8 * bal};
@@ -271,7 +274,6 @@ hipError_t launch_hash(const void *x, bool bf16, int64_t bh, int64_t n, const fl
     if (rows == 0) return hipSuccess;
     const HashShape shape = hash_shape(m, tau);
     const int waves = shape.waves;
-    const int64_t tiles = (rows + waves * kHashWaveRows - 1) / (waves * kHashWaveRows);
     const size_t lds = shape.lds;
     // Persistent workgroups, as many as are resident at once: each converts R
     // once, and with several tiles per workgroup the register prefetch overlaps
@@ -283,22 +285,21 @@ hipError_t launch_hash(const void *x, bool bf16, int64_t bh, int64_t n, const fl
         cus = 256;
     }
     const int64_t resident = static_cast<int64_t>(cus) * shape.per_cu;
+    // 32-row wave tiles where they fill the resident workgroups, else 16-row ones
+    const int64_t tiles2 = (rows + waves * 32 - 1) / (waves * 32);
+    const int rt = tiles2 < resident ? 1 : 2;
+    const int64_t tiles = rt == 2 ? tiles2 : (rows + waves * 16 - 1) / (waves * 16);
     const int64_t grid = tiles < resident ? tiles : resident;
     KernelTimer timer("hash_kernel", stream);
+    auto launch = [&](auto kernel, int threads) {
+        hipLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(threads), lds, stream, x, rows, R, m, tau, codes, tiles);
+    };
     if (bf16) {
-        if (waves == 8)
-            hipLaunchKernelGGL((hash_kernel<true, 8>), dim3((unsigned)grid), dim3(512), lds, stream, x, rows, R, m,
-                               tau, codes, tiles);
-        else
-            hipLaunchKernelGGL((hash_kernel<true, 16>), dim3((unsigned)grid), dim3(1024), lds, stream, x, rows, R,
-                               m, tau, codes, tiles);
+        if (waves == 8) rt == 2 ? launch(hash_kernel<true, 8, 2>, 512) : launch(hash_kernel<true, 8, 1>, 512);
+        else rt == 2 ? launch(hash_kernel<true, 16, 2>, 1024) : launch(hash_kernel<true, 16, 1>, 1024);
     } else {
-        if (waves == 8)
-            hipLaunchKernelGGL((hash_kernel<false, 8>), dim3((unsigned)grid), dim3(512), lds, stream, x, rows, R, m,
-                               tau, codes, tiles);
-        else
-            hipLaunchKernelGGL((hash_kernel<false, 16>), dim3((unsigned)grid), dim3(1024), lds, stream, x, rows, R,
-                               m, tau, codes, tiles);
+        if (waves == 8) rt == 2 ? launch(hash_kernel<false, 8, 2>, 512) : launch(hash_kernel<false, 8, 1>, 512);
+        else rt == 2 ? launch(hash_kernel<false, 16, 2>, 1024) : launch(hash_kernel<false, 16, 1>, 1024);
     }
     return hipGetLastError();
 }
