@@ -127,7 +127,7 @@ def backward_d2(qc, kc, q, k, v, dy, m: int, tau: int):
 
 
 # Bound of 1 - x^2 in *YOSO's weight 1/(pi sqrt(1 - x^2)) (|x| <= 0.99216, at most
-# 8/pi): the reading this build takes of the divergence that Sec. 3.3 points out.
+# 8/pi): the reading taken here of the divergence that Sec. 3.3 points out.
 STAR_FLOOR = 1.0 / 64.0
 
 
