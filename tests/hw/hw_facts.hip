@@ -138,6 +138,27 @@ __global__ __launch_bounds__(256) void global_atomic_kernel(float *buf, uint32_t
 }
 
 // ---- MFMA issue rate: each wave runs ACC independent accumulator chains of one instruction shape.
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+template <int ACC>
+__global__ __launch_bounds__(256) void mfma32_kernel(float *out, int iters, float seed) {
+  floatx16 acc[ACC];
+  for (int i = 0; i < ACC; i++)
+    for (int j = 0; j < 16; j++) acc[i][j] = 0.f;
+  half8 a8, b8;
+  for (int i = 0; i < 8; i++) {
+    a8[i] = static_cast<_Float16>(seed * (threadIdx.x + i));
+    b8[i] = static_cast<_Float16>(seed * i);
+  }
+  for (int it = 0; it < iters; it++) {
+#pragma unroll
+    for (int i = 0; i < ACC; i++) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a8, b8, acc[i], 0, 0, 0);
+  }
+  float s = 0.f;
+  for (int i = 0; i < ACC; i++)
+    for (int j = 0; j < 16; j++) s += acc[i][j];
+  out[blockIdx.x * 256 + threadIdx.x] = s;
+}
+
 template <bool K32, int ACC>
 __global__ __launch_bounds__(256) void mfma_kernel(float *out, int iters, float seed) {
   floatx4 acc[ACC];
@@ -256,6 +277,17 @@ static void mfma(float *scratch, const char *name) {
               flops / (ms * 1e-3) / 1e15, clk_per_instr);
 }
 
+static void mfma32(float *scratch) {
+  const int blocks = 2048, iters = 2048;
+  constexpr int ACC = 4;
+  Timer t;
+  const double ms = t.ms([&] { mfma32_kernel<ACC><<<blocks, 256>>>(scratch, iters, 1e-3f); });
+  const double flops = 2.0 * 32 * 32 * 16 * ACC * iters * (blocks * 4.0);
+  const double clk_per_instr = ms * 1e-3 * kClock / (double(ACC) * iters * blocks * 4 / (4.0 * g_cus));
+  std::printf("| `v_mfma_f32_32x32x16_f16`, %d independent accumulators per wave | %.3g PFLOP/s, %.1f clk per instruction per SIMD |\n",
+              ACC, flops / (ms * 1e-3) / 1e15, clk_per_instr);
+}
+
 static bool check_subnormals() {
   float *d;
   CK(hipMalloc(&d, 64 * 4 * sizeof(float)));
@@ -352,6 +384,7 @@ int main(int argc, char **argv) {
 
     mfma<true>(static_cast<float *>(scratch), "`v_mfma_f32_16x16x32_f16`");
     mfma<false>(static_cast<float *>(scratch), "`v_mfma_f32_16x16x16_f16`");
+    mfma32(static_cast<float *>(scratch));
     CK(hipFree(scratch));
     std::printf("\n");
   }
